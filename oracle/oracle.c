@@ -1,0 +1,263 @@
+/*
+ * CPU oracle for sequentially-correct sparse SGD.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header or constant table with the GPU library; it is a plain, slow,
+ * single-threaded restatement of what the paper defines:
+ *
+ *   - Sequential computation (Algorithm 1, Definition 4): iterations run one
+ *     after another; in each, every parameter the iteration touches is read,
+ *     the update is computed, then the parameters are written.  With SGD one
+ *     iteration is one training example (Sec. 6.3), and the gradient step is
+ *     the scalar form of the gradient-descent update of Sec. 2.
+ *   - Conflict levels: the read and write constraints (Sec. 4.4, Theorem 2)
+ *     order only accesses to the same parameter partition.  With one feature
+ *     per partition, example i must follow the most recent earlier example
+ *     that touched any of its features.  level(i) = 1 + max level over those
+ *     examples (0 when there is none); examples of equal level touch disjoint
+ *     features and may run concurrently.
+ *
+ * Floating point is IEEE binary32, round to nearest, no flush to zero; fused
+ * multiply-add appears only where fmaf() is written (build with
+ * -ffp-contract=off).  Two summation orders exist for the dot product:
+ *   natural: z = fmaf(w[c_k], x_k, z) for k = 0..m-1;
+ *   matched: 64 partial sums, entry k goes to partial k mod 64, then a
+ *            butterfly: for off = 32,16,8,4,2,1 every partial l becomes
+ *            p[l] + p[l xor off]; z is the common final value.
+ * The exponential is the library expf in natural mode and, in matched mode,
+ * orc_exp below (Cody-Waite range reduction and the degree-7 Taylor
+ * polynomial of e^r in Horner form).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORC_NATURAL = 0, ORC_MATCHED = 1 };
+enum { ORC_LOGISTIC = 0, ORC_SQUARED = 1 };
+
+/* ------------------------------------------------------------------------ */
+/* exp(x) = 2^k * e^r with k = rint(x log2 e), r = x - k ln 2 (ln 2 split in
+ * two floats so r carries the low bits), e^r by its Taylor series to r^7. */
+float orc_exp(float x) {
+    if (x != x) return x;
+    if (x > 89.0f) return INFINITY;
+    if (x < -104.0f) return 0.0f;
+    const float log2e = 0x1.715476p+0f;
+    const float ln2_hi = 0x1.62e430p-1f;
+    const float ln2_lo = -0x1.05c610p-29f;
+    float k = rintf(x * log2e);
+    float r = fmaf(-k, ln2_hi, x);
+    r = fmaf(-k, ln2_lo, r);
+    /* 1/7!, 1/6!, ..., 1/2!, 1, 1 rounded to binary32 */
+    float q = 0x1.a01a02p-13f;
+    q = fmaf(q, r, 0x1.6c16c2p-10f);
+    q = fmaf(q, r, 0x1.111112p-7f);
+    q = fmaf(q, r, 0x1.555556p-5f);
+    q = fmaf(q, r, 0x1.555556p-3f);
+    q = fmaf(q, r, 0.5f);
+    q = fmaf(q, r, 1.0f);
+    q = fmaf(q, r, 1.0f);
+    int ki = (int)k;
+    float two_k;
+    if (ki > 127) {
+        /* q * 2^127 is exact; the second product overflows or not by itself */
+        uint32_t b127 = (uint32_t)(127 + 127) << 23, b1 = (uint32_t)(ki - 127 + 127) << 23;
+        float s127, s1;
+        memcpy(&s127, &b127, 4);
+        memcpy(&s1, &b1, 4);
+        return (q * s127) * s1;
+    }
+    if (ki < -126) {
+        /* q * 2^(k+126) is exact and normal; one rounding into the subnormals */
+        uint32_t ba = (uint32_t)(ki + 126 + 127) << 23, bb = (uint32_t)(-126 + 127) << 23;
+        float sa, sb;
+        memcpy(&sa, &ba, 4);
+        memcpy(&sb, &bb, 4);
+        return (q * sa) * sb;
+    }
+    uint32_t bk = (uint32_t)(ki + 127) << 23;
+    memcpy(&two_k, &bk, 4);
+    return q * two_k;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Conflict levels                                                          */
+
+static int rows_share_feature(const int64_t *row_ptr, const int32_t *col, int64_t a, int64_t b) {
+    /* columns of a row are sorted ascending: merge */
+    int64_t p = row_ptr[a], pe = row_ptr[a + 1], q = row_ptr[b], qe = row_ptr[b + 1];
+    while (p < pe && q < qe) {
+        if (col[p] == col[q]) return 1;
+        if (col[p] < col[q]) ++p; else ++q;
+    }
+    return 0;
+}
+
+/* Brute force from the definition: level(i) = 1 + max{ level(j) : j < i, S(j) and S(i)
+ * intersect }, max of the empty set = 0.  O(n^2 m); tiny inputs only. */
+int32_t orc_levels_brute(int64_t n, const int64_t *row_ptr, const int32_t *col, int32_t *level) {
+    int32_t L = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t lv = 1;
+        for (int64_t j = 0; j < i; ++j)
+            if (level[j] + 1 > lv && rows_share_feature(row_ptr, col, j, i)) lv = level[j] + 1;
+        level[i] = lv;
+        if (lv > L) L = lv;
+    }
+    return L;
+}
+
+/* One pass in example order.  last[f] = level of the latest example so far
+ * that touched feature f (0 if none).  Returns L = max level, -1 on failure. */
+int32_t orc_levels_seq(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                       int32_t *level) {
+    int32_t *last = (int32_t *)calloc((size_t)(d > 0 ? d : 1), sizeof(int32_t));
+    if (!last) return -1;
+    int32_t L = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t lv = 0;
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+            if (last[col[p]] > lv) lv = last[col[p]];
+        lv += 1;
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) last[col[p]] = lv;
+        level[i] = lv;
+        if (lv > L) L = lv;
+    }
+    free(last);
+    return L;
+}
+
+/* Examples grouped by level, ascending index inside a level.
+ * level_ptr[l] = number of examples with level <= l, l = 0..L. */
+int orc_bucket(int64_t n, const int32_t *level, int32_t L, int32_t *perm, int64_t *level_ptr) {
+    memset(level_ptr, 0, (size_t)(L + 1) * sizeof(int64_t));
+    for (int64_t i = 0; i < n; ++i) {
+        if (level[i] < 1 || level[i] > L) return -1;
+        level_ptr[level[i]] += 1;
+    }
+    for (int32_t l = 1; l <= L; ++l) level_ptr[l] += level_ptr[l - 1];
+    int64_t *next = (int64_t *)malloc((size_t)(L + 1) * sizeof(int64_t));
+    if (!next) return -1;
+    for (int32_t l = 1; l <= L; ++l) next[l] = level_ptr[l - 1];
+    for (int64_t i = 0; i < n; ++i) perm[next[level[i]]++] = (int32_t)i;
+    free(next);
+    return 0;
+}
+
+/* For every stored entry (CSR order): the latest earlier example that touched
+ * the same feature, or -1. */
+int orc_prev_writer(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                    int32_t *prev_row) {
+    int32_t *last = (int32_t *)malloc((size_t)(d > 0 ? d : 1) * sizeof(int32_t));
+    if (!last) return -1;
+    for (int64_t f = 0; f < d; ++f) last[f] = -1;
+    for (int64_t i = 0; i < n; ++i) {
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) prev_row[p] = last[col[p]];
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) last[col[p]] = (int32_t)i;
+    }
+    free(last);
+    return 0;
+}
+
+/* Per-feature occurrence lists (CSC): col_ptr[d+1], rows ascending per feature. */
+int orc_transpose(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                  int64_t *col_ptr, int32_t *csc_row) {
+    memset(col_ptr, 0, (size_t)(d + 1) * sizeof(int64_t));
+    int64_t nnz = row_ptr[n];
+    for (int64_t p = 0; p < nnz; ++p) col_ptr[col[p] + 1] += 1;
+    for (int64_t f = 0; f < d; ++f) col_ptr[f + 1] += col_ptr[f];
+    int64_t *next = (int64_t *)malloc((size_t)(d > 0 ? d : 1) * sizeof(int64_t));
+    if (!next) return -1;
+    memcpy(next, col_ptr, (size_t)d * sizeof(int64_t));
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) csc_row[next[col[p]]++] = (int32_t)i;
+    free(next);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sequential SGD                                                           */
+
+static float dot_natural(const float *w, const int32_t *c, const float *v, int64_t m) {
+    float z = 0.0f;
+    for (int64_t k = 0; k < m; ++k) z = fmaf(w[c[k]], v ? v[k] : 1.0f, z);
+    return z;
+}
+
+static float butterfly64(float *acc, int width) {
+    float nxt[64];
+    for (int off = width / 2; off >= 1; off /= 2) {
+        for (int l = 0; l < width; ++l) nxt[l] = acc[l] + acc[l ^ off];
+        memcpy(acc, nxt, (size_t)width * sizeof(float));
+    }
+    return acc[0];
+}
+
+static float dot_matched(const float *w, const int32_t *c, const float *v, int64_t m) {
+    float acc[64];
+    for (int l = 0; l < 64; ++l) acc[l] = 0.0f;
+    for (int64_t k = 0; k < m; ++k) acc[k & 63] = fmaf(w[c[k]], v ? v[k] : 1.0f, acc[k & 63]);
+    return butterfly64(acc, 64);
+}
+
+/* One SGD step per example, examples taken in the given order (NULL: index
+ * order 0..n-1, which is Algorithm 1).  Per example i with entries (c_k, x_k):
+ *   z = <w, x_i>;  logistic: g = 1/(1+exp(-z)) - [y_i > 0];  squared: g = z - y_i
+ *   s = lr * g;    w[c_k] <- fmaf(-s, x_k, w[c_k])  (all reads before any write). */
+void orc_sgd_apply(int64_t count, const int32_t *order, const int64_t *row_ptr,
+                   const int32_t *col, const float *val, const float *y, float *w, float lr,
+                   int32_t loss, int32_t mode) {
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t i = order ? order[t] : t;
+        int64_t b = row_ptr[i], m = row_ptr[i + 1] - b;
+        const int32_t *c = col + b;
+        const float *v = val ? val + b : NULL;
+        float z = (mode == ORC_MATCHED) ? dot_matched(w, c, v, m) : dot_natural(w, c, v, m);
+        float g;
+        if (loss == ORC_LOGISTIC) {
+            float e = (mode == ORC_MATCHED) ? orc_exp(-z) : expf(-z);
+            float sig = 1.0f / (1.0f + e);
+            g = sig - ((y[i] > 0.0f) ? 1.0f : 0.0f);
+        } else {
+            g = z - y[i];
+        }
+        float s = lr * g;
+        /* the new values depend only on values read before any write: the
+         * columns of a row are distinct, so writing in place is the same */
+        for (int64_t k = 0; k < m; ++k) w[c[k]] = fmaf(-s, v ? v[k] : 1.0f, w[c[k]]);
+    }
+}
+
+/* Matrix completion, one rating per iteration:
+ *   e = r - <U_u, V_i>
+ *   U_u <- U_u + lr (e V_i - reg U_u),  V_i <- V_i + lr (e U_u - reg V_i)
+ * with both right-hand sides using the values read before the step (the L2
+ * regulariser of Eq. 2 applied to the two touched rows). */
+void orc_mf_apply(int64_t count, const int32_t *order, const int32_t *user, const int32_t *item,
+                  const float *rating, float *U, float *V, int32_t rank, float lr, float reg,
+                  int32_t mode) {
+    float acc[64];
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t i = order ? order[t] : t;
+        float *u = U + (int64_t)user[i] * rank;
+        float *v = V + (int64_t)item[i] * rank;
+        float dot;
+        if (mode == ORC_MATCHED) {
+            for (int l = 0; l < rank; ++l) acc[l] = fmaf(u[l], v[l], 0.0f);
+            dot = butterfly64(acc, rank);
+        } else {
+            dot = 0.0f;
+            for (int l = 0; l < rank; ++l) dot = fmaf(u[l], v[l], dot);
+        }
+        float e = rating[i] - dot;
+        for (int l = 0; l < rank; ++l) {
+            float ul = u[l], vl = v[l];
+            float a = e * vl, b = reg * ul;
+            float a2 = e * ul, b2 = reg * vl;
+            u[l] = fmaf(lr, a - b, ul);
+            v[l] = fmaf(lr, a2 - b2, vl);
+        }
+    }
+}
