@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Throughput of sequentially-correct sparse SGD on one MI355X.
+
+A step is one pass of the whole path over the workload, inputs resident in
+HBM: conflict levels (pdb_schedule: transpose, previous writers, levels,
+grouping) and one SGD epoch (pdb_sgd_epoch / pdb_mf_epoch), weights reset to
+w0 at the start of the step.  `value` = stored entries updated per second
+over the K timed steps (ratings per second for matrix completion).
+
+Default workload: 10M examples x 1M features, 50 entries per example with
+Zipf(1.2) feature ids, binary values, logistic loss, lr 0.01.
+
+Prints one JSON line.  `roofline` prices the dominant kernel (the epoch)
+against HBM bandwidth with its algorithmic bytes; `cpu_baseline` times the
+CPU oracle on a bounded prefix of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+_ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, _ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "sequentially-correct nnz-updates/sec per epoch + achieved HBM GB/s fraction"
+
+
+def algorithmic_bytes(g, L, mf=False):
+    """Bytes one epoch must move at least once (the design doc lists the terms)."""
+    if mf:
+        # per rating: user, item, rating, perm (16 B) + read and write of a
+        # 128-byte user row and a 128-byte item row (512 B); level_ptr per level
+        return g["n"] * (16 + 512) + L * 8
+    per_nz = 4 + 8 + (4 if g["val"] is not None else 0)   # col, w read + write, val
+    per_ex = 8 + 4 + 4                                      # row_ptr, y, perm
+    return g["nnz"] * per_nz + g["n"] * per_ex + L * 8
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for f in ("apply.hip", "pdb_internal.h"):
+        with open(os.path.join(_ROOT, "paper_1508_00703_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload, digest):
+    """HBM bytes per epoch launch from the committed counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(_ROOT, "profiles", "traffic_%s.md" % workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if line.startswith("traffic_json:"):
+            vals = json.loads(line.split(":", 1)[1])
+    if vals.get("source_digest") != digest:
+        return None
+    return vals.get("hbm_bytes_per_launch")
+
+
+def trimmed_mean(xs):
+    xs = sorted(xs)
+    if len(xs) >= 10:
+        xs = xs[2:-2]
+    return sum(xs) / len(xs)
+
+
+def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None):
+    """The oracle (one-pass levels + grouping + natural-order epoch), single
+    thread, on the first rows of the same workload."""
+    import numpy as np
+
+    import oracle
+
+    mf = cfg_id == 5
+
+    def run(rows):
+        rp = g["row_ptr"][:rows + 1]
+        col = g["col"][:rp[-1]]
+        t0 = time.perf_counter()
+        level, perm, level_ptr, L = oracle.schedule(rp, col, g["d"])
+        if mf:
+            oracle.mf_epoch(g["user"][:rows], g["item"][:rows], g["rating"][:rows], g["U0"],
+                            g["V0"], g["lr"], g["reg"], oracle.NATURAL)
+        else:
+            val = None if g["val"] is None else g["val"][:rp[-1]]
+            oracle.sgd_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
+                             g["loss"], oracle.NATURAL)
+        return time.perf_counter() - t0, int(rp[-1]), level
+
+    n = g["n"]
+    probe = min(n, 20000)
+    t, _, _ = run(probe)
+    rows = int(min(n, max(probe, probe * budget_s / max(t, 1e-6))))
+    t, nnz_s, level = run(rows)
+    units = rows if mf else nnz_s
+    res = {"value": units / t, "unit": "ratings/s" if mf else "nnz-updates/s", "cores": 1,
+           "kind": "oracle",
+           "sample": "first %d of %d %s (%d stored entries), one-pass levels + grouping + "
+                     "natural-order epoch, %.1f s" % (rows, n, "ratings" if mf else "examples",
+                                                      nnz_s, t),
+           "host_cpu": platform.processor() or platform.machine()}
+    if gpu_levels is not None:
+        res["sample_levels_equal_gpu"] = bool(np.array_equal(gpu_levels[:rows], level))
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--method", type=int, default=0, help="0 auto, 1 chain-scan, 2 dataflow")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: the path does not shard across GPUs "
+              "(see DESIGN.md, 'More than one GPU'); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import datagen
+    from paper_1508_00703_amd import native
+
+    native.load()
+    dev = torch.device("cuda:0")
+    cfg_id = args.config
+    mf = cfg_id == 5
+    t0 = time.perf_counter()
+    g = datagen.generate_mf(cfg_id) if mf else datagen.generate(cfg_id)
+    t_gen = time.perf_counter() - t0
+    print("generated %s: n=%d nnz=%d in %.1f s" % (g["name"], g["n"], g["nnz"], t_gen),
+          file=sys.stderr, flush=True)
+
+    n, d, nnz = g["n"], g["d"], g["nnz"]
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None if mf else g["val"], dev)
+    lv = native.Levels(n, nnz, dev)
+    ws_s = native.workspace(native.pdb_schedule_workspace_bytes(n, d, nnz), dev)
+    ws_e = native.workspace(native.pdb_epoch_workspace_bytes(), dev)
+    if mf:
+        user = torch.from_numpy(g["user"]).to(dev)
+        item = torch.from_numpy(g["item"]).to(dev)
+        rating = torch.from_numpy(g["rating"]).to(dev)
+        U0 = torch.from_numpy(g["U0"]).to(dev)
+        V0 = torch.from_numpy(g["V0"]).to(dev)
+        U, V = U0.clone(), V0.clone()
+    else:
+        y = torch.from_numpy(g["y"]).to(dev)
+        w0 = torch.zeros(d, dtype=torch.float32, device=dev)
+        w = w0.clone()
+    stream = torch.cuda.current_stream(dev)
+    ev = []
+    sched_ms = []
+    info = {}
+
+    def step(timed):
+        nonlocal info
+        ts = time.perf_counter()
+        info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s)
+        sched_ms.append((time.perf_counter() - ts) * 1e3)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if mf:
+            U.copy_(U0)
+            V.copy_(V0)
+            a.record(stream)
+            native.pdb_mf_epoch(user, item, rating, n, U, g["n_users"], V, g["n_items"],
+                                g["rank"], float(g["lr"]), float(g["reg"]), lv, ws=ws_e)
+            b.record(stream)
+        else:
+            w.copy_(w0)
+            a.record(stream)
+            native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], lv, ws=ws_e)
+            b.record(stream)
+        if timed:
+            ev.append((a, b))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    if native.pdb_workspace_status(ws_e) != native.PDB_OK:
+        raise SystemExit("device-side failure during warmup")
+    sched_ms.clear()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(True)
+        print("step %d done" % k, file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if native.pdb_workspace_status(ws_e) != native.PDB_OK:
+        raise SystemExit("device-side failure during the timed steps")
+    elapsed = t1 - t0
+    epoch_ms = [a.elapsed_time(b) for a, b in ev]
+    ep = trimmed_mean(epoch_ms)
+    L = lv.L_host
+    units = n if mf else nnz
+    value = units * args.steps / elapsed
+    abytes = algorithmic_bytes(g, L, mf)
+    achieved = abytes / (ep * 1e-3) / 1e9
+    workload = "c%d" % cfg_id
+    digest = source_digest()
+    traffic = read_traffic(workload, digest)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "ratings/s" if mf else "nnz-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "%s: %s" % (workload, g["name"]), "n": n, "d": d, "nnz": nnz,
+                   "seed": g["seed"], "levels": L, "max_level_width": lv.max_width_host,
+                   "schedule_method": info.get("method_used"),
+                   "chain_scan_rounds": info.get("rounds")},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_levels_apply (epoch)", "algorithmic_bytes": abytes,
+                     "epoch_ms": ep, "epoch_ms_all": epoch_ms, "source_digest": digest},
+        "schedule_ms": trimmed_mean(sched_ms),
+        "epoch_ms": ep,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget, lv.level.cpu().numpy())
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,180 @@
+/*
+ * pdb -- sequentially-correct parallel SGD over sparse examples on one
+ * MI355X (gfx950) GPU.  C ABI.
+ *
+ * The method (Goel, Agrawal, Chawla, Elmagarmid, "Parameter Database:
+ * Data-centric Synchronization for Scalable Machine Learning"):
+ *   - the sequential computation of Algorithm 1 and Definition 4 is the
+ *     correctness target: iterations apply one after another, each reading
+ *     the parameters it needs before writing them;
+ *   - with stochastic gradient descent an iteration is one training example
+ *     (Sec. 6.3) and its update is the gradient step of Sec. 2;
+ *   - the read and write constraints of Sec. 4.4 only order accesses to the
+ *     same parameter partition, and Theorem 2 shows that enforcing them gives
+ *     the sequential result.  Here a partition is a single feature, so two
+ *     examples must keep their order exactly when they share a feature, and
+ *     examples that share none may run concurrently.
+ *
+ * pdb_schedule computes, per example, its conflict level: 1 + the largest
+ * level among the earlier examples that share a feature with it (1 if
+ * none).  Examples of one level touch pairwise disjoint features.
+ * pdb_sgd_epoch / pdb_mf_epoch apply one epoch level by level; the result is
+ * bitwise the sequential result of the fixed per-example arithmetic below.
+ *
+ * Conventions for every entry point:
+ *   - pointers named as device pointers must point to device memory owned
+ *     by the caller (e.g. allocated through PyTorch); the library never
+ *     frees or keeps them past the call;
+ *   - work is enqueued on the caller's stream; entry points that say
+ *     "synchronous" wait for that stream before returning;
+ *   - every entry point returns PDB_OK (0) or a negative pdb_status; no
+ *     exception or abort crosses the ABI;
+ *   - sizes: n, d, nnz < 2^31.
+ *
+ * Per-example arithmetic (binary32, round to nearest, subnormals kept,
+ * fused multiply-add only where written as fma):
+ *   entries (c_k, x_k), k = 0..m-1 in CSR order (x_k = 1 when val is NULL);
+ *   partial sums p_j = 0 for j = 0..63; p_{k mod 64} = fma(w[c_k], x_k, p_{k mod 64});
+ *   butterfly: for o = 32,16,8,4,2,1 every p_j becomes p_j + p_{j xor o}; z = p_0;
+ *   logistic: g = 1/(1 + exp(-z)) - (y > 0 ? 1 : 0), exp by Cody-Waite
+ *   reduction (k = rint(x log2 e)) and the degree-7 Taylor polynomial in
+ *   Horner form, scaled by 2^k;   least squares: g = z - y;
+ *   s = lr * g;  w[c_k] = fma(-s, x_k, w[c_k]) (values read before any write).
+ * Matrix completion (rank 32): q_j = fma(U_u[j], V_i[j], 0), butterfly over
+ *   o = 16..1, e = r - q_0;  U_u[j] = fma(lr, e*V_i[j] - reg*U_u[j], U_u[j]),
+ *   V_i[j] = fma(lr, e*U_u[j] - reg*V_i[j], V_i[j]) with the old U_u[j], V_i[j].
+ */
+#ifndef PDB_H
+#define PDB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hipStream_t;
+
+typedef enum pdb_status {
+    PDB_OK = 0,
+    PDB_ERR_INVALID_ARG = -1, /* null pointer, negative size, unsupported rank or loss */
+    PDB_ERR_BAD_CSR = -2,     /* malformed CSR (see pdb_validate_csr) */
+    PDB_ERR_WORKSPACE = -3,   /* workspace pointer NULL or smaller than required */
+    PDB_ERR_HIP = -4,         /* a HIP runtime call failed; pdb_last_hip_error() has the code */
+    PDB_ERR_DEVICE = -5,      /* a device-side check failed (spin-wait watchdog, inconsistent schedule) */
+    PDB_ERR_UNSUPPORTED = -6  /* sizes beyond 2^31 - 1 */
+} pdb_status;
+
+typedef enum pdb_loss { PDB_LOGISTIC = 0, PDB_SQUARED = 1 } pdb_loss;
+
+typedef enum pdb_sched_method {
+    PDB_SCHED_AUTO = 0,      /* chain-scan relaxation, then dataflow if it has not converged */
+    PDB_SCHED_CHAINSCAN = 1, /* chain-scan relaxation until the fixed point */
+    PDB_SCHED_DATAFLOW = 2   /* each example waits for its previous writers' levels */
+} pdb_sched_method;
+
+/* Sparse examples in CSR form (Definition 1: the immutable data set D). */
+typedef struct pdb_csr {
+    const int64_t *row_ptr; /* device, [n+1]; row_ptr[0] = 0, non-decreasing */
+    const int32_t *col;     /* device, [nnz]; within a row strictly increasing, in [0, d) */
+    const float *val;       /* device, [nnz]; NULL means every stored value is 1.0f */
+    int64_t nnz;            /* = row_ptr[n] */
+} pdb_csr;
+
+/* Output of pdb_schedule (all device arrays owned by the caller). */
+typedef struct pdb_levels {
+    int32_t *level;     /* [n]   conflict level of each example, 1-based */
+    int32_t *perm;      /* [n]   examples ordered by (level, index) */
+    int64_t *level_ptr; /* [n+1] level l holds perm[level_ptr[l-1] .. level_ptr[l]), l = 1..L;
+                                 level_ptr[0] = 0, level_ptr[L] = n */
+    int32_t *n_levels;  /* [1]   L */
+    int32_t *prev_nz;   /* [nnz] or NULL: for each stored entry, the CSR index of the previous
+                                 entry (earlier example) on the same feature, -1 if none */
+    /* host-side summary written by pdb_schedule; zero means unknown */
+    int64_t L_host;         /* L */
+    int64_t max_width_host; /* largest level width */
+} pdb_levels;
+
+/* Optional host-side report of pdb_schedule. */
+typedef struct pdb_schedule_info {
+    int32_t method_used;  /* pdb_sched_method that produced the levels */
+    int32_t rounds;       /* chain-scan rounds run */
+    int64_t n_levels;     /* L */
+    int64_t max_width;    /* largest level width */
+} pdb_schedule_info;
+
+/* Human-readable text for a pdb_status code (static storage). */
+const char *pdb_strerror(int status);
+
+/* hipError_t of the last failing HIP call in this thread (0 if none). */
+int pdb_last_hip_error(void);
+
+/* Device workspace (bytes) needed by pdb_schedule, pdb_transpose and
+ * pdb_prev_writer for these sizes.  Host-only arithmetic. */
+int pdb_schedule_workspace_bytes(int64_t n, int64_t d, int64_t nnz, size_t *bytes);
+
+/* Device workspace (bytes) needed by pdb_sgd_epoch, pdb_mf_epoch,
+ * pdb_validate_csr and pdb_workspace_status.  Host-only arithmetic. */
+int pdb_epoch_workspace_bytes(size_t *bytes);
+
+/* Conflict levels (read/write constraints of Sec. 4.4 at feature grain,
+ * Theorem 2): fills levels->level, perm, level_ptr, n_levels, prev_nz (when
+ * not NULL) and the host fields L_host, max_width_host.  labels is accepted
+ * for symmetry with pdb_sgd_epoch and ignored: conflicts depend only on the
+ * sparsity pattern.  ws: device workspace of at least
+ * pdb_schedule_workspace_bytes().  Synchronous (it waits for the stream).
+ * Does not check the CSR: call pdb_validate_csr first on untrusted input. */
+int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
+                 pdb_levels *levels, int method, pdb_schedule_info *info, void *ws,
+                 size_t ws_bytes, hipStream_t stream);
+
+/* One SGD epoch over all n examples in place on w (device, [d]), with the
+ * per-example arithmetic stated at the top of this header, for loss
+ * PDB_LOGISTIC (labels y in {-1,+1}: target y > 0) or PDB_SQUARED.  levels
+ * must come from pdb_schedule on the same CSR (or be an equivalent
+ * grouping: every level's examples pairwise feature-disjoint, every
+ * conflicting pair in index order across levels).  Asynchronous; a device
+ * error (watchdog) is reported by pdb_workspace_status on ws. */
+int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
+                  float lr, int loss, const pdb_levels *levels, void *ws, size_t ws_bytes,
+                  hipStream_t stream);
+
+/* One matrix-completion SGD epoch (rank 32): rating t touches user row
+ * U[user[t]] (device [n_users*32]) and item row V[item[t]] (device
+ * [n_items*32]); levels from pdb_schedule on the CSR whose row t is
+ * {user[t], n_users + item[t]}.  Asynchronous. */
+int pdb_mf_epoch(const int32_t *user, const int32_t *item, const float *rating, int64_t n,
+                 float *U, int64_t n_users, float *V, int64_t n_items, int32_t rank, float lr,
+                 float reg, const pdb_levels *levels, void *ws, size_t ws_bytes,
+                 hipStream_t stream);
+
+/* Checks row_ptr[0] == 0, row_ptr non-decreasing, row_ptr[n] == nnz, every
+ * column in [0, d) and strictly increasing within its row.  Synchronous.
+ * Returns PDB_OK or PDB_ERR_BAD_CSR.  ws: pdb_epoch_workspace_bytes(). */
+int pdb_validate_csr(const pdb_csr *csr, int64_t n, int64_t d, void *ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* Waits for the stream, then returns PDB_ERR_DEVICE if a kernel that used
+ * ws recorded a device-side failure (and clears it), else PDB_OK. */
+int pdb_workspace_status(void *ws, hipStream_t stream);
+
+/* Per-feature occurrence lists (the transpose that exposes which examples
+ * share a feature): col_ptr (device, [d+1]) and csc_row (device, [nnz],
+ * rows ascending within a feature).  ws as for pdb_schedule.  Synchronous. */
+int pdb_transpose(const pdb_csr *csr, int64_t n, int64_t d, int64_t *col_ptr, int32_t *csc_row,
+                  void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Previous writer of every stored entry (the per-feature version the Read
+ * Protocol of Sec. 5 waits for): prev_row (device, [nnz]) = the latest
+ * earlier example touching the same feature, -1 if none; prev_nz (device,
+ * [nnz], may be NULL) = the CSR index of that example's entry.  ws as for
+ * pdb_schedule.  Synchronous. */
+int pdb_prev_writer(const pdb_csr *csr, int64_t n, int64_t d, int32_t *prev_row,
+                    int32_t *prev_nz, void *ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDB_H */

@@ -1,0 +1,271 @@
+"""ctypes binding of libpdb.so (argument marshalling only).
+
+Every entry point has the C name.  Arrays are torch tensors on the GPU (torch
+is used for device memory and streams only); all computation happens in the
+HIP kernels of libpdb.so.  If the library is missing, ``load()`` raises:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpdb.so")
+
+PDB_OK = 0
+PDB_ERR_INVALID_ARG = -1
+PDB_ERR_BAD_CSR = -2
+PDB_ERR_WORKSPACE = -3
+PDB_ERR_HIP = -4
+PDB_ERR_DEVICE = -5
+PDB_ERR_UNSUPPORTED = -6
+PDB_LOGISTIC, PDB_SQUARED = 0, 1
+PDB_SCHED_AUTO, PDB_SCHED_CHAINSCAN, PDB_SCHED_DATAFLOW = 0, 1, 2
+
+# every symbol declared in include/pdb.h
+EXPORTS = (
+    "pdb_strerror", "pdb_last_hip_error", "pdb_schedule_workspace_bytes",
+    "pdb_epoch_workspace_bytes", "pdb_schedule", "pdb_sgd_epoch", "pdb_mf_epoch",
+    "pdb_validate_csr", "pdb_workspace_status", "pdb_transpose", "pdb_prev_writer",
+)
+
+
+class PdbCsr(ctypes.Structure):
+    _fields_ = [("row_ptr", ctypes.c_void_p), ("col", ctypes.c_void_p), ("val", ctypes.c_void_p),
+                ("nnz", ctypes.c_int64)]
+
+
+class PdbLevels(ctypes.Structure):
+    _fields_ = [("level", ctypes.c_void_p), ("perm", ctypes.c_void_p),
+                ("level_ptr", ctypes.c_void_p), ("n_levels", ctypes.c_void_p),
+                ("prev_nz", ctypes.c_void_p), ("L_host", ctypes.c_int64),
+                ("max_width_host", ctypes.c_int64)]
+
+
+class PdbScheduleInfo(ctypes.Structure):
+    _fields_ = [("method_used", ctypes.c_int32), ("rounds", ctypes.c_int32),
+                ("n_levels", ctypes.c_int64), ("max_width", ctypes.c_int64)]
+
+
+class PdbError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        lib = load()
+        msg = lib.pdb_strerror(code).decode()
+        hip = lib.pdb_last_hip_error() if code == PDB_ERR_HIP else 0
+        super().__init__("%s: %s (status %d%s)" % (where, msg, code,
+                                                     ", hipError %d" % hip if hip else ""))
+        self.code = code
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libpdb.so not built: run paper_1508_00703_amd/build.py "
+                          "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i64, i32, f32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
+                            ctypes.c_size_t)
+    lib.pdb_strerror.argtypes = [ctypes.c_int]
+    lib.pdb_strerror.restype = ctypes.c_char_p
+    lib.pdb_last_hip_error.argtypes = []
+    lib.pdb_schedule_workspace_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(sz)]
+    lib.pdb_epoch_workspace_bytes.argtypes = [ctypes.POINTER(sz)]
+    lib.pdb_schedule.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, ctypes.POINTER(PdbLevels),
+                                 ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, P]
+    lib.pdb_sgd_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int,
+                                  ctypes.POINTER(PdbLevels), P, sz, P]
+    lib.pdb_mf_epoch.argtypes = [P, P, P, i64, P, i64, P, i64, i32, f32, f32,
+                                 ctypes.POINTER(PdbLevels), P, sz, P]
+    lib.pdb_validate_csr.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, sz, P]
+    lib.pdb_workspace_status.argtypes = [P, P]
+    lib.pdb_transpose.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, P, P, sz, P]
+    lib.pdb_prev_writer.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, P, P, sz, P]
+    for name in EXPORTS:
+        if name not in ("pdb_strerror",):
+            getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(code: int, where: str):
+    if code != PDB_OK:
+        raise PdbError(code, where)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device):
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Csr:
+    """Device CSR: row_ptr int64[n+1], col int32[nnz], val float32[nnz] or None."""
+
+    def __init__(self, row_ptr: torch.Tensor, col: torch.Tensor, val: torch.Tensor | None):
+        if row_ptr.dtype != torch.int64 or col.dtype != torch.int32:
+            raise TypeError("row_ptr must be int64 and col int32")
+        if val is not None and val.dtype != torch.float32:
+            raise TypeError("val must be float32")
+        self.row_ptr, self.col, self.val = row_ptr, col, val
+        self.n = row_ptr.numel() - 1
+        self.nnz = col.numel()
+        self.device = row_ptr.device
+
+    @classmethod
+    def from_numpy(cls, row_ptr, col, val=None, device="cuda"):
+        rp = torch.from_numpy(row_ptr).to(device)
+        c = torch.from_numpy(col).to(device)
+        v = None if val is None else torch.from_numpy(val).to(device)
+        return cls(rp, c, v)
+
+    def c(self) -> PdbCsr:
+        return PdbCsr(_ptr(self.row_ptr), _ptr(self.col), _ptr(self.val), self.nnz)
+
+
+class Levels:
+    """Device output of pdb_schedule."""
+
+    def __init__(self, n: int, nnz: int, device, with_prev_nz: bool = False):
+        self.level = torch.empty(max(n, 0), dtype=torch.int32, device=device)
+        self.perm = torch.empty(max(n, 0), dtype=torch.int32, device=device)
+        self.level_ptr = torch.empty(n + 1, dtype=torch.int64, device=device)
+        self.n_levels = torch.empty(1, dtype=torch.int32, device=device)
+        self.prev_nz = (torch.empty(max(nnz, 0), dtype=torch.int32, device=device)
+                        if with_prev_nz else None)
+        self.L_host = 0
+        self.max_width_host = 0
+
+    @classmethod
+    def from_host(cls, level, perm, level_ptr, device, max_width=None):
+        """Schedule given as host arrays (e.g. from another implementation)."""
+        import numpy as np
+
+        n = len(level)
+        lv = cls(n, 0, device)
+        lv.level.copy_(torch.from_numpy(np.asarray(level, np.int32)))
+        lv.perm.copy_(torch.from_numpy(np.asarray(perm, np.int32)))
+        lv.level_ptr = torch.from_numpy(np.asarray(level_ptr, np.int64)).to(device)
+        L = len(level_ptr) - 1
+        lv.n_levels.fill_(L)
+        lv.L_host = L
+        lv.max_width_host = int(max_width if max_width is not None else
+                                (np.diff(level_ptr).max() if L > 0 else 0))
+        return lv
+
+    def c(self) -> PdbLevels:
+        return PdbLevels(_ptr(self.level), _ptr(self.perm), _ptr(self.level_ptr),
+                         _ptr(self.n_levels), _ptr(self.prev_nz), self.L_host,
+                         self.max_width_host)
+
+
+def pdb_strerror(code: int) -> str:
+    return load().pdb_strerror(code).decode()
+
+
+def pdb_schedule_workspace_bytes(n: int, d: int, nnz: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().pdb_schedule_workspace_bytes(n, d, nnz, ctypes.byref(out)),
+           "pdb_schedule_workspace_bytes")
+    return out.value
+
+
+def pdb_epoch_workspace_bytes() -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().pdb_epoch_workspace_bytes(ctypes.byref(out)), "pdb_epoch_workspace_bytes")
+    return out.value
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def pdb_schedule(csr: Csr, labels, n: int, d: int, levels: Levels, method: int = PDB_SCHED_AUTO,
+                 ws: torch.Tensor | None = None, stream=None) -> dict:
+    if ws is None:
+        ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
+    lv = levels.c()
+    info = PdbScheduleInfo()
+    _check(load().pdb_schedule(ctypes.byref(csr.c()), _ptr(labels), n, d, ctypes.byref(lv),
+                               method, ctypes.byref(info), _ptr(ws), ws.numel(),
+                               _stream(stream, csr.device)), "pdb_schedule")
+    levels.L_host, levels.max_width_host = lv.L_host, lv.max_width_host
+    return dict(method_used=info.method_used, rounds=info.rounds, n_levels=info.n_levels,
+                max_width=info.max_width)
+
+
+def pdb_sgd_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor, lr: float,
+                  loss: int, levels: Levels, ws: torch.Tensor | None = None, stream=None):
+    if w.dtype != torch.float32 or labels.dtype != torch.float32:
+        raise TypeError("w and labels must be float32")
+    if w.numel() < d or labels.numel() < n:
+        raise ValueError("w must hold d entries and labels n entries")
+    if ws is None:
+        ws = workspace(pdb_epoch_workspace_bytes(), csr.device)
+    _check(load().pdb_sgd_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
+                                ctypes.c_float(lr), loss, ctypes.byref(levels.c()), _ptr(ws),
+                                ws.numel(), _stream(stream, csr.device)), "pdb_sgd_epoch")
+    return ws
+
+
+def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, rank: int,
+                 lr: float, reg: float, levels: Levels, ws=None, stream=None):
+    for t, name in ((user, "user"), (item, "item")):
+        if t.dtype != torch.int32 or t.numel() < n:
+            raise TypeError("%s must be int32[n]" % name)
+    if U.numel() < n_users * rank or V.numel() < n_items * rank:
+        raise ValueError("U / V too small")
+    if ws is None:
+        ws = workspace(pdb_epoch_workspace_bytes(), U.device)
+    _check(load().pdb_mf_epoch(_ptr(user), _ptr(item), _ptr(rating), n, _ptr(U), n_users,
+                               _ptr(V), n_items, rank, ctypes.c_float(lr), ctypes.c_float(reg),
+                               ctypes.byref(levels.c()), _ptr(ws), ws.numel(),
+                               _stream(stream, U.device)), "pdb_mf_epoch")
+    return ws
+
+
+def pdb_validate_csr(csr: Csr, n: int, d: int, ws=None, stream=None) -> int:
+    """Returns the status code (PDB_OK or PDB_ERR_BAD_CSR); raises on other errors."""
+    if ws is None:
+        ws = workspace(pdb_epoch_workspace_bytes(), csr.device)
+    rc = load().pdb_validate_csr(ctypes.byref(csr.c()), n, d, _ptr(ws), ws.numel(),
+                                 _stream(stream, csr.device))
+    if rc not in (PDB_OK, PDB_ERR_BAD_CSR):
+        raise PdbError(rc, "pdb_validate_csr")
+    return rc
+
+
+def pdb_workspace_status(ws: torch.Tensor, stream=None) -> int:
+    return load().pdb_workspace_status(_ptr(ws), _stream(stream, ws.device))
+
+
+def pdb_transpose(csr: Csr, n: int, d: int, col_ptr, csc_row, ws=None, stream=None):
+    if ws is None:
+        ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
+    _check(load().pdb_transpose(ctypes.byref(csr.c()), n, d, _ptr(col_ptr), _ptr(csc_row),
+                                _ptr(ws), ws.numel(), _stream(stream, csr.device)),
+           "pdb_transpose")
+
+
+def pdb_prev_writer(csr: Csr, n: int, d: int, prev_row, prev_nz=None, ws=None, stream=None):
+    if ws is None:
+        ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
+    _check(load().pdb_prev_writer(ctypes.byref(csr.c()), n, d, _ptr(prev_row), _ptr(prev_nz),
+                                  _ptr(ws), ws.numel(), _stream(stream, csr.device)),
+           "pdb_prev_writer")

@@ -1,0 +1,193 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Levels, perm and level_ptr must be bit-exact; weights
+bitwise equal to the oracle's matched summation order and within 1e-5 of its
+natural order."""
+import numpy as np
+import pytest
+
+import datagen
+import oracle
+from pdbtest import check_mf, check_schedule, check_sgd, csr_from_rows, gpu_schedule
+
+pytestmark = pytest.mark.gpu
+
+METHODS = [0, 1, 2]  # auto, chain-scan, dataflow
+
+
+def native_mod():
+    from paper_1508_00703_amd import native
+    return native
+
+
+def structured_cases():
+    n = 300
+    return {
+        "single": [{3}],
+        "fully_conflicting": [{0, 1 + i % 7} for i in range(n)],
+        "disjoint": [{2 * i, 2 * i + 1} for i in range(n)],
+        "chain": [{i, i + 1} for i in range(n)],
+        "interleaved": [{i % 2} for i in range(n)],
+        "empty_rows": [set() if i % 3 == 0 else {i % 5, 7} for i in range(n)],
+        "wide_rows": [set(range(i % 4, 200 + i % 4, 1 + i % 3)) for i in range(40)],
+        "row_64_65": [set(range(64)), set(range(64, 129)), set(range(1, 66)), set(range(200, 263))],
+        "one_feature": [{0}] * 50,
+    }
+
+
+@pytest.mark.parametrize("name", sorted(structured_cases()))
+@pytest.mark.parametrize("method", METHODS)
+def test_structured_schedules(gpu, name, method):
+    rows = structured_cases()[name]
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1 if len(col) else 1
+    check_schedule(native_mod(), gpu, row_ptr, col, d, method)
+
+
+def test_no_stored_entries(gpu):
+    row_ptr = np.zeros(17, np.int64)
+    col = np.zeros(0, np.int32)
+    lv, _ = check_schedule(native_mod(), gpu, row_ptr, col, 5, 0)
+    assert lv.L_host == 1
+
+
+def test_no_examples(gpu):
+    native = native_mod()
+    lv, info = gpu_schedule(native, gpu, np.zeros(1, np.int64), np.zeros(0, np.int32), 4, 0)
+    assert lv.L_host == 0 and int(lv.n_levels.item()) == 0
+
+
+@pytest.mark.parametrize("name", sorted(structured_cases()))
+@pytest.mark.parametrize("loss", [0, 1])
+@pytest.mark.parametrize("with_val", [True, False])
+def test_structured_epochs(gpu, name, loss, with_val):
+    native = native_mod()
+    rows = structured_cases()[name]
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1 if len(col) else 1
+    n = len(rows)
+    rng = np.random.default_rng(len(col) + loss)
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=loss, lr=np.float32(0.05),
+             val=rng.normal(size=len(col)).astype(np.float32) if with_val else None,
+             y=(np.sign(rng.normal(size=n)) if loss == 0 else rng.normal(size=n)).astype(np.float32))
+    lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
+    w0 = (0.1 * rng.normal(size=d)).astype(np.float32)
+    check_sgd(native, gpu, g, lv, w0=w0)
+
+
+SCALED = {
+    1: dict(),                                  # the full 10k x 1k workload
+    2: dict(n=60_000, d=6_000),
+    3: dict(n=30_000, d=30_000),
+    4: dict(n=30_000, d=12_000),
+}
+
+
+@pytest.mark.parametrize("cfg", sorted(SCALED))
+@pytest.mark.parametrize("method", METHODS)
+def test_config_schedules(gpu, cfg, method):
+    g = datagen.generate(cfg, **SCALED[cfg])
+    check_schedule(native_mod(), gpu, g["row_ptr"], g["col"], g["d"], method)
+
+
+@pytest.mark.parametrize("cfg", sorted(SCALED))
+def test_config_epochs(gpu, cfg):
+    native = native_mod()
+    g = datagen.generate(cfg, **SCALED[cfg])
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    check_sgd(native, gpu, g, lv)
+
+
+@pytest.mark.parametrize("cfg", [1, 4])
+def test_epoch_with_oracle_schedule(gpu, cfg):
+    """The apply kernel alone, fed the oracle's grouping."""
+    native = native_mod()
+    g = datagen.generate(cfg, **SCALED[cfg])
+    level, perm, level_ptr, L = oracle.schedule(g["row_ptr"], g["col"], g["d"])
+    lv = native.Levels.from_host(level, perm, level_ptr, gpu)
+    check_sgd(native, gpu, g, lv)
+
+
+def test_mf_scaled(gpu):
+    native = native_mod()
+    g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    check_mf(native, gpu, g, lv)
+
+
+def test_transpose_and_prev_writer(gpu):
+    import torch
+
+    native = native_mod()
+    for cfg in (1, 3):
+        g = datagen.generate(cfg, **SCALED[cfg])
+        csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None, gpu)
+        col_ptr = torch.empty(g["d"] + 1, dtype=torch.int64, device=gpu)
+        csc_row = torch.empty(g["nnz"], dtype=torch.int32, device=gpu)
+        native.pdb_transpose(csr, g["n"], g["d"], col_ptr, csc_row)
+        ref_ptr, ref_row = oracle.transpose(g["row_ptr"], g["col"], g["d"])
+        assert np.array_equal(col_ptr.cpu().numpy(), ref_ptr)
+        assert np.array_equal(csc_row.cpu().numpy(), ref_row)
+        prev_row = torch.empty(g["nnz"], dtype=torch.int32, device=gpu)
+        prev_nz = torch.empty(g["nnz"], dtype=torch.int32, device=gpu)
+        native.pdb_prev_writer(csr, g["n"], g["d"], prev_row, prev_nz)
+        ref_prev = oracle.prev_writer(g["row_ptr"], g["col"], g["d"])
+        pr, pn = prev_row.cpu().numpy(), prev_nz.cpu().numpy()
+        assert np.array_equal(pr, ref_prev)
+        has = pn >= 0
+        assert np.array_equal(has, ref_prev >= 0)
+        # prev_nz points at the same feature in the previous writer's row
+        assert np.array_equal(g["col"][pn[has]], g["col"][has])
+        rows = np.searchsorted(g["row_ptr"], pn[has], side="right") - 1
+        assert np.array_equal(rows, ref_prev[has])
+
+
+def test_deterministic_repeat(gpu):
+    native = native_mod()
+    g = datagen.generate(2, **SCALED[2])
+    lv1, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 2)
+    from pdbtest import gpu_sgd
+    a = gpu_sgd(native, gpu, g, lv1)
+    b = gpu_sgd(native, gpu, g, lv1)
+    assert np.array_equal(a.view(np.int32), b.view(np.int32))
+
+
+def test_bad_csr_and_arguments(gpu):
+    import torch
+
+    native = native_mod()
+    ok_rows = [{0, 2}, {1}, {2, 3}]
+    row_ptr, col = csr_from_rows(ok_rows)
+    assert native.pdb_validate_csr(native.Csr.from_numpy(row_ptr, col, None, gpu), 3, 4) == 0
+    bad = [
+        (row_ptr, np.array([0, 2, 1, 2, 5], np.int32), 4),     # column out of range
+        (row_ptr, np.array([2, 0, 1, 2, 3], np.int32), 4),     # unsorted in a row
+        (row_ptr, np.array([0, 0, 1, 2, 3], np.int32), 4),     # duplicate in a row
+        (np.array([0, 3, 2, 5], np.int64), col, 4),            # row_ptr not monotone
+        (np.array([0, 2, 3, 4], np.int64), col, 4),            # row_ptr[n] != nnz
+        (np.array([1, 2, 3, 5], np.int64), col, 4),            # row_ptr[0] != 0
+        (row_ptr, np.array([0, 2, -1, 2, 3], np.int32), 4),    # negative column
+    ]
+    for rp, c, d in bad:
+        assert native.pdb_validate_csr(native.Csr.from_numpy(rp, c, None, gpu), 3, d) == \
+            native.PDB_ERR_BAD_CSR
+    csr = native.Csr.from_numpy(row_ptr, col, None, gpu)
+    lv = native.Levels(3, len(col), gpu)
+    small = torch.empty(16, dtype=torch.uint8, device=gpu)
+    with pytest.raises(native.PdbError) as e:
+        native.pdb_schedule(csr, None, 3, 4, lv, ws=small)
+    assert e.value.code == native.PDB_ERR_WORKSPACE
+    with pytest.raises(native.PdbError) as e:
+        native.pdb_schedule(csr, None, 3, 4, lv, method=7)
+    assert e.value.code == native.PDB_ERR_INVALID_ARG
+    native.pdb_schedule(csr, None, 3, 4, lv)
+    w = torch.zeros(4, dtype=torch.float32, device=gpu)
+    y = torch.ones(3, dtype=torch.float32, device=gpu)
+    with pytest.raises(native.PdbError) as e:
+        native.pdb_sgd_epoch(csr, y, 3, 4, w, 0.1, 5, lv)
+    assert e.value.code == native.PDB_ERR_INVALID_ARG
+    with pytest.raises(native.PdbError) as e:
+        U = torch.zeros(4 * 16, device=gpu)
+        native.pdb_mf_epoch(torch.zeros(3, dtype=torch.int32, device=gpu),
+                            torch.zeros(3, dtype=torch.int32, device=gpu), y, 3, U, 4, U, 4, 16,
+                            0.1, 0.0, lv)
+    assert e.value.code == native.PDB_ERR_INVALID_ARG
