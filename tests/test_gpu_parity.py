@@ -66,8 +66,14 @@ def test_structured_epochs(gpu, name, loss, with_val):
     d = int(col.max()) + 1 if len(col) else 1
     n = len(rows)
     rng = np.random.default_rng(len(col) + loss)
-    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=loss, lr=np.float32(0.05),
-             val=rng.normal(size=len(col)).astype(np.float32) if with_val else None,
+    val = rng.normal(size=len(col)).astype(np.float32) if with_val else None
+    # a step size that keeps the iteration contractive (lr * |x|^2 < 1/2):
+    # diverging weights would make every summation order disagree
+    sq = np.bincount(np.repeat(np.arange(n), np.diff(row_ptr)),
+                     weights=(val.astype(np.float64) ** 2 if with_val else np.ones(len(col))),
+                     minlength=n)
+    lr = np.float32(min(0.05, 0.5 / max(sq.max(), 1.0)))
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=loss, lr=lr, val=val,
              y=(np.sign(rng.normal(size=n)) if loss == 0 else rng.normal(size=n)).astype(np.float32))
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     w0 = (0.1 * rng.normal(size=d)).astype(np.float32)
