@@ -142,7 +142,7 @@ class Csr:
 class Levels:
     """Device output of pdb_schedule."""
 
-    def __init__(self, n: int, nnz: int, device, with_prev_nz: bool = False):
+    def __init__(self, n: int, nnz: int, device, with_prev_nz: bool = True):
         self.level = torch.empty(max(n, 0), dtype=torch.int32, device=device)
         self.perm = torch.empty(max(n, 0), dtype=torch.int32, device=device)
         self.level_ptr = torch.empty(n + 1, dtype=torch.int64, device=device)
@@ -158,7 +158,7 @@ class Levels:
         import numpy as np
 
         n = len(level)
-        lv = cls(n, 0, device)
+        lv = cls(n, 0, device, with_prev_nz=False)
         lv.level.copy_(torch.from_numpy(np.asarray(level, np.int32)))
         lv.perm.copy_(torch.from_numpy(np.asarray(perm, np.int32)))
         lv.level_ptr = torch.from_numpy(np.asarray(level_ptr, np.int64)).to(device)

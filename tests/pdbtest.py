@@ -14,7 +14,7 @@ def csr_from_rows(rows):
     return row_ptr, col
 
 
-def gpu_schedule(native, dev, row_ptr, col, d, method, with_prev=False):
+def gpu_schedule(native, dev, row_ptr, col, d, method, with_prev=True):
     import torch
 
     csr = native.Csr.from_numpy(row_ptr, col, None, dev)
@@ -35,7 +35,20 @@ def check_schedule(native, dev, row_ptr, col, d, method):
     assert np.array_equal(lv.level_ptr.cpu().numpy()[:L + 1], level_ptr)
     widths = np.diff(level_ptr)
     assert lv.max_width_host == (widths.max() if L else 0)
+    if lv.prev_nz is not None:
+        check_prev_nz(row_ptr, col, d, lv.prev_nz.cpu().numpy())
     return lv, info
+
+
+def check_prev_nz(row_ptr, col, d, pn):
+    """pn[p] is the entry, on the same feature, of the latest earlier example
+    touching it (columns are unique in a row, so feature + row fix it)."""
+    prev = oracle.prev_writer(row_ptr, col, d)
+    has = prev >= 0
+    assert np.array_equal(pn >= 0, has)
+    assert np.array_equal(col[pn[has]], col[has])
+    rows = np.searchsorted(row_ptr, pn[has], side="right") - 1
+    assert np.array_equal(rows, prev[has])
 
 
 def gpu_sgd(native, dev, g, lv, w0=None):

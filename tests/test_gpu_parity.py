@@ -197,3 +197,49 @@ def test_bad_csr_and_arguments(gpu):
                             torch.zeros(3, dtype=torch.int32, device=gpu), y, 3, U, 4, U, 4, 16,
                             0.1, 0.0, lv)
     assert e.value.code == native.PDB_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("hot", ["0", "5", "64", None])
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_width1_pipeline_hot_and_cold(gpu, cfg, hot, monkeypatch):
+    """Runs of width-1 levels through the staged pipeline, with the LDS weight
+    cache shrunk so that cold features (ring, prefetch, forwarding) appear."""
+    if hot is not None:
+        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
+    native = native_mod()
+    g = datagen.generate(cfg, **SCALED[cfg])
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    assert lv.prev_nz is not None
+    check_sgd(native, gpu, g, lv)
+
+
+def test_plain_path_matches_pipeline(gpu, monkeypatch):
+    native = native_mod()
+    g = datagen.generate(3, **SCALED[3])
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    from pdbtest import gpu_sgd
+    a = gpu_sgd(native, gpu, g, lv)
+    monkeypatch.setenv("PDB_CHAIN", "0")
+    b = gpu_sgd(native, gpu, g, lv)
+    assert np.array_equal(a.view(np.int32), b.view(np.int32))
+
+
+@pytest.mark.parametrize("hot", ["0", "40", None])
+@pytest.mark.parametrize("with_val", [True, False])
+def test_width1_pipeline_long_rows(gpu, hot, with_val, monkeypatch):
+    """A chain (feature 0 everywhere) mixing 50- and 70-entry examples: the
+    pipeline stops at each example over 64 entries and resumes after it."""
+    if hot is not None:
+        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
+    native = native_mod()
+    rows = [{0} | set(range(1 + i % 11, 1 + i % 11 + (69 if i % 5 == 3 else 49)))
+            for i in range(400)]
+    row_ptr, col = csr_from_rows(rows)
+    n, d = len(rows), int(col.max()) + 1
+    rng = np.random.default_rng(9)
+    val = (0.3 * rng.normal(size=len(col))).astype(np.float32) if with_val else None
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=0, lr=np.float32(0.01), val=val,
+             y=np.sign(rng.normal(size=n)).astype(np.float32))
+    lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert lv.L_host == n
+    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
