@@ -23,7 +23,7 @@
  * -ffp-contract=off).  Two summation orders exist for the dot product:
  *   natural: z = fmaf(w[c_k], x_k, z) for k = 0..m-1;
  *   matched: 64 partial sums, entry k goes to partial k mod 64, then a
- *            butterfly: for off = 32,16,8,4,2,1 every partial l becomes
+ *            butterfly: for off = 1,2,4,8,16,32 every partial l becomes
  *            p[l] + p[l xor off]; z is the common final value.
  * The exponential is the library expf in natural mode and, in matched mode,
  * orc_exp below (Cody-Waite range reduction and the degree-7 Taylor
@@ -188,7 +188,7 @@ static float dot_natural(const float *w, const int32_t *c, const float *v, int64
 
 static float butterfly64(float *acc, int width) {
     float nxt[64];
-    for (int off = width / 2; off >= 1; off /= 2) {
+    for (int off = 1; off < width; off *= 2) {
         for (int l = 0; l < width; ++l) nxt[l] = acc[l] + acc[l ^ off];
         memcpy(acc, nxt, (size_t)width * sizeof(float));
     }

@@ -243,3 +243,19 @@ def test_width1_pipeline_long_rows(gpu, hot, with_val, monkeypatch):
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     assert lv.L_host == n
     check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
+
+
+def test_summation_order_adversarial(gpu):
+    """A row whose dot product depends on the pairing order of the butterfly."""
+    import sys, os
+    sys.path.insert(0, os.path.dirname(__file__))
+    from test_oracle_apply import adversarial_order_row
+    native = native_mod()
+    row_ptr, col, x, w0 = adversarial_order_row()
+    g = dict(row_ptr=row_ptr, col=col, n=1, d=65, loss=1, lr=np.float32(1.0), val=x,
+             y=np.zeros(1, np.float32))
+    lv, _ = check_schedule(native, gpu, row_ptr, col, 65, 0)
+    from pdbtest import gpu_sgd
+    got = gpu_sgd(native, gpu, g, lv, w0=w0)
+    assert got[64] == -1.0
+    check_sgd(native, gpu, g, lv, w0=w0, tol=float("inf"))
