@@ -44,11 +44,11 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 // e^r from its Taylor series through r^7 (Horner), times 2^k built from the
 // exponent field (two factors near the ends of the range).
 __device__ __forceinline__ float dev_exp(float x) {
-    if (!(x == x)) return x;
-    if (x > 89.0f) return __builtin_huge_valf();
-    if (x < -104.0f) return 0.0f;
-    const float kf = __builtin_rintf(x * 0x1.715476p+0f);
-    float r = __builtin_fmaf(-kf, 0x1.62e430p-1f, x);
+    // branch-free: the input is clamped for the arithmetic and the three
+    // out-of-range answers (NaN, +inf, 0) are selected at the end
+    const float xc = __builtin_fminf(__builtin_fmaxf(x, -104.0f), 89.0f);
+    const float kf = __builtin_rintf(xc * 0x1.715476p+0f);
+    float r = __builtin_fmaf(-kf, 0x1.62e430p-1f, xc);
     r = __builtin_fmaf(-kf, -0x1.05c610p-29f, r);
     float q = 0x1.a01a02p-13f;                  // 1/5040
     q = __builtin_fmaf(q, r, 0x1.6c16c2p-10f);  // 1/720
@@ -58,16 +58,22 @@ __device__ __forceinline__ float dev_exp(float x) {
     q = __builtin_fmaf(q, r, 0.5f);
     q = __builtin_fmaf(q, r, 1.0f);
     q = __builtin_fmaf(q, r, 1.0f);
+    // 2^k as (2^k1) * (2^k2): k1 = k, k2 = 0 inside the normal range; near
+    // the ends k1 = 127, k2 = k - 127 or k1 = k + 126, k2 = -126, so that
+    // q * 2^k1 is exact and the second product rounds once
     const int k = (int)kf;
-    if (k > 127) return (q * __int_as_float(254 << 23)) * __int_as_float(k << 23);
-    if (k < -126) return (q * __int_as_float((k + 253) << 23)) * __int_as_float(1 << 23);
-    return q * __int_as_float((k + 127) << 23);
+    const int k1 = k > 127 ? 127 : (k < -126 ? k + 126 : k);
+    const int k2 = k - k1;
+    const float e = (q * __int_as_float((k1 + 127) << 23)) * __int_as_float((k2 + 127) << 23);
+    const float big = x > 89.0f ? __builtin_huge_valf() : e;
+    const float res = x < -104.0f ? 0.0f : big;
+    return (x == x) ? res : x;
 }
 
 // v + v[partner] with the partner chosen by a DPP lane pattern
 template <int CTRL>
 __device__ __forceinline__ float dpp_add(float v) {
-    return v + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 
 __device__ __forceinline__ float lane_value(float v, int l) {
@@ -201,265 +207,346 @@ struct MfOp {
 // ---------------------------------------------------------------------------
 // width-1 chain pipeline
 
-constexpr int kD = 8;     // examples of look-ahead for cold prefetch; ring depth
-constexpr int kRB = 32;   // staged examples (power of two)
-constexpr int kPB = 8;    // examples per producer batch
+constexpr int kD = 8;          // window of fresh values (ring) and cold-prefetch distance
+constexpr int kRB = 32;        // staged examples (power of two, > 2 kD)
+constexpr int kPB = 8;         // examples per producer batch
 constexpr int kChainMin = 32;  // shorter runs take the plain path
+// buffer offset past the end of any weight vector: a load there returns 0
+// and a store is dropped (buffer range checking), so lanes with nothing to
+// load or store still issue the instruction
+constexpr unsigned kOOR = 0x80000000u;
+enum : unsigned { kSrcLds = 0, kSrcFwd = 1, kSrcGlobal = 2 };
 
-struct ChainLds {
-    float *wcache;  // [hot]
-    float *ring;    // [kD][64]
-    int *st_col;    // [kRB][64]
-    float *st_val;  // [kRB][64]
-    int *st_pn;     // [kRB][64]
-    int *mt_b;      // [kRB] first entry (CSR index) of the staged example
-    int *mt_m;      // [kRB] its number of entries
-    float *mt_y;    // [kRB] its label
-    int *seq;       // [kRB] position staged in the slot (-1 none)
-    int *ctl;       // [0] examples the consumer no longer needs staged, [1] stop
+typedef __attribute__((address_space(3))) float lds_f32;
+__device__ __forceinline__ unsigned lds_addr(const float *p) {
+    return (unsigned)(uintptr_t)(const lds_f32 *)p;
+}
+__device__ __forceinline__ float lds_read(unsigned a) { return *(const lds_f32 *)(uintptr_t)a; }
+__device__ __forceinline__ void lds_write(unsigned a, float v) { *(lds_f32 *)(uintptr_t)a = v; }
+
+// Fixed part of the pipeline's LDS; the cached weights live in dynamic LDS.
+struct ChainShared {
+    // per staged example (slot t mod kRB) and lane:
+    //   a = {x bits, read address (or the lane to take a forwarded value from,
+    //        times 4), source kind, LDS write address}
+    //   b = {buffer offset of the global write (or kOOR), of the prefetch (or kOOR)}
+    uint4 st_a[kRB * 64];
+    uint2 st_b[kRB * 64];
+    float mt_t[kRB];     // target: [y > 0] (logistic) or y (least squares)
+    int mt_m[kRB];       // number of entries
+    int seq[kRB];        // position staged in the slot (-1 none)
+    int ctl[4];          // [0] consumer no longer needs positions < ctl[0]; [1] stop
+    float ring[kD * 64]; // new weights of the example at position t mod kD, by lane
+    float lsink[64];     // LDS write target of lanes without a hot entry
+    float zero[4];       // read source of lanes without an entry
 };
 
-constexpr size_t kChainFixedLds =
-    sizeof(float) * kD * 64 + (sizeof(int) * 2 + sizeof(float)) * kRB * 64 +
-    (sizeof(int) * 3 + sizeof(float)) * kRB + sizeof(int) * 4;
+extern __shared__ __align__(16) float g_wcache[];
 
-__device__ __forceinline__ ChainLds chain_lds(unsigned char *base, int hot) {
-    ChainLds S;
-    S.ring = reinterpret_cast<float *>(base);
-    S.st_col = reinterpret_cast<int *>(S.ring + kD * 64);
-    S.st_val = reinterpret_cast<float *>(S.st_col + kRB * 64);
-    S.st_pn = reinterpret_cast<int *>(S.st_val + kRB * 64);
-    S.mt_b = S.st_pn + kRB * 64;
-    S.mt_m = S.mt_b + kRB;
-    S.mt_y = reinterpret_cast<float *>(S.mt_m + kRB);
-    S.seq = reinterpret_cast<int *>(S.mt_y + kRB);
-    S.ctl = S.seq + kRB;
-    S.wcache = reinterpret_cast<float *>(S.ctl + 4);
-    (void)hot;
-    return S;
+__device__ __forceinline__ int lds_load(const int *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
-
+__device__ __forceinline__ void lds_store(int *p, int v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
 __device__ __forceinline__ void compiler_fence() { __asm__ __volatile__("" ::: "memory"); }
 
-// Producer wave pid (0..2): stages examples perm[e_beg + t] for t in its
-// batches, in order, never more than kRB ahead of the consumer.
+template <int LOSS>
+__device__ __forceinline__ float target_of(float y) {
+    return LOSS == PDB_LOGISTIC ? (y > 0.0f ? 1.0f : 0.0f) : y;
+}
+
+template <int LOSS>
+__device__ __forceinline__ float sgd_scale_t(float z, float tgt, float lr) {
+    float g;
+    if (LOSS == PDB_LOGISTIC) {
+        const float e = dev_exp(-z);
+        g = 1.0f / (1.0f + e) - tgt;
+    } else {
+        g = z - tgt;
+    }
+    return lr * g;
+}
+
+// Producer wave pid (0..2): stages examples t of the run (batches of kPB, in
+// turn), never more than kRB ahead of the consumer.  For every entry it finds
+// the previous writer among the kD examples before it (its CSR index lies in
+// one of their entry ranges) and picks where the consumer will read the
+// current weight: forwarded from the previous example's lane, the LDS cache
+// (hot feature), the ring (cold feature written within kD examples), or the
+// prefetched global value.
 template <int LOSS, bool VAL>
 __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_beg, int64_t len,
-                               const ChainLds &S) {
+                               int64_t dense_r0, int hot, ChainShared &S) {
     const int lane = lane_id();
-    volatile int *ctl = S.ctl;
-    volatile int *seq = S.seq;
+    const unsigned wc_base = lds_addr(&g_wcache[0]);
+    const unsigned zero_a = lds_addr(&S.zero[0]);
+    const unsigned lsink_a = lds_addr(&S.lsink[lane]);
+    const unsigned ring_a = lds_addr(&S.ring[0]);
     for (int64_t t0 = (int64_t)pid * kPB; t0 < len; t0 += 3 * kPB) {
-        while (t0 + kPB - 1 >= (int64_t)ctl[0] + kRB) {
-            if (ctl[1]) return;
+        while (t0 + kPB - 1 >= (int64_t)lds_load(&S.ctl[0]) + kRB) {
+            if (lds_load(&S.ctl[1])) return;
             __builtin_amdgcn_s_sleep(1);
         }
-        if (ctl[1]) return;
-        int b = 0, e = 0;
-        float yv = 0.0f;
-        if (lane < kPB && t0 + lane < len) {
-            const int64_t r = op.perm[e_beg + t0 + lane];
+        if (lds_load(&S.ctl[1])) return;
+        // lane i: position t0 - kD + i (the window before the batch, then the batch)
+        int b = 0, m = 0;
+        float tg = 0.0f;
+        const int64_t q = t0 - kD + lane;
+        if (lane < kD + kPB && q >= 0 && q < len) {
+            const int64_t r = dense_r0 >= 0 ? dense_r0 + q : op.perm[e_beg + q];
             b = (int)op.row_ptr[r];
-            e = (int)op.row_ptr[r + 1];
-            yv = op.y[r];
+            m = (int)op.row_ptr[r + 1] - b;
+            tg = target_of<LOSS>(op.y[r]);
         }
-        int c[kPB], p[kPB];
-        float x[kPB];
+        uint4 A[kPB];
+        uint2 B[kPB];
 #pragma unroll
         for (int i = 0; i < kPB; ++i) {
-            const int bi = __builtin_amdgcn_readlane(b, i);
-            const int mi = __builtin_amdgcn_readlane(e, i) - bi;
-            c[i] = 0;
-            p[i] = -1;
-            x[i] = 1.0f;
-            if (lane < mi && lane < kWave) {
-                c[i] = op.col[bi + lane];
-                p[i] = op.prev_nz[bi + lane];
-                if (VAL) x[i] = op.val[bi + lane];
+            const int bi = __builtin_amdgcn_readlane(b, kD + i);
+            const int mi = __builtin_amdgcn_readlane(m, kD + i);
+            const bool live = lane < mi;
+            int c = 0, p = -1;
+            float x = 0.0f;
+            if (live) {
+                c = op.col[bi + lane];
+                p = op.prev_nz[bi + lane];
+                x = VAL ? op.val[bi + lane] : 1.0f;
             }
+            int rel = 0, off = 0;
+#pragma unroll
+            for (int j = 1; j <= kD; ++j) {
+                const int bj = __builtin_amdgcn_readlane(b, kD + i - j);
+                const int mj = __builtin_amdgcn_readlane(m, kD + i - j);
+                const unsigned o = (unsigned)(p - bj);
+                if (o < (unsigned)mj) {
+                    rel = j;
+                    off = (int)o;
+                }
+            }
+            const bool is_hot = (unsigned)c < (unsigned)hot;
+            unsigned kind = kSrcLds, rd = zero_a;
+            if (live) {
+                if (rel == 1) {
+                    kind = kSrcFwd;
+                    rd = (unsigned)off << 2;
+                } else if (is_hot) {
+                    rd = wc_base + ((unsigned)c << 2);
+                } else if (rel >= 2) {
+                    const unsigned slot = (unsigned)(t0 + i - rel) & (kD - 1);
+                    rd = ring_a + (slot << 8) + ((unsigned)off << 2);
+                } else {
+                    kind = kSrcGlobal;
+                }
+            }
+            const unsigned laddr = (live && is_hot) ? wc_base + ((unsigned)c << 2) : lsink_a;
+            const unsigned goff = (live && !is_hot) ? ((unsigned)c << 2) : kOOR;
+            const unsigned pfoff = (kind == kSrcGlobal) ? ((unsigned)c << 2) : kOOR;
+            A[i] = make_uint4(__float_as_uint(x), rd, kind, laddr);
+            B[i] = make_uint2(goff, pfoff);
         }
 #pragma unroll
         for (int i = 0; i < kPB; ++i) {
             const int slot = (int)((t0 + i) & (kRB - 1));
-            S.st_col[slot * 64 + lane] = c[i];
-            S.st_pn[slot * 64 + lane] = p[i];
-            if (VAL) S.st_val[slot * 64 + lane] = x[i];
+            S.st_a[slot * 64 + lane] = A[i];
+            S.st_b[slot * 64 + lane] = B[i];
         }
-        if (lane < kPB) {
-            const int slot = (int)((t0 + lane) & (kRB - 1));
-            S.mt_b[slot] = b;
-            S.mt_m[slot] = e - b;
-            S.mt_y[slot] = yv;
+        if (lane >= kD && lane < kD + kPB) {
+            const int slot = (int)((q) & (kRB - 1));
+            S.mt_t[slot] = tg;
+            S.mt_m[slot] = m;
         }
         compiler_fence();  // LDS executes one wave's operations in order
-        if (lane < kPB && t0 + lane < len) seq[(t0 + lane) & (kRB - 1)] = (int)(t0 + lane);
+        if (lane < kPB && t0 + lane < len)
+            lds_store(&S.seq[(t0 + lane) & (kRB - 1)], (int)(t0 + lane));
         compiler_fence();
     }
 }
 
-struct Staged {
-    int c, pn, b, m;
-    float x, y;
-};
-
-// Waits until examples lo .. hi-1 (hi - lo <= kRB) are staged.
-__device__ __forceinline__ void wait_staged(const ChainLds &S, int64_t lo, int64_t hi) {
-    volatile int *seq = S.seq;
+// Waits until positions lo .. hi-1 (hi - lo <= kRB) are staged; returns the
+// first of them holding an example with more than 64 entries, or INT64_MAX.
+__device__ __forceinline__ int64_t wait_staged(ChainShared &S, int64_t lo, int64_t hi,
+                                               long long *waited) {
     const int64_t t = lo + lane_id();
+    const int slot = (int)(t & (kRB - 1));
+    long long c0 = 0;
+    bool first = true;
     for (;;) {
-        const bool ok = t >= hi || seq[t & (kRB - 1)] == (int)t;
+        const bool ok = t >= hi || lds_load(&S.seq[slot]) == (int)t;
         if (__ballot(!ok) == 0ull) break;
+        if (first) c0 = (long long)__builtin_readcyclecounter();
+        first = false;
         __builtin_amdgcn_s_sleep(0);
     }
+    if (!first) *waited += (long long)__builtin_readcyclecounter() - c0;
     compiler_fence();
+    const unsigned long long longrow = __ballot(t < hi && S.mt_m[slot] > kWave);
+    return longrow ? lo + __ffsll(longrow) - 1 : INT64_MAX;
 }
 
-template <bool VAL>
-__device__ __forceinline__ Staged read_staged(const ChainLds &S, int64_t t) {
+struct Stg {
+    uint4 a;  // x, read address, kind, LDS write address
+    uint2 b;  // global write offset, prefetch offset
+    float t;  // target
+};
+
+__device__ __forceinline__ Stg read_stg(const ChainShared &S, int64_t t) {
     const int slot = (int)(t & (kRB - 1)), lane = lane_id();
-    Staged r;
-    r.c = S.st_col[slot * 64 + lane];
-    r.pn = S.st_pn[slot * 64 + lane];
-    r.x = VAL ? S.st_val[slot * 64 + lane] : 1.0f;
-    r.b = __builtin_amdgcn_readfirstlane(S.mt_b[slot]);
-    r.m = __builtin_amdgcn_readfirstlane(S.mt_m[slot]);
-    r.y = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(S.mt_y[slot])));
+    Stg r;
+    r.a = S.st_a[slot * 64 + lane];
+    r.b = S.st_b[slot * 64 + lane];
+    r.t = S.mt_t[slot];
     return r;
+}
+
+struct ChainState {
+    Stg cur, nxt;                 // examples t and t+1
+    float cur_v, cur_fw, cur_fx;  // example t's weight, or the forwarded (w_old, x) pair
+    bool cur_fwd;
+    float s_prev;                 // step of example t-1
+    float gv[kD];                 // prefetched cold values, example at t mod kD
+    unsigned pf[kD];              // prefetch offsets of the next examples
+};
+
+// One example, position t, slot SL = t mod kD.  Every memory operation is
+// issued unconditionally, so the count of outstanding loads and stores is
+// the same on every path and the waits stay exact.
+template <int SL, int LOSS, bool VAL>
+__device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL> &op,
+                                           ChainShared &S, int64_t t,
+                                           __amdgpu_buffer_rsrc_t wbuf) {
+    const int lane = lane_id();
+    const float x = __uint_as_float(st.cur.a.x);
+    // (a) this example's weights: forwarded ones get the previous step now
+    const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
+    const float acc = __builtin_fmaf(w_old, x, 0.0f);
+    // (b) example t+1: read its weights (those that example t writes are forwarded)
+    const unsigned rd = st.nxt.a.y;
+    const float v1 = lds_read(rd);
+    const float fw1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(w_old)));
+    const float fx1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x)));
+    const bool fwd1 = st.nxt.a.z == kSrcFwd;
+    const float n_v = (st.nxt.a.z == kSrcGlobal) ? st.gv[(SL + 1) % kD] : v1;
+    const Stg nxt2 = read_stg(S, t + 2);
+    // (c) the step of example t
+    const float s = sgd_scale_t<LOSS>(butterfly64(acc), st.cur.t, op.lr);
+    const float w_new = __builtin_fmaf(-s, x, w_old);
+    lds_write(st.cur.a.w, w_new);
+    S.ring[SL * 64 + lane] = w_new;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_new), wbuf, st.cur.b.x, 0, 0);
+    // (d) prefetch cold values of example t+kD (writes up to t are issued)
+    st.gv[SL] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
+    // (e) rotate
+    st.s_prev = s;
+    st.cur = st.nxt;
+    st.cur_v = n_v;
+    st.cur_fw = fw1;
+    st.cur_fx = fx1;
+    st.cur_fwd = fwd1;
+    st.nxt = nxt2;
+}
+
+__device__ __forceinline__ void chain_prefetch_offsets(ChainState &st, const ChainShared &S,
+                                                       int64_t q0, int64_t stop) {
+#pragma unroll
+    for (int j = 0; j < kD; ++j) {
+        const int64_t q = q0 + j;
+        const unsigned o = S.st_b[(int)(q & (kRB - 1)) * 64 + lane_id()].y;
+        st.pf[j] = q < stop ? o : kOOR;
+    }
 }
 
 // Consumer: runs examples t = 0.. of the run in order.  Returns the number
 // processed: len, or the position of the first example with more than 64
 // entries (the caller runs that one on the plain path).
 template <int LOSS, bool VAL>
-__device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int hot,
-                                  const ChainLds &S) {
+__device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64_t d,
+                                  ChainShared &S, Ctrl *ctrl) {
     const int lane = lane_id();
-    volatile int *ctl = S.ctl;
-    float *__restrict__ w = op.w;
-    int64_t stop = len;
-    int wb[kD], wm[kD];   // window: first entry and count of the example at t mod kD
-    float gv[kD];         // cold values prefetched for the example at t mod kD
+    const long long cyc0 = (long long)__builtin_readcyclecounter();
+    long long waited = 0;
+    const __amdgpu_buffer_rsrc_t wbuf =
+        __builtin_amdgcn_make_buffer_rsrc(op.w, 0, (int)(d * 4), 0x00020000);
+    ChainState st;
+    int64_t stop = std::min(len, wait_staged(S, 0, std::min<int64_t>(kD, len), &waited));
+    chain_prefetch_offsets(st, S, 0, stop);
 #pragma unroll
-    for (int j = 0; j < kD; ++j) {
-        wb[j] = 0;
-        wm[j] = 0;
-        gv[j] = 0.0f;
-    }
-    // prefetch cold values for the first kD examples (nothing written yet)
-    wait_staged(S, 0, std::min<int64_t>(kD, stop));
-#pragma unroll
-    for (int j = 0; j < kD; ++j) {
-        if (j < stop) {
-            const Staged r = read_staged<VAL>(S, j);
-            if (r.m > kWave) stop = j;
-            else if (lane < r.m && r.c >= hot) gv[j] = w[r.c];
-        }
-    }
-    // example 0: no earlier example of the run wrote anything
-    Staged cur = {0, -1, 0, 0, 1.0f, 0.0f};
-    float cur_v = 0.0f, cur_fw = 0.0f, cur_fx = 0.0f;
-    bool cur_fwd = false;
-    if (stop > 0) {
-        cur = read_staged<VAL>(S, 0);
-        cur_v = (lane < cur.m) ? (cur.c < hot ? S.wcache[cur.c] : gv[0]) : 0.0f;
-    }
-    Staged nxt = {0, -1, 0, 0, 1.0f, 0.0f};
-    if (stop > 1) nxt = read_staged<VAL>(S, 1);
-    float s_prev = 0.0f;
+    for (int j = 0; j < kD; ++j)
+        st.gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[j], 0, 0));
+    st.cur = read_stg(S, 0);
+    st.nxt = read_stg(S, 1);
+    st.cur_v = (st.cur.a.z == kSrcGlobal) ? st.gv[0] : lds_read(st.cur.a.y);
+    st.cur_fw = st.cur_fx = 0.0f;
+    st.cur_fwd = false;
+    st.s_prev = 0.0f;
 
-    for (int64_t t0 = 0; t0 < stop; t0 += kD) {
-        // examples read in this block: t+2 and t+kD for t in [t0, t0+kD)
-        wait_staged(S, t0 + 2, std::min<int64_t>(t0 + 2 * kD, stop));
-#pragma unroll
-        for (int s = 0; s < kD; ++s) {
-            const int64_t t = t0 + s;
-            if (t < stop) {
-                // (a) this example's weights: forwarded ones get the previous step now
-                const float w_old = cur_fwd ? __builtin_fmaf(-s_prev, cur_fx, cur_fw) : cur_v;
-                const bool live = lane < cur.m;
-                const float acc = live ? __builtin_fmaf(w_old, cur.x, 0.0f) : 0.0f;
-                wb[s] = cur.b;
-                wm[s] = cur.m;
-                // (b) resolve example t+1 against the window t+1-kD .. t
-                float n_v = 0.0f, n_fw = 0.0f, n_fx = 0.0f;
-                bool n_fwd = false;
-                if (t + 1 < stop) {
-                    int src = -1, off = 0;
-#pragma unroll
-                    for (int j = 0; j < kD; ++j) {
-                        const unsigned o = (unsigned)(nxt.pn - wb[j]);
-                        if (nxt.pn >= 0 && o < (unsigned)wm[j]) {
-                            src = j;
-                            off = (int)o;
-                        }
-                    }
-                    n_fwd = (src == s);
-                    const int addr = (n_fwd ? off : lane) << 2;
-                    n_fw = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(w_old)));
-                    n_fx = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(cur.x)));
-                    if (lane < nxt.m && !n_fwd) {
-                        if (nxt.c < hot) n_v = S.wcache[nxt.c];
-                        else if (src >= 0) n_v = S.ring[src * 64 + off];
-                        else n_v = gv[(s + 1) % kD];
-                    }
-                }
-                Staged nxt2 = {0, -1, 0, 0, 1.0f, 0.0f};
-                if (t + 2 < stop) nxt2 = read_staged<VAL>(S, t + 2);
-                // (c) the step of example t
-                const float st = sgd_scale<LOSS>(butterfly64(acc), cur.y, op.lr);
-                const float w_new = __builtin_fmaf(-st, cur.x, w_old);
-                if (live) {
-                    if (cur.c < hot) S.wcache[cur.c] = w_new;
-                    else w[cur.c] = w_new;
-                    S.ring[s * 64 + lane] = w_new;
-                }
-                // (d) prefetch cold values of example t+kD (writes up to t are issued)
-                if (t + kD < stop) {
-                    const Staged r = read_staged<VAL>(S, t + kD);
-                    if (r.m > kWave) {
-                        stop = t + kD;  // producers keep staging until the run ends
-                    } else {
-                        gv[s] = (lane < r.m && r.c >= hot) ? w[r.c] : 0.0f;
-                    }
-                }
-                ctl[0] = (int)(t + 3);
-                // (e) rotate
-                s_prev = st;
-                cur = nxt;
-                cur_v = n_v;
-                cur_fw = n_fw;
-                cur_fx = n_fx;
-                cur_fwd = n_fwd;
-                nxt = nxt2;
-            }
-        }
+    int64_t t0 = 0;
+    for (; t0 < stop; t0 += kD) {
+        // positions read in this block: t+2 and t+kD for t in [t0, t0+kD)
+        stop = std::min(stop, wait_staged(S, t0 + 2, std::min<int64_t>(t0 + 2 * kD, len), &waited));
+        if (t0 + kD > stop) break;
+        chain_prefetch_offsets(st, S, t0 + kD, stop);
+        lds_store(&S.ctl[0], (int)(t0 + 2));
+        chain_step<0>(st, op, S, t0 + 0, wbuf);
+        chain_step<1>(st, op, S, t0 + 1, wbuf);
+        chain_step<2>(st, op, S, t0 + 2, wbuf);
+        chain_step<3>(st, op, S, t0 + 3, wbuf);
+        chain_step<4>(st, op, S, t0 + 4, wbuf);
+        chain_step<5>(st, op, S, t0 + 5, wbuf);
+        chain_step<6>(st, op, S, t0 + 6, wbuf);
+        chain_step<7>(st, op, S, t0 + 7, wbuf);
     }
-    ctl[1] = 1;
+    if (t0 < stop) {  // last, partial block
+        chain_prefetch_offsets(st, S, t0 + kD, stop);
+        if (t0 + 0 < stop) chain_step<0>(st, op, S, t0 + 0, wbuf);
+        if (t0 + 1 < stop) chain_step<1>(st, op, S, t0 + 1, wbuf);
+        if (t0 + 2 < stop) chain_step<2>(st, op, S, t0 + 2, wbuf);
+        if (t0 + 3 < stop) chain_step<3>(st, op, S, t0 + 3, wbuf);
+        if (t0 + 4 < stop) chain_step<4>(st, op, S, t0 + 4, wbuf);
+        if (t0 + 5 < stop) chain_step<5>(st, op, S, t0 + 5, wbuf);
+        if (t0 + 6 < stop) chain_step<6>(st, op, S, t0 + 6, wbuf);
+    }
+    lds_store(&S.ctl[1], 1);
+    if (lane == 0) {
+        atomicAdd((unsigned long long *)&ctrl->stat_cycles,
+                  (unsigned long long)((long long)__builtin_readcyclecounter() - cyc0));
+        atomicAdd((unsigned long long *)&ctrl->stat_wait, (unsigned long long)waited);
+        atomicAdd((unsigned long long *)&ctrl->stat_rows, (unsigned long long)stop);
+        atomicAdd((unsigned long long *)&ctrl->stat_runs, 1ull);
+    }
     return stop;
 }
 
 // Runs perm[e_beg .. e_end) (consecutive width-1 levels) with the whole block.
 template <int LOSS, bool VAL>
 __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_end, int hot,
-                          unsigned char *lds) {
-    const ChainLds S = chain_lds(lds, hot);
-    const int wave = wave_in_block(), lane = lane_id();
+                          int64_t d, Ctrl *ctrl) {
+    __shared__ ChainShared S;
+    __shared__ int64_t s_done;
+    const int wave = wave_in_block();
     int64_t pos = e_beg;
     while (pos < e_end) {
-        for (int i = threadIdx.x; i < hot; i += kBlock) S.wcache[i] = op.w[i];
+        // examples of a width-1 run have increasing indices: the run is a range
+        // of consecutive examples exactly when its ends differ by its length - 1
+        const int64_t r_first = op.perm[pos], r_last = op.perm[e_end - 1];
+        const int64_t dense_r0 = (r_last - r_first == e_end - 1 - pos) ? r_first : -1;
+        for (int i = threadIdx.x; i < hot; i += kBlock) g_wcache[i] = op.w[i];
         for (int i = threadIdx.x; i < kRB; i += kBlock) S.seq[i] = -1;
-        if (threadIdx.x < 4) S.ctl[threadIdx.x] = 0;
+        if (threadIdx.x < 4) {
+            S.ctl[threadIdx.x] = 0;
+            S.zero[threadIdx.x] = 0.0f;
+        }
         __syncthreads();
-        int64_t done = e_end - pos;
-        if (wave == 0) done = chain_consumer(op, e_end - pos, hot, S);
-        else chain_producer(op, wave - 1, pos, e_end - pos, S);
+        if (wave == 0) {
+            const int64_t done = chain_consumer(op, e_end - pos, d, S, ctrl);
+            if (lane_id() == 0) s_done = done;
+        } else {
+            chain_producer(op, wave - 1, pos, e_end - pos, dense_r0, hot, S);
+        }
         __syncthreads();
-        __shared__ int64_t s_done;
-        if (threadIdx.x == 0) s_done = done;
-        for (int i = threadIdx.x; i < hot; i += kBlock) op.w[i] = S.wcache[i];
+        for (int i = threadIdx.x; i < hot; i += kBlock) op.w[i] = g_wcache[i];
         __syncthreads();
-        done = s_done;
-        pos += done;
+        pos += s_done;
         if (pos < e_end) {
             // an example with more than 64 entries: plain path, then resume
             if (wave == 0) op(pos, pos + 1);
@@ -467,7 +554,6 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
             ++pos;
         }
     }
-    (void)lane;
 }
 
 // first level >= l whose width exceeds thin_max (L if none); block-uniform
@@ -491,13 +577,11 @@ __device__ int64_t find_run_end(int64_t l, int64_t L, const int64_t *level_ptr,
     return L;
 }
 
-extern __shared__ __align__(16) unsigned char g_dyn_lds[];
-
 template <class Op>
 __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *level_ptr,
                                                          const int32_t *n_levels,
-                                                         int64_t thin_max, int hot, Ctrl *ctrl,
-                                                         int64_t timeout) {
+                                                         int64_t thin_max, int hot, int64_t d,
+                                                         Ctrl *ctrl, int64_t timeout) {
     constexpr int U = Op::kUnits;
     const int64_t L = *n_levels;
     const int wave = wave_in_block();
@@ -519,7 +603,7 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
                         if (hot >= 0 && end - beg == 1 && l2 >= no_chain_before) {
                             const int64_t l3 = find_run_end(l2, L, level_ptr, 1);
                             if (l3 - l2 >= kChainMin) {
-                                chain_run(op, beg, level_ptr[l3], hot, g_dyn_lds);
+                                chain_run(op, beg, level_ptr[l3], hot, d, ctrl);
                                 l2 = l3;
                                 continue;
                             }
@@ -578,12 +662,12 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
     int hot = -1;
     size_t lds = 0;
     if (Op::kChain && chain_ok) {
-        const int64_t room = (int64_t)max_lds - (int64_t)kChainFixedLds - 1024;
+        const int64_t room = (int64_t)max_lds - (int64_t)sizeof(ChainShared) - 2048;
         int64_t h = std::min<int64_t>(room / 4, d);
         if (hot_cap >= 0) h = std::min<int64_t>(h, hot_cap);
         h = std::max<int64_t>(h, 0);
         hot = (int)h;
-        lds = kChainFixedLds + (size_t)h * 4;
+        lds = (size_t)std::max<int64_t>(h, 1) * 4;
         PDB_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     }
     int grid = 1;
@@ -600,12 +684,14 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
     const int64_t *level_ptr = lv->level_ptr;
     const int32_t *n_levels = lv->n_levels;
     if (grid == 1) {
-        k_levels_apply<Op><<<1, kBlock, lds, s>>>(o, level_ptr, n_levels, thin, hot, ctrl, timeout);
+        k_levels_apply<Op><<<1, kBlock, lds, s>>>(o, level_ptr, n_levels, thin, hot, d, ctrl,
+                                                  timeout);
         PDB_LAUNCHED();
     } else {
         int64_t thin_arg = thin, to = timeout;
         int hot_arg = hot;
-        void *args[] = {&o, &level_ptr, &n_levels, &thin_arg, &hot_arg, &ctrl, &to};
+        int64_t d_arg = d;
+        void *args[] = {&o, &level_ptr, &n_levels, &thin_arg, &hot_arg, &d_arg, &ctrl, &to};
         PDB_HIP(hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBlock), args, lds, s));
     }
     return PDB_OK;

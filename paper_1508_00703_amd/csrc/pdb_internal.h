@@ -59,9 +59,13 @@ struct Ctrl {
     int pad0;
     unsigned long long ticket;  // work ticket for dataflow kernels
     long long max_width;
-    int pad[52];
+    // width-1 pipeline counters (clock cycles of the consumer wave): total,
+    // waiting for staged examples, examples run, runs started
+    long long stat_cycles, stat_wait, stat_rows, stat_runs;
+    int pad[44];
+    float sink[64];  // target of stores from lanes with nothing to store
 };
-static_assert(sizeof(Ctrl) == 256, "Ctrl is one 256-byte line");
+static_assert(sizeof(Ctrl) == 512, "Ctrl is two 256-byte lines");
 
 enum DeviceErr { DERR_NONE = 0, DERR_BARRIER_TIMEOUT = 1, DERR_WAIT_TIMEOUT = 2 };
 
