@@ -39,7 +39,9 @@ enum { ORC_LOGISTIC = 0, ORC_SQUARED = 1 };
 
 /* ------------------------------------------------------------------------ */
 /* exp(x) = 2^k * e^r with k = rint(x log2 e), r = x - k ln 2 (ln 2 split in
- * two floats so r carries the low bits), e^r by its Taylor series to r^7. */
+ * two floats so r carries the low bits), e^r by its Taylor series to r^7,
+ * evaluated by Estrin's scheme: pairs c_j + c_{j+1} r, combined with r^2,
+ * then r^4. */
 float orc_exp(float x) {
     if (x != x) return x;
     if (x > 89.0f) return INFINITY;
@@ -50,15 +52,16 @@ float orc_exp(float x) {
     float k = rintf(x * log2e);
     float r = fmaf(-k, ln2_hi, x);
     r = fmaf(-k, ln2_lo, r);
-    /* 1/7!, 1/6!, ..., 1/2!, 1, 1 rounded to binary32 */
-    float q = 0x1.a01a02p-13f;
-    q = fmaf(q, r, 0x1.6c16c2p-10f);
-    q = fmaf(q, r, 0x1.111112p-7f);
-    q = fmaf(q, r, 0x1.555556p-5f);
-    q = fmaf(q, r, 0x1.555556p-3f);
-    q = fmaf(q, r, 0.5f);
-    q = fmaf(q, r, 1.0f);
-    q = fmaf(q, r, 1.0f);
+    /* c_j = 1/j! rounded to binary32 */
+    const float c0 = 1.0f, c1 = 1.0f, c2 = 0.5f, c3 = 0x1.555556p-3f;
+    const float c4 = 0x1.555556p-5f, c5 = 0x1.111112p-7f, c6 = 0x1.6c16c2p-10f,
+                c7 = 0x1.a01a02p-13f;
+    float r2 = r * r;
+    float r4 = r2 * r2;
+    float p01 = fmaf(c1, r, c0), p23 = fmaf(c3, r, c2);
+    float p45 = fmaf(c5, r, c4), p67 = fmaf(c7, r, c6);
+    float p03 = fmaf(p23, r2, p01), p47 = fmaf(p67, r2, p45);
+    float q = fmaf(p47, r4, p03);
     int ki = (int)k;
     float two_k;
     if (ki > 127) {

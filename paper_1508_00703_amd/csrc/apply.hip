@@ -41,33 +41,28 @@ namespace {
 constexpr int kWavesPerBlock = kBlock / kWave;
 
 // e^x: k = rint(x log2 e), r = x - k ln 2 with ln 2 in two binary32 pieces,
-// e^r from its Taylor series through r^7 (Horner), times 2^k built from the
-// exponent field (two factors near the ends of the range).
+// e^r from its Taylor series through r^7 by Estrin's scheme (pairs
+// c_j + c_{j+1} r, combined with r^2, then r^4), times 2^k by ldexp: exact
+// in the normal range, one rounding into the subnormals, +inf past the top.
 __device__ __forceinline__ float dev_exp(float x) {
-    // branch-free: the input is clamped for the arithmetic and the three
-    // out-of-range answers (NaN, +inf, 0) are selected at the end
+    // branch-free: the arithmetic runs on x clamped to [-104, 89]; past the
+    // ends that gives the same answers (e^-104 rounds to 0, k = 128
+    // overflows), only NaN needs a select
     const float xc = __builtin_fminf(__builtin_fmaxf(x, -104.0f), 89.0f);
     const float kf = __builtin_rintf(xc * 0x1.715476p+0f);
     float r = __builtin_fmaf(-kf, 0x1.62e430p-1f, xc);
     r = __builtin_fmaf(-kf, -0x1.05c610p-29f, r);
-    float q = 0x1.a01a02p-13f;                  // 1/5040
-    q = __builtin_fmaf(q, r, 0x1.6c16c2p-10f);  // 1/720
-    q = __builtin_fmaf(q, r, 0x1.111112p-7f);   // 1/120
-    q = __builtin_fmaf(q, r, 0x1.555556p-5f);   // 1/24
-    q = __builtin_fmaf(q, r, 0x1.555556p-3f);   // 1/6
-    q = __builtin_fmaf(q, r, 0.5f);
-    q = __builtin_fmaf(q, r, 1.0f);
-    q = __builtin_fmaf(q, r, 1.0f);
-    // 2^k as (2^k1) * (2^k2): k1 = k, k2 = 0 inside the normal range; near
-    // the ends k1 = 127, k2 = k - 127 or k1 = k + 126, k2 = -126, so that
-    // q * 2^k1 is exact and the second product rounds once
-    const int k = (int)kf;
-    const int k1 = k > 127 ? 127 : (k < -126 ? k + 126 : k);
-    const int k2 = k - k1;
-    const float e = (q * __int_as_float((k1 + 127) << 23)) * __int_as_float((k2 + 127) << 23);
-    const float big = x > 89.0f ? __builtin_huge_valf() : e;
-    const float res = x < -104.0f ? 0.0f : big;
-    return (x == x) ? res : x;
+    const float r2 = r * r;
+    const float r4 = r2 * r2;
+    const float p01 = __builtin_fmaf(1.0f, r, 1.0f);
+    const float p23 = __builtin_fmaf(0x1.555556p-3f, r, 0.5f);            // 1/6, 1/2
+    const float p45 = __builtin_fmaf(0x1.111112p-7f, r, 0x1.555556p-5f);  // 1/120, 1/24
+    const float p67 = __builtin_fmaf(0x1.a01a02p-13f, r, 0x1.6c16c2p-10f);  // 1/5040, 1/720
+    const float p03 = __builtin_fmaf(p23, r2, p01);
+    const float p47 = __builtin_fmaf(p67, r2, p45);
+    const float q = __builtin_fmaf(p47, r4, p03);
+    const float e = __builtin_amdgcn_ldexpf(q, (int)kf);
+    return (x == x) ? e : x;
 }
 
 // v + v[partner] with the partner chosen by a DPP lane pattern
@@ -76,24 +71,21 @@ __device__ __forceinline__ float dpp_add(float v) {
     return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 
-__device__ __forceinline__ float lane_value(float v, int l) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-
-// Butterfly p_l <- p_l + p_{l xor o} for o = 1, 2, 4, 8, 16, 32; returns the
-// common result.  o = 1, 2: quad permutations.  o = 4: mirror within each
-// group of 8 lanes -- once the quads hold equal values the mirrored partner
-// holds the same value as lane l xor 4.  o = 8: mirror within each row of 16,
-// likewise.  o = 16, 32: the four row values r0..r3 combine as
-// (r0 + r1) + (r2 + r3).  Bitwise the same as the xor butterfly.
+// Butterfly p_l <- p_l + p_{l xor o} for o = 1, 2, 4, 8, 16, 32; every lane
+// ends with the common result.  o = 1, 2: quad permutations.  o = 4: mirror
+// within each group of 8 lanes -- once the quads hold equal values the
+// mirrored partner holds the same value as lane l xor 4.  o = 8: mirror within
+// each row of 16, likewise.  o = 16: the row swap pairs rows 0-1 and 2-3;
+// o = 32: the half swap pairs the two halves.  Bitwise the xor butterfly.
 __device__ __forceinline__ float butterfly64(float v) {
     v = dpp_add<0xB1>(v);   // quad_perm [1,0,3,2]
     v = dpp_add<0x4E>(v);   // quad_perm [2,3,0,1]
     v = dpp_add<0x141>(v);  // row_half_mirror
     v = dpp_add<0x140>(v);  // row_mirror
-    const float r0 = lane_value(v, 0), r1 = lane_value(v, 16);
-    const float r2 = lane_value(v, 32), r3 = lane_value(v, 48);
-    return (r0 + r1) + (r2 + r3);
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(h[0]) + __uint_as_float(h[1]);
 }
 
 // The same over each 32-lane half (o = 1..16); lanes of half h get half h's sum.
@@ -102,9 +94,8 @@ __device__ __forceinline__ float butterfly32(float v) {
     v = dpp_add<0x4E>(v);
     v = dpp_add<0x141>(v);
     v = dpp_add<0x140>(v);
-    const float r0 = lane_value(v, 0), r1 = lane_value(v, 16);
-    const float r2 = lane_value(v, 32), r3 = lane_value(v, 48);
-    return lane_id() < 32 ? r0 + r1 : r2 + r3;
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 template <int LOSS>
@@ -208,14 +199,13 @@ struct MfOp {
 // width-1 chain pipeline
 
 constexpr int kD = 8;          // window of fresh values (ring) and cold-prefetch distance
-constexpr int kRB = 32;        // staged examples (power of two, > 2 kD)
+constexpr int kRB = 64;        // staged examples (power of two, > 2 kD)
 constexpr int kPB = 8;         // examples per producer batch
 constexpr int kChainMin = 32;  // shorter runs take the plain path
 // buffer offset past the end of any weight vector: a load there returns 0
 // and a store is dropped (buffer range checking), so lanes with nothing to
 // load or store still issue the instruction
 constexpr unsigned kOOR = 0x80000000u;
-enum : unsigned { kSrcLds = 0, kSrcFwd = 1, kSrcGlobal = 2 };
 
 typedef __attribute__((address_space(3))) float lds_f32;
 __device__ __forceinline__ unsigned lds_addr(const float *p) {
@@ -226,19 +216,21 @@ __device__ __forceinline__ void lds_write(unsigned a, float v) { *(lds_f32 *)(ui
 
 // Fixed part of the pipeline's LDS; the cached weights live in dynamic LDS.
 struct ChainShared {
-    // per staged example (slot t mod kRB) and lane:
-    //   a = {x bits, read address (or the lane to take a forwarded value from,
-    //        times 4), source kind, LDS write address}
-    //   b = {buffer offset of the global write (or kOOR), of the prefetch (or kOOR)}
-    uint4 st_a[kRB * 64];
-    uint2 st_b[kRB * 64];
+    // per staged example (slot t mod kRB) and lane: {x bits, LDS write
+    // address, read source, buffer offset of the global write}.  The read
+    // source is 4 x the lane to take a forwarded value from (< 256), the
+    // address of zero[1] for a value to prefetch from global memory, or an
+    // LDS address to read (cache, ring, zero[0] for lanes without an entry).
+    // The write offset has bit 31 set (out of range: dropped) unless the
+    // feature is cold.
+    uint4 st[kRB * 64];
     float mt_t[kRB];     // target: [y > 0] (logistic) or y (least squares)
     int mt_m[kRB];       // number of entries
     int seq[kRB];        // position staged in the slot (-1 none)
     int ctl[4];          // [0] consumer no longer needs positions < ctl[0]; [1] stop
     float ring[kD * 64]; // new weights of the example at position t mod kD, by lane
     float lsink[64];     // LDS write target of lanes without a hot entry
-    float zero[4];       // read source of lanes without an entry
+    float zero[4];       // [0] read by lanes without an entry; [1] marks global sources
 };
 
 extern __shared__ __align__(16) float g_wcache[];
@@ -281,6 +273,7 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
     const int lane = lane_id();
     const unsigned wc_base = lds_addr(&g_wcache[0]);
     const unsigned zero_a = lds_addr(&S.zero[0]);
+    const unsigned gsrc_a = lds_addr(&S.zero[1]);
     const unsigned lsink_a = lds_addr(&S.lsink[lane]);
     const unsigned ring_a = lds_addr(&S.ring[0]);
     for (int64_t t0 = (int64_t)pid * kPB; t0 < len; t0 += 3 * kPB) {
@@ -300,7 +293,6 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
             tg = target_of<LOSS>(op.y[r]);
         }
         uint4 A[kPB];
-        uint2 B[kPB];
 #pragma unroll
         for (int i = 0; i < kPB; ++i) {
             const int bi = __builtin_amdgcn_readlane(b, kD + i);
@@ -325,10 +317,9 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
                 }
             }
             const bool is_hot = (unsigned)c < (unsigned)hot;
-            unsigned kind = kSrcLds, rd = zero_a;
+            unsigned rd = zero_a;
             if (live) {
                 if (rel == 1) {
-                    kind = kSrcFwd;
                     rd = (unsigned)off << 2;
                 } else if (is_hot) {
                     rd = wc_base + ((unsigned)c << 2);
@@ -336,21 +327,15 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
                     const unsigned slot = (unsigned)(t0 + i - rel) & (kD - 1);
                     rd = ring_a + (slot << 8) + ((unsigned)off << 2);
                 } else {
-                    kind = kSrcGlobal;
+                    rd = gsrc_a;
                 }
             }
             const unsigned laddr = (live && is_hot) ? wc_base + ((unsigned)c << 2) : lsink_a;
-            const unsigned goff = (live && !is_hot) ? ((unsigned)c << 2) : kOOR;
-            const unsigned pfoff = (kind == kSrcGlobal) ? ((unsigned)c << 2) : kOOR;
-            A[i] = make_uint4(__float_as_uint(x), rd, kind, laddr);
-            B[i] = make_uint2(goff, pfoff);
+            const unsigned goff = ((unsigned)c << 2) | ((live && !is_hot) ? 0u : kOOR);
+            A[i] = make_uint4(__float_as_uint(x), laddr, rd, goff);
         }
 #pragma unroll
-        for (int i = 0; i < kPB; ++i) {
-            const int slot = (int)((t0 + i) & (kRB - 1));
-            S.st_a[slot * 64 + lane] = A[i];
-            S.st_b[slot * 64 + lane] = B[i];
-        }
+        for (int i = 0; i < kPB; ++i) S.st[(int)((t0 + i) & (kRB - 1)) * 64 + lane] = A[i];
         if (lane >= kD && lane < kD + kPB) {
             const int slot = (int)((q) & (kRB - 1));
             S.mt_t[slot] = tg;
@@ -385,16 +370,14 @@ __device__ __forceinline__ int64_t wait_staged(ChainShared &S, int64_t lo, int64
 }
 
 struct Stg {
-    uint4 a;  // x, read address, kind, LDS write address
-    uint2 b;  // global write offset, prefetch offset
+    uint4 a;  // x bits, LDS write address, read source, global write offset
     float t;  // target
 };
 
 __device__ __forceinline__ Stg read_stg(const ChainShared &S, int64_t t) {
     const int slot = (int)(t & (kRB - 1)), lane = lane_id();
     Stg r;
-    r.a = S.st_a[slot * 64 + lane];
-    r.b = S.st_b[slot * 64 + lane];
+    r.a = S.st[slot * 64 + lane];
     r.t = S.mt_t[slot];
     return r;
 }
@@ -410,49 +393,55 @@ struct ChainState {
 
 // One example, position t, slot SL = t mod kD.  Every memory operation is
 // issued unconditionally, so the count of outstanding loads and stores is
-// the same on every path and the waits stay exact.
+// the same on every path and the waits stay exact.  Issue order: the LDS
+// reads and lane permutes for example t+1 go out first, the arithmetic of
+// example t's step runs while they are in flight, and only then are their
+// results used (scheduling barriers keep the compiler from reordering).
 template <int SL, int LOSS, bool VAL>
 __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL> &op,
                                            ChainShared &S, int64_t t,
-                                           __amdgpu_buffer_rsrc_t wbuf) {
+                                           __amdgpu_buffer_rsrc_t wbuf, unsigned gsrc_a) {
     const int lane = lane_id();
     const float x = __uint_as_float(st.cur.a.x);
     // (a) this example's weights: forwarded ones get the previous step now
     const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
     const float acc = __builtin_fmaf(w_old, x, 0.0f);
-    // (b) example t+1: read its weights (those that example t writes are forwarded)
-    const unsigned rd = st.nxt.a.y;
+    // (b) example t+1: its weights (those example t writes are forwarded),
+    // the staged example t+2, and the cold values of example t+kD (their
+    // last writers are before t)
+    const unsigned rd = st.nxt.a.z;
     const float v1 = lds_read(rd);
     const float fw1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(w_old)));
     const float fx1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x)));
-    const bool fwd1 = st.nxt.a.z == kSrcFwd;
-    const float n_v = (st.nxt.a.z == kSrcGlobal) ? st.gv[(SL + 1) % kD] : v1;
     const Stg nxt2 = read_stg(S, t + 2);
+    const float g_pf = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
+    __builtin_amdgcn_sched_barrier(0);
     // (c) the step of example t
     const float s = sgd_scale_t<LOSS>(butterfly64(acc), st.cur.t, op.lr);
     const float w_new = __builtin_fmaf(-s, x, w_old);
-    lds_write(st.cur.a.w, w_new);
+    __builtin_amdgcn_sched_barrier(0);
+    // (d) writes, then the rotation
+    lds_write(st.cur.a.y, w_new);
     S.ring[SL * 64 + lane] = w_new;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_new), wbuf, st.cur.b.x, 0, 0);
-    // (d) prefetch cold values of example t+kD (writes up to t are issued)
-    st.gv[SL] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
-    // (e) rotate
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_new), wbuf, st.cur.a.w, 0, 0);
+    const float n_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
+    st.gv[SL] = g_pf;
     st.s_prev = s;
     st.cur = st.nxt;
     st.cur_v = n_v;
     st.cur_fw = fw1;
     st.cur_fx = fx1;
-    st.cur_fwd = fwd1;
+    st.cur_fwd = rd < 256u;
     st.nxt = nxt2;
 }
 
 __device__ __forceinline__ void chain_prefetch_offsets(ChainState &st, const ChainShared &S,
-                                                       int64_t q0, int64_t stop) {
+                                                       int64_t q0, int64_t stop, unsigned gsrc_a) {
 #pragma unroll
     for (int j = 0; j < kD; ++j) {
         const int64_t q = q0 + j;
-        const unsigned o = S.st_b[(int)(q & (kRB - 1)) * 64 + lane_id()].y;
-        st.pf[j] = q < stop ? o : kOOR;
+        const uint2 e = reinterpret_cast<const uint2 *>(&S.st[(int)(q & (kRB - 1)) * 64 + lane_id()])[1];
+        st.pf[j] = (q < stop && e.x == gsrc_a) ? e.y : kOOR;
     }
 }
 
@@ -467,15 +456,16 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
     long long waited = 0;
     const __amdgpu_buffer_rsrc_t wbuf =
         __builtin_amdgcn_make_buffer_rsrc(op.w, 0, (int)(d * 4), 0x00020000);
+    const unsigned gsrc_a = lds_addr(&S.zero[1]);
     ChainState st;
     int64_t stop = std::min(len, wait_staged(S, 0, std::min<int64_t>(kD, len), &waited));
-    chain_prefetch_offsets(st, S, 0, stop);
+    chain_prefetch_offsets(st, S, 0, stop, gsrc_a);
 #pragma unroll
     for (int j = 0; j < kD; ++j)
         st.gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[j], 0, 0));
     st.cur = read_stg(S, 0);
     st.nxt = read_stg(S, 1);
-    st.cur_v = (st.cur.a.z == kSrcGlobal) ? st.gv[0] : lds_read(st.cur.a.y);
+    st.cur_v = (st.cur.a.z == gsrc_a) ? st.gv[0] : lds_read(st.cur.a.z);
     st.cur_fw = st.cur_fx = 0.0f;
     st.cur_fwd = false;
     st.s_prev = 0.0f;
@@ -485,26 +475,26 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
         // positions read in this block: t+2 and t+kD for t in [t0, t0+kD)
         stop = std::min(stop, wait_staged(S, t0 + 2, std::min<int64_t>(t0 + 2 * kD, len), &waited));
         if (t0 + kD > stop) break;
-        chain_prefetch_offsets(st, S, t0 + kD, stop);
+        chain_prefetch_offsets(st, S, t0 + kD, stop, gsrc_a);
         lds_store(&S.ctl[0], (int)(t0 + 2));
-        chain_step<0>(st, op, S, t0 + 0, wbuf);
-        chain_step<1>(st, op, S, t0 + 1, wbuf);
-        chain_step<2>(st, op, S, t0 + 2, wbuf);
-        chain_step<3>(st, op, S, t0 + 3, wbuf);
-        chain_step<4>(st, op, S, t0 + 4, wbuf);
-        chain_step<5>(st, op, S, t0 + 5, wbuf);
-        chain_step<6>(st, op, S, t0 + 6, wbuf);
-        chain_step<7>(st, op, S, t0 + 7, wbuf);
+        chain_step<0>(st, op, S, t0 + 0, wbuf, gsrc_a);
+        chain_step<1>(st, op, S, t0 + 1, wbuf, gsrc_a);
+        chain_step<2>(st, op, S, t0 + 2, wbuf, gsrc_a);
+        chain_step<3>(st, op, S, t0 + 3, wbuf, gsrc_a);
+        chain_step<4>(st, op, S, t0 + 4, wbuf, gsrc_a);
+        chain_step<5>(st, op, S, t0 + 5, wbuf, gsrc_a);
+        chain_step<6>(st, op, S, t0 + 6, wbuf, gsrc_a);
+        chain_step<7>(st, op, S, t0 + 7, wbuf, gsrc_a);
     }
     if (t0 < stop) {  // last, partial block
-        chain_prefetch_offsets(st, S, t0 + kD, stop);
-        if (t0 + 0 < stop) chain_step<0>(st, op, S, t0 + 0, wbuf);
-        if (t0 + 1 < stop) chain_step<1>(st, op, S, t0 + 1, wbuf);
-        if (t0 + 2 < stop) chain_step<2>(st, op, S, t0 + 2, wbuf);
-        if (t0 + 3 < stop) chain_step<3>(st, op, S, t0 + 3, wbuf);
-        if (t0 + 4 < stop) chain_step<4>(st, op, S, t0 + 4, wbuf);
-        if (t0 + 5 < stop) chain_step<5>(st, op, S, t0 + 5, wbuf);
-        if (t0 + 6 < stop) chain_step<6>(st, op, S, t0 + 6, wbuf);
+        chain_prefetch_offsets(st, S, t0 + kD, stop, gsrc_a);
+        if (t0 + 0 < stop) chain_step<0>(st, op, S, t0 + 0, wbuf, gsrc_a);
+        if (t0 + 1 < stop) chain_step<1>(st, op, S, t0 + 1, wbuf, gsrc_a);
+        if (t0 + 2 < stop) chain_step<2>(st, op, S, t0 + 2, wbuf, gsrc_a);
+        if (t0 + 3 < stop) chain_step<3>(st, op, S, t0 + 3, wbuf, gsrc_a);
+        if (t0 + 4 < stop) chain_step<4>(st, op, S, t0 + 4, wbuf, gsrc_a);
+        if (t0 + 5 < stop) chain_step<5>(st, op, S, t0 + 5, wbuf, gsrc_a);
+        if (t0 + 6 < stop) chain_step<6>(st, op, S, t0 + 6, wbuf, gsrc_a);
     }
     lds_store(&S.ctl[1], 1);
     if (lane == 0) {
@@ -731,7 +721,8 @@ extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n,
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
     const bool has_val = csr->val != nullptr;
     const bool chain_env = env_setting("PDB_CHAIN", 1) != 0;
-    const bool chain_ok = chain_env && lv->prev_nz != nullptr;
+    // the width-1 pipeline addresses weights with 32-bit buffer offsets
+    const bool chain_ok = chain_env && lv->prev_nz != nullptr && d < (int64_t(1) << 29);
 #define PDB_SGD_CASE(LS, HV)                                                                 \
     if (loss == LS && has_val == HV) {                                                       \
         SgdOp<LS, HV> op{csr->row_ptr, csr->col, csr->val, labels, w, lv->perm, lv->prev_nz, lr}; \

@@ -245,13 +245,14 @@ def test_width1_pipeline_long_rows(gpu, hot, with_val, monkeypatch):
     check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
 
 
-def test_summation_order_adversarial(gpu):
-    """A row whose dot product depends on the pairing order of the butterfly."""
+@pytest.mark.parametrize("name", ["pairs_1_before_32", "pairs_16_before_32"])
+def test_summation_order_adversarial(gpu, name):
+    """Rows whose dot product depends on the pairing order of the butterfly."""
     import sys, os
     sys.path.insert(0, os.path.dirname(__file__))
-    from test_oracle_apply import adversarial_order_row
+    from test_oracle_apply import ADVERSARIAL_LANES, adversarial_order_row
     native = native_mod()
-    row_ptr, col, x, w0 = adversarial_order_row()
+    row_ptr, col, x, w0 = adversarial_order_row(ADVERSARIAL_LANES[name])
     g = dict(row_ptr=row_ptr, col=col, n=1, d=65, loss=1, lr=np.float32(1.0), val=x,
              y=np.zeros(1, np.float32))
     lv, _ = check_schedule(native, gpu, row_ptr, col, 65, 0)

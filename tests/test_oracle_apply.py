@@ -199,26 +199,33 @@ def test_natural_and_matched_orders_agree_closely():
     assert np.max(np.abs(a - b)) < 1e-4
 
 
-def adversarial_order_row():
-    """64 entries with w = 1: x_0 = 2^24, x_1 = 1, x_32 = -2^24, x_33 = 1, the
-    rest 0, plus entry 64 (partial 0) on a feature with w = 0 and x = 1 that
-    reads out the step.  Pairing partials l, l^1 first (ascending offsets)
-    rounds 2^24 + 1 to 2^24 and gives z = 1; pairing l, l^32 first would give
-    the exact sum 2."""
+ADVERSARIAL_LANES = {"pairs_1_before_32": (0, 1, 32, 33), "pairs_16_before_32": (0, 16, 32, 48)}
+
+
+def adversarial_order_row(lanes=(0, 1, 32, 33)):
+    """64 entries with w = 1: x_a = 2^24, x_b = 1, x_c = -2^24, x_d = 1 for
+    lanes (a, b, c, d), the rest 0, plus entry 64 (partial 0) on a feature
+    with w = 0 and x = 1 that reads out the step.  With (0, 1, 32, 33),
+    pairing partials l, l^1 first (ascending offsets) rounds 2^24 + 1 to 2^24
+    and gives z = 1, while pairing l, l^32 first gives the exact sum 2.  With
+    (0, 16, 32, 48), pairing rows 0-1 and 2-3 of 16 lanes before the halves
+    gives 1, pairing 0-2 and 1-3 first gives 2."""
+    a, b, c, d = lanes
     x = np.zeros(65, np.float32)
-    x[0], x[1], x[32], x[33], x[64] = 2.0 ** 24, 1.0, -(2.0 ** 24), 1.0, 1.0
+    x[a], x[b], x[c], x[d], x[64] = 2.0 ** 24, 1.0, -(2.0 ** 24), 1.0, 1.0
     w0 = np.ones(65, np.float32)
     w0[64] = 0.0
     return np.array([0, 65], np.int64), np.arange(65, dtype=np.int32), x, w0
 
 
-def test_matched_order_is_ascending_butterfly():
-    row_ptr, col, x, w0 = adversarial_order_row()
+@pytest.mark.parametrize("name", sorted(ADVERSARIAL_LANES))
+def test_matched_order_is_ascending_butterfly(name):
+    row_ptr, col, x, w0 = adversarial_order_row(ADVERSARIAL_LANES[name])
     y = np.zeros(1, np.float32)
     # least squares, lr = 1, y = 0: s = z, and the read-out feature ends at -z
     wm = oracle.sgd_epoch(row_ptr, col, x, y, w0, 1.0, SQUARED, MATCHED)
     wn = oracle.sgd_epoch(row_ptr, col, x, y, w0, 1.0, SQUARED, NATURAL)
     assert wm[64] == -1.0
-    # natural order accumulates in CSR order: 2^24, 2^24 (the +1 is lost), ...,
-    # 0 after x_32, then 1 after x_33
+    # natural order accumulates in CSR order: 2^24, 2^24 (the +1 is lost), 0
+    # after -2^24, then 1
     assert wn[64] == -1.0
