@@ -37,8 +37,9 @@
  *   partial sums p_j = 0 for j = 0..63; p_{k mod 64} = fma(w[c_k], x_k, p_{k mod 64});
  *   butterfly: for o = 1,2,4,8,16,32 every p_j becomes p_j + p_{j xor o}; z = p_0;
  *   logistic: g = 1/(1 + exp(-z)) - (y > 0 ? 1 : 0), exp by Cody-Waite
- *   reduction (k = rint(x log2 e)) and the degree-7 Taylor polynomial in
- *   Horner form, scaled by 2^k;   least squares: g = z - y;
+ *   reduction (k = rint(x log2 e), ln 2 split into two floats) and the
+ *   degree-7 Taylor polynomial of e^r evaluated by Estrin's scheme, scaled
+ *   by 2^k;   least squares: g = z - y;
  *   s = lr * g;  w[c_k] = fma(-s, x_k, w[c_k]) (values read before any write).
  * Matrix completion (rank 32): q_j = fma(U_u[j], V_i[j], 0), butterfly over
  *   o = 1..16, e = r - q_0;  U_u[j] = fma(lr, e*V_i[j] - reg*U_u[j], U_u[j]),

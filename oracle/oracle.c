@@ -27,7 +27,7 @@
  *            p[l] + p[l xor off]; z is the common final value.
  * The exponential is the library expf in natural mode and, in matched mode,
  * orc_exp below (Cody-Waite range reduction and the degree-7 Taylor
- * polynomial of e^r in Horner form).
+ * polynomial of e^r evaluated by Estrin's scheme).
  */
 #include <math.h>
 #include <stdint.h>

@@ -1,0 +1,68 @@
+"""Host-side checks of the C ABI (no GPU needed, no kernel launched):
+the library loads, exports every function that include/pdb.h declares, the
+binding names the same set, and the host-only entry points behave."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pdb.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pdb_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_1508_00703_amd import native
+
+    if not os.path.exists(native.LIB_PATH):
+        pytest.fail("libpdb.so is not built (run __graft_entry__.build())")
+    return native.load()
+
+
+def test_header_declares_the_binding_exports():
+    from paper_1508_00703_amd import native
+
+    assert declared_functions() == sorted(native.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_strerror_covers_every_status(lib):
+    texts = [lib.pdb_strerror(c).decode() for c in range(0, -7, -1)]
+    assert len(set(texts)) == 7 and all(texts)
+    assert lib.pdb_strerror(-99)          # unknown codes still give text
+
+
+def test_workspace_size_queries(lib):
+    from paper_1508_00703_amd import native
+
+    sz = ctypes.c_size_t(0)
+    assert lib.pdb_epoch_workspace_bytes(ctypes.byref(sz)) == native.PDB_OK and sz.value >= 512
+    prev = 0
+    for nnz in (0, 1000, 10 ** 6, 5 * 10 ** 8):
+        assert lib.pdb_schedule_workspace_bytes(10 ** 4, 10 ** 3, nnz, ctypes.byref(sz)) == 0
+        assert sz.value >= prev and sz.value % 256 == 0
+        prev = sz.value
+    assert lib.pdb_schedule_workspace_bytes(-1, 10, 10, ctypes.byref(sz)) == native.PDB_ERR_INVALID_ARG
+    assert lib.pdb_schedule_workspace_bytes(10, 10, 10, None) == native.PDB_ERR_INVALID_ARG
+    assert (lib.pdb_schedule_workspace_bytes(2 ** 31, 10, 10, ctypes.byref(sz))
+            == native.PDB_ERR_UNSUPPORTED)
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    from paper_1508_00703_amd import native
+
+    monkeypatch.setattr(native, "_lib", None)
+    monkeypatch.setattr(native, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        native.load()
