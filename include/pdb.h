@@ -36,10 +36,12 @@
  *   entries (c_k, x_k), k = 0..m-1 in CSR order (x_k = 1 when val is NULL);
  *   partial sums p_j = 0 for j = 0..63; p_{k mod 64} = fma(w[c_k], x_k, p_{k mod 64});
  *   butterfly: for o = 1,2,4,8,16,32 every p_j becomes p_j + p_{j xor o}; z = p_0;
- *   logistic: g = 1/(1 + exp(-z)) - (y > 0 ? 1 : 0), exp by Cody-Waite
- *   reduction (k = rint(x log2 e), ln 2 split into two floats) and the
- *   degree-7 Taylor polynomial of e^r evaluated by Estrin's scheme, scaled
- *   by 2^k;   least squares: g = z - y;
+ *   logistic: g = 1/(1 + exp(min(-z, 87))) - (y > 0 ? 1 : 0) with one
+ *   correctly rounded division (the cap keeps 1 + exp below 2^126; it only
+ *   changes results for z < -87, where the logistic value is below 1.7e-38),
+ *   exp by Cody-Waite reduction (k = rint(x log2 e), ln 2 split into two
+ *   floats) and the degree-7 Taylor polynomial of e^r evaluated by Estrin's
+ *   scheme, scaled by 2^k;   least squares: g = z - y;
  *   s = lr * g;  w[c_k] = fma(-s, x_k, w[c_k]) (values read before any write).
  * Matrix completion (rank 32): q_j = fma(U_u[j], V_i[j], 0), butterfly over
  *   o = 1..16, e = r - q_0;  U_u[j] = fma(lr, e*V_i[j] - reg*U_u[j], U_u[j]),
@@ -173,6 +175,16 @@ int pdb_transpose(const pdb_csr *csr, int64_t n, int64_t d, int64_t *col_ptr, in
  * pdb_schedule.  Synchronous. */
 int pdb_prev_writer(const pdb_csr *csr, int64_t n, int64_t d, int32_t *prev_row,
                     int32_t *prev_nz, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Self-check of the division in the logistic step on this device: for every
+ * binary32 b whose bit pattern lies in [lo_bits, hi_bits) (within
+ * [0x3F800000, 0x7E800000), i.e. 1 <= b < 2^126, the range of 1 + exp above),
+ * compares the kernels' reciprocal of b with the IEEE quotient 1/b.  Writes
+ * the number of mismatches and the smallest mismatching bit pattern
+ * (0xFFFFFFFF if none) to host memory.  ws: pdb_epoch_workspace_bytes().
+ * Synchronous. */
+int pdb_check_reciprocal(uint32_t lo_bits, uint32_t hi_bits, uint64_t *mismatches,
+                         uint32_t *first_bad, void *ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -55,6 +55,8 @@ def _load():
     P, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
     lib.orc_exp.argtypes = [f32]
     lib.orc_exp.restype = f32
+    lib.orc_sigmoid.argtypes = [f32]
+    lib.orc_sigmoid.restype = f32
     lib.orc_levels_brute.argtypes = [i64, P, P, P]
     lib.orc_levels_brute.restype = i32
     lib.orc_levels_seq.argtypes = [i64, i64, P, P, P]
@@ -85,6 +87,11 @@ def _ptr(a):
 def exp(x: float) -> np.float32:
     """e^x by Cody-Waite reduction and the degree-7 Taylor polynomial (binary32)."""
     return np.float32(_load().orc_exp(np.float32(x)))
+
+
+def sigmoid(z: float) -> np.float32:
+    """The logistic function of the matched mode: 1/(1 + exp(min(-z, 87)))."""
+    return np.float32(_load().orc_sigmoid(np.float32(z)))
 
 
 def levels_brute(row_ptr, col, n=None):

@@ -25,9 +25,10 @@
  *   matched: 64 partial sums, entry k goes to partial k mod 64, then a
  *            butterfly: for off = 1,2,4,8,16,32 every partial l becomes
  *            p[l] + p[l xor off]; z is the common final value.
- * The exponential is the library expf in natural mode and, in matched mode,
- * orc_exp below (Cody-Waite range reduction and the degree-7 Taylor
- * polynomial of e^r evaluated by Estrin's scheme).
+ * The logistic function is 1/(1 + expf(-z)) in natural mode and, in matched
+ * mode, orc_sigmoid below: the same with orc_exp (Cody-Waite range reduction
+ * and the degree-7 Taylor polynomial of e^r evaluated by Estrin's scheme)
+ * and the exponent argument capped at 87.
  */
 #include <math.h>
 #include <stdint.h>
@@ -198,6 +199,17 @@ static float butterfly64(float *acc, int width) {
     return acc[0];
 }
 
+/* The logistic function in matched mode: 1 / (1 + exp(x)) with x = -z
+ * capped at 87 (NaN stays NaN).  Below the cap this is the logistic function
+ * itself, with orc_exp and one correctly rounded division; for z < -87 it is
+ * 1/(1 + e^87) ~ 1.6e-38 instead of a smaller value, so that 1 + e stays
+ * below 2^126 and the quotient is a normal number. */
+float orc_sigmoid(float z) {
+    float x = -z;
+    if (x > 87.0f) x = 87.0f;
+    return 1.0f / (1.0f + orc_exp(x));
+}
+
 static float dot_matched(const float *w, const int32_t *c, const float *v, int64_t m) {
     float acc[64];
     for (int l = 0; l < 64; ++l) acc[l] = 0.0f;
@@ -207,7 +219,7 @@ static float dot_matched(const float *w, const int32_t *c, const float *v, int64
 
 /* One SGD step per example, examples taken in the given order (NULL: index
  * order 0..n-1, which is Algorithm 1).  Per example i with entries (c_k, x_k):
- *   z = <w, x_i>;  logistic: g = 1/(1+exp(-z)) - [y_i > 0];  squared: g = z - y_i
+ *   z = <w, x_i>;  logistic: g = sigma(z) - [y_i > 0];  squared: g = z - y_i
  *   s = lr * g;    w[c_k] <- fmaf(-s, x_k, w[c_k])  (all reads before any write). */
 void orc_sgd_apply(int64_t count, const int32_t *order, const int64_t *row_ptr,
                    const int32_t *col, const float *val, const float *y, float *w, float lr,
@@ -220,8 +232,7 @@ void orc_sgd_apply(int64_t count, const int32_t *order, const int64_t *row_ptr,
         float z = (mode == ORC_MATCHED) ? dot_matched(w, c, v, m) : dot_natural(w, c, v, m);
         float g;
         if (loss == ORC_LOGISTIC) {
-            float e = (mode == ORC_MATCHED) ? orc_exp(-z) : expf(-z);
-            float sig = 1.0f / (1.0f + e);
+            float sig = (mode == ORC_MATCHED) ? orc_sigmoid(z) : 1.0f / (1.0f + expf(-z));
             g = sig - ((y[i] > 0.0f) ? 1.0f : 0.0f);
         } else {
             g = z - y[i];

@@ -40,15 +40,15 @@ namespace {
 
 constexpr int kWavesPerBlock = kBlock / kWave;
 
-// e^x: k = rint(x log2 e), r = x - k ln 2 with ln 2 in two binary32 pieces,
-// e^r from its Taylor series through r^7 by Estrin's scheme (pairs
-// c_j + c_{j+1} r, combined with r^2, then r^4), times 2^k by ldexp: exact
-// in the normal range, one rounding into the subnormals, +inf past the top.
-__device__ __forceinline__ float dev_exp(float x) {
-    // branch-free: the arithmetic runs on x clamped to [-104, 89]; past the
-    // ends that gives the same answers (e^-104 rounds to 0, k = 128
-    // overflows), only NaN needs a select
-    const float xc = __builtin_fminf(__builtin_fmaxf(x, -104.0f), 89.0f);
+// e^x for x <= 87 (larger x count as 87): k = rint(x log2 e), r = x - k ln 2
+// with ln 2 in two binary32 pieces, e^r from its Taylor series through r^7
+// by Estrin's scheme (pairs c_j + c_{j+1} r, combined with r^2, then r^4),
+// times 2^k by ldexp: one rounding into the subnormals.
+__device__ __forceinline__ float dev_exp87(float x) {
+    // branch-free: the arithmetic runs on x clamped to [-104, 87]; below the
+    // bottom that gives the same answer (e^-104 rounds to 0), only NaN needs a
+    // select
+    const float xc = __builtin_fminf(__builtin_fmaxf(x, -104.0f), 87.0f);
     const float kf = __builtin_rintf(xc * 0x1.715476p+0f);
     float r = __builtin_fmaf(-kf, 0x1.62e430p-1f, xc);
     r = __builtin_fmaf(-kf, -0x1.05c610p-29f, r);
@@ -63,6 +63,25 @@ __device__ __forceinline__ float dev_exp(float x) {
     const float q = __builtin_fmaf(p47, r4, p03);
     const float e = __builtin_amdgcn_ldexpf(q, (int)kf);
     return (x == x) ? e : x;
+}
+
+// 1/b, correctly rounded, for b in [1, 2^126) (NaN gives NaN).  y0 = v_rcp
+// (within about 1 ulp), one Newton step y1 = y0 + y0 (1 - b y0), whose error
+// is far below 2^-24 relative; then Markstein's correction q = y1 + y1 r with
+// the residual r = 1 - b y1, exact in binary32 because y1 is a faithful
+// reciprocal: q is 1/b rounded to nearest.  The result is a normal number, so
+// no scaling is needed.  pdb_check_reciprocal compares it with IEEE division
+// for every b in the range.
+__device__ __forceinline__ float recip_normal(float b) {
+    const float y0 = __builtin_amdgcn_rcpf(b);
+    const float y1 = __builtin_fmaf(__builtin_fmaf(-b, y0, 1.0f), y0, y0);
+    return __builtin_fmaf(__builtin_fmaf(-b, y1, 1.0f), y1, y1);
+}
+
+// The logistic function 1/(1 + e^min(-z, 87)): the cap keeps 1 + e below
+// 2^126 (e^87 < 2^126), where recip_normal is exact.
+__device__ __forceinline__ float dev_sigmoid(float z) {
+    return recip_normal(1.0f + dev_exp87(-z));
 }
 
 // v + v[partner] with the partner chosen by a DPP lane pattern
@@ -102,9 +121,7 @@ template <int LOSS>
 __device__ __forceinline__ float sgd_scale(float z, float y, float lr) {
     float g;
     if (LOSS == PDB_LOGISTIC) {
-        const float e = dev_exp(-z);
-        const float sig = 1.0f / (1.0f + e);
-        g = sig - (y > 0.0f ? 1.0f : 0.0f);
+        g = dev_sigmoid(z) - (y > 0.0f ? 1.0f : 0.0f);
     } else {
         g = z - y;
     }
@@ -198,10 +215,11 @@ struct MfOp {
 // ---------------------------------------------------------------------------
 // width-1 chain pipeline
 
-constexpr int kD = 8;          // window of fresh values (ring) and cold-prefetch distance
-constexpr int kRB = 64;        // staged examples (power of two, > 2 kD)
-constexpr int kPB = 8;         // examples per producer batch
-constexpr int kChainMin = 32;  // shorter runs take the plain path
+constexpr int kD = 16;           // window of fresh values and cold-prefetch distance
+constexpr int kRB = 64;          // staged examples (power of two, >= 2 kD + kPB)
+constexpr int kPB = 16;          // examples per producer batch
+constexpr int kRing = kD * 64;   // LDS ring of recent cold writes
+constexpr int kChainMin = 32;    // shorter runs take the plain path
 // buffer offset past the end of any weight vector: a load there returns 0
 // and a store is dropped (buffer range checking), so lanes with nothing to
 // load or store still issue the instruction
@@ -221,16 +239,19 @@ struct ChainShared {
     // source is 4 x the lane to take a forwarded value from (< 256), the
     // address of zero[1] for a value to prefetch from global memory, or an
     // LDS address to read (cache, ring, zero[0] for lanes without an entry).
-    // The write offset has bit 31 set (out of range: dropped) unless the
-    // feature is cold.
-    uint4 st[kRB * 64];
-    float mt_t[kRB];     // target: [y > 0] (logistic) or y (least squares)
-    int mt_m[kRB];       // number of entries
-    int seq[kRB];        // position staged in the slot (-1 none)
-    int ctl[4];          // [0] consumer no longer needs positions < ctl[0]; [1] stop
-    float ring[kD * 64]; // new weights of the example at position t mod kD, by lane
-    float lsink[64];     // LDS write target of lanes without a hot entry
-    float zero[4];       // [0] read by lanes without an entry; [1] marks global sources
+    // The write address is the cache slot of a hot feature, the ring slot of
+    // a cold one, or lsink.  The write offset has bit 31 set (out of range:
+    // dropped) unless the feature is cold.  Slots kRB and kRB + 1 repeat
+    // slots 0 and 1, so that the consumer reads a block of kD + 2
+    // consecutive slots without wrapping.
+    uint4 st[(kRB + 2) * 64];
+    float mt_t[kRB + 2];  // target: [y > 0] (logistic) or y (least squares)
+    int mt_m[kRB];        // number of entries
+    int seq[kRB];         // position staged in the slot (-1 none)
+    int ctl[4];           // [0] consumer no longer needs positions < ctl[0]; [1] stop
+    float ring[kRing];    // new weights of cold features written within kD examples
+    float lsink[64];      // LDS write target of lanes without an entry
+    float zero[4];        // [0] read by lanes without an entry; [1] marks global sources
 };
 
 extern __shared__ __align__(16) float g_wcache[];
@@ -252,8 +273,7 @@ template <int LOSS>
 __device__ __forceinline__ float sgd_scale_t(float z, float tgt, float lr) {
     float g;
     if (LOSS == PDB_LOGISTIC) {
-        const float e = dev_exp(-z);
-        g = 1.0f / (1.0f + e) - tgt;
+        g = dev_sigmoid(z) - tgt;
     } else {
         g = z - tgt;
     }
@@ -262,88 +282,156 @@ __device__ __forceinline__ float sgd_scale_t(float z, float tgt, float lr) {
 
 // Producer wave pid (0..2): stages examples t of the run (batches of kPB, in
 // turn), never more than kRB ahead of the consumer.  For every entry it finds
-// the previous writer among the kD examples before it (its CSR index lies in
-// one of their entry ranges) and picks where the consumer will read the
-// current weight: forwarded from the previous example's lane, the LDS cache
-// (hot feature), the ring (cold feature written within kD examples), or the
-// prefetched global value.
-template <int LOSS, bool VAL>
+// whether the previous writer is among the kD examples before it and picks
+// where the consumer will read the current weight: forwarded from the
+// previous example's lane, the LDS cache (hot feature), the ring (cold
+// feature written within kD examples), or the prefetched global value.
+//
+// DENSE: the run is the consecutive rows r0, r0 + 1, ..., so the entries of
+// the kD examples before position t are the CSR range [b(t - kD), b(t)): one
+// comparison tells whether the previous writer is in the window, and the ring
+// is indexed by the writer's CSR index (the window spans at most kD * 64
+// entries, so no two of them share a ring slot).  Otherwise each entry is
+// matched against the kD preceding examples' entry ranges and the ring is
+// indexed by (position mod kD, lane).
+// Row bounds and targets of the positions a producer batch at t0 needs:
+// lane i describes position t0 - kD + i (the window before the batch, the
+// batch, and for DENSE one more that ends the batch's last example).
+struct BatchMeta {
+    int b, m;
+    float tg;  // label of the position (clamped into the run)
+};
+
+template <int LOSS, bool VAL, bool DENSE>
+__device__ __forceinline__ BatchMeta batch_meta(const SgdOp<LOSS, VAL> &op, int64_t t0,
+                                                int64_t e_beg, int64_t len, int64_t r0) {
+    // every lane loads (positions clamped into the run), so no load sits in
+    // a branch and none has to complete before the batch's entry loads
+    const int lane = lane_id();
+    const int64_t q = t0 - kD + lane;
+    const int64_t qc = min(max(q, (int64_t)0), len - 1);
+    BatchMeta mt;
+    if (DENSE) {
+        // b of positions clamped to [0, len]; m comes later from the next lane
+        mt.b = (int)op.row_ptr[r0 + min(max(q, (int64_t)0), len)];
+        mt.m = 0;
+        mt.tg = op.y[r0 + qc];
+    } else {
+        const int64_t r = op.perm[e_beg + qc];
+        const int64_t b0 = op.row_ptr[r], b1 = op.row_ptr[r + 1];
+        const float yv = op.y[r];
+        const bool ok = lane < kD + kPB && q >= 0 && q < len;
+        mt.b = ok ? (int)b0 : 0;
+        mt.m = ok ? (int)(b1 - b0) : 0;
+        mt.tg = yv;
+    }
+    return mt;
+}
+
+template <int LOSS, bool VAL, bool DENSE>
 __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_beg, int64_t len,
-                               int64_t dense_r0, int hot, ChainShared &S) {
+                               int64_t r0, int hot, ChainShared &S) {
     const int lane = lane_id();
     const unsigned wc_base = lds_addr(&g_wcache[0]);
     const unsigned zero_a = lds_addr(&S.zero[0]);
     const unsigned gsrc_a = lds_addr(&S.zero[1]);
     const unsigned lsink_a = lds_addr(&S.lsink[lane]);
     const unsigned ring_a = lds_addr(&S.ring[0]);
-    for (int64_t t0 = (int64_t)pid * kPB; t0 < len; t0 += 3 * kPB) {
+    // lanes without an entry load from here (a valid address) and ignore it
+    const int32_t *dummy_i = reinterpret_cast<const int32_t *>(op.row_ptr);
+    const float *dummy_f = reinterpret_cast<const float *>(op.row_ptr);
+    int64_t t0 = (int64_t)pid * kPB;
+    BatchMeta nxt = batch_meta<LOSS, VAL, DENSE>(op, t0, e_beg, len, r0);
+    for (; t0 < len; t0 += 3 * kPB) {
         while (t0 + kPB - 1 >= (int64_t)lds_load(&S.ctl[0]) + kRB) {
             if (lds_load(&S.ctl[1])) return;
             __builtin_amdgcn_s_sleep(1);
         }
         if (lds_load(&S.ctl[1])) return;
-        // lane i: position t0 - kD + i (the window before the batch, then the batch)
-        int b = 0, m = 0;
-        float tg = 0.0f;
-        const int64_t q = t0 - kD + lane;
-        if (lane < kD + kPB && q >= 0 && q < len) {
-            const int64_t r = dense_r0 >= 0 ? dense_r0 + q : op.perm[e_beg + q];
-            b = (int)op.row_ptr[r];
-            m = (int)op.row_ptr[r + 1] - b;
-            tg = target_of<LOSS>(op.y[r]);
+        const int b = nxt.b;
+        const int m = DENSE ? __shfl_down(b, 1) - b : nxt.m;
+        const float tg = target_of<LOSS>(nxt.tg);
+        // every entry load of the batch first (unconditional, so they all go
+        // out before the first wait), then this wave's next batch
+        int c[kPB], pn[kPB];
+        float x[kPB];
+#pragma unroll
+        for (int i = 0; i < kPB; ++i) {
+            const int bi = __builtin_amdgcn_readlane(b, kD + i);
+            const int mi = __builtin_amdgcn_readlane(m, kD + i);
+            const bool live = lane < mi;  // mi = 0 past the end of the run
+            const int64_t e = (int64_t)bi + lane;
+            c[i] = *(live ? op.col + e : dummy_i);
+            pn[i] = *(live ? op.prev_nz + e : dummy_i);
+            x[i] = VAL ? *(live ? op.val + e : dummy_f) : 1.0f;
         }
+        nxt = batch_meta<LOSS, VAL, DENSE>(op, t0 + 3 * kPB, e_beg, len, r0);
+        // classify every entry with comparisons on all lanes and a chain of
+        // selects (no branch holds a use of the loaded values, so the loads
+        // stay where they were issued)
         uint4 A[kPB];
 #pragma unroll
         for (int i = 0; i < kPB; ++i) {
             const int bi = __builtin_amdgcn_readlane(b, kD + i);
             const int mi = __builtin_amdgcn_readlane(m, kD + i);
             const bool live = lane < mi;
-            int c = 0, p = -1;
-            float x = 0.0f;
-            if (live) {
-                c = op.col[bi + lane];
-                p = op.prev_nz[bi + lane];
-                x = VAL ? op.val[bi + lane] : 1.0f;
-            }
-            int rel = 0, off = 0;
+            const bool is_hot = live & ((unsigned)c[i] < (unsigned)hot);
+            const unsigned cache = wc_base + ((unsigned)c[i] << 2);
+            unsigned rd, laddr;
+            if (DENSE) {
+                // previous example starts at bprev, the window at bwin (both
+                // clamp to the run's first example at its start)
+                const int bprev = __builtin_amdgcn_readlane(b, kD + i - 1);
+                const int bwin = __builtin_amdgcn_readlane(b, i);
+                const bool fwd = pn[i] >= bprev;
+                const bool win = pn[i] >= bwin;
+                rd = win ? ring_a + (((unsigned)pn[i] & (kRing - 1)) << 2) : gsrc_a;
+                rd = is_hot ? cache : rd;
+                rd = fwd ? (unsigned)(pn[i] - bprev) << 2 : rd;
+                rd = live ? rd : zero_a;
+                laddr = ring_a + (((unsigned)(bi + lane) & (kRing - 1)) << 2);
+            } else {
+                int rel = 0, off = 0;
 #pragma unroll
-            for (int j = 1; j <= kD; ++j) {
-                const int bj = __builtin_amdgcn_readlane(b, kD + i - j);
-                const int mj = __builtin_amdgcn_readlane(m, kD + i - j);
-                const unsigned o = (unsigned)(p - bj);
-                if (o < (unsigned)mj) {
-                    rel = j;
-                    off = (int)o;
+                for (int j = 1; j <= kD; ++j) {
+                    const int bj = __builtin_amdgcn_readlane(b, kD + i - j);
+                    const int mj = __builtin_amdgcn_readlane(m, kD + i - j);
+                    const unsigned o = (unsigned)(pn[i] - bj);
+                    const bool hit = o < (unsigned)mj;
+                    rel = hit ? j : rel;
+                    off = hit ? (int)o : off;
                 }
+                const int64_t t = t0 + i;
+                const unsigned wslot = (unsigned)(t - rel) & (kD - 1);
+                rd = rel >= 2 ? ring_a + (wslot << 8) + ((unsigned)off << 2) : gsrc_a;
+                rd = is_hot ? cache : rd;
+                rd = rel == 1 ? (unsigned)off << 2 : rd;
+                rd = live ? rd : zero_a;
+                laddr = ring_a + (((unsigned)t & (kD - 1)) << 8) + ((unsigned)lane << 2);
             }
-            const bool is_hot = (unsigned)c < (unsigned)hot;
-            unsigned rd = zero_a;
-            if (live) {
-                if (rel == 1) {
-                    rd = (unsigned)off << 2;
-                } else if (is_hot) {
-                    rd = wc_base + ((unsigned)c << 2);
-                } else if (rel >= 2) {
-                    const unsigned slot = (unsigned)(t0 + i - rel) & (kD - 1);
-                    rd = ring_a + (slot << 8) + ((unsigned)off << 2);
-                } else {
-                    rd = gsrc_a;
-                }
-            }
-            const unsigned laddr = (live && is_hot) ? wc_base + ((unsigned)c << 2) : lsink_a;
-            const unsigned goff = ((unsigned)c << 2) | ((live && !is_hot) ? 0u : kOOR);
-            A[i] = make_uint4(__float_as_uint(x), laddr, rd, goff);
+            laddr = is_hot ? cache : laddr;
+            laddr = live ? laddr : lsink_a;
+            const unsigned goff = ((unsigned)c[i] << 2) | ((live & !is_hot) ? 0u : kOOR);
+            A[i] = make_uint4(__float_as_uint(live ? x[i] : 0.0f), laddr, rd, goff);
         }
+        const int sb = (int)(t0 & (kRB - 1));  // a multiple of kPB: no wrap inside the batch
 #pragma unroll
-        for (int i = 0; i < kPB; ++i) S.st[(int)((t0 + i) & (kRB - 1)) * 64 + lane] = A[i];
-        if (lane >= kD && lane < kD + kPB) {
-            const int slot = (int)((q) & (kRB - 1));
-            S.mt_t[slot] = tg;
-            S.mt_m[slot] = m;
+        for (int i = 0; i < kPB; ++i) S.st[(sb + i) * 64 + lane] = A[i];
+        if (sb == 0) {
+            S.st[kRB * 64 + lane] = A[0];
+            S.st[(kRB + 1) * 64 + lane] = A[1];
+        }
+        {
+            // every lane stores (lanes outside the batch into the sink), so
+            // the label load is never moved into a branch
+            const bool in_batch = lane >= kD && lane < kD + kPB;
+            const int slot = sb + lane - kD;
+            lds_write(in_batch ? lds_addr(&S.mt_t[slot]) : lsink_a, tg);
+            lds_write(in_batch ? lds_addr((const float *)&S.mt_m[slot]) : lsink_a, __int_as_float(m));
+            lds_write((in_batch && slot < 2) ? lds_addr(&S.mt_t[kRB + slot]) : lsink_a, tg);
         }
         compiler_fence();  // LDS executes one wave's operations in order
-        if (lane < kPB && t0 + lane < len)
-            lds_store(&S.seq[(t0 + lane) & (kRB - 1)], (int)(t0 + lane));
+        if (lane < kPB && t0 + lane < len) lds_store(&S.seq[sb + lane], (int)(t0 + lane));
         compiler_fence();
     }
 }
@@ -374,11 +462,38 @@ struct Stg {
     float t;  // target
 };
 
-__device__ __forceinline__ Stg read_stg(const ChainShared &S, int64_t t) {
-    const int slot = (int)(t & (kRB - 1)), lane = lane_id();
+// slot in [0, kRB + 2)
+__device__ __forceinline__ Stg read_slot(const ChainShared &S, int slot) {
     Stg r;
-    r.a = S.st[slot * 64 + lane];
+    r.a = S.st[slot * 64 + lane_id()];
     r.t = S.mt_t[slot];
+    return r;
+}
+
+// The staged slots of one consumer block (kD + 2 consecutive slots from sb):
+// LDS addresses of this lane's first record and of the first target, so that
+// every read in the block is that address plus a constant offset.
+struct SlotBlock {
+    unsigned st, mt;
+};
+
+__device__ __forceinline__ SlotBlock slot_block(const ChainShared &S, int sb) {
+    SlotBlock b;
+    b.st = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) uint4 *)&S.st[sb * 64 + lane_id()];
+    b.mt = lds_addr(&S.mt_t[sb]);
+    __asm__ volatile("" : "+v"(b.mt));  // a vector register: reads then take constant offsets
+    return b;
+}
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+template <int K>
+__device__ __forceinline__ Stg read_slot_at(SlotBlock b) {
+    const u32x4 v =
+        *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(b.st + K * 64 * 16);
+    Stg r;
+    r.a = make_uint4(v.x, v.y, v.z, v.w);
+    r.t = lds_read(b.mt + K * 4);
     return r;
 }
 
@@ -391,17 +506,17 @@ struct ChainState {
     unsigned pf[kD];              // prefetch offsets of the next examples
 };
 
-// One example, position t, slot SL = t mod kD.  Every memory operation is
-// issued unconditionally, so the count of outstanding loads and stores is
-// the same on every path and the waits stay exact.  Issue order: the LDS
-// reads and lane permutes for example t+1 go out first, the arithmetic of
-// example t's step runs while they are in flight, and only then are their
-// results used (scheduling barriers keep the compiler from reordering).
+// One example, position t = t0 + SL with sb = t0 mod kRB.  Every memory
+// operation is issued unconditionally, so the count of outstanding loads and
+// stores is the same on every path and the waits stay exact.  Issue order:
+// the LDS reads and lane permutes for example t+1 go out first, the
+// arithmetic of example t's step runs while they are in flight, and only then
+// are their results used (scheduling barriers keep the compiler from
+// reordering).
 template <int SL, int LOSS, bool VAL>
 __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL> &op,
-                                           ChainShared &S, int64_t t,
-                                           __amdgpu_buffer_rsrc_t wbuf, unsigned gsrc_a) {
-    const int lane = lane_id();
+                                           SlotBlock sblk, __amdgpu_buffer_rsrc_t wbuf,
+                                           unsigned gsrc_a) {
     const float x = __uint_as_float(st.cur.a.x);
     // (a) this example's weights: forwarded ones get the previous step now
     const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
@@ -413,7 +528,7 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     const float v1 = lds_read(rd);
     const float fw1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(w_old)));
     const float fx1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x)));
-    const Stg nxt2 = read_stg(S, t + 2);
+    const Stg nxt2 = read_slot_at<SL + 2>(sblk);
     const float g_pf = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
     __builtin_amdgcn_sched_barrier(0);
     // (c) the step of example t
@@ -422,7 +537,6 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     __builtin_amdgcn_sched_barrier(0);
     // (d) writes, then the rotation
     lds_write(st.cur.a.y, w_new);
-    S.ring[SL * 64 + lane] = w_new;
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_new), wbuf, st.cur.a.w, 0, 0);
     const float n_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
     st.gv[SL] = g_pf;
@@ -435,15 +549,23 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     st.nxt = nxt2;
 }
 
+// Prefetch offsets of positions q0 .. q0 + kD - 1 (kOOR for positions at or
+// past stop, and for lanes whose value does not come from global memory).
+// The slots are read unconditionally: positions past stop read stale slots.
 __device__ __forceinline__ void chain_prefetch_offsets(ChainState &st, const ChainShared &S,
                                                        int64_t q0, int64_t stop, unsigned gsrc_a) {
+    uint2 e[kD];
 #pragma unroll
-    for (int j = 0; j < kD; ++j) {
-        const int64_t q = q0 + j;
-        const uint2 e = reinterpret_cast<const uint2 *>(&S.st[(int)(q & (kRB - 1)) * 64 + lane_id()])[1];
-        st.pf[j] = (q < stop && e.x == gsrc_a) ? e.y : kOOR;
-    }
+    for (int j = 0; j < kD; ++j)
+        e[j] = reinterpret_cast<const uint2 *>(&S.st[(int)((q0 + j) & (kRB - 1)) * 64 + lane_id()])[1];
+#pragma unroll
+    for (int j = 0; j < kD; ++j) st.pf[j] = ((q0 + j < stop) & (e[j].x == gsrc_a)) ? e[j].y : kOOR;
 }
+
+#define PDB_CHAIN_STEPS(STEP) \
+    STEP(0) STEP(1) STEP(2) STEP(3) STEP(4) STEP(5) STEP(6) STEP(7) \
+    STEP(8) STEP(9) STEP(10) STEP(11) STEP(12) STEP(13) STEP(14) STEP(15)
+static_assert(kD == 16, "PDB_CHAIN_STEPS lists kD steps");
 
 // Consumer: runs examples t = 0.. of the run in order.  Returns the number
 // processed: len, or the position of the first example with more than 64
@@ -456,15 +578,16 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
     long long waited = 0;
     const __amdgpu_buffer_rsrc_t wbuf =
         __builtin_amdgcn_make_buffer_rsrc(op.w, 0, (int)(d * 4), 0x00020000);
-    const unsigned gsrc_a = lds_addr(&S.zero[1]);
+    unsigned gsrc_a = lds_addr(&S.zero[1]);
+    __asm__ volatile("" : "+s"(gsrc_a));  // computed once, kept in a register
     ChainState st;
     int64_t stop = std::min(len, wait_staged(S, 0, std::min<int64_t>(kD, len), &waited));
     chain_prefetch_offsets(st, S, 0, stop, gsrc_a);
 #pragma unroll
     for (int j = 0; j < kD; ++j)
         st.gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[j], 0, 0));
-    st.cur = read_stg(S, 0);
-    st.nxt = read_stg(S, 1);
+    st.cur = read_slot(S, 0);
+    st.nxt = read_slot(S, 1);
     st.cur_v = (st.cur.a.z == gsrc_a) ? st.gv[0] : lds_read(st.cur.a.z);
     st.cur_fw = st.cur_fx = 0.0f;
     st.cur_fwd = false;
@@ -477,24 +600,18 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
         if (t0 + kD > stop) break;
         chain_prefetch_offsets(st, S, t0 + kD, stop, gsrc_a);
         lds_store(&S.ctl[0], (int)(t0 + 2));
-        chain_step<0>(st, op, S, t0 + 0, wbuf, gsrc_a);
-        chain_step<1>(st, op, S, t0 + 1, wbuf, gsrc_a);
-        chain_step<2>(st, op, S, t0 + 2, wbuf, gsrc_a);
-        chain_step<3>(st, op, S, t0 + 3, wbuf, gsrc_a);
-        chain_step<4>(st, op, S, t0 + 4, wbuf, gsrc_a);
-        chain_step<5>(st, op, S, t0 + 5, wbuf, gsrc_a);
-        chain_step<6>(st, op, S, t0 + 6, wbuf, gsrc_a);
-        chain_step<7>(st, op, S, t0 + 7, wbuf, gsrc_a);
+        const SlotBlock sblk = slot_block(S, (int)(t0 & (kRB - 1)));
+#define PDB_STEP(SL) chain_step<SL>(st, op, sblk, wbuf, gsrc_a);
+        PDB_CHAIN_STEPS(PDB_STEP)
+#undef PDB_STEP
     }
     if (t0 < stop) {  // last, partial block
         chain_prefetch_offsets(st, S, t0 + kD, stop, gsrc_a);
-        if (t0 + 0 < stop) chain_step<0>(st, op, S, t0 + 0, wbuf, gsrc_a);
-        if (t0 + 1 < stop) chain_step<1>(st, op, S, t0 + 1, wbuf, gsrc_a);
-        if (t0 + 2 < stop) chain_step<2>(st, op, S, t0 + 2, wbuf, gsrc_a);
-        if (t0 + 3 < stop) chain_step<3>(st, op, S, t0 + 3, wbuf, gsrc_a);
-        if (t0 + 4 < stop) chain_step<4>(st, op, S, t0 + 4, wbuf, gsrc_a);
-        if (t0 + 5 < stop) chain_step<5>(st, op, S, t0 + 5, wbuf, gsrc_a);
-        if (t0 + 6 < stop) chain_step<6>(st, op, S, t0 + 6, wbuf, gsrc_a);
+        const SlotBlock sblk = slot_block(S, (int)(t0 & (kRB - 1)));
+#define PDB_STEP(SL) \
+    if (SL < kD - 1 && t0 + SL < stop) chain_step<SL>(st, op, sblk, wbuf, gsrc_a);
+        PDB_CHAIN_STEPS(PDB_STEP)
+#undef PDB_STEP
     }
     lds_store(&S.ctl[1], 1);
     if (lane == 0) {
@@ -530,8 +647,10 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
         if (wave == 0) {
             const int64_t done = chain_consumer(op, e_end - pos, d, S, ctrl);
             if (lane_id() == 0) s_done = done;
+        } else if (dense_r0 >= 0) {
+            chain_producer<LOSS, VAL, true>(op, wave - 1, pos, e_end - pos, dense_r0, hot, S);
         } else {
-            chain_producer(op, wave - 1, pos, e_end - pos, dense_r0, hot, S);
+            chain_producer<LOSS, VAL, false>(op, wave - 1, pos, e_end - pos, -1, hot, S);
         }
         __syncthreads();
         for (int i = threadIdx.x; i < hot; i += kBlock) op.w[i] = g_wcache[i];
@@ -620,6 +739,28 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
             ++l;
         }
         if (!single && l < L && !grid_barrier(ctrl, timeout)) return;
+    }
+}
+
+// Counts b in [lo, hi) (as bit patterns) whose recip_normal differs from the
+// IEEE quotient 1/b; keeps the smallest such pattern.
+__global__ __launch_bounds__(kBlock) void k_check_recip(uint32_t lo, uint32_t hi, Ctrl *ctrl) {
+    unsigned long long bad = 0;
+    uint32_t first = 0xFFFFFFFFu;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t u = lo + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; u < hi; u += stride) {
+        const float b = __uint_as_float((uint32_t)u);
+        const float q = recip_normal(b);
+        const float ref = 1.0f / b;
+        if (__float_as_uint(q) != __float_as_uint(ref)) {
+            ++bad;
+            first = min(first, (uint32_t)u);
+        }
+    }
+    if (bad) {
+        atomicAdd((unsigned long long *)&ctrl->stat_cycles, bad);
+        // stat_wait holds 2^32 - 1 - (smallest bad pattern); zero means none
+        atomicMax((unsigned long long *)&ctrl->stat_wait, (unsigned long long)(0xFFFFFFFFu - first));
     }
 }
 
@@ -748,4 +889,29 @@ extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const floa
     if (n == 0) return PDB_OK;
     MfOp op{user, item, rating, U, V, lv->perm, lr, reg};
     return launch_levels(op, lv, n_users + n_items, false, static_cast<Ctrl *>(ws), s);
+}
+
+extern "C" int pdb_check_reciprocal(uint32_t lo_bits, uint32_t hi_bits, uint64_t *mismatches,
+                                    uint32_t *first_bad, void *ws, size_t ws_bytes,
+                                    hipStream_t s) {
+    if (!mismatches || !first_bad || !ws) return PDB_ERR_INVALID_ARG;
+    if (ws_bytes < sizeof(Ctrl)) return PDB_ERR_WORKSPACE;
+    // the reciprocal is defined for b in [1, 2^126)
+    if (lo_bits < 0x3F800000u || hi_bits > 0x7E800000u || lo_bits > hi_bits)
+        return PDB_ERR_INVALID_ARG;
+    Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
+    PDB_LAUNCHED();
+    if (hi_bits > lo_bits) {
+        const uint64_t count = hi_bits - lo_bits;
+        const unsigned grid = (unsigned)std::min<uint64_t>(cdiv((int64_t)count, kBlock), 8192);
+        k_check_recip<<<grid, kBlock, 0, s>>>(lo_bits, hi_bits, ctrl);
+        PDB_LAUNCHED();
+    }
+    Ctrl host;
+    PDB_HIP(hipMemcpyAsync(&host, ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, s));
+    PDB_HIP(hipStreamSynchronize(s));
+    *mismatches = (uint64_t)host.stat_cycles;
+    *first_bad = 0xFFFFFFFFu - (uint32_t)host.stat_wait;
+    return PDB_OK;
 }

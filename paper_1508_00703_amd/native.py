@@ -30,6 +30,7 @@ EXPORTS = (
     "pdb_strerror", "pdb_last_hip_error", "pdb_schedule_workspace_bytes",
     "pdb_epoch_workspace_bytes", "pdb_schedule", "pdb_sgd_epoch", "pdb_mf_epoch",
     "pdb_validate_csr", "pdb_workspace_status", "pdb_transpose", "pdb_prev_writer",
+    "pdb_check_reciprocal",
 )
 
 
@@ -88,6 +89,9 @@ def load() -> ctypes.CDLL:
     lib.pdb_workspace_status.argtypes = [P, P]
     lib.pdb_transpose.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, P, P, sz, P]
     lib.pdb_prev_writer.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, P, P, sz, P]
+    lib.pdb_check_reciprocal.argtypes = [ctypes.c_uint32, ctypes.c_uint32,
+                                         ctypes.POINTER(ctypes.c_uint64),
+                                         ctypes.POINTER(ctypes.c_uint32), P, sz, P]
     for name in EXPORTS:
         if name not in ("pdb_strerror",):
             getattr(lib, name).restype = ctypes.c_int
@@ -269,3 +273,15 @@ def pdb_prev_writer(csr: Csr, n: int, d: int, prev_row, prev_nz=None, ws=None, s
     _check(load().pdb_prev_writer(ctypes.byref(csr.c()), n, d, _ptr(prev_row), _ptr(prev_nz),
                                   _ptr(ws), ws.numel(), _stream(stream, csr.device)),
            "pdb_prev_writer")
+
+
+def pdb_check_reciprocal(lo_bits: int, hi_bits: int, device, ws=None, stream=None):
+    """(mismatches, first mismatching bit pattern or 0xFFFFFFFF)."""
+    if ws is None:
+        ws = workspace(pdb_epoch_workspace_bytes(), device)
+    bad = ctypes.c_uint64(0)
+    first = ctypes.c_uint32(0)
+    _check(load().pdb_check_reciprocal(lo_bits, hi_bits, ctypes.byref(bad), ctypes.byref(first),
+                                       _ptr(ws), ws.numel(), _stream(stream, device)),
+           "pdb_check_reciprocal")
+    return bad.value, first.value

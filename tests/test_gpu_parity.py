@@ -260,3 +260,66 @@ def test_summation_order_adversarial(gpu, name):
     got = gpu_sgd(native, gpu, g, lv, w0=w0)
     assert got[64] == -1.0
     check_sgd(native, gpu, g, lv, w0=w0, tol=float("inf"))
+
+
+def test_reciprocal_exhaustive(gpu):
+    """The division of the logistic step equals IEEE 1/b for every binary32 b
+    in [1, 2^126), the range of 1 + exp(min(-z, 87))."""
+    native = native_mod()
+    bad, first = native.pdb_check_reciprocal(0x3F800000, 0x7E800000, gpu)
+    assert bad == 0, "first mismatch at bits %#x" % first
+    with pytest.raises(native.PdbError):
+        native.pdb_check_reciprocal(0x3F000000, 0x3F800000, gpu)   # below 1
+
+
+@pytest.mark.parametrize("hot", ["0", None])
+def test_extreme_logits(gpu, hot, monkeypatch):
+    """Logistic steps whose logits pass the exponent cap (z < -87), overflow
+    exp (z > 88.7) or round the logistic value to 0 or 1, on both the plain
+    path and the pipeline."""
+    if hot is not None:
+        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
+    native = native_mod()
+    zs = [-1e30, -200.0, -104.5, -88.0, -87.5, -87.0, -86.9, -30.0, -17.0, -1e-3, 0.0, 1e-3,
+          17.0, 30.0, 88.8, 103.9, 104.5, 200.0, 1e30]
+    # a chain through feature 0 (weight 0 throughout: x0 = 0) plus one fresh
+    # feature per example carrying the logit
+    rows = [{0, 1 + i} for i in range(len(zs) * 3)]
+    row_ptr, col = csr_from_rows(rows)
+    n, d = len(rows), len(rows) + 1
+    val = np.zeros(len(col), np.float32)
+    val[1::2] = 1.0
+    w0 = np.zeros(d, np.float32)
+    w0[1:] = np.tile(np.float32(zs), 3)
+    y = np.tile(np.float32([1.0, -1.0, 1.0]), len(zs))[:n]
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=0, lr=np.float32(0.5), val=val, y=y)
+    lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert lv.L_host == n
+    check_sgd(native, gpu, g, lv, w0=w0)
+
+
+@pytest.mark.parametrize("hot", ["0", "3", None])
+def test_width1_pipeline_rows_with_gaps(gpu, hot, monkeypatch):
+    """A run of width-1 levels whose examples are not consecutive rows (rows
+    in between sit on level 1 with fresh features), so the pipeline matches
+    each entry against the preceding examples' entry ranges."""
+    if hot is not None:
+        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
+    native = native_mod()
+    rng = np.random.default_rng(21)
+    rows = []
+    for i in range(600):
+        if i >= 10 and i % 2 == 1:
+            rows.append({5000 + i})
+        else:
+            k = int(rng.integers(1, 40))
+            rows.append({0} | set(rng.choice(np.arange(1, 300), size=k, replace=False).tolist()))
+    row_ptr, col = csr_from_rows(rows)
+    n, d = len(rows), int(col.max()) + 1
+    val = (0.5 * rng.normal(size=len(col))).astype(np.float32)
+    y = np.sign(rng.normal(size=n)).astype(np.float32)
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=0, lr=np.float32(0.05), val=val, y=y)
+    lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
+    widths = np.diff(lv.level_ptr.cpu().numpy()[:lv.L_host + 1])
+    assert widths[0] > 1 and np.all(widths[1:] == 1) and lv.L_host > 300
+    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))

@@ -53,6 +53,30 @@ def test_exp_special_values():
     assert oracle.exp(-103.0) > 0.0                          # subnormal, not flushed
 
 
+def test_sigmoid_against_fp64_logistic():
+    # matched-mode logistic: within 4 ulp of the fp64 value 1/(1+e^-z) (exp
+    # within 2 ulp, then one rounding for 1 + e and one for the division)
+    # wherever -z <= 87; the cap keeps the value at 1/(1 + e^87) below
+    zs = np.concatenate([np.linspace(-87.0, 104.0, 40001), np.linspace(-2, 2, 4001)]).astype(np.float32)
+    for z in zs:
+        ref = np.float32(1.0 / (1.0 + math.exp(-float(z))))
+        assert ulp_distance(oracle.sigmoid(float(z)), ref) <= 4, z
+    floor = oracle.sigmoid(-87.0)
+    assert floor == np.float32(1.0) / (np.float32(1.0) + oracle.exp(87.0))
+    assert np.float32(1.1754944e-38) < floor < np.float32(1.7e-38)  # normal, tiny
+    for z in (-87.5, -100.0, -1e30, -np.inf):
+        assert oracle.sigmoid(z) == floor
+    assert oracle.sigmoid(np.inf) == np.float32(1.0) and oracle.sigmoid(200.0) == np.float32(1.0)
+    assert oracle.sigmoid(0.0) == np.float32(0.5)
+    assert np.isnan(oracle.sigmoid(float("nan")))
+
+
+def test_sigmoid_monotone():
+    zs = np.linspace(-90.0, 20.0, 200001).astype(np.float32)
+    v = np.array([oracle.sigmoid(float(z)) for z in zs], dtype=np.float32)
+    assert np.all(np.diff(v) >= 0)
+
+
 def one_feature_rows(k):
     return np.arange(k + 1, dtype=np.int64), np.zeros(k, dtype=np.int32)
 
