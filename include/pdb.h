@@ -72,9 +72,12 @@ typedef enum pdb_status {
 typedef enum pdb_loss { PDB_LOGISTIC = 0, PDB_SQUARED = 1 } pdb_loss;
 
 typedef enum pdb_sched_method {
-    PDB_SCHED_AUTO = 0,      /* chain-scan relaxation, then dataflow if it has not converged */
+    PDB_SCHED_AUTO = 0,      /* spine when it applies, else dataflow */
     PDB_SCHED_CHAINSCAN = 1, /* chain-scan relaxation until the fixed point */
-    PDB_SCHED_DATAFLOW = 2   /* each example waits for its previous writers' levels */
+    PDB_SCHED_DATAFLOW = 2,  /* each example waits for its previous writers' levels */
+    PDB_SCHED_SPINE = 3      /* the most frequent feature's rows as a spine: applies when that
+                                feature misses at most 1024 rows whose entries number at most
+                                4096; otherwise dataflow runs (method_used says which) */
 } pdb_sched_method;
 
 /* Sparse examples in CSR form (Definition 1: the immutable data set D). */
@@ -102,7 +105,7 @@ typedef struct pdb_levels {
 /* Optional host-side report of pdb_schedule. */
 typedef struct pdb_schedule_info {
     int32_t method_used;  /* pdb_sched_method that produced the levels */
-    int32_t rounds;       /* chain-scan rounds run */
+    int32_t rounds;       /* chain-scan rounds, or spine solver rounds */
     int64_t n_levels;     /* L */
     int64_t max_width;    /* largest level width */
 } pdb_schedule_info;

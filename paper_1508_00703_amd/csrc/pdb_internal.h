@@ -62,7 +62,14 @@ struct Ctrl {
     // width-1 pipeline counters (clock cycles of the consumer wave): total,
     // waiting for staged examples, examples run, runs started
     long long stat_cycles, stat_wait, stat_rows, stat_runs;
-    int pad[44];
+    // spine levels: (count << 32) | (2^32 - 1 - feature) of the most frequent
+    // feature; exceptional rows found; the solver's outcome
+    unsigned long long top_feature;
+    int spine_n_e;
+    int spine_status;  // 0 solved, 1 too many exceptional rows or entries
+    int spine_rounds;
+    int pad1;
+    int pad[38];
     float sink[64];  // target of stores from lanes with nothing to store
 };
 static_assert(sizeof(Ctrl) == 512, "Ctrl is two 256-byte lines");
@@ -79,8 +86,9 @@ struct SchedWs {
     uint32_t *kA, *vA, *kB, *vB;  // [M] radix double buffers, M = max(nnz, n, 1)
     uint32_t *hist;     // [256 * tiles(M)]
     uint32_t *scan_tmp; // [scan partials]
-    int32_t *prev_row;  // [nnz]
-    int32_t *cand;      // [nnz]
+    int32_t *pn;        // [nnz] previous-writer entries when the caller passes no prev_nz
+    int32_t *cand;      // [nnz] chain-scan candidates, or previous-writer rows for dataflow
+    void *spine;        // spine solver state (fixed size)
     int2 *seg_agg;      // [tiles(nnz)]
     int2 *seg_carry;    // [tiles(nnz)]
     int64_t *col_ptr;   // [d+1]

@@ -14,6 +14,9 @@
 //       lists in example order;
 //   K2  previous writer of every entry = its predecessor in its feature's list;
 //   K3  levels, by one of
+//         spine: when one feature is held by all rows but a few, levels
+//         along that feature's rows follow from a prefix maximum over the
+//         few side inputs from the other rows (see the spine kernels);
 //         chain-scan relaxation: along every feature's list the level grows
 //         by at least one per step, so a segmented max-scan of
 //         (level - position) per feature followed by a max per example
@@ -105,30 +108,37 @@ __global__ __launch_bounds__(kBlock) void k_row_index(const int64_t *__restrict_
     }
 }
 
-// K2: previous writer of every entry from the feature-sorted order.
+// K2: previous writer of every entry from the feature-sorted order: pn[p] =
+// the entry just before p in p's feature list (its CSR index), -1 at a head.
 __global__ __launch_bounds__(kBlock) void k_prev_writer(
     const uint32_t *__restrict__ skeys, const uint32_t *__restrict__ svals, int64_t nnz,
-    int64_t d, const int32_t *__restrict__ row_idx, int32_t *__restrict__ prev_row,
-    int32_t *__restrict__ prev_nz, int64_t *__restrict__ col_ptr, int32_t *__restrict__ csc_row) {
+    int64_t d, const int32_t *__restrict__ row_idx, int32_t *__restrict__ pn,
+    int64_t *__restrict__ col_ptr, int32_t *__restrict__ csc_row) {
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
          q += (int64_t)gridDim.x * blockDim.x) {
         const uint32_t f = skeys[q];
         const uint32_t p = svals[q];
         const bool head = (q == 0) || skeys[q - 1] != f;
+        pn[p] = head ? -1 : (int32_t)svals[q - 1];
         if (head) {
-            prev_row[p] = -1;
-            if (prev_nz) prev_nz[p] = -1;
             const int64_t lo = (q == 0) ? 0 : (int64_t)skeys[q - 1] + 1;
             const int64_t hi = min((int64_t)f, d - 1);  // columns >= d: malformed input
             for (int64_t g = lo; g <= hi; ++g) col_ptr[g] = q;
-        } else {
-            const uint32_t pp = svals[q - 1];
-            prev_row[p] = row_idx[pp];
-            if (prev_nz) prev_nz[p] = (int32_t)pp;
         }
         if (q == nnz - 1)
             for (int64_t g = (int64_t)f + 1; g <= d; ++g) col_ptr[g] = nnz;
         if (csc_row) csc_row[q] = row_idx[p];
+    }
+}
+
+// Previous-writer row of every entry: prev_row[p] = row of pn[p], -1 if none.
+__global__ __launch_bounds__(kBlock) void k_prev_row(const int32_t *__restrict__ pn, int64_t nnz,
+                                                     const int32_t *__restrict__ row_idx,
+                                                     int32_t *__restrict__ prev_row) {
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < nnz;
+         p += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t q = pn[p];
+        prev_row[p] = q < 0 ? -1 : row_idx[q];
     }
 }
 
@@ -303,6 +313,316 @@ __global__ __launch_bounds__(kBlock) void k_max_level(const int32_t *__restrict_
     if (lane_id() == 0 && m > 0) atomicMax(&ctrl->max_level, m);
 }
 
+// ---- K3 spine --------------------------------------------------------------
+// When one feature f* is held by all rows but a few (the exceptional rows E),
+// the rows holding it form a spine c_0 < c_1 < ... < c_{K-1}.  Consecutive
+// spine rows share f*, so level(c_k) >= level(c_{k-1}) + 1; a previous writer
+// of c_k that lies on the spine is some c_j, j < k, whose level is below
+// level(c_{k-1}), so it cannot raise level(c_k).  Only previous writers in E
+// can, through side edges e -> c_j (e's entry on some feature is followed in
+// that feature's list by c_j's).  Hence
+//   level(c_k) = k + M(k),
+//   M(k) = max(1, max over side edges e -> c_j with j <= k of level(e) + 1 - j),
+// and level(e) = 1 + max over e's previous writers (spine rows by the first
+// formula, exceptional rows directly).  Starting from level(e) = 1 and
+// applying both formulas repeatedly raises lower bounds to the least fixed
+// point, the exact levels, in at most |E| + 1 rounds.  One block does this on
+// the exceptional rows; a grid pass then writes the spine's levels.
+constexpr int kSpineMaxE = 1024;    // exceptional rows
+constexpr int kSpineMaxEnt = 4096;  // their stored entries
+constexpr int kSpineThreads = 1024;
+
+struct SpineWs {
+    int e_rows[kSpineMaxE];       // exceptional rows (ascending once solved)
+    int e_lv[kSpineMaxE];         // their levels
+    int ent_pred[kSpineMaxEnt];   // per entry of an exceptional row: spine index of its
+                                  // previous writer, -1 - (exceptional index), or kNone
+    int ent_kt[kSpineMaxEnt];     // spine index of the entry's next writer, -1 if off the spine
+    int ent_owner[kSpineMaxEnt];  // exceptional index of the entry's row
+    int side_kt[kSpineMaxEnt];    // side edges sorted by spine index
+    int side_pm[kSpineMaxEnt];    // prefix max of level(e) + 1 - kt along them
+    int n_e, n_side, pad[2];
+};
+
+__global__ __launch_bounds__(kBlock) void k_top_feature(const int64_t *__restrict__ col_ptr,
+                                                        int64_t d, Ctrl *ctrl) {
+    unsigned long long best = 0;
+    for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
+         f += (int64_t)gridDim.x * blockDim.x) {
+        const unsigned long long cnt = (unsigned long long)(col_ptr[f + 1] - col_ptr[f]);
+        best = max(best, (cnt << 32) | (0xFFFFFFFFull - (unsigned long long)f));
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) best = max(best, (unsigned long long)__shfl_xor(best, off));
+    if (lane_id() == 0 && best > 0) atomicMax(&ctrl->top_feature, best);
+}
+
+__global__ __launch_bounds__(kBlock) void k_spine_rows(const uint32_t *__restrict__ svals,
+                                                       const int32_t *__restrict__ row_idx,
+                                                       int64_t lo, int64_t K,
+                                                       int32_t *__restrict__ rows) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < K;
+         k += (int64_t)gridDim.x * blockDim.x)
+        rows[k] = row_idx[svals[lo + k]];
+}
+
+// The exceptional rows are the gaps of the spine: rows strictly between
+// consecutive spine rows, before the first and after the last.
+__global__ __launch_bounds__(kBlock) void k_spine_gaps(const int32_t *__restrict__ rows, int64_t K,
+                                                       int64_t n, SpineWs *sp) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k <= K;
+         k += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t prev = k > 0 ? rows[k - 1] : -1;
+        const int64_t cur = k < K ? rows[k] : n;
+        const int64_t g = cur - prev - 1;
+        if (g <= 0) continue;
+        const int base = atomicAdd(&sp->n_e, (int)min(g, (int64_t)INT_MAX / 2));
+        for (int64_t j = 0; j < g && base + j < kSpineMaxE; ++j)
+            sp->e_rows[base + j] = (int)(prev + 1 + j);
+    }
+}
+
+// index of row r in the ascending spine rows[0..K), or -1
+__device__ __forceinline__ int64_t spine_find(const int32_t *rows, int64_t K, int64_t r) {
+    int64_t lo = 0, hi = K;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (rows[mid] < r) lo = mid + 1;
+        else hi = mid;
+    }
+    return (lo < K && rows[lo] == r) ? lo : -1;
+}
+
+// last j < cnt with kt[j] <= k, or -1
+__device__ __forceinline__ int last_at_most(const int *kt, int cnt, int64_t k) {
+    int lo = 0, hi = cnt;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (kt[mid] <= k) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo - 1;
+}
+
+// Block-wide exclusive max-scan of one value per thread (INT_MIN first).
+__device__ int block_excl_max(int v, int *s_wave) {
+    const int lane = lane_id(), wave = wave_in_block();
+    int inc = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(inc, off);
+        if (lane >= off) inc = max(inc, y);
+    }
+    if (lane == kWave - 1) s_wave[wave] = inc;
+    __syncthreads();
+    int before = INT_MIN;
+    for (int w = 0; w < wave; ++w) before = max(before, s_wave[w]);
+    __syncthreads();
+    const int prev = __shfl_up(inc, 1);
+    return lane == 0 ? before : max(before, prev);
+}
+
+__device__ int block_excl_sum(int v, int *s_wave, int *total) {
+    const int lane = lane_id(), wave = wave_in_block();
+    int inc = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(inc, off);
+        if (lane >= off) inc += y;
+    }
+    if (lane == kWave - 1) s_wave[wave] = inc;
+    __syncthreads();
+    int before = 0, all = 0;
+    for (int w = 0; w < kSpineThreads / kWave; ++w) {
+        if (w < wave) before += s_wave[w];
+        all += s_wave[w];
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - v;
+}
+
+__global__ __launch_bounds__(kSpineThreads) void k_spine_solve(
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    const int32_t *__restrict__ pn, const int32_t *__restrict__ row_idx,
+    const uint32_t *__restrict__ svals, const int64_t *__restrict__ col_ptr,
+    const int32_t *__restrict__ rows, int64_t K, SpineWs *sp, Ctrl *ctrl, int max_rounds) {
+    __shared__ int s_e[kSpineMaxE];
+    __shared__ int s_beg[kSpineMaxE + 1];
+    __shared__ int s_lv[kSpineMaxE];
+    __shared__ int s_skt[kSpineMaxEnt];
+    __shared__ int s_pm[kSpineMaxEnt];
+    __shared__ int s_wave[kSpineThreads / kWave];
+    const int tid = threadIdx.x;
+    const int n_e = sp->n_e;
+    if (n_e > kSpineMaxE) {
+        if (tid == 0) ctrl->spine_status = 1;
+        return;
+    }
+    // the exceptional rows in ascending order (they are distinct)
+    const int mine = tid < n_e ? sp->e_rows[tid] : INT_MAX;
+    s_lv[tid] = mine;
+    __syncthreads();
+    if (tid < n_e) {
+        int rank = 0;
+        for (int j = 0; j < n_e; ++j) rank += s_lv[j] < mine;
+        s_e[rank] = mine;
+    }
+    __syncthreads();
+    // entry offsets
+    const int m = tid < n_e ? (int)(row_ptr[s_e[tid] + 1] - row_ptr[s_e[tid]]) : 0;
+    int n_ent = 0;
+    const int beg = block_excl_sum(m, s_wave, &n_ent);
+    if (n_ent > kSpineMaxEnt) {
+        if (tid == 0) ctrl->spine_status = 1;
+        return;
+    }
+    s_beg[tid] = beg;
+    if (tid == 0) s_beg[n_e] = n_ent;
+    __syncthreads();
+    // previous writer and next writer of every entry
+    for (int idx = tid; idx < n_ent; idx += kSpineThreads) {
+        int lo = 0, hi = n_e;  // owner: last i with s_beg[i] <= idx
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (s_beg[mid] <= idx) lo = mid + 1;
+            else hi = mid;
+        }
+        const int i = lo - 1;
+        const int64_t p = row_ptr[s_e[i]] + (idx - s_beg[i]);
+        int pred = kNone;
+        const int32_t q = pn[p];
+        if (q >= 0) {
+            const int r = row_idx[q];
+            const int64_t kb = spine_find(rows, K, r);
+            if (kb >= 0) {
+                pred = (int)kb;
+            } else {
+                int a = 0, b = n_e;  // r is an earlier exceptional row
+                while (a < b) {
+                    const int mid = (a + b) >> 1;
+                    if (s_e[mid] < r) a = mid + 1;
+                    else b = mid;
+                }
+                pred = -1 - a;
+            }
+        }
+        const int f = col[p];
+        int64_t a = col_ptr[f], b = col_ptr[f + 1];
+        const int64_t end = b;
+        while (a < b) {  // position of entry p in its feature's list
+            const int64_t mid = (a + b) >> 1;
+            if ((int64_t)svals[mid] < p) a = mid + 1;
+            else b = mid;
+        }
+        int kt = -1;
+        if (a + 1 < end) kt = (int)spine_find(rows, K, row_idx[svals[a + 1]]);
+        sp->ent_pred[idx] = pred;
+        sp->ent_kt[idx] = kt;
+        sp->ent_owner[idx] = i;
+    }
+    __syncthreads();
+    // side edges sorted by (spine index, entry)
+    int n_side = 0;
+    for (int idx = tid; idx < n_ent; idx += kSpineThreads) {
+        const int kt = sp->ent_kt[idx];
+        if (kt < 0) continue;
+        int rank = 0;
+        for (int j = 0; j < n_ent; ++j) {
+            const int kj = sp->ent_kt[j];
+            rank += kj >= 0 && (kj < kt || (kj == kt && j < idx));
+        }
+        s_skt[rank] = kt;
+        sp->side_kt[rank] = kt;
+        s_pm[rank] = sp->ent_owner[idx];  // owner for now
+    }
+    {
+        int cnt = 0;
+        for (int idx = tid; idx < n_ent; idx += kSpineThreads) cnt += sp->ent_kt[idx] >= 0;
+        int total = 0;
+        block_excl_sum(cnt, s_wave, &total);
+        n_side = total;
+    }
+    __syncthreads();
+    // owners of the sorted side edges, kept while the prefix max is recomputed
+    constexpr int kPer = kSpineMaxEnt / kSpineThreads;
+    int owner[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int e = tid * kPer + j;
+        owner[j] = e < n_side ? s_pm[e] : 0;
+    }
+    s_lv[tid] = 1;
+    __syncthreads();
+    int rounds = 0;
+    bool converged = false;
+    while (rounds < max_rounds) {
+        ++rounds;
+        // prefix max of level(owner) + 1 - kt over the sorted side edges
+        // (thread tid holds edges tid * kPer .. tid * kPer + kPer - 1)
+        int v[kPer];
+        int run = INT_MIN;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int e = tid * kPer + j;
+            run = max(run, e < n_side ? s_lv[owner[j]] + 1 - s_skt[e] : INT_MIN);
+            v[j] = run;
+        }
+        const int carry = block_excl_max(run, s_wave);
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int e = tid * kPer + j;
+            if (e < n_side) s_pm[e] = max(v[j], carry);
+        }
+        __syncthreads();
+        // levels of the exceptional rows from the current bounds
+        int nl = 0;
+        if (tid < n_e) {
+            nl = 1;
+            for (int idx = s_beg[tid]; idx < s_beg[tid + 1]; ++idx) {
+                const int pred = sp->ent_pred[idx];
+                if (pred >= 0) {
+                    const int j = last_at_most(s_skt, n_side, pred);
+                    const int M = max(1, j >= 0 ? s_pm[j] : INT_MIN);
+                    nl = max(nl, pred + M + 1);
+                } else if (pred != kNone) {
+                    nl = max(nl, s_lv[-1 - pred] + 1);
+                }
+            }
+        }
+        const bool ch = tid < n_e && nl != s_lv[tid];
+        __syncthreads();
+        if (tid < n_e) s_lv[tid] = nl;
+        if (!__syncthreads_or(ch)) {
+            converged = true;
+            break;
+        }
+    }
+    if (tid < n_e) {
+        sp->e_rows[tid] = s_e[tid];
+        sp->e_lv[tid] = s_lv[tid];
+    }
+    for (int e = tid; e < n_side; e += kSpineThreads) sp->side_pm[e] = s_pm[e];
+    if (tid == 0) {
+        sp->n_side = n_side;
+        ctrl->spine_rounds = rounds;
+        ctrl->spine_status = converged ? 0 : 2;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_spine_write(const int32_t *__restrict__ rows, int64_t K,
+                                                        const SpineWs *__restrict__ sp,
+                                                        int32_t *__restrict__ level) {
+    const int n_side = sp->n_side;
+    const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    for (int64_t k = i0; k < K; k += (int64_t)gridDim.x * blockDim.x) {
+        const int j = last_at_most(sp->side_kt, n_side, k);
+        const int M = max(1, j >= 0 ? sp->side_pm[j] : INT_MIN);
+        level[rows[k]] = (int32_t)(k + M);
+    }
+    if (i0 < sp->n_e) level[sp->e_rows[i0]] = sp->e_lv[i0];
+}
+
 // ---- K4 ------------------------------------------------------------------
 __global__ void k_level_keys(const int32_t *__restrict__ level, int64_t n,
                              uint32_t *__restrict__ keys) {
@@ -363,8 +683,9 @@ int check_sizes(int64_t n, int64_t d, int64_t nnz) {
     return PDB_OK;
 }
 
-// K0 + K1 + K2 into the workspace.  col_ptr, csc_row, prev_nz optional.
-int build_conflicts(const pdb_csr *csr, int64_t n, int64_t d, SchedWs &w, int32_t *prev_nz,
+// K0 + K1 + K2 into the workspace: previous-writer entries into pn, col_ptr,
+// and csc_row when not null.
+int build_conflicts(const pdb_csr *csr, int64_t n, int64_t d, SchedWs &w, int32_t *pn,
                     int64_t *col_ptr, int32_t *csc_row, const uint32_t **skeys_out,
                     const uint32_t **svals_out, hipStream_t s) {
     const int64_t nnz = csr->nnz;
@@ -379,7 +700,7 @@ int build_conflicts(const pdb_csr *csr, int64_t n, int64_t d, SchedWs &w, int32_
                              w.kA, w.vA, w.kB, w.vB, w.hist, w.scan_tmp, &sk, &sv, s));
     if (nnz > 0) {
         k_prev_writer<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(
-            sk, sv, nnz, d, w.row_idx, w.prev_row, prev_nz, col_ptr, csc_row);
+            sk, sv, nnz, d, w.row_idx, pn, col_ptr, csc_row);
         PDB_LAUNCHED();
     } else {
         k_fill_i64<<<grid_for(d + 1, kBlock, 4096), kBlock, 0, s>>>(col_ptr, d + 1, 0);
@@ -412,8 +733,9 @@ SchedWs sched_ws_layout(void *base, int64_t n, int64_t d, int64_t nnz) {
     w.vB = reinterpret_cast<uint32_t *>(take(M * 4));
     w.hist = reinterpret_cast<uint32_t *>(take(256 * tilesM * 4));
     w.scan_tmp = reinterpret_cast<uint32_t *>(take((int64_t)scan_tmp_elems(256 * tilesM) * 4));
-    w.prev_row = reinterpret_cast<int32_t *>(take(std::max<int64_t>(nnz, 1) * 4));
+    w.pn = reinterpret_cast<int32_t *>(take(std::max<int64_t>(nnz, 1) * 4));
     w.cand = reinterpret_cast<int32_t *>(take(std::max<int64_t>(nnz, 1) * 4));
+    w.spine = take(sizeof(SpineWs));
     w.seg_agg = reinterpret_cast<int2 *>(take(tilesZ * 8));
     w.seg_carry = reinterpret_cast<int2 *>(take(tilesZ * 8));
     w.col_ptr = reinterpret_cast<int64_t *>(take((d + 1) * 8));
@@ -453,7 +775,7 @@ extern "C" int pdb_transpose(const pdb_csr *csr, int64_t n, int64_t d, int64_t *
     if (rc != PDB_OK) return rc;
     if (!col_ptr || (csr->nnz > 0 && !csc_row)) return PDB_ERR_INVALID_ARG;
     const uint32_t *sk, *sv;
-    rc = build_conflicts(csr, n, d, w, nullptr, col_ptr, csc_row, &sk, &sv, stream);
+    rc = build_conflicts(csr, n, d, w, w.pn, col_ptr, csc_row, &sk, &sv, stream);
     if (rc != PDB_OK) return rc;
     PDB_HIP(hipStreamSynchronize(stream));
     return PDB_OK;
@@ -465,12 +787,15 @@ extern "C" int pdb_prev_writer(const pdb_csr *csr, int64_t n, int64_t d, int32_t
     int rc = sched_common_checks(csr, n, d, ws, ws_bytes, &w);
     if (rc != PDB_OK) return rc;
     if (csr->nnz > 0 && !prev_row) return PDB_ERR_INVALID_ARG;
+    int32_t *pn = prev_nz ? prev_nz : w.pn;
     const uint32_t *sk, *sv;
-    rc = build_conflicts(csr, n, d, w, prev_nz, w.col_ptr, nullptr, &sk, &sv, stream);
+    rc = build_conflicts(csr, n, d, w, pn, w.col_ptr, nullptr, &sk, &sv, stream);
     if (rc != PDB_OK) return rc;
-    if (csr->nnz > 0)
-        PDB_HIP(hipMemcpyAsync(prev_row, w.prev_row, csr->nnz * 4, hipMemcpyDeviceToDevice,
-                               stream));
+    if (csr->nnz > 0) {
+        k_prev_row<<<grid_for(csr->nnz, kBlock, 1 << 16), kBlock, 0, stream>>>(pn, csr->nnz,
+                                                                              w.row_idx, prev_row);
+        PDB_LAUNCHED();
+    }
     PDB_HIP(hipStreamSynchronize(stream));
     return PDB_OK;
 }
@@ -484,7 +809,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     if (rc != PDB_OK) return rc;
     if (!lv || !lv->level_ptr || !lv->n_levels || (n > 0 && (!lv->level || !lv->perm)))
         return PDB_ERR_INVALID_ARG;
-    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_DATAFLOW) return PDB_ERR_INVALID_ARG;
+    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_SPINE) return PDB_ERR_INVALID_ARG;
     const int64_t nnz = csr->nnz;
     Ctrl host{};
     k_ctrl_init<<<1, 64, 0, s>>>(w.ctrl);
@@ -501,36 +826,67 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     }
 
     // K0-K2
+    int32_t *pn = lv->prev_nz ? lv->prev_nz : w.pn;
     const uint32_t *sk, *sv;
-    rc = build_conflicts(csr, n, d, w, lv->prev_nz, w.col_ptr, nullptr, &sk, &sv, s);
+    rc = build_conflicts(csr, n, d, w, pn, w.col_ptr, nullptr, &sk, &sv, s);
     if (rc != PDB_OK) return rc;
+    // the radix buffer pair that does not hold the sorted entries is free
+    int32_t *free_k = reinterpret_cast<int32_t *>((sk == w.kA) ? w.kB : w.kA);
+    const int64_t timeout = spin_timeout_ticks();
 
-    // which method: chain-scan converges in about (examples not holding the
-    // most frequent feature) + 1 rounds; use it only when that is small.
+    // which method: the spine when the most frequent feature misses at most
+    // kSpineMaxE rows, else dataflow
     int use = method;
     int rounds = 0;
-    if (method == PDB_SCHED_AUTO) {
-        k_max_diff<<<grid_for(d, kBlock, 4096), kBlock, 0, s>>>(w.col_ptr, d, w.ctrl);
+    int64_t top_count = 0, top_f = 0;
+    if (method == PDB_SCHED_AUTO || method == PDB_SCHED_SPINE) {
+        k_top_feature<<<grid_for(d, kBlock, 4096), kBlock, 0, s>>>(w.col_ptr, d, w.ctrl);
         PDB_LAUNCHED();
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
-        use = (n - host.max_width <= 64) ? PDB_SCHED_CHAINSCAN : PDB_SCHED_DATAFLOW;
+        top_count = (int64_t)(host.top_feature >> 32);
+        top_f = (int64_t)(0xFFFFFFFFull - (host.top_feature & 0xFFFFFFFFull));
+        const bool fits = top_count > 0 && n - top_count <= kSpineMaxE;
+        use = fits ? PDB_SCHED_SPINE : PDB_SCHED_DATAFLOW;
     }
-    const int64_t timeout = spin_timeout_ticks();
+
+    if (use == PDB_SCHED_SPINE) {
+        SpineWs *sp = static_cast<SpineWs *>(w.spine);
+        int32_t *rows = free_k;  // the spine rows, ascending
+        // spine rows: the entries of top_f in feature order
+        int64_t lo = 0;
+        PDB_HIP(hipMemcpyAsync(&lo, w.col_ptr + top_f, sizeof(lo), hipMemcpyDeviceToHost, s));
+        PDB_HIP(hipStreamSynchronize(s));
+        k_spine_rows<<<grid_for(top_count, kBlock, 65536), kBlock, 0, s>>>(sv, w.row_idx, lo,
+                                                                            top_count, rows);
+        k_fill_i32<<<1, 64, 0, s>>>(&sp->n_e, 4, 0);
+        k_spine_gaps<<<grid_for(top_count + 1, kBlock, 65536), kBlock, 0, s>>>(rows, top_count, n,
+                                                                                sp);
+        k_spine_solve<<<1, kSpineThreads, 0, s>>>(csr->row_ptr, csr->col, pn, w.row_idx, sv,
+                                                  w.col_ptr, rows, top_count, sp, w.ctrl,
+                                                  kSpineMaxE + 2);
+        PDB_LAUNCHED();
+        rc = read_ctrl(w.ctrl, &host, s);
+        if (rc != PDB_OK) return rc;
+        if (host.spine_status == 0) {
+            k_spine_write<<<grid_for(std::max<int64_t>(top_count, kSpineMaxE), kBlock, 65536),
+                            kBlock, 0, s>>>(rows, top_count, sp, lv->level);
+            PDB_LAUNCHED();
+            rounds = host.spine_rounds;
+        } else {
+            use = PDB_SCHED_DATAFLOW;  // too many exceptional rows or entries
+        }
+    }
 
     if (use == PDB_SCHED_CHAINSCAN) {
-        // csc_row[q] = row of the q-th entry in feature order; the free radix
-        // key buffer holds it (the sorted pair lives in the other pair)
-        uint32_t *free_k = (sk == w.kA) ? w.kB : w.kA;
-        int32_t *crow = reinterpret_cast<int32_t *>(free_k);
+        // csc_row[q] = row of the q-th entry in feature order
+        int32_t *crow = free_k;
         if (nnz > 0)
             k_csc_row<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(sv, nnz, w.row_idx, crow);
         k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 1);
         PDB_LAUNCHED();
         const int64_t tiles = cdiv(std::max<int64_t>(nnz, 1), kTile);
-        const int64_t max_rounds = (method == PDB_SCHED_AUTO) ? 256 : n + 1;
-        bool converged = false;
-        while (rounds < max_rounds) {
+        while (true) {
             k_fill_i32<<<1, 64, 0, s>>>(&w.ctrl->changed, 1, 0);
             if (nnz > 0) {
                 k_cs_reduce<<<(unsigned)tiles, kBlock, 0, s>>>(sk, crow, lv->level, nnz,
@@ -546,18 +902,20 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
             ++rounds;
             rc = read_ctrl(w.ctrl, &host, s);
             if (rc != PDB_OK) return rc;
-            if (!host.changed) {
-                converged = true;
-                break;
-            }
+            if (!host.changed) break;  // at most n + 1 rounds
         }
-        if (!converged) use = PDB_SCHED_DATAFLOW;
     }
     if (use == PDB_SCHED_DATAFLOW) {
+        // previous-writer rows into cand
+        if (nnz > 0) {
+            k_prev_row<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(pn, nnz, w.row_idx,
+                                                                        w.cand);
+            PDB_LAUNCHED();
+        }
         k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 0);
         k_fill_i32<<<1, 64, 0, s>>>(reinterpret_cast<int32_t *>(&w.ctrl->ticket), 2, 0);
         PDB_LAUNCHED();
-        k_levels_dataflow<<<device_cus() * 4, kBlock, 0, s>>>(csr->row_ptr, w.prev_row, n,
+        k_levels_dataflow<<<device_cus() * 4, kBlock, 0, s>>>(csr->row_ptr, w.cand, n,
                                                               lv->level, w.ctrl, timeout);
         PDB_LAUNCHED();
         rc = read_ctrl(w.ctrl, &host, s);

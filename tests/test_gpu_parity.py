@@ -11,7 +11,7 @@ from pdbtest import check_mf, check_schedule, check_sgd, csr_from_rows, gpu_sche
 
 pytestmark = pytest.mark.gpu
 
-METHODS = [0, 1, 2]  # auto, chain-scan, dataflow
+METHODS = [0, 1, 2, 3]  # auto, chain-scan, dataflow, spine
 
 
 def native_mod():
@@ -323,3 +323,54 @@ def test_width1_pipeline_rows_with_gaps(gpu, hot, monkeypatch):
     widths = np.diff(lv.level_ptr.cpu().numpy()[:lv.L_host + 1])
     assert widths[0] > 1 and np.all(widths[1:] == 1) and lv.L_host > 300
     check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
+
+
+def test_spine_selection_and_fallback(gpu):
+    """Auto takes the spine when the most frequent feature misses few rows;
+    with more exceptional rows (or entries) than the solver holds, both auto
+    and an explicit spine request run dataflow.  Levels are exact each time."""
+    native = native_mod()
+    rng = np.random.default_rng(5)
+    # feature 0 in all rows but every 37th; the others chain through 1..6
+    rows = [({0} if i % 37 else set()) | {1 + int(rng.integers(0, 6)), 10 + int(rng.integers(0, 500))}
+            for i in range(3000)]
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1
+    _, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert info["method_used"] == 3 and info["rounds"] >= 1
+    _, info = check_schedule(native, gpu, row_ptr, col, d, 3)
+    assert info["method_used"] == 3
+    # 1500 exceptional rows
+    rows = [{0, 1 + i % 5} if i % 2 else {6 + i % 9} for i in range(3000)]
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1
+    _, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert info["method_used"] == 2
+    _, info = check_schedule(native, gpu, row_ptr, col, d, 3)
+    assert info["method_used"] == 2
+    # 100 exceptional rows with 60 entries each
+    rows = [{0, 1 + i % 3} if i % 30 else set(range(100 + i % 7, 160 + i % 7)) for i in range(3000)]
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1
+    _, info = check_schedule(native, gpu, row_ptr, col, d, 3)
+    assert info["method_used"] == 2
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_spine_random_exceptions(gpu, seed):
+    """Spine levels where exceptional rows feed the spine and each other:
+    random rows over a few features, feature 0 added to all but ~1%."""
+    native = native_mod()
+    rng = np.random.default_rng(100 + seed)
+    n, d = 5000, 6
+    rows = []
+    for i in range(n):
+        r = set(rng.choice(np.arange(1, d), size=int(rng.integers(0, 4)), replace=False).tolist())
+        if rng.random() > 0.01:
+            r.add(0)
+        rows.append(r)
+    row_ptr, col = csr_from_rows(rows)
+    lv, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert info["method_used"] == 3
+    # exceptional rows raised the spine above its own length
+    assert lv.L_host > np.bincount(col).max()
