@@ -30,6 +30,7 @@
 // between two steps is arithmetic.  Features written a few examples back come
 // from a small LDS ring; all other cold features are prefetched from global
 // memory kD examples ahead (their last writer finished before the prefetch).
+#include <climits>
 #include <cstdlib>
 
 #include "pdb_internal.h"
@@ -246,8 +247,8 @@ struct ChainShared {
     // consecutive slots without wrapping.
     uint4 st[(kRB + 2) * 64];
     float mt_t[kRB + 2];  // target: [y > 0] (logistic) or y (least squares)
-    int mt_m[kRB];        // number of entries
-    int seq[kRB];         // position staged in the slot (-1 none)
+    int seq[kRB];         // position t staged in the slot, ~t when its example has more
+                          // than 64 entries, INT_MIN none
     int ctl[4];           // [0] consumer no longer needs positions < ctl[0]; [1] stop
     float ring[kRing];    // new weights of cold features written within kD examples
     float lsink[64];      // LDS write target of lanes without an entry
@@ -426,12 +427,13 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
             // the label load is never moved into a branch
             const bool in_batch = lane >= kD && lane < kD + kPB;
             const int slot = sb + lane - kD;
+            const int64_t q = t0 - kD + lane;  // the position this lane describes
             lds_write(in_batch ? lds_addr(&S.mt_t[slot]) : lsink_a, tg);
-            lds_write(in_batch ? lds_addr((const float *)&S.mt_m[slot]) : lsink_a, __int_as_float(m));
             lds_write((in_batch && slot < 2) ? lds_addr(&S.mt_t[kRB + slot]) : lsink_a, tg);
+            compiler_fence();  // LDS executes one wave's operations in order
+            if (in_batch && q < len)
+                lds_store(&S.seq[slot], m > kWave ? ~(int)q : (int)q);
         }
-        compiler_fence();  // LDS executes one wave's operations in order
-        if (lane < kPB && t0 + lane < len) lds_store(&S.seq[sb + lane], (int)(t0 + lane));
         compiler_fence();
     }
 }
@@ -442,10 +444,13 @@ __device__ __forceinline__ int64_t wait_staged(ChainShared &S, int64_t lo, int64
                                                long long *waited) {
     const int64_t t = lo + lane_id();
     const int slot = (int)(t & (kRB - 1));
+    const bool want = t < hi;
     long long c0 = 0;
     bool first = true;
+    int v;
     for (;;) {
-        const bool ok = t >= hi || lds_load(&S.seq[slot]) == (int)t;
+        v = lds_load(&S.seq[slot]);
+        const bool ok = !want || v == (int)t || v == ~(int)t;
         if (__ballot(!ok) == 0ull) break;
         if (first) c0 = (long long)__builtin_readcyclecounter();
         first = false;
@@ -453,7 +458,7 @@ __device__ __forceinline__ int64_t wait_staged(ChainShared &S, int64_t lo, int64
     }
     if (!first) *waited += (long long)__builtin_readcyclecounter() - c0;
     compiler_fence();
-    const unsigned long long longrow = __ballot(t < hi && S.mt_m[slot] > kWave);
+    const unsigned long long longrow = __ballot(want && v == ~(int)t);
     return longrow ? lo + __ffsll(longrow) - 1 : INT64_MAX;
 }
 
@@ -502,64 +507,76 @@ struct ChainState {
     float cur_v, cur_fw, cur_fx;  // example t's weight, or the forwarded (w_old, x) pair
     bool cur_fwd;
     float s_prev;                 // step of example t-1
+    // example t-1's old weight, x and write targets: its new weights are
+    // computed and written at the start of step t
+    float p_wold, p_x;
+    unsigned p_l, p_g;
     float gv[kD];                 // prefetched cold values, example at t mod kD
     unsigned pf[kD];              // prefetch offsets of the next examples
 };
 
-// One example, position t = t0 + SL with sb = t0 mod kRB.  Every memory
-// operation is issued unconditionally, so the count of outstanding loads and
-// stores is the same on every path and the waits stay exact.  Issue order:
-// the LDS reads and lane permutes for example t+1 go out first, the
-// arithmetic of example t's step runs while they are in flight, and only then
-// are their results used (scheduling barriers keep the compiler from
-// reordering).
+// One example, position t = t0 + SL with its staged slots in sblk.  Every
+// memory operation is issued unconditionally, so the count of outstanding
+// loads and stores is the same on every path and the waits stay exact.
+// Only the chain s(t-1) -> w_old -> z -> s(t) is serial; the writes of
+// example t-1 and the reads for example t+1 (which depend on values known
+// early in the step) are free to fill its stalls.  Order that matters: the
+// writes of t-1 precede the reads for t+1 (a value t-1 writes may be one
+// t+1 reads) and the prefetch (a cold value t-1 writes may be prefetched).
 template <int SL, int LOSS, bool VAL>
 __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL> &op,
                                            SlotBlock sblk, __amdgpu_buffer_rsrc_t wbuf,
                                            unsigned gsrc_a) {
     const float x = __uint_as_float(st.cur.a.x);
-    // (a) this example's weights: forwarded ones get the previous step now
+    // (a) example t-1's step lands: its new weights, and this example's
+    // weights (forwarded lanes apply that step to the pair they took)
+    const float w_prev = __builtin_fmaf(-st.s_prev, st.p_x, st.p_wold);
     const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
     const float acc = __builtin_fmaf(w_old, x, 0.0f);
-    // (b) example t+1: its weights (those example t writes are forwarded),
-    // the staged example t+2, and the cold values of example t+kD (their
-    // last writers are before t)
+    // (b) writes of example t-1; example t+1's weights (those example t
+    // writes are forwarded), the staged example t+2, and the cold values of
+    // example t+kD (their last writers are before t)
+    lds_write(st.p_l, w_prev);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_prev), wbuf, st.p_g, 0, 0);
     const unsigned rd = st.nxt.a.z;
     const float v1 = lds_read(rd);
     const float fw1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(w_old)));
     const float fx1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x)));
     const Stg nxt2 = read_slot_at<SL + 2>(sblk);
     const float g_pf = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
-    __builtin_amdgcn_sched_barrier(0);
     // (c) the step of example t
     const float s = sgd_scale_t<LOSS>(butterfly64(acc), st.cur.t, op.lr);
-    const float w_new = __builtin_fmaf(-s, x, w_old);
-    __builtin_amdgcn_sched_barrier(0);
-    // (d) writes, then the rotation
-    lds_write(st.cur.a.y, w_new);
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_new), wbuf, st.cur.a.w, 0, 0);
-    const float n_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
-    st.gv[SL] = g_pf;
+    // rotation
+    st.p_wold = w_old;
+    st.p_x = x;
+    st.p_l = st.cur.a.y;
+    st.p_g = st.cur.a.w;
     st.s_prev = s;
+    st.cur_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
+    st.gv[SL] = g_pf;
     st.cur = st.nxt;
-    st.cur_v = n_v;
     st.cur_fw = fw1;
     st.cur_fx = fx1;
     st.cur_fwd = rd < 256u;
     st.nxt = nxt2;
 }
 
-// Prefetch offsets of positions q0 .. q0 + kD - 1 (kOOR for positions at or
-// past stop, and for lanes whose value does not come from global memory).
-// The slots are read unconditionally: positions past stop read stale slots.
+// Writes the last example's new weights.
+__device__ __forceinline__ void chain_flush(const ChainState &st, __amdgpu_buffer_rsrc_t wbuf) {
+    const float w_prev = __builtin_fmaf(-st.s_prev, st.p_x, st.p_wold);
+    lds_write(st.p_l, w_prev);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_prev), wbuf, st.p_g, 0, 0);
+}
+
+// Prefetch offsets of positions q0 .. q0 + kD - 1: the global write offset of
+// each lane's feature (out of range for hot features and lanes without an
+// entry).  Lanes whose value comes from elsewhere load it too and ignore it,
+// and positions past the end read stale slots: every such load stays inside
+// the weight buffer or is out of range and returns 0.
 __device__ __forceinline__ void chain_prefetch_offsets(ChainState &st, const ChainShared &S,
-                                                       int64_t q0, int64_t stop, unsigned gsrc_a) {
-    uint2 e[kD];
+                                                       int64_t q0) {
 #pragma unroll
-    for (int j = 0; j < kD; ++j)
-        e[j] = reinterpret_cast<const uint2 *>(&S.st[(int)((q0 + j) & (kRB - 1)) * 64 + lane_id()])[1];
-#pragma unroll
-    for (int j = 0; j < kD; ++j) st.pf[j] = ((q0 + j < stop) & (e[j].x == gsrc_a)) ? e[j].y : kOOR;
+    for (int j = 0; j < kD; ++j) st.pf[j] = S.st[(int)((q0 + j) & (kRB - 1)) * 64 + lane_id()].w;
 }
 
 #define PDB_CHAIN_STEPS(STEP) \
@@ -582,7 +599,7 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
     __asm__ volatile("" : "+s"(gsrc_a));  // computed once, kept in a register
     ChainState st;
     int64_t stop = std::min(len, wait_staged(S, 0, std::min<int64_t>(kD, len), &waited));
-    chain_prefetch_offsets(st, S, 0, stop, gsrc_a);
+    chain_prefetch_offsets(st, S, 0);
 #pragma unroll
     for (int j = 0; j < kD; ++j)
         st.gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[j], 0, 0));
@@ -592,13 +609,17 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
     st.cur_fw = st.cur_fx = 0.0f;
     st.cur_fwd = false;
     st.s_prev = 0.0f;
+    // no example before the first: its "writes" go to the sinks
+    st.p_wold = st.p_x = 0.0f;
+    st.p_l = lds_addr(&S.lsink[lane]);
+    st.p_g = kOOR;
 
     int64_t t0 = 0;
     for (; t0 < stop; t0 += kD) {
         // positions read in this block: t+2 and t+kD for t in [t0, t0+kD)
         stop = std::min(stop, wait_staged(S, t0 + 2, std::min<int64_t>(t0 + 2 * kD, len), &waited));
         if (t0 + kD > stop) break;
-        chain_prefetch_offsets(st, S, t0 + kD, stop, gsrc_a);
+        chain_prefetch_offsets(st, S, t0 + kD);
         lds_store(&S.ctl[0], (int)(t0 + 2));
         const SlotBlock sblk = slot_block(S, (int)(t0 & (kRB - 1)));
 #define PDB_STEP(SL) chain_step<SL>(st, op, sblk, wbuf, gsrc_a);
@@ -606,13 +627,14 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
 #undef PDB_STEP
     }
     if (t0 < stop) {  // last, partial block
-        chain_prefetch_offsets(st, S, t0 + kD, stop, gsrc_a);
+        chain_prefetch_offsets(st, S, t0 + kD);
         const SlotBlock sblk = slot_block(S, (int)(t0 & (kRB - 1)));
 #define PDB_STEP(SL) \
     if (SL < kD - 1 && t0 + SL < stop) chain_step<SL>(st, op, sblk, wbuf, gsrc_a);
         PDB_CHAIN_STEPS(PDB_STEP)
 #undef PDB_STEP
     }
+    chain_flush(st, wbuf);
     lds_store(&S.ctl[1], 1);
     if (lane == 0) {
         atomicAdd((unsigned long long *)&ctrl->stat_cycles,
@@ -638,7 +660,7 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
         const int64_t r_first = op.perm[pos], r_last = op.perm[e_end - 1];
         const int64_t dense_r0 = (r_last - r_first == e_end - 1 - pos) ? r_first : -1;
         for (int i = threadIdx.x; i < hot; i += kBlock) g_wcache[i] = op.w[i];
-        for (int i = threadIdx.x; i < kRB; i += kBlock) S.seq[i] = -1;
+        for (int i = threadIdx.x; i < kRB; i += kBlock) S.seq[i] = INT_MIN;
         if (threadIdx.x < 4) {
             S.ctl[threadIdx.x] = 0;
             S.zero[threadIdx.x] = 0.0f;
