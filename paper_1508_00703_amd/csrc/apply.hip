@@ -66,17 +66,16 @@ __device__ __forceinline__ float dev_exp87(float x) {
     return (x == x) ? e : x;
 }
 
-// 1/b, correctly rounded, for b in [1, 2^126) (NaN gives NaN).  y0 = v_rcp
-// (within about 1 ulp), one Newton step y1 = y0 + y0 (1 - b y0), whose error
-// is far below 2^-24 relative; then Markstein's correction q = y1 + y1 r with
-// the residual r = 1 - b y1, exact in binary32 because y1 is a faithful
-// reciprocal: q is 1/b rounded to nearest.  The result is a normal number, so
-// no scaling is needed.  pdb_check_reciprocal compares it with IEEE division
-// for every b in the range.
+// 1/b, correctly rounded, for b in [1, 2^126) (NaN gives NaN): y0 = v_rcp,
+// then one Newton step y0 + y0 (1 - b y0) with the residual exact in an fma.
+// On gfx950 this gives the IEEE quotient for every b in the range -- an
+// exhaustive property of the hardware reciprocal, not a theorem: v_rcp alone
+// is off in about a tenth of the cases, the corrected value in none.
+// pdb_check_reciprocal repeats that comparison on the device at hand.  The
+// range keeps the quotient a normal number, so no scaling is needed.
 __device__ __forceinline__ float recip_normal(float b) {
     const float y0 = __builtin_amdgcn_rcpf(b);
-    const float y1 = __builtin_fmaf(__builtin_fmaf(-b, y0, 1.0f), y0, y0);
-    return __builtin_fmaf(__builtin_fmaf(-b, y1, 1.0f), y1, y1);
+    return __builtin_fmaf(__builtin_fmaf(-b, y0, 1.0f), y0, y0);
 }
 
 // The logistic function 1/(1 + e^min(-z, 87)): the cap keeps 1 + e below
@@ -541,7 +540,9 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     const unsigned rd = st.nxt.a.z;
     const float v1 = lds_read(rd);
     const float fw1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(w_old)));
-    const float fx1 = __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x)));
+    // without stored values every x is 1: nothing to forward
+    const float fx1 =
+        VAL ? __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x))) : 1.0f;
     const Stg nxt2 = read_slot_at<SL + 2>(sblk);
     const float g_pf = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
     // (c) the step of example t
