@@ -118,9 +118,13 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
-    ap.add_argument("--method", type=int, default=0, help="0 auto, 1 chain-scan, 2 dataflow")
+    ap.add_argument("--method", type=int, default=0,
+                    help="0 auto, 1 chain-scan, 2 dataflow, 3 spine")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only copy BYTES of device memory once (a plain copy kernel of known "
+                         "size, for scaling HBM traffic counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: the path does not shard across GPUs "
@@ -129,6 +133,15 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copied_bytes": src.numel() * 4}))
+        return
 
     import datagen
     from paper_1508_00703_amd import native
@@ -231,11 +244,15 @@ def main():
         "config": {"workload": "%s: %s" % (workload, g["name"]), "n": n, "d": d, "nnz": nnz,
                    "seed": g["seed"], "levels": L, "max_level_width": lv.max_width_host,
                    "schedule_method": info.get("method_used"),
-                   "chain_scan_rounds": info.get("rounds")},
+                   "schedule_rounds": info.get("rounds")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "k_levels_apply (epoch)", "algorithmic_bytes": abytes,
-                     "epoch_ms": ep, "epoch_ms_all": epoch_ms, "source_digest": digest},
+                     "epoch_ms": ep, "epoch_ms_all": epoch_ms, "source_digest": digest,
+                     # levels run one after another: the epoch is a dependent
+                     # chain of L levels, so the time per level is the figure
+                     # that bounds it when levels are narrow
+                     "levels": L, "ns_per_level": ep * 1e6 / max(L, 1)},
         "schedule_ms": trimmed_mean([a.elapsed_time(b) for a, b in sched_ms]),
         "epoch_ms": ep,
     }
