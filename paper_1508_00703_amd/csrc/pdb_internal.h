@@ -144,6 +144,23 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
     return v;
 }
 
+// max over the wave, every lane gets it: DPP within rows of 16, then the
+// row and half swaps (max is idempotent, so any covering pattern works)
+template <int CTRL>
+__device__ __forceinline__ int dpp_max_i32(int v) {
+    return max(v, __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ int wave_max_dpp(int v) {
+    v = dpp_max_i32<0xB1>(v);   // quad_perm [1,0,3,2]
+    v = dpp_max_i32<0x4E>(v);   // quad_perm [2,3,0,1]
+    v = dpp_max_i32<0x141>(v);  // row_half_mirror
+    v = dpp_max_i32<0x140>(v);  // row_mirror
+    const auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    v = max((int)r[0], (int)r[1]);
+    const auto h = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+    return max((int)h[0], (int)h[1]);
+}
+
 __device__ __forceinline__ int64_t now_ticks() { return (int64_t)wall_clock64(); }
 
 __device__ __forceinline__ void record_error(Ctrl *c, int code) {

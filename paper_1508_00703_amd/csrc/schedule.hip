@@ -247,36 +247,101 @@ __global__ __launch_bounds__(kBlock) void k_cs_rows(const int64_t *__restrict__ 
 }
 
 // ---- K3 dataflow ---------------------------------------------------------
-constexpr int kFlowBatch = 32;
+// Every example waits for its previous writers' levels and publishes its own.
+// Waves take batches of kFlowB consecutive examples by ticket, so the
+// smallest unfinished example always runs.  Per batch:
+//   1. the batch's row bounds and the previous-writer rows of all its
+//      entries go to LDS, with the levels of previous writers outside the
+//      batch loaded at the same time (device-scope loads, as levels are
+//      published with device-scope stores: a level is written once, so a
+//      load sees 0, re-polled later, or the final value);
+//   2. lane j owns example j of the batch: it walks its entries from where
+//      it stopped, taking known levels and the batch's own examples from
+//      LDS, and publishes its level as soon as every writer is known.  No
+//      example waits for more than its own writers.  Outside writers not
+//      seen yet sit in a list that is re-polled as a whole (all loads in
+//      flight at once) before each walk; past the list's capacity the walk
+//      polls them itself.
+constexpr int kFlowB = 64;             // examples per batch, one per lane
+constexpr int kFlowEnt = 64 * 96;      // entries of a batch kept in LDS
+constexpr int kFlowPend = 2048;        // outside writers tracked in a re-poll list
+constexpr int kFlowWaveLds = kFlowEnt + kFlowB + kFlowPend;  // ints of LDS per wave
+constexpr int kFlowUnroll = 8;         // entry chunks whose loads are in flight together
+constexpr int kFlowShort = 4;          // longest row resolved by Jacobi rounds
+// Entry codes: >= 0 a known level (0: no previous writer); -1 - j the
+// batch's example j (j < 64); kPendBase + r an outside writer r whose level
+// was not seen yet (r < n <= kFlowMaxN keeps the two ranges apart).
+constexpr int kPendBase = INT_MIN;
+constexpr int64_t kFlowMaxN = (int64_t)INT_MAX - 128;
+
+// Level of entry e's writer: known, an example of the batch (already
+// resolved when this is called), or an outside writer polled until set.
+__device__ __forceinline__ bool flow_entry(const int *src, int e, const int *lvb,
+                                           const int32_t *level, int *v, Ctrl *ctrl,
+                                           int64_t timeout) {
+    const int c = src[e];
+    if (c >= 0) {
+        *v = c;
+        return true;
+    }
+    if (c >= -kFlowB) {
+        *v = lvb[-1 - c];
+        return true;
+    }
+    const int64_t t0 = now_ticks();
+    int idle = 0;
+    while ((*v = __hip_atomic_load(&level[c - kPendBase], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT)) == 0) {
+        if (aborted(ctrl)) return false;
+        if (now_ticks() - t0 > timeout) {
+            record_error(ctrl, DERR_WAIT_TIMEOUT);
+            return false;
+        }
+        if (++idle < 16) __builtin_amdgcn_s_sleep(1);
+        else __builtin_amdgcn_s_sleep(8);
+    }
+    return true;
+}
 
 __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__restrict__ row_ptr,
                                                             const int32_t *__restrict__ prev_row,
                                                             int64_t n, int32_t *level, Ctrl *ctrl,
                                                             int64_t timeout) {
-    __shared__ int32_t s_lv[kBlock / kWave][kFlowBatch];
+    // per wave (dynamic LDS, kFlowWaveLds ints): entry codes, levels of the
+    // batch, the list of entries whose outside writer was not seen yet
+    extern __shared__ int g_flow[];
     const int lane = lane_id(), wave = wave_in_block();
-    volatile int32_t *my = s_lv[wave];
+    int *src = g_flow + wave * kFlowWaveLds;
+    int *lvb = src + kFlowEnt;
+    int *pend = lvb + kFlowB;
     for (;;) {
         long long tk = 0;
-        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kFlowBatch);
+        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kFlowB);
         tk = __shfl(tk, 0);
         if (tk >= n) return;
-        const int base = (int)tk;
-        const int64_t end = min((int64_t)base + kFlowBatch, n);
-        for (int64_t i = base; i < end; ++i) {
-            int mx = 0;
-            int bad = 0;
-            for (int64_t p = row_ptr[i] + lane; p < row_ptr[i + 1]; p += kWave) {
-                const int pr = prev_row[p];
-                if (pr < 0) continue;
-                int v;
-                if (pr >= base) {
-                    v = my[pr - base];
-                } else {
-                    v = __hip_atomic_load(&level[pr], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if (v == 0) {
+        const int64_t base = tk;
+        const int cnt = (int)min((int64_t)kFlowB, n - base);
+        const bool mine_ok = lane < cnt;
+        const int64_t r0 = row_ptr[base + min(lane, cnt)];
+        const int64_t r1 = row_ptr[base + min(lane + 1, cnt)];
+        const int64_t b0 = __shfl(r0, 0);
+        const int64_t E = row_ptr[base + cnt] - b0;
+        lvb[lane] = 0;
+        if (E > kFlowEnt) {
+            // too many entries for LDS: one example at a time, direct reads
+            for (int i = 0; i < cnt; ++i) {
+                int mx = 0, bad = 0;
+                const int64_t p0 = row_ptr[base + i], p1 = row_ptr[base + i + 1];
+                for (int64_t p = p0 + lane; p < p1; p += kWave) {
+                    const int pr = prev_row[p];
+                    if (pr < 0) continue;
+                    int v = 0;
+                    if (pr >= base) {
+                        v = lvb[pr - base];
+                    } else {
                         const int64_t t0 = now_ticks();
-                        while (v == 0) {
+                        while ((v = __hip_atomic_load(&level[pr], __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)) == 0) {
                             if (aborted(ctrl)) { bad = 1; break; }
                             if (now_ticks() - t0 > timeout) {
                                 record_error(ctrl, DERR_WAIT_TIMEOUT);
@@ -284,21 +349,213 @@ __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__res
                                 break;
                             }
                             __builtin_amdgcn_s_sleep(1);
-                            v = __hip_atomic_load(&level[pr], __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                    }
+                    mx = max(mx, v);
+                }
+                if (__ballot(bad) != 0ull) return;
+                const int lv = wave_max_dpp(mx) + 1;
+                if (lane == 0) {
+                    lvb[i] = lv;
+                    __hip_atomic_store(&level[base + i], lv, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            continue;
+        }
+        // 1. codes of every entry, outside levels loaded with them
+        int npend = 0;          // wave-uniform
+        bool overflow = false;  // some unseen writer did not fit in the list
+        int64_t ninner = 0;     // entries whose writer is in the batch
+        for (int64_t e0 = 0; e0 < E; e0 += kWave * kFlowUnroll) {
+            int pr[kFlowUnroll], v[kFlowUnroll];
+#pragma unroll
+            for (int u = 0; u < kFlowUnroll; ++u)
+                pr[u] = prev_row[b0 + min(e0 + u * kWave + lane, E - 1)];
+#pragma unroll
+            for (int u = 0; u < kFlowUnroll; ++u)
+                v[u] = __hip_atomic_load(&level[max(pr[u], 0)], __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+            for (int u = 0; u < kFlowUnroll; ++u) {
+                const int64_t e = e0 + u * kWave + lane;
+                const int code = pr[u] < 0       ? 0
+                                 : pr[u] >= base ? -1 - (int)(pr[u] - base)
+                                 : v[u] != 0     ? v[u]
+                                                 : kPendBase + pr[u];
+                if (e < E) src[e] = code;
+                const unsigned long long pb = __ballot(e < E && code < -kFlowB);
+                const int at = npend + (int)lanes_below(pb);
+                if (e < E && code < -kFlowB && at < kFlowPend) pend[at] = (int)e;
+                overflow |= npend + __popcll(pb) > kFlowPend;
+                npend = min(npend + __popcll(pb), kFlowPend);
+                ninner += __popcll(__ballot(e < E && code < 0 && code >= -kFlowB));
+            }
+        }
+        // row bounds of this lane's example inside the batch's entries
+        const int my0 = (int)(r0 - b0), my1 = (int)(r1 - b0);
+        const int longest = wave_max_dpp(mine_ok ? my1 - my0 : 0);
+        const bool chainlike = E >= 8 * (int64_t)cnt && 4 * ninner >= E;
+        const bool shortrows = longest <= kFlowShort;
+        int64_t t0 = now_ticks();  // last time anything moved
+        int idle = 0;
+        if (chainlike || shortrows) {
+            // 2a. wait for every listed outside writer, re-polling the list as
+            // a whole (all loads in flight at once)
+            while (npend > 0) {
+                int kept = 0;
+                for (int k0 = 0; k0 < npend; k0 += kWave * kFlowUnroll) {
+                    int ent[kFlowUnroll], v[kFlowUnroll];
+#pragma unroll
+                    for (int u = 0; u < kFlowUnroll; ++u) {
+                        ent[u] = pend[min(k0 + u * kWave + lane, npend - 1)];
+                        v[u] = __hip_atomic_load(&level[src[ent[u]] - kPendBase],
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+#pragma unroll
+                    for (int u = 0; u < kFlowUnroll; ++u) {
+                        const bool live = k0 + u * kWave + lane < npend;
+                        if (live && v[u] != 0) src[ent[u]] = v[u];
+                        const unsigned long long kb = __ballot(live && v[u] == 0);
+                        if (live && v[u] == 0) pend[kept + (int)lanes_below(kb)] = ent[u];
+                        kept += __popcll(kb);
+                    }
+                }
+                if (kept < npend) {
+                    t0 = now_ticks();
+                    idle = 0;
+                } else {
+                    if (aborted(ctrl)) return;
+                    if (now_ticks() - t0 > timeout) {
+                        record_error(ctrl, DERR_WAIT_TIMEOUT);
+                        return;
+                    }
+                    if (++idle < 16) __builtin_amdgcn_s_sleep(1);
+                    else __builtin_amdgcn_s_sleep(8);
+                }
+                npend = kept;
+            }
+            // outside writers that did not fit in the list: waited for in
+            // place (flow_entry)
+            if (chainlike) {
+                // 2b. chain-like batch (long rows, many writers inside the
+                // batch): one example at a time, the whole wave over its entries
+                for (int i = 0; i < cnt; ++i) {
+                    const int o0 = __builtin_amdgcn_readlane(my0, i);
+                    const int o1 = __builtin_amdgcn_readlane(my1, i);
+                    int mx = 0, bad = 0;
+                    for (int e = o0 + lane; e < o1; e += kWave) {
+                        int v = 0;
+                        if (!flow_entry(src, e, lvb, level, &v, ctrl, timeout)) bad = 1;
+                        mx = max(mx, v);
+                    }
+                    if (__ballot(bad) != 0ull) return;
+                    const int lv = wave_max_dpp(mx) + 1;
+                    if (lane == 0) {
+                        lvb[i] = lv;
+                        __hip_atomic_store(&level[base + i], lv, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+            } else {
+                // 2c. short rows (matrix completion): lane j holds example j;
+                // Jacobi rounds from the outside bounds until nothing changes
+                int known = 0, nin = 0, bad = 0;
+                int pin[kFlowShort];
+                for (int k = 0; k < kFlowShort; ++k) {
+                    pin[k] = 0;
+                    if (mine_ok && my0 + k < my1) {
+                        const int c = src[my0 + k];
+                        if (c < 0 && c >= -kFlowB) {
+                            pin[nin++] = -1 - c;
+                        } else {
+                            int v = 0;
+                            if (!flow_entry(src, my0 + k, lvb, level, &v, ctrl, timeout)) bad = 1;
+                            known = max(known, v);
                         }
                     }
                 }
-                mx = max(mx, v);
+                if (__ballot(bad) != 0ull) return;
+                int lv = known + 1;
+                lvb[lane] = mine_ok ? lv : 0;
+                for (;;) {
+                    int nl = known + 1;
+                    for (int k = 0; k < kFlowShort; ++k)
+                        if (k < nin) nl = max(nl, lvb[pin[k]] + 1);
+                    const bool ch = mine_ok && nl != lv;
+                    lv = nl;
+                    if (mine_ok) lvb[lane] = lv;
+                    if (__ballot(ch) == 0ull) break;
+                }
+                if (mine_ok)
+                    __hip_atomic_store(&level[base + lane], lv, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
             }
-            if (__ballot(bad) != 0ull) return;
-            const int lv = wave_max_i32(mx) + 1;
-            if (lane == 0) {
-                my[i - base] = lv;
-                __hip_atomic_store(&level[i], lv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            continue;
+        }
+        // 2d. otherwise (wide levels) lane j resolves example j and publishes
+        // it as soon as its own writers are known.  First one pass over its
+        // row: known levels fold into kmax, the other entries are compacted
+        // to the front of the row's own range.
+        int kmax = 0, nun = 0;
+        for (int e = my0; e < my1; e += 4) {
+            int c[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) c[u] = src[min(e + u, my1 - 1)];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (e + u >= my1) continue;
+                if (c[u] >= 0) kmax = max(kmax, c[u]);
+                else src[my0 + nun++] = c[u];
             }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
+        }
+        bool done = !mine_ok;
+        for (;;) {
+            bool moved = false;
+            if (!done) {
+                // every remaining writer: batch examples from LDS, outside
+                // ones polled, four requests in flight at a time
+                int keep = 0;
+                for (int k = 0; k < nun; k += 4) {
+                    int c[4], v[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        c[u] = src[my0 + min(k + u, nun - 1)];
+                        v[u] = c[u] >= -kFlowB ? lvb[-1 - c[u]]
+                                               : __hip_atomic_load(&level[c[u] - kPendBase],
+                                                                   __ATOMIC_RELAXED,
+                                                                   __HIP_MEMORY_SCOPE_AGENT);
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        if (k + u >= nun) continue;
+                        if (v[u] != 0) kmax = max(kmax, v[u]);
+                        else src[my0 + keep++] = c[u];
+                    }
+                }
+                moved = keep < nun;
+                nun = keep;
+                if (nun == 0) {
+                    lvb[lane] = kmax + 1;
+                    __hip_atomic_store(&level[base + lane], kmax + 1, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    done = true;
+                    moved = true;
+                }
+            }
+            if (__ballot(!done) == 0ull) break;
+            if (__ballot(moved) == 0ull) {
+                if (aborted(ctrl)) return;
+                if (now_ticks() - t0 > timeout) {
+                    record_error(ctrl, DERR_WAIT_TIMEOUT);
+                    return;
+                }
+                if (++idle < 16) __builtin_amdgcn_s_sleep(1);
+                else __builtin_amdgcn_s_sleep(8);
+            } else {
+                t0 = now_ticks();
+                idle = 0;
+            }
         }
     }
 }
@@ -915,8 +1172,16 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 0);
         k_fill_i32<<<1, 64, 0, s>>>(reinterpret_cast<int32_t *>(&w.ctrl->ticket), 2, 0);
         PDB_LAUNCHED();
-        k_levels_dataflow<<<device_cus() * 4, kBlock, 0, s>>>(csr->row_ptr, w.cand, n,
-                                                              lv->level, w.ctrl, timeout);
+        if (n > kFlowMaxN) return PDB_ERR_UNSUPPORTED;
+        const size_t lds = (size_t)kFlowWaveLds * 4 * (kBlock / kWave);
+        const void *fn = reinterpret_cast<const void *>(&k_levels_dataflow);
+        PDB_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        int per_cu = 0;
+        PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, lds));
+        const int64_t grid = std::min<int64_t>((int64_t)device_cus() * std::max(per_cu, 1),
+                                               cdiv(n, (int64_t)kFlowB * (kBlock / kWave)));
+        k_levels_dataflow<<<(unsigned)std::max<int64_t>(grid, 1), kBlock, lds, s>>>(
+            csr->row_ptr, w.cand, n, lv->level, w.ctrl, timeout);
         PDB_LAUNCHED();
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
