@@ -120,9 +120,11 @@ int pdb_last_hip_error(void);
  * pdb_prev_writer for these sizes.  Host-only arithmetic. */
 int pdb_schedule_workspace_bytes(int64_t n, int64_t d, int64_t nnz, size_t *bytes);
 
-/* Device workspace (bytes) needed by pdb_sgd_epoch, pdb_mf_epoch,
- * pdb_validate_csr and pdb_workspace_status.  Host-only arithmetic. */
-int pdb_epoch_workspace_bytes(size_t *bytes);
+/* Device workspace (bytes) for pdb_sgd_epoch with d features, or for
+ * pdb_mf_epoch with d = n_users + n_items; d = 0 for pdb_validate_csr,
+ * pdb_workspace_status and pdb_check_reciprocal.  Host-only arithmetic.  A
+ * workspace of this size lets pdb_sgd_epoch run sync-free. */
+int pdb_epoch_workspace_bytes(int64_t d, size_t *bytes);
 
 /* Conflict levels (read/write constraints of Sec. 4.4 at feature grain,
  * Theorem 2): fills levels->level, perm, level_ptr, n_levels, prev_nz (when
@@ -140,8 +142,17 @@ int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
  * PDB_LOGISTIC (labels y in {-1,+1}: target y > 0) or PDB_SQUARED.  levels
  * must come from pdb_schedule on the same CSR (or be an equivalent
  * grouping: every level's examples pairwise feature-disjoint, every
- * conflicting pair in index order across levels).  Asynchronous; a device
- * error (watchdog) is reported by pdb_workspace_status on ws. */
+ * conflicting pair in index order across levels).  Two executions, bitwise
+ * the same result:
+ *   - level by level (narrow levels: a width-1 run is one dependent chain);
+ *   - sync-free, the Read Protocol of Sec. 5 at feature grain: examples in
+ *     index order, each entry waiting only until its feature was written by
+ *     its previous writer (levels->prev_nz), no barriers.  Chosen when
+ *     n >= 8 L, levels->prev_nz is set and ws_bytes covers
+ *     pdb_epoch_workspace_bytes(d) (environment PDB_EPOCH_MODE=1 or 2 forces
+ *     levels or sync-free).
+ * ws: at least pdb_epoch_workspace_bytes(0).  Asynchronous; a device error
+ * (watchdog) is reported by pdb_workspace_status on ws. */
 int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
                   float lr, int loss, const pdb_levels *levels, void *ws, size_t ws_bytes,
                   hipStream_t stream);

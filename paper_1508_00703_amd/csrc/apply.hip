@@ -851,6 +851,196 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
     return PDB_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Sync-free epoch (the Read Protocol of Sec. 5 at feature grain): no levels
+// and no barriers.  Each feature's weight and the CSR index of the entry that
+// last wrote it share one 64-bit word.  Examples are taken in index order;
+// entry p reads its feature once the word carries p's previous writer
+// (prev_nz[p], -1 for none), and writes back its new weight together with p.
+// One word carries both, so a single 64-bit access is the whole handshake.
+// The earliest unfinished example never waits for a later one, so the grid
+// always makes progress.
+constexpr int kSyncB = 4;  // examples per ticket, run in order by one wave
+
+__device__ __forceinline__ unsigned long long wv_pack(float w, int tag) {
+    return ((unsigned long long)(unsigned)tag << 32) | (unsigned long long)__float_as_uint(w);
+}
+__device__ __forceinline__ float wv_value(unsigned long long v) {
+    return __uint_as_float((unsigned)v);
+}
+
+__global__ void k_wv_in(const float *__restrict__ w, unsigned long long *__restrict__ wv,
+                        int64_t d) {
+    for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
+         f += (int64_t)gridDim.x * blockDim.x)
+        wv[f] = wv_pack(w[f], -1);
+}
+
+__global__ void k_wv_out(const unsigned long long *__restrict__ wv, float *__restrict__ w,
+                         int64_t d) {
+    for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
+         f += (int64_t)gridDim.x * blockDim.x)
+        w[f] = wv_value(wv[f]);
+}
+
+// Sleeps about 2^min(round, 6) x 64 cycles (s_sleep takes a constant).
+__device__ __forceinline__ void wave_backoff(int round) {
+    switch (round < 6 ? round : 6) {
+        case 0: __builtin_amdgcn_s_sleep(1); break;
+        case 1: __builtin_amdgcn_s_sleep(2); break;
+        case 2: __builtin_amdgcn_s_sleep(4); break;
+        case 3: __builtin_amdgcn_s_sleep(8); break;
+        case 4: __builtin_amdgcn_s_sleep(16); break;
+        case 5: __builtin_amdgcn_s_sleep(32); break;
+        default: __builtin_amdgcn_s_sleep(64); break;
+    }
+}
+
+// The word of feature c once entry p's previous writer pn has written it;
+// false on timeout or abort.
+__device__ __forceinline__ bool wv_wait(unsigned long long *wv, int c, int pn,
+                                        unsigned long long *out, Ctrl *ctrl, int64_t timeout) {
+    unsigned long long v =
+        __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((int)(unsigned)(v >> 32) == pn) {
+        *out = v;
+        return true;
+    }
+    const int64_t t0 = now_ticks();
+    int idle = 0;
+    for (;;) {
+        if (aborted(ctrl)) return false;
+        if (now_ticks() - t0 > timeout) {
+            record_error(ctrl, DERR_WAIT_TIMEOUT);
+            return false;
+        }
+        if (++idle < 16) __builtin_amdgcn_s_sleep(1);
+        else __builtin_amdgcn_s_sleep(8);
+        v = __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((int)(unsigned)(v >> 32) == pn) {
+            *out = v;
+            return true;
+        }
+    }
+}
+
+template <int LOSS, bool VAL>
+__global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
+                                                         unsigned long long *wv, int64_t n,
+                                                         Ctrl *ctrl, int64_t timeout) {
+    const int lane = lane_id();
+    for (;;) {
+        long long tk = 0;
+        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kSyncB);
+        tk = __shfl(tk, 0);
+        if (tk >= n) return;
+        const int64_t stop = min((int64_t)tk + kSyncB, n);
+        for (int64_t i = tk; i < stop; ++i) {
+            const int64_t b = op.row_ptr[i];
+            const int m = (int)(op.row_ptr[i + 1] - b);
+            const float yi = op.y[i];
+            int bad = 0;
+            if (m <= kWave) {
+                int c = 0, pn = -1;
+                float x = 1.0f, wold = 0.0f, acc = 0.0f;
+                if (lane < m) {
+                    c = op.col[b + lane];
+                    pn = op.prev_nz[b + lane];
+                    if (VAL) x = op.val[b + lane];
+                }
+                // the whole wave polls its features in rounds, backing off
+                // while nothing arrives (waiting waves far from the frontier
+                // then barely load the memory system)
+                bool ready = lane >= m;
+                int64_t t0 = 0;
+                for (int round = 0;; ++round) {
+                    if (!ready) {
+                        const unsigned long long v =
+                            __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if ((int)(unsigned)(v >> 32) == pn) {
+                            wold = wv_value(v);
+                            ready = true;
+                        }
+                    }
+                    if (__ballot(!ready) == 0ull) break;
+                    if (round == 0) t0 = now_ticks();
+                    if (aborted(ctrl)) return;
+                    if (now_ticks() - t0 > timeout) {
+                        record_error(ctrl, DERR_WAIT_TIMEOUT);
+                        return;
+                    }
+                    wave_backoff(round);
+                }
+                if (lane < m) acc = __builtin_fmaf(wold, x, 0.0f);
+                const float s = sgd_scale<LOSS>(butterfly64(acc), yi, op.lr);
+                if (lane < m)
+                    __hip_atomic_store(&wv[c], wv_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                float acc = 0.0f;
+                for (int k = lane; k < m; k += kWave) {
+                    const int c = op.col[b + k];
+                    unsigned long long v = 0;
+                    if (!wv_wait(wv, c, op.prev_nz[b + k], &v, ctrl, timeout)) {
+                        bad = 1;
+                        break;
+                    }
+                    acc = __builtin_fmaf(wv_value(v), VAL ? op.val[b + k] : 1.0f, acc);
+                }
+                if (__ballot(bad) != 0ull) return;
+                const float s = sgd_scale<LOSS>(butterfly64(acc), yi, op.lr);
+                // nothing else writes these features before this example does
+                for (int k = lane; k < m; k += kWave) {
+                    const int c = op.col[b + k];
+                    const float wold = wv_value(
+                        __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                    __hip_atomic_store(&wv[c],
+                                       wv_pack(__builtin_fmaf(-s, VAL ? op.val[b + k] : 1.0f, wold),
+                                               (int)(b + k)),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        }
+    }
+}
+
+int64_t syncfree_ws_bytes(int64_t d) { return (int64_t)sizeof(Ctrl) + align_up(8 * d); }
+
+template <int LOSS, bool VAL>
+int launch_syncfree(const SgdOp<LOSS, VAL> &op, int64_t n, int64_t d, int64_t L, void *ws,
+                    hipStream_t s) {
+    Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    unsigned long long *wv = reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) +
+                                                                    sizeof(Ctrl));
+    const int64_t timeout = spin_timeout_ticks();
+    k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
+    PDB_LAUNCHED();
+    if (d > 0) {
+        k_wv_in<<<grid_for(d, kBlock, 8192), kBlock, 0, s>>>(op.w, wv, d);
+        PDB_LAUNCHED();
+    }
+    const void *fn = reinterpret_cast<const void *>(&k_sgd_syncfree<LOSS, VAL>);
+    int dev = 0, cus = 0, per_cu = 0;
+    PDB_HIP(hipGetDevice(&dev));
+    PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0));
+    // every block resident (a wave spinning on a writer never keeps that
+    // writer's wave from running), and about 8 levels' worth of examples in
+    // flight: more would only add waiting waves
+    const int64_t width = L > 0 ? cdiv(n, L) : n;
+    int64_t grid = std::min<int64_t>((int64_t)cus * std::max(per_cu, 1),
+                                     cdiv(n, (int64_t)kSyncB * kWavesPerBlock));
+    grid = std::min<int64_t>(grid, std::max<int64_t>(cdiv(8 * width, kWavesPerBlock), cus));
+    k_sgd_syncfree<LOSS, VAL><<<(unsigned)std::max<int64_t>(grid, 1), kBlock, 0, s>>>(
+        op, wv, n, ctrl, timeout);
+    PDB_LAUNCHED();
+    if (d > 0) {
+        k_wv_out<<<grid_for(d, kBlock, 8192), kBlock, 0, s>>>(wv, op.w, d);
+        PDB_LAUNCHED();
+    }
+    return PDB_OK;
+}
+
 int epoch_checks(const pdb_levels *lv, int64_t n, void *ws, size_t ws_bytes) {
     if (!lv || !ws) return PDB_ERR_INVALID_ARG;
     if (n > 0 && (!lv->perm || !lv->level_ptr || !lv->n_levels)) return PDB_ERR_INVALID_ARG;
@@ -865,9 +1055,10 @@ int epoch_checks(const pdb_levels *lv, int64_t n, void *ws, size_t ws_bytes) {
 
 using namespace pdbk;
 
-extern "C" int pdb_epoch_workspace_bytes(size_t *bytes) {
-    if (!bytes) return PDB_ERR_INVALID_ARG;
-    *bytes = sizeof(Ctrl);
+extern "C" int pdb_epoch_workspace_bytes(int64_t d, size_t *bytes) {
+    if (!bytes || d < 0) return PDB_ERR_INVALID_ARG;
+    if (d >= INT32_MAX) return PDB_ERR_UNSUPPORTED;
+    *bytes = (size_t)syncfree_ws_bytes(d);
     return PDB_OK;
 }
 
@@ -887,9 +1078,18 @@ extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n,
     const bool chain_env = env_setting("PDB_CHAIN", 1) != 0;
     // the width-1 pipeline addresses weights with 32-bit buffer offsets
     const bool chain_ok = chain_env && lv->prev_nz != nullptr && d < (int64_t(1) << 29);
+    // sync-free when the levels are wide on average (a barrier per level
+    // would cost more than a wait per feature), the previous writers are
+    // known and the workspace holds the packed words; PDB_EPOCH_MODE 1 / 2
+    // forces levels / sync-free
+    const int64_t mode = env_setting("PDB_EPOCH_MODE", 0);
+    const bool sf_ok = lv->prev_nz != nullptr && (int64_t)ws_bytes >= syncfree_ws_bytes(d);
+    const bool wide = lv->L_host > 0 && n >= 8 * lv->L_host;
+    const bool syncfree = sf_ok && (mode == 2 || (mode == 0 && wide));
 #define PDB_SGD_CASE(LS, HV)                                                                 \
     if (loss == LS && has_val == HV) {                                                       \
         SgdOp<LS, HV> op{csr->row_ptr, csr->col, csr->val, labels, w, lv->perm, lv->prev_nz, lr}; \
+        if (syncfree) return launch_syncfree(op, n, d, lv->L_host, ws, s);                    \
         return launch_levels(op, lv, d, chain_ok, ctrl, s);                                  \
     }
     PDB_SGD_CASE(PDB_LOGISTIC, true)

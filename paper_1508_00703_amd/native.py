@@ -78,7 +78,7 @@ def load() -> ctypes.CDLL:
     lib.pdb_strerror.restype = ctypes.c_char_p
     lib.pdb_last_hip_error.argtypes = []
     lib.pdb_schedule_workspace_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(sz)]
-    lib.pdb_epoch_workspace_bytes.argtypes = [ctypes.POINTER(sz)]
+    lib.pdb_epoch_workspace_bytes.argtypes = [i64, ctypes.POINTER(sz)]
     lib.pdb_schedule.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, ctypes.POINTER(PdbLevels),
                                  ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, P]
     lib.pdb_sgd_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int,
@@ -190,9 +190,9 @@ def pdb_schedule_workspace_bytes(n: int, d: int, nnz: int) -> int:
     return out.value
 
 
-def pdb_epoch_workspace_bytes() -> int:
+def pdb_epoch_workspace_bytes(d: int = 0) -> int:
     out = ctypes.c_size_t(0)
-    _check(load().pdb_epoch_workspace_bytes(ctypes.byref(out)), "pdb_epoch_workspace_bytes")
+    _check(load().pdb_epoch_workspace_bytes(d, ctypes.byref(out)), "pdb_epoch_workspace_bytes")
     return out.value
 
 
@@ -221,7 +221,7 @@ def pdb_sgd_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tenso
     if w.numel() < d or labels.numel() < n:
         raise ValueError("w must hold d entries and labels n entries")
     if ws is None:
-        ws = workspace(pdb_epoch_workspace_bytes(), csr.device)
+        ws = workspace(pdb_epoch_workspace_bytes(d), csr.device)
     _check(load().pdb_sgd_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
                                 ctypes.c_float(lr), loss, ctypes.byref(levels.c()), _ptr(ws),
                                 ws.numel(), _stream(stream, csr.device)), "pdb_sgd_epoch")
@@ -236,7 +236,7 @@ def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, r
     if U.numel() < n_users * rank or V.numel() < n_items * rank:
         raise ValueError("U / V too small")
     if ws is None:
-        ws = workspace(pdb_epoch_workspace_bytes(), U.device)
+        ws = workspace(pdb_epoch_workspace_bytes(n_users + n_items), U.device)
     _check(load().pdb_mf_epoch(_ptr(user), _ptr(item), _ptr(rating), n, _ptr(U), n_users,
                                _ptr(V), n_items, rank, ctypes.c_float(lr), ctypes.c_float(reg),
                                ctypes.byref(levels.c()), _ptr(ws), ws.numel(),

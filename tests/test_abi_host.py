@@ -47,7 +47,11 @@ def test_workspace_size_queries(lib):
     from paper_1508_00703_amd import native
 
     sz = ctypes.c_size_t(0)
-    assert lib.pdb_epoch_workspace_bytes(ctypes.byref(sz)) == native.PDB_OK and sz.value >= 512
+    assert lib.pdb_epoch_workspace_bytes(0, ctypes.byref(sz)) == native.PDB_OK and sz.value >= 512
+    small = sz.value
+    assert lib.pdb_epoch_workspace_bytes(10 ** 6, ctypes.byref(sz)) == native.PDB_OK
+    assert sz.value >= small + 8 * 10 ** 6     # one packed word per feature
+    assert lib.pdb_epoch_workspace_bytes(-1, ctypes.byref(sz)) == native.PDB_ERR_INVALID_ARG
     prev = 0
     for nnz in (0, 1000, 10 ** 6, 5 * 10 ** 8):
         assert lib.pdb_schedule_workspace_bytes(10 ** 4, 10 ** 3, nnz, ctypes.byref(sz)) == 0

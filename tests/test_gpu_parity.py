@@ -56,10 +56,15 @@ def test_no_examples(gpu):
     assert lv.L_host == 0 and int(lv.n_levels.item()) == 0
 
 
+EPOCH_MODES = ["1", "2"]  # level by level, sync-free
+
+
 @pytest.mark.parametrize("name", sorted(structured_cases()))
 @pytest.mark.parametrize("loss", [0, 1])
 @pytest.mark.parametrize("with_val", [True, False])
-def test_structured_epochs(gpu, name, loss, with_val):
+@pytest.mark.parametrize("mode", EPOCH_MODES)
+def test_structured_epochs(gpu, name, loss, with_val, mode, monkeypatch):
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     rows = structured_cases()[name]
     row_ptr, col = csr_from_rows(rows)
@@ -96,7 +101,9 @@ def test_config_schedules(gpu, cfg, method):
 
 
 @pytest.mark.parametrize("cfg", sorted(SCALED))
-def test_config_epochs(gpu, cfg):
+@pytest.mark.parametrize("mode", ["0"] + EPOCH_MODES)
+def test_config_epochs(gpu, cfg, mode, monkeypatch):
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     g = datagen.generate(cfg, **SCALED[cfg])
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
