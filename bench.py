@@ -160,7 +160,8 @@ def main():
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None if mf else g["val"], dev)
     lv = native.Levels(n, nnz, dev)
     ws_s = native.workspace(native.pdb_schedule_workspace_bytes(n, d, nnz), dev)
-    ws_e = native.workspace(native.pdb_epoch_workspace_bytes(d), dev)
+    ws_e = native.workspace(native.pdb_epoch_workspace_bytes(
+        (g["n_users"] + g["n_items"]) * g["rank"] if mf else d), dev)
     if mf:
         user = torch.from_numpy(g["user"]).to(dev)
         item = torch.from_numpy(g["item"]).to(dev)

@@ -121,7 +121,7 @@ int pdb_last_hip_error(void);
 int pdb_schedule_workspace_bytes(int64_t n, int64_t d, int64_t nnz, size_t *bytes);
 
 /* Device workspace (bytes) for pdb_sgd_epoch with d features, or for
- * pdb_mf_epoch with d = n_users + n_items; d = 0 for pdb_validate_csr,
+ * pdb_mf_epoch with d = (n_users + n_items) * rank; d = 0 for pdb_validate_csr,
  * pdb_workspace_status and pdb_check_reciprocal.  Host-only arithmetic.  A
  * workspace of this size lets pdb_sgd_epoch run sync-free. */
 int pdb_epoch_workspace_bytes(int64_t d, size_t *bytes);
@@ -160,7 +160,9 @@ int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
 /* One matrix-completion SGD epoch (rank 32): rating t touches user row
  * U[user[t]] (device [n_users*32]) and item row V[item[t]] (device
  * [n_items*32]); levels from pdb_schedule on the CSR whose row t is
- * {user[t], n_users + item[t]}.  Asynchronous. */
+ * {user[t], n_users + item[t]}.  Runs level by level or sync-free under the
+ * rule of pdb_sgd_epoch (the sync-free run needs levels->prev_nz and
+ * pdb_epoch_workspace_bytes((n_users + n_items) * 32)).  Asynchronous. */
 int pdb_mf_epoch(const int32_t *user, const int32_t *item, const float *rating, int64_t n,
                  float *U, int64_t n_users, float *V, int64_t n_items, int32_t rank, float lr,
                  float reg, const pdb_levels *levels, void *ws, size_t ws_bytes,

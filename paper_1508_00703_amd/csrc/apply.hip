@@ -1006,6 +1006,123 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
 
 int64_t syncfree_ws_bytes(int64_t d) { return (int64_t)sizeof(Ctrl) + align_up(8 * d); }
 
+// Matrix completion, sync-free: every component of a U or V row is a
+// (value, last rating) word; rating t waits until the user row's words carry
+// the previous rating on that user (prev_nz[2t] / 2) and the item row's the
+// previous rating on that item (prev_nz[2t + 1] / 2), then writes both rows
+// tagged t.  Two ratings per wave, one per 32-lane half, unless the second
+// depends on the first.
+constexpr int kSyncMfB = 8;  // ratings per ticket
+
+__device__ __forceinline__ int prev_rating(const int32_t *prev_nz, int64_t e) {
+    const int32_t q = prev_nz[e];
+    return q < 0 ? -1 : (q >> 1);
+}
+
+__global__ __launch_bounds__(kBlock) void k_mf_syncfree(
+    const int32_t *__restrict__ user, const int32_t *__restrict__ item,
+    const float *__restrict__ rating, const int32_t *__restrict__ prev_nz,
+    unsigned long long *uw, unsigned long long *vw, int64_t n, float lr, float reg, Ctrl *ctrl,
+    int64_t timeout) {
+    const int lane = lane_id();
+    const int h = lane >> 5, j = lane & 31;
+    for (;;) {
+        long long tk = 0;
+        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kSyncMfB);
+        tk = __shfl(tk, 0);
+        if (tk >= n) return;
+        const int64_t stop = min((int64_t)tk + kSyncMfB, n);
+        for (int64_t t = tk; t < stop;) {
+            const bool pair = t + 1 < stop && prev_rating(prev_nz, 2 * (t + 1)) != t &&
+                              prev_rating(prev_nz, 2 * (t + 1) + 1) != t;
+            const int count = pair ? 2 : 1;
+            const int64_t tt = t + h;
+            const bool valid = h < count;
+            int64_t uo = 0, vo = 0;
+            int tu = -1, ti = -1;
+            float r = 0.0f;
+            if (valid) {
+                uo = (int64_t)user[tt] * 32 + j;
+                vo = (int64_t)item[tt] * 32 + j;
+                tu = prev_rating(prev_nz, 2 * tt);
+                ti = prev_rating(prev_nz, 2 * tt + 1);
+                r = rating[tt];
+            }
+            float uj = 0.0f, vj = 0.0f;
+            bool got_u = !valid, got_v = !valid;
+            int64_t t0 = 0;
+            for (int round = 0;; ++round) {
+                if (!got_u) {
+                    const unsigned long long v =
+                        __hip_atomic_load(&uw[uo], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if ((int)(unsigned)(v >> 32) == tu) {
+                        uj = wv_value(v);
+                        got_u = true;
+                    }
+                }
+                if (!got_v) {
+                    const unsigned long long v =
+                        __hip_atomic_load(&vw[vo], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if ((int)(unsigned)(v >> 32) == ti) {
+                        vj = wv_value(v);
+                        got_v = true;
+                    }
+                }
+                if (__ballot(!(got_u && got_v)) == 0ull) break;
+                if (round == 0) t0 = now_ticks();
+                if (aborted(ctrl)) return;
+                if (now_ticks() - t0 > timeout) {
+                    record_error(ctrl, DERR_WAIT_TIMEOUT);
+                    return;
+                }
+                wave_backoff(round);
+            }
+            const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
+            if (valid) {
+                const float a = err * vj, b = reg * uj;
+                const float a2 = err * uj, b2 = reg * vj;
+                __hip_atomic_store(&uw[uo], wv_pack(__builtin_fmaf(lr, a - b, uj), (int)tt),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&vw[vo], wv_pack(__builtin_fmaf(lr, a2 - b2, vj), (int)tt),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            t += count;
+        }
+    }
+}
+
+int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_t n_users,
+                       int64_t n_items, int64_t L, void *ws, hipStream_t s) {
+    Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    unsigned long long *uw =
+        reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
+    unsigned long long *vw = uw + n_users * 32;
+    const int64_t timeout = spin_timeout_ticks();
+    k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
+    PDB_LAUNCHED();
+    if (n_users > 0) k_wv_in<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(op.U, uw, n_users * 32);
+    if (n_items > 0) k_wv_in<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(op.V, vw, n_items * 32);
+    PDB_LAUNCHED();
+    const void *fn = reinterpret_cast<const void *>(&k_mf_syncfree);
+    int dev = 0, cus = 0, per_cu = 0;
+    PDB_HIP(hipGetDevice(&dev));
+    PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0));
+    const int64_t width = L > 0 ? cdiv(n, L) : n;
+    int64_t grid = std::min<int64_t>((int64_t)cus * std::max(per_cu, 1),
+                                     cdiv(n, (int64_t)kSyncMfB * kWavesPerBlock));
+    grid = std::min<int64_t>(grid, std::max<int64_t>(cdiv(8 * width, 2 * kWavesPerBlock), cus));
+    k_mf_syncfree<<<(unsigned)std::max<int64_t>(grid, 1), kBlock, 0, s>>>(
+        op.user, op.item, op.rating, prev_nz, uw, vw, n, op.lr, op.reg, ctrl, timeout);
+    PDB_LAUNCHED();
+    if (n_users > 0) k_wv_out<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(uw, op.U, n_users * 32);
+    if (n_items > 0) k_wv_out<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(vw, op.V, n_items * 32);
+    PDB_LAUNCHED();
+    return PDB_OK;
+}
+
+
+
 template <int LOSS, bool VAL>
 int launch_syncfree(const SgdOp<LOSS, VAL> &op, int64_t n, int64_t d, int64_t L, void *ws,
                     hipStream_t s) {
@@ -1111,6 +1228,15 @@ extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const floa
     if (n > 0 && (!user || !item || !rating || !U || !V)) return PDB_ERR_INVALID_ARG;
     if (n == 0) return PDB_OK;
     MfOp op{user, item, rating, U, V, lv->perm, lr, reg};
+    // sync-free under the same rule as pdb_sgd_epoch; the packed words need
+    // pdb_epoch_workspace_bytes((n_users + n_items) * 32)
+    const int64_t mode = env_setting("PDB_EPOCH_MODE", 0);
+    const bool sf_ok = lv->prev_nz != nullptr &&
+                       (int64_t)ws_bytes >= syncfree_ws_bytes((n_users + n_items) * 32) &&
+                       n < INT32_MAX / 2;
+    const bool wide = lv->L_host > 0 && n >= 8 * lv->L_host;
+    if (sf_ok && (mode == 2 || (mode == 0 && wide)))
+        return launch_mf_syncfree(op, lv->prev_nz, n, n_users, n_items, lv->L_host, ws, s);
     return launch_levels(op, lv, n_users + n_items, false, static_cast<Ctrl *>(ws), s);
 }
 

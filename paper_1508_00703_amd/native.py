@@ -236,7 +236,7 @@ def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, r
     if U.numel() < n_users * rank or V.numel() < n_items * rank:
         raise ValueError("U / V too small")
     if ws is None:
-        ws = workspace(pdb_epoch_workspace_bytes(n_users + n_items), U.device)
+        ws = workspace(pdb_epoch_workspace_bytes((n_users + n_items) * rank), U.device)
     _check(load().pdb_mf_epoch(_ptr(user), _ptr(item), _ptr(rating), n, _ptr(U), n_users,
                                _ptr(V), n_items, rank, ctypes.c_float(lr), ctypes.c_float(reg),
                                ctypes.byref(levels.c()), _ptr(ws), ws.numel(),

@@ -120,7 +120,9 @@ def test_epoch_with_oracle_schedule(gpu, cfg):
     check_sgd(native, gpu, g, lv)
 
 
-def test_mf_scaled(gpu):
+@pytest.mark.parametrize("mode", ["0"] + EPOCH_MODES)
+def test_mf_scaled(gpu, mode, monkeypatch):
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
@@ -381,3 +383,29 @@ def test_spine_random_exceptions(gpu, seed):
     assert info["method_used"] == 3
     # exceptional rows raised the spine above its own length
     assert lv.L_host > np.bincount(col).max()
+
+
+@pytest.mark.parametrize("mode", EPOCH_MODES)
+def test_mf_structured_pairs(gpu, mode, monkeypatch):
+    """Ratings whose neighbours share a user or an item (a wave takes two
+    ratings at once only when the second does not depend on the first),
+    repeated users and items, and a hot item."""
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+    native = native_mod()
+    rng = np.random.default_rng(77)
+    n, nu, ni = 2000, 40, 25
+    user = rng.integers(0, nu, size=n).astype(np.int32)
+    item = rng.integers(0, ni, size=n).astype(np.int32)
+    user[1::7] = user[0::7][:len(user[1::7])]      # same user as the rating before
+    item[2::5] = item[1::5][:len(item[2::5])]      # same item as the rating before
+    item[::3] = 0                                  # a hot item
+    row_ptr = np.arange(0, 2 * n + 1, 2, dtype=np.int64)
+    col = np.empty(2 * n, np.int32)
+    col[0::2] = user
+    col[1::2] = item + nu
+    g = dict(user=user, item=item, rating=rng.normal(size=n).astype(np.float32),
+             U0=(0.2 * rng.normal(size=(nu, 32))).astype(np.float32),
+             V0=(0.2 * rng.normal(size=(ni, 32))).astype(np.float32),
+             n=n, n_users=nu, n_items=ni, rank=32, lr=np.float32(0.01), reg=np.float32(0.05))
+    lv, _ = check_schedule(native, gpu, row_ptr, col, nu + ni, 0)
+    check_mf(native, gpu, g, lv)
