@@ -883,9 +883,18 @@ __global__ void k_wv_out(const unsigned long long *__restrict__ wv, float *__res
         w[f] = wv_value(wv[f]);
 }
 
-// Sleeps about 2^min(round, 6) x 64 cycles (s_sleep takes a constant).
+// Access to the packed words: device-scope atomics (a relaxed 64-bit load or
+// store is single-copy atomic, so the tag and the value always match).
+__device__ __forceinline__ unsigned long long wv_get(unsigned long long *base, int64_t i) {
+    return __hip_atomic_load(&base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void wv_put(unsigned long long *base, int64_t i, unsigned long long v) {
+    __hip_atomic_store(&base[i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Sleeps about 2^min(round, 3) x 64 cycles (s_sleep takes a constant).
 __device__ __forceinline__ void wave_backoff(int round) {
-    switch (round < 6 ? round : 6) {
+    switch (round < 3 ? round : 3) {
         case 0: __builtin_amdgcn_s_sleep(1); break;
         case 1: __builtin_amdgcn_s_sleep(2); break;
         case 2: __builtin_amdgcn_s_sleep(4); break;
@@ -896,38 +905,40 @@ __device__ __forceinline__ void wave_backoff(int round) {
     }
 }
 
-// The word of feature c once entry p's previous writer pn has written it;
-// false on timeout or abort.
-__device__ __forceinline__ bool wv_wait(unsigned long long *wv, int c, int pn,
-                                        unsigned long long *out, Ctrl *ctrl, int64_t timeout) {
-    unsigned long long v =
-        __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if ((int)(unsigned)(v >> 32) == pn) {
-        *out = v;
-        return true;
-    }
-    const int64_t t0 = now_ticks();
-    int idle = 0;
-    for (;;) {
+// Polls words idx (one per lane; lanes with want = false take part in the
+// rounds only) until each carries tag; the whole wave backs off while
+// nothing arrives, so waves far from the frontier barely load the memory
+// system.  False on timeout or abort.
+__device__ __forceinline__ bool wv_wait_wave(unsigned long long *base, bool want, int64_t idx, int tag,
+                                             unsigned long long *out, Ctrl *ctrl,
+                                             int64_t timeout) {
+    bool ready = !want;
+    int64_t t0 = 0;
+    for (int round = 0;; ++round) {
+        if (!ready) {
+            const unsigned long long v = wv_get(base, idx);
+            if ((int)(unsigned)(v >> 32) == tag) {
+                *out = v;
+                ready = true;
+            }
+        }
+        if (__ballot(!ready) == 0ull) return true;
+        if (round == 0) t0 = now_ticks();
         if (aborted(ctrl)) return false;
         if (now_ticks() - t0 > timeout) {
             record_error(ctrl, DERR_WAIT_TIMEOUT);
             return false;
         }
-        if (++idle < 16) __builtin_amdgcn_s_sleep(1);
-        else __builtin_amdgcn_s_sleep(8);
-        v = __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if ((int)(unsigned)(v >> 32) == pn) {
-            *out = v;
-            return true;
-        }
+        wave_backoff(round);
+        compiler_fence();  // the next round loads again
     }
 }
 
 template <int LOSS, bool VAL>
 __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
-                                                         unsigned long long *wv, int64_t n,
-                                                         Ctrl *ctrl, int64_t timeout) {
+                                                         unsigned long long *wv, int64_t d,
+                                                         int64_t n, Ctrl *ctrl, int64_t timeout) {
+    (void)d;
     const int lane = lane_id();
     for (;;) {
         long long tk = 0;
@@ -939,65 +950,40 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
             const int64_t b = op.row_ptr[i];
             const int m = (int)(op.row_ptr[i + 1] - b);
             const float yi = op.y[i];
-            int bad = 0;
             if (m <= kWave) {
                 int c = 0, pn = -1;
-                float x = 1.0f, wold = 0.0f, acc = 0.0f;
+                float x = 1.0f;
                 if (lane < m) {
                     c = op.col[b + lane];
                     pn = op.prev_nz[b + lane];
                     if (VAL) x = op.val[b + lane];
                 }
-                // the whole wave polls its features in rounds, backing off
-                // while nothing arrives (waiting waves far from the frontier
-                // then barely load the memory system)
-                bool ready = lane >= m;
-                int64_t t0 = 0;
-                for (int round = 0;; ++round) {
-                    if (!ready) {
-                        const unsigned long long v =
-                            __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        if ((int)(unsigned)(v >> 32) == pn) {
-                            wold = wv_value(v);
-                            ready = true;
-                        }
-                    }
-                    if (__ballot(!ready) == 0ull) break;
-                    if (round == 0) t0 = now_ticks();
-                    if (aborted(ctrl)) return;
-                    if (now_ticks() - t0 > timeout) {
-                        record_error(ctrl, DERR_WAIT_TIMEOUT);
-                        return;
-                    }
-                    wave_backoff(round);
-                }
-                if (lane < m) acc = __builtin_fmaf(wold, x, 0.0f);
+                unsigned long long v = 0;
+                if (!wv_wait_wave(wv, lane < m, c, pn, &v, ctrl, timeout)) return;
+                const float wold = wv_value(v);
+                const float acc = lane < m ? __builtin_fmaf(wold, x, 0.0f) : 0.0f;
                 const float s = sgd_scale<LOSS>(butterfly64(acc), yi, op.lr);
                 if (lane < m)
-                    __hip_atomic_store(&wv[c], wv_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    wv_put(wv, c, wv_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)));
             } else {
                 float acc = 0.0f;
-                for (int k = lane; k < m; k += kWave) {
-                    const int c = op.col[b + k];
+                for (int k0 = 0; k0 < m; k0 += kWave) {
+                    const int k = k0 + lane;
+                    const bool live = k < m;
+                    const int c = live ? op.col[b + k] : 0;
+                    const int pn = live ? op.prev_nz[b + k] : -1;
                     unsigned long long v = 0;
-                    if (!wv_wait(wv, c, op.prev_nz[b + k], &v, ctrl, timeout)) {
-                        bad = 1;
-                        break;
-                    }
-                    acc = __builtin_fmaf(wv_value(v), VAL ? op.val[b + k] : 1.0f, acc);
+                    if (!wv_wait_wave(wv, live, c, pn, &v, ctrl, timeout)) return;
+                    if (live) acc = __builtin_fmaf(wv_value(v), VAL ? op.val[b + k] : 1.0f, acc);
                 }
-                if (__ballot(bad) != 0ull) return;
                 const float s = sgd_scale<LOSS>(butterfly64(acc), yi, op.lr);
                 // nothing else writes these features before this example does
                 for (int k = lane; k < m; k += kWave) {
                     const int c = op.col[b + k];
-                    const float wold = wv_value(
-                        __hip_atomic_load(&wv[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                    __hip_atomic_store(&wv[c],
-                                       wv_pack(__builtin_fmaf(-s, VAL ? op.val[b + k] : 1.0f, wold),
-                                               (int)(b + k)),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const float wold = wv_value(wv_get(wv, c));
+                    wv_put(wv, c,
+                               wv_pack(__builtin_fmaf(-s, VAL ? op.val[b + k] : 1.0f, wold),
+                                       (int)(b + k)));
                 }
             }
         }
@@ -1022,10 +1008,11 @@ __device__ __forceinline__ int prev_rating(const int32_t *prev_nz, int64_t e) {
 __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
     const int32_t *__restrict__ user, const int32_t *__restrict__ item,
     const float *__restrict__ rating, const int32_t *__restrict__ prev_nz,
-    unsigned long long *uw, unsigned long long *vw, int64_t n, float lr, float reg, Ctrl *ctrl,
-    int64_t timeout) {
+    unsigned long long *uvw, int64_t n_users, int64_t n_items, int64_t n, float lr, float reg,
+    Ctrl *ctrl, int64_t timeout) {
+    (void)n_items;
     const int lane = lane_id();
-    const int h = lane >> 5, j = lane & 31;
+    const int h = lane >> 5, j = lane & 31;  // user rows first, then item rows, 32 words each
     for (;;) {
         long long tk = 0;
         if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kSyncMfB);
@@ -1043,85 +1030,72 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
             float r = 0.0f;
             if (valid) {
                 uo = (int64_t)user[tt] * 32 + j;
-                vo = (int64_t)item[tt] * 32 + j;
+                vo = (n_users + (int64_t)item[tt]) * 32 + j;
                 tu = prev_rating(prev_nz, 2 * tt);
                 ti = prev_rating(prev_nz, 2 * tt + 1);
                 r = rating[tt];
             }
-            float uj = 0.0f, vj = 0.0f;
-            bool got_u = !valid, got_v = !valid;
-            int64_t t0 = 0;
-            for (int round = 0;; ++round) {
-                if (!got_u) {
-                    const unsigned long long v =
-                        __hip_atomic_load(&uw[uo], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if ((int)(unsigned)(v >> 32) == tu) {
-                        uj = wv_value(v);
-                        got_u = true;
-                    }
-                }
-                if (!got_v) {
-                    const unsigned long long v =
-                        __hip_atomic_load(&vw[vo], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if ((int)(unsigned)(v >> 32) == ti) {
-                        vj = wv_value(v);
-                        got_v = true;
-                    }
-                }
-                if (__ballot(!(got_u && got_v)) == 0ull) break;
-                if (round == 0) t0 = now_ticks();
-                if (aborted(ctrl)) return;
-                if (now_ticks() - t0 > timeout) {
-                    record_error(ctrl, DERR_WAIT_TIMEOUT);
-                    return;
-                }
-                wave_backoff(round);
-            }
+            unsigned long long u = 0, v = 0;
+            if (!wv_wait_wave(uvw, valid, uo, tu, &u, ctrl, timeout)) return;
+            if (!wv_wait_wave(uvw, valid, vo, ti, &v, ctrl, timeout)) return;
+            const float uj = valid ? wv_value(u) : 0.0f, vj = valid ? wv_value(v) : 0.0f;
             const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
             if (valid) {
                 const float a = err * vj, b = reg * uj;
                 const float a2 = err * uj, b2 = reg * vj;
-                __hip_atomic_store(&uw[uo], wv_pack(__builtin_fmaf(lr, a - b, uj), (int)tt),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&vw[vo], wv_pack(__builtin_fmaf(lr, a2 - b2, vj), (int)tt),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                wv_put(uvw, uo, wv_pack(__builtin_fmaf(lr, a - b, uj), (int)tt));
+                wv_put(uvw, vo, wv_pack(__builtin_fmaf(lr, a2 - b2, vj), (int)tt));
             }
             t += count;
         }
     }
 }
 
-int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_t n_users,
-                       int64_t n_items, int64_t L, void *ws, hipStream_t s) {
-    Ctrl *ctrl = static_cast<Ctrl *>(ws);
-    unsigned long long *uw =
-        reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
-    unsigned long long *vw = uw + n_users * 32;
-    const int64_t timeout = spin_timeout_ticks();
-    k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
-    PDB_LAUNCHED();
-    if (n_users > 0) k_wv_in<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(op.U, uw, n_users * 32);
-    if (n_items > 0) k_wv_in<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(op.V, vw, n_items * 32);
-    PDB_LAUNCHED();
-    const void *fn = reinterpret_cast<const void *>(&k_mf_syncfree);
+// Grid of a sync-free kernel: every block resident (a wave spinning on a
+// writer never keeps that writer's wave from running) and about 8 levels'
+// worth of examples in flight (more only adds waiting waves).
+int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *grid) {
     int dev = 0, cus = 0, per_cu = 0;
     PDB_HIP(hipGetDevice(&dev));
     PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
     PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0));
     const int64_t width = L > 0 ? cdiv(n, L) : n;
-    int64_t grid = std::min<int64_t>((int64_t)cus * std::max(per_cu, 1),
-                                     cdiv(n, (int64_t)kSyncMfB * kWavesPerBlock));
-    grid = std::min<int64_t>(grid, std::max<int64_t>(cdiv(8 * width, 2 * kWavesPerBlock), cus));
-    k_mf_syncfree<<<(unsigned)std::max<int64_t>(grid, 1), kBlock, 0, s>>>(
-        op.user, op.item, op.rating, prev_nz, uw, vw, n, op.lr, op.reg, ctrl, timeout);
-    PDB_LAUNCHED();
-    if (n_users > 0) k_wv_out<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(uw, op.U, n_users * 32);
-    if (n_items > 0) k_wv_out<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(vw, op.V, n_items * 32);
-    PDB_LAUNCHED();
+    int64_t g = std::min<int64_t>((int64_t)cus * std::max(per_cu, 1), cdiv(n, per_block));
+    g = std::min<int64_t>(g, std::max<int64_t>(cdiv(8 * width, per_block), cus));
+    *grid = std::max<int64_t>(g, 1);
     return PDB_OK;
 }
 
-
+int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_t n_users,
+                       int64_t n_items, int64_t L, void *ws, hipStream_t s) {
+    Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    unsigned long long *uvw =
+        reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
+    const int64_t timeout = spin_timeout_ticks();
+    k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
+    PDB_LAUNCHED();
+    if (n_users > 0)
+        k_wv_in<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(op.U, uvw, n_users * 32);
+    if (n_items > 0)
+        k_wv_in<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(op.V, uvw + n_users * 32,
+                                                                       n_items * 32);
+    PDB_LAUNCHED();
+    const void *fn = reinterpret_cast<const void *>(&k_mf_syncfree);
+    int64_t grid = 1;
+    int rc = syncfree_grid(fn, n, L, 2 * kWavesPerBlock, &grid);
+    if (rc != PDB_OK) return rc;
+    k_mf_syncfree<<<(unsigned)grid, kBlock, 0, s>>>(op.user, op.item, op.rating, prev_nz, uvw,
+                                                    n_users, n_items, n, op.lr, op.reg, ctrl,
+                                                    timeout);
+    PDB_LAUNCHED();
+    if (n_users > 0)
+        k_wv_out<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(uvw, op.U, n_users * 32);
+    if (n_items > 0)
+        k_wv_out<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(uvw + n_users * 32, op.V,
+                                                                        n_items * 32);
+    PDB_LAUNCHED();
+    return PDB_OK;
+}
 
 template <int LOSS, bool VAL>
 int launch_syncfree(const SgdOp<LOSS, VAL> &op, int64_t n, int64_t d, int64_t L, void *ws,
@@ -1137,19 +1111,10 @@ int launch_syncfree(const SgdOp<LOSS, VAL> &op, int64_t n, int64_t d, int64_t L,
         PDB_LAUNCHED();
     }
     const void *fn = reinterpret_cast<const void *>(&k_sgd_syncfree<LOSS, VAL>);
-    int dev = 0, cus = 0, per_cu = 0;
-    PDB_HIP(hipGetDevice(&dev));
-    PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0));
-    // every block resident (a wave spinning on a writer never keeps that
-    // writer's wave from running), and about 8 levels' worth of examples in
-    // flight: more would only add waiting waves
-    const int64_t width = L > 0 ? cdiv(n, L) : n;
-    int64_t grid = std::min<int64_t>((int64_t)cus * std::max(per_cu, 1),
-                                     cdiv(n, (int64_t)kSyncB * kWavesPerBlock));
-    grid = std::min<int64_t>(grid, std::max<int64_t>(cdiv(8 * width, kWavesPerBlock), cus));
-    k_sgd_syncfree<LOSS, VAL><<<(unsigned)std::max<int64_t>(grid, 1), kBlock, 0, s>>>(
-        op, wv, n, ctrl, timeout);
+    int64_t grid = 1;
+    int rc = syncfree_grid(fn, n, L, kSyncB * kWavesPerBlock, &grid);
+    if (rc != PDB_OK) return rc;
+    k_sgd_syncfree<LOSS, VAL><<<(unsigned)grid, kBlock, 0, s>>>(op, wv, d, n, ctrl, timeout);
     PDB_LAUNCHED();
     if (d > 0) {
         k_wv_out<<<grid_for(d, kBlock, 8192), kBlock, 0, s>>>(wv, op.w, d);
