@@ -59,12 +59,16 @@ def test_no_examples(gpu):
 EPOCH_MODES = ["1", "2"]  # level by level, sync-free
 
 
+def set_epoch_mode(monkeypatch, mode):
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+
+
 @pytest.mark.parametrize("name", sorted(structured_cases()))
 @pytest.mark.parametrize("loss", [0, 1])
 @pytest.mark.parametrize("with_val", [True, False])
 @pytest.mark.parametrize("mode", EPOCH_MODES)
 def test_structured_epochs(gpu, name, loss, with_val, mode, monkeypatch):
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+    set_epoch_mode(monkeypatch, mode)
     native = native_mod()
     rows = structured_cases()[name]
     row_ptr, col = csr_from_rows(rows)
@@ -103,7 +107,7 @@ def test_config_schedules(gpu, cfg, method):
 @pytest.mark.parametrize("cfg", sorted(SCALED))
 @pytest.mark.parametrize("mode", ["0"] + EPOCH_MODES)
 def test_config_epochs(gpu, cfg, mode, monkeypatch):
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+    set_epoch_mode(monkeypatch, mode)
     native = native_mod()
     g = datagen.generate(cfg, **SCALED[cfg])
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
@@ -122,7 +126,7 @@ def test_epoch_with_oracle_schedule(gpu, cfg):
 
 @pytest.mark.parametrize("mode", ["0"] + EPOCH_MODES)
 def test_mf_scaled(gpu, mode, monkeypatch):
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+    set_epoch_mode(monkeypatch, mode)
     native = native_mod()
     g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
@@ -390,7 +394,7 @@ def test_mf_structured_pairs(gpu, mode, monkeypatch):
     """Ratings whose neighbours share a user or an item (a wave takes two
     ratings at once only when the second does not depend on the first),
     repeated users and items, and a hot item."""
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+    set_epoch_mode(monkeypatch, mode)
     native = native_mod()
     rng = np.random.default_rng(77)
     n, nu, ni = 2000, 40, 25
