@@ -44,12 +44,13 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 // e^x for x <= 87 (larger x count as 87): k = rint(x log2 e), r = x - k ln 2
 // with ln 2 in two binary32 pieces, e^r from its Taylor series through r^7
 // by Estrin's scheme (pairs c_j + c_{j+1} r, combined with r^2, then r^4),
-// times 2^k by ldexp: one rounding into the subnormals.
+// times 2^k by ldexp: one rounding into the subnormals.  A NaN x gives some
+// finite value: the callers carry NaN past this function (logistic_grad), so
+// that no select sits on the serial path of a dependent chain.
 __device__ __forceinline__ float dev_exp87(float x) {
-    // branch-free: the arithmetic runs on x clamped to [-104, 87]; below the
-    // bottom that gives the same answer (e^-104 rounds to 0), only NaN needs a
-    // select
-    const float xc = __builtin_fminf(__builtin_fmaxf(x, -104.0f), 87.0f);
+    // branch-free: the arithmetic runs on x clamped to [-104, 87] (one med3);
+    // below the bottom that gives the same answer (e^-104 rounds to 0)
+    const float xc = __builtin_amdgcn_fmed3f(x, -104.0f, 87.0f);
     const float kf = __builtin_rintf(xc * 0x1.715476p+0f);
     float r = __builtin_fmaf(-kf, 0x1.62e430p-1f, xc);
     r = __builtin_fmaf(-kf, -0x1.05c610p-29f, r);
@@ -62,8 +63,7 @@ __device__ __forceinline__ float dev_exp87(float x) {
     const float p03 = __builtin_fmaf(p23, r2, p01);
     const float p47 = __builtin_fmaf(p67, r2, p45);
     const float q = __builtin_fmaf(p47, r4, p03);
-    const float e = __builtin_amdgcn_ldexpf(q, (int)kf);
-    return (x == x) ? e : x;
+    return __builtin_amdgcn_ldexpf(q, (int)kf);
 }
 
 // 1/b, correctly rounded, for b in [1, 2^126) (NaN gives NaN): y0 = v_rcp,
@@ -78,10 +78,14 @@ __device__ __forceinline__ float recip_normal(float b) {
     return __builtin_fmaf(__builtin_fmaf(-b, y0, 1.0f), y0, y0);
 }
 
-// The logistic function 1/(1 + e^min(-z, 87)): the cap keeps 1 + e below
-// 2^126 (e^87 < 2^126), where recip_normal is exact.
-__device__ __forceinline__ float dev_sigmoid(float z) {
-    return recip_normal(1.0f + dev_exp87(-z));
+// The gradient factor of the logistic loss, g = 1/(1 + e^min(-z, 87)) - tgt:
+// the cap keeps 1 + e below 2^126 (e^87 < 2^126), where recip_normal is
+// exact.  A NaN z gives a NaN g (the logistic function of NaN is NaN); the
+// NaN enters through the subtrahend, chosen while the exponential is still
+// being evaluated.
+__device__ __forceinline__ float logistic_grad(float z, float tgt) {
+    const float sub = (z == z) ? tgt : -z;
+    return recip_normal(1.0f + dev_exp87(-z)) - sub;
 }
 
 // v + v[partner] with the partner chosen by a DPP lane pattern
@@ -90,29 +94,38 @@ __device__ __forceinline__ float dpp_add(float v) {
     return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 
-// Butterfly p_l <- p_l + p_{l xor o} for o = 1, 2, 4, 8, 16, 32; every lane
-// ends with the common result.  o = 1, 2: quad permutations.  o = 4: mirror
-// within each group of 8 lanes -- once the quads hold equal values the
-// mirrored partner holds the same value as lane l xor 4.  o = 8: mirror within
-// each row of 16, likewise.  o = 16: the row swap pairs rows 0-1 and 2-3;
-// o = 32: the half swap pairs the two halves.  Bitwise the xor butterfly.
-__device__ __forceinline__ float butterfly64(float v) {
+// Intra-row part of the butterfly p_l <- p_l + p_{l xor o}, o = 1, 2, 4, 8:
+// o = 1, 2 are quad permutations; o = 4 is the mirror within each group of 8
+// lanes -- once the quads hold equal values the mirrored partner holds the
+// same value as lane l xor 4; o = 8 is the mirror within each row of 16,
+// likewise.  Every lane of row r ends with the row's sum R_r.
+__device__ __forceinline__ float butterfly16(float v) {
     v = dpp_add<0xB1>(v);   // quad_perm [1,0,3,2]
     v = dpp_add<0x4E>(v);   // quad_perm [2,3,0,1]
     v = dpp_add<0x141>(v);  // row_half_mirror
-    v = dpp_add<0x140>(v);  // row_mirror
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-    const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return __uint_as_float(h[0]) + __uint_as_float(h[1]);
+    return dpp_add<0x140>(v);  // row_mirror
 }
 
-// The same over each 32-lane half (o = 1..16); lanes of half h get half h's sum.
+// Sum over the 64 lanes, bitwise the xor butterfly for o = 1, ..., 32, whose
+// common result is (R_0 + R_1) + (R_2 + R_3).  After the intra-row part,
+// row_bcast:15 adds lane 15 of the previous row (row 3 then holds R_3 + R_2,
+// row 1 R_1 + R_0) and row_bcast:31 adds lane 31 to rows 2 and 3, so lane 63
+// holds (R_3 + R_2) + (R_1 + R_0): the same sums, each with its operands
+// swapped, which IEEE addition does not notice.  Rows without a source lane
+// add their own value; they are not read.  The result is read out of lane 63
+// as a wave-uniform value: two DPP adds and a readlane instead of two
+// cross-row swaps.
+__device__ __forceinline__ float wave_sum64(float v) {
+    v = butterfly16(v);
+    v = dpp_add<0x142>(v);  // row_bcast:15
+    v = dpp_add<0x143>(v);  // row_bcast:31
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// The butterfly over each 32-lane half (o = 1..16); lanes of half h get half
+// h's sum R_{2h} + R_{2h+1} (the row swap pairs rows 0-1 and 2-3).
 __device__ __forceinline__ float butterfly32(float v) {
-    v = dpp_add<0xB1>(v);
-    v = dpp_add<0x4E>(v);
-    v = dpp_add<0x141>(v);
-    v = dpp_add<0x140>(v);
+    v = butterfly16(v);
     const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
@@ -121,7 +134,7 @@ template <int LOSS>
 __device__ __forceinline__ float sgd_scale(float z, float y, float lr) {
     float g;
     if (LOSS == PDB_LOGISTIC) {
-        g = dev_sigmoid(z) - (y > 0.0f ? 1.0f : 0.0f);
+        g = logistic_grad(z, y > 0.0f ? 1.0f : 0.0f);
     } else {
         g = z - y;
     }
@@ -157,7 +170,7 @@ struct SgdOp {
                 wv = w[c];
                 acc = __builtin_fmaf(wv, x, 0.0f);
             }
-            const float s = sgd_scale<LOSS>(butterfly64(acc), yi, lr);
+            const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, lr);
             if (lane < m) w[c] = __builtin_fmaf(-s, x, wv);
         } else {
             float acc = 0.0f;
@@ -165,7 +178,7 @@ struct SgdOp {
                 const int c = col[b + k];
                 acc = __builtin_fmaf(w[c], VAL ? val[b + k] : 1.0f, acc);
             }
-            const float s = sgd_scale<LOSS>(butterfly64(acc), yi, lr);
+            const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, lr);
             // no other example of this level touches these features and this
             // one has not written yet: w[c] still holds the value read above
             for (int k = lane; k < m; k += kWave) {
@@ -220,6 +233,10 @@ constexpr int kRB = 64;          // staged examples (power of two, >= 2 kD + kPB
 constexpr int kPB = 16;          // examples per producer batch
 constexpr int kRing = kD * 64;   // LDS ring of recent cold writes
 constexpr int kChainMin = 32;    // shorter runs take the plain path
+// staged records the consumer holds in registers (examples t, t+1, t+2): a
+// slot is read a full step before its read source is needed, so the LDS
+// latency of that read never stalls the chain
+constexpr int kMirror = 3;
 // buffer offset past the end of any weight vector: a load there returns 0
 // and a store is dropped (buffer range checking), so lanes with nothing to
 // load or store still issue the instruction
@@ -241,11 +258,11 @@ struct ChainShared {
     // LDS address to read (cache, ring, zero[0] for lanes without an entry).
     // The write address is the cache slot of a hot feature, the ring slot of
     // a cold one, or lsink.  The write offset has bit 31 set (out of range:
-    // dropped) unless the feature is cold.  Slots kRB and kRB + 1 repeat
-    // slots 0 and 1, so that the consumer reads a block of kD + 2
+    // dropped) unless the feature is cold.  Slots kRB .. kRB + 2 repeat
+    // slots 0 .. 2, so that the consumer reads a block of kD + 3
     // consecutive slots without wrapping.
-    uint4 st[(kRB + 2) * 64];
-    float mt_t[kRB + 2];  // target: [y > 0] (logistic) or y (least squares)
+    uint4 st[(kRB + kMirror) * 64];
+    float mt_t[kRB + kMirror];  // target: [y > 0] (logistic) or y (least squares)
     int seq[kRB];         // position t staged in the slot, ~t when its example has more
                           // than 64 entries, INT_MIN none
     int ctl[4];           // [0] consumer no longer needs positions < ctl[0]; [1] stop
@@ -273,7 +290,7 @@ template <int LOSS>
 __device__ __forceinline__ float sgd_scale_t(float z, float tgt, float lr) {
     float g;
     if (LOSS == PDB_LOGISTIC) {
-        g = dev_sigmoid(z) - tgt;
+        g = logistic_grad(z, tgt);
     } else {
         g = z - tgt;
     }
@@ -412,7 +429,11 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
             laddr = is_hot ? cache : laddr;
             laddr = live ? laddr : lsink_a;
             const unsigned goff = ((unsigned)c[i] << 2) | ((live & !is_hot) ? 0u : kOOR);
-            A[i] = make_uint4(__float_as_uint(live ? x[i] : 0.0f), laddr, rd, goff);
+            // without stored values every x is 1 and the word carries the
+            // example's target instead, saving the consumer a read
+            const unsigned xw = VAL ? __float_as_uint(live ? x[i] : 0.0f)
+                                    : (unsigned)__builtin_amdgcn_readlane(__float_as_int(tg), kD + i);
+            A[i] = make_uint4(xw, laddr, rd, goff);
         }
         const int sb = (int)(t0 & (kRB - 1));  // a multiple of kPB: no wrap inside the batch
 #pragma unroll
@@ -420,6 +441,7 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
         if (sb == 0) {
             S.st[kRB * 64 + lane] = A[0];
             S.st[(kRB + 1) * 64 + lane] = A[1];
+            S.st[(kRB + 2) * 64 + lane] = A[2];
         }
         {
             // every lane stores (lanes outside the batch into the sink), so
@@ -428,7 +450,7 @@ __device__ void chain_producer(const SgdOp<LOSS, VAL> &op, int pid, int64_t e_be
             const int slot = sb + lane - kD;
             const int64_t q = t0 - kD + lane;  // the position this lane describes
             lds_write(in_batch ? lds_addr(&S.mt_t[slot]) : lsink_a, tg);
-            lds_write((in_batch && slot < 2) ? lds_addr(&S.mt_t[kRB + slot]) : lsink_a, tg);
+            lds_write((in_batch && slot < kMirror) ? lds_addr(&S.mt_t[kRB + slot]) : lsink_a, tg);
             compiler_fence();  // LDS executes one wave's operations in order
             if (in_batch && q < len)
                 lds_store(&S.seq[slot], m > kWave ? ~(int)q : (int)q);
@@ -466,7 +488,7 @@ struct Stg {
     float t;  // target
 };
 
-// slot in [0, kRB + 2)
+// slot in [0, kRB + kMirror)
 __device__ __forceinline__ Stg read_slot(const ChainShared &S, int slot) {
     Stg r;
     r.a = S.st[slot * 64 + lane_id()];
@@ -474,7 +496,7 @@ __device__ __forceinline__ Stg read_slot(const ChainShared &S, int slot) {
     return r;
 }
 
-// The staged slots of one consumer block (kD + 2 consecutive slots from sb):
+// The staged slots of one consumer block (kD + 3 consecutive slots from sb):
 // LDS addresses of this lane's first record and of the first target, so that
 // every read in the block is that address plus a constant offset.
 struct SlotBlock {
@@ -491,18 +513,19 @@ __device__ __forceinline__ SlotBlock slot_block(const ChainShared &S, int sb) {
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-template <int K>
+// the target is read only with stored values (else the x word holds it)
+template <int K, bool VAL>
 __device__ __forceinline__ Stg read_slot_at(SlotBlock b) {
     const u32x4 v =
         *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(b.st + K * 64 * 16);
     Stg r;
     r.a = make_uint4(v.x, v.y, v.z, v.w);
-    r.t = lds_read(b.mt + K * 4);
+    r.t = VAL ? lds_read(b.mt + K * 4) : 0.0f;
     return r;
 }
 
 struct ChainState {
-    Stg cur, nxt;                 // examples t and t+1
+    Stg cur, nxt, nxt2;           // examples t, t+1 and t+2
     float cur_v, cur_fw, cur_fx;  // example t's weight, or the forwarded (w_old, x) pair
     bool cur_fwd;
     float s_prev;                 // step of example t-1
@@ -526,14 +549,19 @@ template <int SL, int LOSS, bool VAL>
 __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL> &op,
                                            SlotBlock sblk, __amdgpu_buffer_rsrc_t wbuf,
                                            unsigned gsrc_a) {
-    const float x = __uint_as_float(st.cur.a.x);
+    // without stored values every x is 1 and the x word is the target
+    const float x = VAL ? __uint_as_float(st.cur.a.x) : 1.0f;
+    const float tgt = VAL ? st.cur.t : __uint_as_float(st.cur.a.x);
     // (a) example t-1's step lands: its new weights, and this example's
     // weights (forwarded lanes apply that step to the pair they took)
     const float w_prev = __builtin_fmaf(-st.s_prev, st.p_x, st.p_wold);
     const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
-    const float acc = __builtin_fmaf(w_old, x, 0.0f);
+    // binary logistic: the product w * 1 + 0 differs from w only for w = -0,
+    // which changes z at most in the sign of a zero sum, and the logistic
+    // function is the same at +0 and -0; lanes without an entry hold 0
+    const float acc = (!VAL && LOSS == PDB_LOGISTIC) ? w_old : __builtin_fmaf(w_old, x, 0.0f);
     // (b) writes of example t-1; example t+1's weights (those example t
-    // writes are forwarded), the staged example t+2, and the cold values of
+    // writes are forwarded), the staged example t+3, and the cold values of
     // example t+kD (their last writers are before t)
     lds_write(st.p_l, w_prev);
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_prev), wbuf, st.p_g, 0, 0);
@@ -543,10 +571,10 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     // without stored values every x is 1: nothing to forward
     const float fx1 =
         VAL ? __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x))) : 1.0f;
-    const Stg nxt2 = read_slot_at<SL + 2>(sblk);
+    const Stg nxt3 = read_slot_at<SL + 3, VAL>(sblk);
     const float g_pf = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
     // (c) the step of example t
-    const float s = sgd_scale_t<LOSS>(butterfly64(acc), st.cur.t, op.lr);
+    const float s = sgd_scale_t<LOSS>(wave_sum64(acc), tgt, op.lr);
     // rotation
     st.p_wold = w_old;
     st.p_x = x;
@@ -559,7 +587,8 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     st.cur_fw = fw1;
     st.cur_fx = fx1;
     st.cur_fwd = rd < 256u;
-    st.nxt = nxt2;
+    st.nxt = st.nxt2;
+    st.nxt2 = nxt3;
 }
 
 // Writes the last example's new weights.
@@ -606,6 +635,7 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
         st.gv[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[j], 0, 0));
     st.cur = read_slot(S, 0);
     st.nxt = read_slot(S, 1);
+    st.nxt2 = read_slot(S, 2);
     st.cur_v = (st.cur.a.z == gsrc_a) ? st.gv[0] : lds_read(st.cur.a.z);
     st.cur_fw = st.cur_fx = 0.0f;
     st.cur_fwd = false;
@@ -962,7 +992,7 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
                 if (!wv_wait_wave(wv, lane < m, c, pn, &v, ctrl, timeout)) return;
                 const float wold = wv_value(v);
                 const float acc = lane < m ? __builtin_fmaf(wold, x, 0.0f) : 0.0f;
-                const float s = sgd_scale<LOSS>(butterfly64(acc), yi, op.lr);
+                const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
                 if (lane < m)
                     wv_put(wv, c, wv_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)));
             } else {
@@ -976,7 +1006,7 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
                     if (!wv_wait_wave(wv, live, c, pn, &v, ctrl, timeout)) return;
                     if (live) acc = __builtin_fmaf(wv_value(v), VAL ? op.val[b + k] : 1.0f, acc);
                 }
-                const float s = sgd_scale<LOSS>(butterfly64(acc), yi, op.lr);
+                const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
                 // nothing else writes these features before this example does
                 for (int k = lane; k < m; k += kWave) {
                     const int c = op.col[b + k];
