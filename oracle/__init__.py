@@ -14,6 +14,11 @@ What it computes (all single-threaded, binary32 arithmetic, see oracle.c):
     feature, and per-feature occurrence lists;
   * ``sgd_epoch`` / ``mf_epoch``: the sequential computation of Algorithm 1,
     one example per iteration (Sec. 6.3), with the gradient step of Sec. 2.
+  * ``batch_levels_brute`` / ``batch_levels_seq`` / ``batch_union`` /
+    ``batch_epoch``: the same with a mini-batch of B examples per iteration
+    (Sec. 6.3's mini-batch gradient descent): batch levels, each batch's
+    union of features with its occurrences in example order, and the
+    sequential mini-batch epoch.
   * ``history``: the execution-history predicates of Definition 4 and
     Sec. 4.3-4.4 (see ``oracle.history``).
 
@@ -71,6 +76,14 @@ def _load():
     lib.orc_sgd_apply.restype = None
     lib.orc_mf_apply.argtypes = [i64, P, P, P, P, P, P, i32, f32, f32, i32]
     lib.orc_mf_apply.restype = None
+    lib.orc_batch_levels_brute.argtypes = [i64, P, P, i64, P]
+    lib.orc_batch_levels_brute.restype = i32
+    lib.orc_batch_levels_seq.argtypes = [i64, i64, P, P, i64, P]
+    lib.orc_batch_levels_seq.restype = i32
+    lib.orc_batch_union.argtypes = [i64, i64, P, P, i64, P, P, P, P]
+    lib.orc_batch_union.restype = i64
+    lib.orc_batch_apply.argtypes = [i64, i64, P, P, P, P, P, P, f32, i32, i32, i64]
+    lib.orc_batch_apply.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -191,3 +204,74 @@ def mf_epoch(user, item, rating, U, V, lr, reg, mode=MATCHED, order=None, count=
     _load().orc_mf_apply(cnt, _ptr(order), _ptr(user), _ptr(item), _ptr(rating), _ptr(U), _ptr(V),
                          rank, np.float32(lr), np.float32(reg), mode)
     return U, V
+
+
+def n_batches(n, B):
+    return (n + B - 1) // B
+
+
+def batch_levels_brute(row_ptr, col, B):
+    """Batch levels from the definition (tiny inputs)."""
+    row_ptr = _c(row_ptr, np.int64)
+    col = _c(col, np.int32)
+    n = len(row_ptr) - 1
+    level = np.empty(n_batches(n, B), dtype=np.int32)
+    L = _load().orc_batch_levels_brute(n, _ptr(row_ptr), _ptr(col), B, _ptr(level))
+    return level, int(L)
+
+
+def batch_levels_seq(row_ptr, col, d, B):
+    row_ptr = _c(row_ptr, np.int64)
+    col = _c(col, np.int32)
+    n = len(row_ptr) - 1
+    level = np.empty(n_batches(n, B), dtype=np.int32)
+    L = _load().orc_batch_levels_seq(n, d, _ptr(row_ptr), _ptr(col), B, _ptr(level))
+    if L < 0:
+        raise MemoryError
+    return level, int(L)
+
+
+def batch_schedule(row_ptr, col, d, B):
+    """Batch levels, batches grouped by level (perm, level_ptr), L."""
+    level, L = batch_levels_seq(row_ptr, col, d, B)
+    perm, level_ptr = bucket(level, L)
+    return level, perm, level_ptr, L
+
+
+def batch_union(row_ptr, col, d, B):
+    """(bptr, ucol, uptr, occ): batch b's union features are ucol[bptr[b]:bptr[b+1]],
+    ascending; union entry u's occurrences are the CSR entries occ[uptr[u]:uptr[u+1]]
+    in example order."""
+    row_ptr = _c(row_ptr, np.int64)
+    col = _c(col, np.int32)
+    n = len(row_ptr) - 1
+    nnz = len(col)
+    bptr = np.empty(n_batches(n, B) + 1, dtype=np.int64)
+    ucol = np.empty(max(nnz, 1), dtype=np.int32)
+    uptr = np.empty(nnz + 1, dtype=np.int64)
+    occ = np.empty(max(nnz, 1), dtype=np.int32)
+    U = _load().orc_batch_union(n, d, _ptr(row_ptr), _ptr(col), B, _ptr(bptr), _ptr(ucol),
+                                _ptr(uptr), _ptr(occ))
+    if U < 0:
+        raise MemoryError
+    return bptr, ucol[:U], uptr[:U + 1], occ[:nnz]
+
+
+def batch_epoch(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, B=100, order=None):
+    """One epoch of mini-batch gradient descent on a copy of w.  order: None =
+    batches 0..nb-1 (the sequential computation), else the batch sequence."""
+    row_ptr = _c(row_ptr, np.int64)
+    col = _c(col, np.int32)
+    val = None if val is None else _c(val, np.float32)
+    y = _c(y, np.float32)
+    w = np.array(w, dtype=np.float32, copy=True)
+    n = len(row_ptr) - 1
+    if order is not None:
+        order = _c(order, np.int32)
+        cnt = len(order)
+    else:
+        cnt = n_batches(n, B)
+    if _load().orc_batch_apply(n, cnt, _ptr(order), _ptr(row_ptr), _ptr(col), _ptr(val), _ptr(y),
+                               _ptr(w), np.float32(lr), loss, mode, B) != 0:
+        raise MemoryError
+    return w

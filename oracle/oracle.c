@@ -275,3 +275,145 @@ void orc_mf_apply(int64_t count, const int32_t *order, const int32_t *user, cons
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Mini-batch gradient descent (Sec. 6.3: gradient descent with a batch of a
+ * fixed number of examples per iteration).  Batch b is examples
+ * [b*B, min((b+1)*B, n)); its parameter set is the union of its examples'
+ * features.  Within an iteration every read precedes every write
+ * (Definition 3), so all examples of a batch see the weights as they were
+ * when the batch started.  The step is the gradient step of Sec. 2 on the
+ * batch's part of h, i.e. the sum of its examples' losses:
+ *   w_f <- w_f - lr * sum_{i in b} g_i x_if,
+ * evaluated as s_i = lr * g_i, then for each example in index order and each
+ * of its entries w[c] = fmaf(-s_i, x, w[c]).  With B = 1 this is the SGD step
+ * above, bit for bit. */
+
+static int batches_share_feature(const int64_t *row_ptr, const int32_t *col, int64_t n,
+                                 int64_t B, int64_t a, int64_t b) {
+    int64_t ae = (a + 1) * B < n ? (a + 1) * B : n, be = (b + 1) * B < n ? (b + 1) * B : n;
+    for (int64_t i = a * B; i < ae; ++i)
+        for (int64_t j = b * B; j < be; ++j)
+            if (rows_share_feature(row_ptr, col, i, j)) return 1;
+    return 0;
+}
+
+/* From the definition: level(b) = 1 + max{ level(a) : a < b, batches a and b
+ * share a feature }, max of the empty set = 0.  Tiny inputs only. */
+int32_t orc_batch_levels_brute(int64_t n, const int64_t *row_ptr, const int32_t *col, int64_t B,
+                               int32_t *level) {
+    int64_t nb = (n + B - 1) / B;
+    int32_t L = 0;
+    for (int64_t b = 0; b < nb; ++b) {
+        int32_t lv = 1;
+        for (int64_t a = 0; a < b; ++a)
+            if (level[a] + 1 > lv && batches_share_feature(row_ptr, col, n, B, a, b)) lv = level[a] + 1;
+        level[b] = lv;
+        if (lv > L) L = lv;
+    }
+    return L;
+}
+
+/* One pass in batch order with last[f] = level of the latest batch that
+ * touched f.  Returns L, -1 on failure. */
+int32_t orc_batch_levels_seq(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                             int64_t B, int32_t *level) {
+    int32_t *last = (int32_t *)calloc((size_t)(d > 0 ? d : 1), sizeof(int32_t));
+    if (!last) return -1;
+    int64_t nb = (n + B - 1) / B;
+    int32_t L = 0;
+    for (int64_t b = 0; b < nb; ++b) {
+        int64_t p0 = row_ptr[b * B], p1 = row_ptr[(b + 1) * B < n ? (b + 1) * B : n];
+        int32_t lv = 0;
+        for (int64_t p = p0; p < p1; ++p)
+            if (last[col[p]] > lv) lv = last[col[p]];
+        lv += 1;
+        for (int64_t p = p0; p < p1; ++p) last[col[p]] = lv;
+        level[b] = lv;
+        if (lv > L) L = lv;
+    }
+    free(last);
+    return L;
+}
+
+static int cmp_i32(const void *a, const void *b) {
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+/* Per batch, the union of its features in ascending order, and for each
+ * union feature the batch's entries on it in example order:
+ *   batch b's union entries are u in [bptr[b], bptr[b+1]), ucol[u] = feature,
+ *   occurrences occ[uptr[u] .. uptr[u+1]) are CSR entry indices.
+ * bptr [nb+1], ucol [nnz], uptr [nnz+1], occ [nnz].  Per batch: the distinct
+ * features, sorted; then a counting sort of the batch's entries by feature,
+ * which keeps each feature's entries in CSR (= example) order.
+ * Returns the union size U, -1 on failure. */
+int64_t orc_batch_union(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                        int64_t B, int64_t *bptr, int32_t *ucol, int64_t *uptr, int32_t *occ) {
+    int64_t *next = (int64_t *)malloc((size_t)(d > 0 ? d : 1) * sizeof(int64_t));
+    if (!next) return -1;
+    for (int64_t f = 0; f < d; ++f) next[f] = -1;
+    int64_t nb = (n + B - 1) / B, U = 0;
+    for (int64_t b = 0; b < nb; ++b) {
+        int64_t p0 = row_ptr[b * B], p1 = row_ptr[(b + 1) * B < n ? (b + 1) * B : n];
+        bptr[b] = U;
+        /* distinct features of the batch (next[f] = 0 marks "seen") */
+        int64_t u0 = U;
+        for (int64_t p = p0; p < p1; ++p)
+            if (next[col[p]] < 0) {
+                next[col[p]] = 0;
+                ucol[U++] = col[p];
+            }
+        qsort(ucol + u0, (size_t)(U - u0), sizeof(int32_t), cmp_i32);
+        /* occurrence counts, then each feature's first slot */
+        for (int64_t p = p0; p < p1; ++p) next[col[p]] += 1;
+        int64_t pos = p0;
+        for (int64_t u = u0; u < U; ++u) {
+            int64_t c = next[ucol[u]];
+            uptr[u] = pos;
+            next[ucol[u]] = pos;
+            pos += c;
+        }
+        for (int64_t p = p0; p < p1; ++p) occ[next[col[p]]++] = (int32_t)p;
+        for (int64_t u = u0; u < U; ++u) next[ucol[u]] = -1;
+    }
+    bptr[nb] = U;
+    uptr[U] = row_ptr[n];
+    free(next);
+    return U;
+}
+
+/* One epoch of mini-batch gradient descent, batches taken in the given order
+ * (NULL: 0..nb-1, the sequential computation).  Returns 0, -1 on failure. */
+int orc_batch_apply(int64_t n, int64_t count, const int32_t *order, const int64_t *row_ptr,
+                    const int32_t *col, const float *val, const float *y, float *w, float lr,
+                    int32_t loss, int32_t mode, int64_t B) {
+    float *s = (float *)malloc((size_t)(B > 0 ? B : 1) * sizeof(float));
+    if (!s) return -1;
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t b = order ? order[t] : t;
+        int64_t i0 = b * B, i1 = (b + 1) * B < n ? (b + 1) * B : n;
+        /* reads: every example of the batch against the batch-start weights */
+        for (int64_t i = i0; i < i1; ++i) {
+            int64_t p = row_ptr[i], m = row_ptr[i + 1] - p;
+            const float *v = val ? val + p : NULL;
+            float z = (mode == ORC_MATCHED) ? dot_matched(w, col + p, v, m)
+                                            : dot_natural(w, col + p, v, m);
+            float g;
+            if (loss == ORC_LOGISTIC) {
+                float sig = (mode == ORC_MATCHED) ? orc_sigmoid(z) : 1.0f / (1.0f + expf(-z));
+                g = sig - ((y[i] > 0.0f) ? 1.0f : 0.0f);
+            } else {
+                g = z - y[i];
+            }
+            s[i - i0] = lr * g;
+        }
+        /* writes: each feature's contributions in example order */
+        for (int64_t i = i0; i < i1; ++i)
+            for (int64_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+                w[col[p]] = fmaf(-s[i - i0], val ? val[p] : 1.0f, w[col[p]]);
+    }
+    free(s);
+    return 0;
+}
