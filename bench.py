@@ -31,8 +31,14 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "sequentially-correct nnz-updates/sec per epoch + achieved HBM GB/s fraction"
 
 
-def algorithmic_bytes(g, L, mf=False):
-    """Bytes one epoch must move at least once (the design doc lists the terms)."""
+def algorithmic_bytes(g, L, mf=False, U=None, nb=None):
+    """Bytes one epoch must move at least once.  Mini-batches (U union
+    entries over nb batches): each stored entry's column (and value) once, each
+    example's row bound and label, each union feature's weight read and
+    written once, and the batch order."""
+    if U is not None:
+        per_nz = 4 + (4 if g["val"] is not None else 0)
+        return g["nnz"] * per_nz + g["n"] * (8 + 4) + U * 8 + nb * (4 + 8) + L * 8
     if mf:
         # per rating: user, item, rating, perm (16 B) + read and write of a
         # 128-byte user row and a 128-byte item row (512 B); level_ptr per level
@@ -42,9 +48,11 @@ def algorithmic_bytes(g, L, mf=False):
     return g["nnz"] * per_nz + g["n"] * per_ex + L * 8
 
 
-def source_digest():
+def source_digest(batch=False):
+    """Digest of the sources of the priced epoch kernel: a traffic record
+    taken on other sources is not reported."""
     h = hashlib.sha256()
-    for f in ("apply.hip", "pdb_internal.h"):
+    for f in ("batch.hip" if batch else "apply.hip", "pdb_math.h", "pdb_internal.h"):
         with open(os.path.join(_ROOT, "paper_1508_00703_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -72,9 +80,10 @@ def trimmed_mean(xs):
     return sum(xs) / len(xs)
 
 
-def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None):
+def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0):
     """The oracle (one-pass levels + grouping + natural-order epoch), single
-    thread, on the first rows of the same workload."""
+    thread, on the first rows of the same workload (with batch > 0: batch
+    levels + grouping + the mini-batch epoch)."""
     import numpy as np
 
     import oracle
@@ -85,6 +94,12 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None):
         rp = g["row_ptr"][:rows + 1]
         col = g["col"][:rp[-1]]
         t0 = time.perf_counter()
+        if batch:
+            level, perm, level_ptr, L = oracle.batch_schedule(rp, col, g["d"], batch)
+            val = None if g["val"] is None else g["val"][:rp[-1]]
+            oracle.batch_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
+                               g["loss"], oracle.NATURAL, batch)
+            return time.perf_counter() - t0, int(rp[-1]), level
         level, perm, level_ptr, L = oracle.schedule(rp, col, g["d"])
         if mf:
             oracle.mf_epoch(g["user"][:rows], g["item"][:rows], g["rating"][:rows], g["U0"],
@@ -99,16 +114,20 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None):
     probe = min(n, 20000)
     t, _, _ = run(probe)
     rows = int(min(n, max(probe, probe * budget_s / max(t, 1e-6))))
+    if batch:
+        rows = min(n, max(batch, rows // batch * batch))  # whole batches
     t, nnz_s, level = run(rows)
     units = rows if mf else nnz_s
     res = {"value": units / t, "unit": "ratings/s" if mf else "nnz-updates/s", "cores": 1,
            "kind": "oracle",
-           "sample": "first %d of %d %s (%d stored entries), one-pass levels + grouping + "
-                     "natural-order epoch, %.1f s" % (rows, n, "ratings" if mf else "examples",
-                                                      nnz_s, t),
+           "sample": "first %d of %d %s (%d stored entries), one-pass %slevels + grouping + "
+                     "natural-order %sepoch, %.1f s" % (
+                         rows, n, "ratings" if mf else "examples", nnz_s,
+                         "batch " if batch else "", "mini-batch (B=%d) " % batch if batch else "", t),
            "host_cpu": platform.processor() or platform.machine()}
     if gpu_levels is not None:
-        res["sample_levels_equal_gpu"] = bool(np.array_equal(gpu_levels[:rows], level))
+        k = len(level) if batch else rows
+        res["sample_levels_equal_gpu"] = bool(np.array_equal(gpu_levels[:k], level[:k]))
     return res
 
 
@@ -118,6 +137,9 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--batch", type=int, default=0,
+                    help="mini-batch gradient descent with this many examples per batch "
+                         "(pdb_batch_schedule + pdb_batch_epoch); 0 = SGD")
     ap.add_argument("--method", type=int, default=0,
                     help="0 auto, 1 chain-scan, 2 dataflow, 3 spine")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -150,15 +172,23 @@ def main():
     dev = torch.device("cuda:0")
     cfg_id = args.config
     mf = cfg_id == 5
+    batch = args.batch
+    if batch and mf:
+        raise SystemExit("--batch applies to the sparse SGD workloads (configs 1-4)")
     t0 = time.perf_counter()
     g = datagen.generate_mf(cfg_id) if mf else datagen.generate(cfg_id)
     t_gen = time.perf_counter() - t0
     print("generated %s: n=%d nnz=%d in %.1f s" % (g["name"], g["n"], g["nnz"], t_gen),
           file=sys.stderr, flush=True)
 
+    if batch:
+        # the workload's mini-batch form: lr / B, the step of the batch's mean gradient
+        g = dict(g)
+        g["lr"] = np.float32(g["lr"] / batch)
     n, d, nnz = g["n"], g["d"], g["nnz"]
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None if mf else g["val"], dev)
-    lv = native.Levels(n, nnz, dev)
+    bt = native.Batches(n, nnz, batch, dev) if batch else None
+    lv = native.Levels(bt.nb if batch else n, nnz, dev)
     ws_s = native.workspace(native.pdb_schedule_workspace_bytes(n, d, nnz), dev)
     ws_e = native.workspace(native.pdb_epoch_workspace_bytes(
         (g["n_users"] + g["n_items"]) * g["rank"] if mf else d), dev)
@@ -184,7 +214,10 @@ def main():
         # previous step's epoch has finished on the device
         s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s0.record(stream)
-        info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s)
+        if batch:
+            info = native.pdb_batch_schedule(csr, n, d, bt, lv, args.method, ws=ws_s)
+        else:
+            info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s)
         s1.record(stream)
         sched_ms.append((s0, s1))
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -194,6 +227,11 @@ def main():
             a.record(stream)
             native.pdb_mf_epoch(user, item, rating, n, U, g["n_users"], V, g["n_items"],
                                 g["rank"], float(g["lr"]), float(g["reg"]), lv, ws=ws_e)
+            b.record(stream)
+        elif batch:
+            w.copy_(w0)
+            a.record(stream)
+            native.pdb_batch_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], bt, lv, ws=ws_e)
             b.record(stream)
         else:
             w.copy_(w0)
@@ -224,10 +262,20 @@ def main():
     L = lv.L_host
     units = n if mf else nnz
     value = units * args.steps / elapsed
-    abytes = algorithmic_bytes(g, L, mf)
+    abytes = (algorithmic_bytes(g, L, U=bt.U_host, nb=bt.nb) if batch
+              else algorithmic_bytes(g, L, mf))
     achieved = abytes / (ep * 1e-3) / 1e9
-    workload = "c%d" % cfg_id
-    digest = source_digest()
+    workload = "c%d" % cfg_id + ("-b%d" % batch if batch else "")
+    # the epoch kernel the library runs (the rule of pdb_sgd_epoch / pdb_mf_epoch)
+    mode = int(os.environ.get("PDB_EPOCH_MODE", "0"))
+    syncfree = mode == 2 or (mode == 0 and L > 0 and n >= 8 * L)
+    if batch:
+        kernel = "k_batch_levels (mini-batch epoch)"
+    elif syncfree:
+        kernel = "k_mf_syncfree (epoch)" if mf else "k_sgd_syncfree (epoch)"
+    else:
+        kernel = "k_levels_apply (epoch)"
+    digest = source_digest(bool(batch))
     traffic = read_traffic(workload, digest)
     out = {
         "metric": METRIC,
@@ -242,13 +290,15 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "%s: %s" % (workload, g["name"]), "n": n, "d": d, "nnz": nnz,
+        "config": {"workload": "%s: %s%s" % (workload, g["name"],
+                                              ", mini-batches of %d" % batch if batch else ""),
+                   "n": n, "d": d, "nnz": nnz,
                    "seed": g["seed"], "levels": L, "max_level_width": lv.max_width_host,
                    "schedule_method": info.get("method_used"),
                    "schedule_rounds": info.get("rounds")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_levels_apply (epoch)", "algorithmic_bytes": abytes,
+                     "kernel": kernel, "algorithmic_bytes": abytes,
                      "epoch_ms": ep, "epoch_ms_all": epoch_ms, "source_digest": digest,
                      # levels run one after another: the epoch is a dependent
                      # chain of L levels, so the time per level is the figure
@@ -258,7 +308,8 @@ def main():
         "epoch_ms": ep,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget, lv.level.cpu().numpy())
+        out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget, lv.level.cpu().numpy(),
+                                           batch)
     print(json.dumps(out))
 
 

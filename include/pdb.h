@@ -178,6 +178,52 @@ int pdb_validate_csr(const pdb_csr *csr, int64_t n, int64_t d, void *ws, size_t 
  * ws recorded a device-side failure (and clears it), else PDB_OK. */
 int pdb_workspace_status(void *ws, hipStream_t stream);
 
+/* Mini-batches (Sec. 6.3: gradient descent with a fixed batch of examples per
+ * iteration).  Batch b is examples [b*B, min((b+1)*B, n)), nb = ceil(n/B);
+ * its parameter set is the union of its examples' features.  Device arrays
+ * owned by the caller, written by pdb_batch_schedule:
+ *   bptr    [nb+1]   batch b's union entries are u in [bptr[b], bptr[b+1]);
+ *   ucol    [nnz]    feature of union entry u, ascending within a batch
+ *                    (the first U entries are used);
+ *   uptr    [nnz+1]  union entry u's occurrences are occ[uptr[u] .. uptr[u+1]);
+ *   occ     [nnz]    CSR entry indices ordered by (batch, feature, index);
+ *   occ_row [nnz]    the example of each of them. */
+typedef struct pdb_batches {
+    int64_t *bptr;
+    int32_t *ucol;
+    int64_t *uptr;
+    int32_t *occ;
+    int32_t *occ_row;
+    int64_t U_host; /* union size U, written by pdb_batch_schedule */
+} pdb_batches;
+
+/* Conflict levels of mini-batches of `batch` examples (1 <= batch <= 4096):
+ * fills *batches, then runs pdb_schedule on the CSR whose rows are the
+ * batches (row_ptr = bptr, col = ucol), so levels describe the nb batches:
+ * level [nb], perm [nb] (batch indices), level_ptr [nb+1], and prev_nz (when
+ * not NULL) over the U union entries.  Two batches conflict when they share
+ * a feature (Sec. 4.4 at feature grain); batches of one level are pairwise
+ * feature-disjoint.  With batch = 1 the levels are those of pdb_schedule.
+ * ws: at least pdb_schedule_workspace_bytes(n, d, nnz).  Synchronous. */
+int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int64_t batch,
+                       pdb_batches *batches, pdb_levels *levels, int method,
+                       pdb_schedule_info *info, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* One epoch of mini-batch gradient descent in place on w (device, [d]).
+ * Batch b, in the sequential order of batches: every example i of b computes
+ * z_i and s_i = lr * g_i with the per-example arithmetic at the top of this
+ * header against the weights as they were when b started (all reads before
+ * any write, Definition 3); then each feature f of b takes, in example
+ * order, w_f = fma(-s_i, x_if, w_f) -- the gradient step of Sec. 2 on the
+ * sum of the batch's losses.  With batch = 1 this is pdb_sgd_epoch's
+ * result.  batches and levels from pdb_batch_schedule with the same batch.
+ * Batches of one level run concurrently (Theorem 2), one block per batch.
+ * ws: at least pdb_epoch_workspace_bytes(0).  Asynchronous; a device error
+ * (watchdog) is reported by pdb_workspace_status on ws. */
+int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, int64_t batch,
+                    float *w, float lr, int loss, const pdb_batches *batches,
+                    const pdb_levels *levels, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Per-feature occurrence lists (the transpose that exposes which examples
  * share a feature): col_ptr (device, [d+1]) and csc_row (device, [nnz],
  * rows ascending within a feature).  ws as for pdb_schedule.  Synchronous. */

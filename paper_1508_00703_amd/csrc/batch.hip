@@ -1,0 +1,368 @@
+// Mini-batch gradient descent (gfx950, wave64): a batch of B consecutive
+// examples is one iteration (Sec. 6.3 runs gradient descent with a fixed
+// batch of examples per iteration).  Its parameter set is the union of its
+// examples' features; within the iteration every read precedes every write
+// (Definition 3), so all examples of a batch see the batch-start weights.
+// Batches conflict when their unions share a feature; the read and write
+// constraints of Sec. 4.4 at feature grain then order them, and Theorem 2
+// lets batches of one conflict level run concurrently.
+//
+// Schedule: the union of each batch (features ascending) with, per union
+// feature, the batch's entries on it in example order -- a stable sort of
+// the entries by feature, then by batch -- is itself a CSR whose rows are the
+// batches.  pdb_schedule on that CSR gives the batch levels.
+//
+// Epoch: one block per batch.  Phase 1: one wave per example, the dot
+// product in the matched order (lane k holds entries k, k+64, ...), the step
+// s_i = lr * g_i into LDS.  Phase 2: one thread per union feature applies the
+// batch's contributions in example order, w = fma(-s_i, x, w), and writes the
+// weight once.  Levels run one after another: a level wider than `thin` is
+// spread over the grid followed by a device-wide barrier, runs of narrow
+// levels go to block 0 with block barriers between batches.
+#include <climits>
+
+#include "pdb_math.h"
+
+namespace pdbk {
+
+namespace {
+
+constexpr int kBB = 1024;                 // threads per batch block
+constexpr int kBWaves = kBB / kWave;
+constexpr int64_t kMaxBatch = 4096;       // examples per batch (LDS steps)
+
+// row of every stored entry, one wave per row
+__global__ __launch_bounds__(kBlock) void k_entry_row(const int64_t *__restrict__ row_ptr,
+                                                      int64_t n, int32_t *__restrict__ row_idx) {
+    const int lane = lane_id();
+    const int64_t nw = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t i = blockIdx.x * (int64_t)(kBlock / kWave) + wave_in_block(); i < n; i += nw) {
+        const int64_t b = row_ptr[i], e = row_ptr[i + 1];
+        for (int64_t p = b + lane; p < e; p += kWave) row_idx[p] = (int32_t)i;
+    }
+}
+
+// keys of the second sort: the batch of each entry, in feature order
+__global__ __launch_bounds__(kBlock) void k_batch_keys(const uint32_t *__restrict__ sv1,
+                                                       int64_t nnz,
+                                                       const int32_t *__restrict__ row_idx,
+                                                       int64_t B, uint32_t *__restrict__ key2,
+                                                       uint32_t *__restrict__ val2) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const uint32_t p = sv1[q];
+        key2[q] = (uint32_t)((int64_t)row_idx[p] / B);
+        val2[q] = p;
+    }
+}
+
+// entries in (batch, feature, index) order: occurrence lists, and a 1 at the
+// first entry of every (batch, feature) group
+__global__ __launch_bounds__(kBlock) void k_union_flags(const uint32_t *__restrict__ sk2,
+                                                        const uint32_t *__restrict__ sv2,
+                                                        int64_t nnz, const int32_t *__restrict__ col,
+                                                        const int32_t *__restrict__ row_idx,
+                                                        uint32_t *__restrict__ flag,
+                                                        int32_t *__restrict__ occ,
+                                                        int32_t *__restrict__ occ_row) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const uint32_t p = sv2[q];
+        occ[q] = (int32_t)p;
+        occ_row[q] = row_idx[p];
+        flag[q] = (q == 0 || sk2[q] != sk2[q - 1] || col[p] != col[sv2[q - 1]]) ? 1u : 0u;
+    }
+}
+
+// union entries: feature, first occurrence, batch; the union size into
+// *u_total (and uptr[U] = nnz)
+__global__ __launch_bounds__(kBlock) void k_union_write(
+    const uint32_t *__restrict__ sk2, const uint32_t *__restrict__ sv2, int64_t nnz,
+    const int32_t *__restrict__ col, const uint32_t *__restrict__ uidx,
+    int32_t *__restrict__ ucol, int64_t *__restrict__ uptr, uint32_t *__restrict__ ubatch,
+    int64_t *__restrict__ u_total) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const uint32_t p = sv2[q];
+        const bool head = q == 0 || sk2[q] != sk2[q - 1] || col[p] != col[sv2[q - 1]];
+        const int64_t u = uidx[q];
+        if (head) {
+            ucol[u] = col[p];
+            uptr[u] = q;
+            ubatch[u] = sk2[q];
+        }
+        if (q == nnz - 1) {
+            const int64_t U = u + (head ? 1 : 0);
+            uptr[U] = nnz;
+            *u_total = U;
+        }
+    }
+}
+
+// bptr[b] = first union entry of batch b (union entries are in batch order);
+// bptr[nb] already holds U
+__global__ __launch_bounds__(kBlock) void k_bptr(const uint32_t *__restrict__ ubatch, int64_t nb,
+                                                 int64_t *__restrict__ bptr) {
+    const int64_t U = bptr[nb];
+    for (int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; b < nb;
+         b += (int64_t)gridDim.x * blockDim.x) {
+        int64_t lo = 0, hi = U;
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if ((int64_t)ubatch[mid] < b) lo = mid + 1; else hi = mid;
+        }
+        bptr[b] = lo;
+    }
+}
+
+__global__ void k_fill64(int64_t *p, int64_t count, int64_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// epoch
+
+template <int LOSS, bool VAL>
+struct BatchOp {
+    const int64_t *row_ptr;
+    const int32_t *col;
+    const float *val;
+    const float *y;
+    float *w;
+    const int64_t *bptr;
+    const int32_t *ucol;
+    const int64_t *uptr;
+    const int32_t *occ;
+    const int32_t *occ_row;
+    int64_t n, B;
+    float lr;
+
+    // batch b with the whole block; s_step holds the batch's steps
+    __device__ __forceinline__ void run(int64_t b, float *s_step) const {
+        const int lane = lane_id();
+        const int wave = (int)(threadIdx.x >> 6);
+        const int64_t i0 = b * B, i1 = min(i0 + B, n);
+        // phase 1: every example against the batch-start weights
+        for (int64_t i = i0 + wave; i < i1; i += kBWaves) {
+            const int64_t p0 = row_ptr[i], m = row_ptr[i + 1] - p0;
+            float acc = 0.0f;
+            for (int64_t k = lane; k < m; k += kWave)
+                acc = __builtin_fmaf(w[col[p0 + k]], VAL ? val[p0 + k] : 1.0f, acc);
+            const float s = sgd_scale<LOSS>(wave_sum64(acc), y[i], lr);
+            if (lane == 0) s_step[i - i0] = s;
+        }
+        __syncthreads();
+        // phase 2: each union feature takes the batch's contributions in
+        // example order; no other batch of the level touches it
+        const int64_t u1 = bptr[b + 1];
+        for (int64_t u = bptr[b] + threadIdx.x; u < u1; u += kBB) {
+            const int32_t f = ucol[u];
+            const int64_t q1 = uptr[u + 1];
+            float wv = w[f];
+            for (int64_t q = uptr[u]; q < q1; ++q)
+                wv = __builtin_fmaf(-s_step[occ_row[q] - i0], VAL ? val[occ[q]] : 1.0f, wv);
+            w[f] = wv;
+        }
+        __syncthreads();
+    }
+};
+
+// first level >= l whose width exceeds thin (L if none); block-uniform
+__device__ int64_t batch_run_end(int64_t l, int64_t L, const int64_t *level_ptr, int64_t thin) {
+    __shared__ int64_t s_w[kBWaves];
+    for (int64_t start = l; start < L; start += kBB) {
+        const int64_t c = start + threadIdx.x;
+        const bool wide = c < L && level_ptr[c + 1] - level_ptr[c] > thin;
+        const unsigned long long bal = __ballot(wide);
+        if (lane_id() == 0)
+            s_w[threadIdx.x >> 6] = bal ? start + (threadIdx.x & ~63) + (__ffsll(bal) - 1)
+                                        : INT64_MAX;
+        __syncthreads();
+        int64_t m = INT64_MAX;
+#pragma unroll
+        for (int v = 0; v < kBWaves; ++v) m = min(m, s_w[v]);
+        __syncthreads();
+        if (m != INT64_MAX) return m;
+    }
+    return L;
+}
+
+template <int LOSS, bool VAL>
+__global__ __launch_bounds__(kBB) void k_batch_levels(BatchOp<LOSS, VAL> op,
+                                                     const int32_t *__restrict__ perm,
+                                                     const int64_t *__restrict__ level_ptr,
+                                                     const int32_t *__restrict__ n_levels,
+                                                     int64_t thin, Ctrl *ctrl, int64_t timeout) {
+    __shared__ float s_step[kMaxBatch];
+    const int64_t L = *n_levels;
+    if (gridDim.x == 1) {
+        // one block: every batch in level order, one after another
+        const int64_t nb = level_ptr[L];
+        for (int64_t e = 0; e < nb; ++e) op.run(perm[e], s_step);
+        return;
+    }
+    int64_t l = 0;
+    while (l < L) {
+        const int64_t beg = level_ptr[l], end = level_ptr[l + 1];
+        if (end - beg <= thin) {
+            const int64_t l2 = batch_run_end(l, L, level_ptr, thin);
+            if (blockIdx.x == 0)
+                for (int64_t e = beg; e < level_ptr[l2]; ++e) op.run(perm[e], s_step);
+            l = l2;
+        } else {
+            for (int64_t e = beg + blockIdx.x; e < end; e += gridDim.x) op.run(perm[e], s_step);
+            ++l;
+        }
+        if (l < L && !grid_barrier(ctrl, timeout)) return;
+    }
+}
+
+__global__ void k_batch_ctrl_zero(Ctrl *c) {
+    int *w = reinterpret_cast<int *>(c);
+    for (int i = threadIdx.x; i < (int)(sizeof(Ctrl) / sizeof(int)); i += blockDim.x) w[i] = 0;
+}
+
+template <int LOSS, bool VAL>
+int launch_batch(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, Ctrl *ctrl, hipStream_t s) {
+    const char *e = getenv("PDB_BATCH_THIN_MAX");
+    const int64_t thin = std::max<int64_t>(e ? atoll(e) : 2, 1);
+    const int64_t timeout = spin_timeout_ticks();
+    k_batch_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
+    PDB_LAUNCHED();
+    const void *fn = reinterpret_cast<const void *>(&k_batch_levels<LOSS, VAL>);
+    int grid = 1;
+    if (lv->max_width_host > thin) {
+        // the level barrier needs every block of the grid resident at once:
+        // one block per CU at most (a 1024-thread block always fits one CU)
+        int dev = 0, cus = 0, per_cu = 0;
+        PDB_HIP(hipGetDevice(&dev));
+        PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+        PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBB, 0));
+        if (per_cu < 1) return PDB_ERR_HIP;
+        grid = (int)std::max<int64_t>(1, std::min<int64_t>(cus, lv->max_width_host));
+    }
+    BatchOp<LOSS, VAL> o = op;
+    const int32_t *perm = lv->perm;
+    const int64_t *level_ptr = lv->level_ptr;
+    const int32_t *n_levels = lv->n_levels;
+    if (grid == 1) {
+        k_batch_levels<LOSS, VAL><<<1, kBB, 0, s>>>(o, perm, level_ptr, n_levels, thin, ctrl,
+                                                    timeout);
+        PDB_LAUNCHED();
+    } else {
+        int64_t thin_arg = thin, to = timeout;
+        void *args[] = {&o, &perm, &level_ptr, &n_levels, &thin_arg, &ctrl, &to};
+        PDB_HIP(hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBB), args, 0, s));
+    }
+    return PDB_OK;
+}
+
+int check_batch_sizes(int64_t n, int64_t d, int64_t nnz, int64_t B) {
+    if (n < 0 || d < 0 || nnz < 0 || B < 1) return PDB_ERR_INVALID_ARG;
+    if (B > kMaxBatch) return PDB_ERR_INVALID_ARG;
+    if (n >= INT32_MAX || d >= INT32_MAX || nnz >= INT32_MAX) return PDB_ERR_UNSUPPORTED;
+    return PDB_OK;
+}
+
+int bits_for(uint64_t maxval) {
+    int b = 0;
+    while (maxval) {
+        ++b;
+        maxval >>= 1;
+    }
+    return b > 0 ? b : 1;
+}
+
+}  // namespace
+}  // namespace pdbk
+
+using namespace pdbk;
+
+extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int64_t batch,
+                                  pdb_batches *bt, pdb_levels *lv, int method,
+                                  pdb_schedule_info *info, void *ws, size_t ws_bytes,
+                                  hipStream_t s) {
+    if (!csr || !bt || !lv || !ws || (n > 0 && !csr->row_ptr) || (csr->nnz > 0 && !csr->col))
+        return PDB_ERR_INVALID_ARG;
+    const int64_t nnz = csr->nnz;
+    int rc = check_batch_sizes(n, d, nnz, batch);
+    if (rc != PDB_OK) return rc;
+    if (d == 0 && nnz > 0) return PDB_ERR_BAD_CSR;
+    if (!bt->bptr || !bt->uptr || (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row)))
+        return PDB_ERR_INVALID_ARG;
+    SchedWs w = sched_ws_layout(ws, n, d, nnz);
+    if (ws_bytes < w.total) return PDB_ERR_WORKSPACE;
+    const int64_t nb = cdiv(n, batch);
+    if (nnz == 0) {
+        k_fill64<<<grid_for(nb + 1, kBlock, 4096), kBlock, 0, s>>>(bt->bptr, nb + 1, 0);
+        k_fill64<<<1, 64, 0, s>>>(bt->uptr, 1, 0);
+        PDB_LAUNCHED();
+        bt->U_host = 0;
+    } else {
+        k_entry_row<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n,
+                                                                          w.row_idx);
+        PDB_LAUNCHED();
+        // entries by feature (stable), then by batch (stable): (batch, feature, index)
+        uint32_t *sk1, *sv1, *sk2, *sv2;
+        PDB_HIP(radix_sort_pairs(reinterpret_cast<const uint32_t *>(csr->col), nullptr, nnz,
+                                 bits_for((uint64_t)(d > 1 ? d - 1 : 1)), w.kA, w.vA, w.kB, w.vB,
+                                 w.hist, w.scan_tmp, &sk1, &sv1, s));
+        // the second sort reads its input from the occurrence arrays, which
+        // are rewritten below
+        uint32_t *key2 = reinterpret_cast<uint32_t *>(bt->occ);
+        uint32_t *val2 = reinterpret_cast<uint32_t *>(bt->occ_row);
+        k_batch_keys<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(sv1, nnz, w.row_idx, batch,
+                                                                      key2, val2);
+        PDB_LAUNCHED();
+        PDB_HIP(radix_sort_pairs(key2, val2, nnz, bits_for((uint64_t)(nb > 1 ? nb - 1 : 1)), w.kA,
+                                 w.vA, w.kB, w.vB, w.hist, w.scan_tmp, &sk2, &sv2, s));
+        uint32_t *flag = (sk2 == w.kA) ? w.kB : w.kA;   // the pair not holding the result
+        uint32_t *ubatch = (sk2 == w.kA) ? w.vB : w.vA;
+        k_union_flags<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(
+            sk2, sv2, nnz, csr->col, w.row_idx, flag, bt->occ, bt->occ_row);
+        PDB_LAUNCHED();
+        PDB_HIP(exclusive_scan_u32(flag, flag, nnz, w.scan_tmp, s));
+        k_union_write<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(
+            sk2, sv2, nnz, csr->col, flag, bt->ucol, bt->uptr, ubatch, bt->bptr + nb);
+        PDB_LAUNCHED();
+        if (nb > 0) {
+            k_bptr<<<grid_for(nb, kBlock, 65536), kBlock, 0, s>>>(ubatch, nb, bt->bptr);
+            PDB_LAUNCHED();
+        }
+        int64_t U = 0;
+        PDB_HIP(hipMemcpyAsync(&U, bt->bptr + nb, sizeof(U), hipMemcpyDeviceToHost, s));
+        PDB_HIP(hipStreamSynchronize(s));
+        bt->U_host = U;
+    }
+    // the batch levels: conflict levels of the union CSR, whose rows are the batches
+    const pdb_csr ucsr{bt->bptr, bt->ucol, nullptr, bt->U_host};
+    return pdb_schedule(&ucsr, nullptr, nb, d, lv, method, info, ws, ws_bytes, s);
+}
+
+extern "C" int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
+                               int64_t batch, float *w, float lr, int loss,
+                               const pdb_batches *bt, const pdb_levels *lv, void *ws,
+                               size_t ws_bytes, hipStream_t s) {
+    if (!csr || !labels || !w || !bt || !lv || !ws || !lv->perm || !lv->level_ptr ||
+        !lv->n_levels)
+        return PDB_ERR_INVALID_ARG;
+    const int64_t nnz = csr->nnz;
+    int rc = check_batch_sizes(n, d, nnz, batch);
+    if (rc != PDB_OK) return rc;
+    if (loss != PDB_LOGISTIC && loss != PDB_SQUARED) return PDB_ERR_INVALID_ARG;
+    if (ws_bytes < sizeof(Ctrl)) return PDB_ERR_WORKSPACE;
+    if (n == 0) return PDB_OK;
+    if (!bt->bptr || !bt->uptr || (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row)))
+        return PDB_ERR_INVALID_ARG;
+    Ctrl *ctrl = static_cast<Ctrl *>(ws);
+#define PDB_BATCH(LOSS, VAL)                                                                     \
+    launch_batch<LOSS, VAL>(BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w,      \
+                                               bt->bptr, bt->ucol, bt->uptr, bt->occ,           \
+                                               bt->occ_row, n, batch, lr},                      \
+                            lv, ctrl, s)
+    if (loss == PDB_LOGISTIC) return csr->val ? PDB_BATCH(PDB_LOGISTIC, true) : PDB_BATCH(PDB_LOGISTIC, false);
+    return csr->val ? PDB_BATCH(PDB_SQUARED, true) : PDB_BATCH(PDB_SQUARED, false);
+#undef PDB_BATCH
+}

@@ -30,7 +30,7 @@ EXPORTS = (
     "pdb_strerror", "pdb_last_hip_error", "pdb_schedule_workspace_bytes",
     "pdb_epoch_workspace_bytes", "pdb_schedule", "pdb_sgd_epoch", "pdb_mf_epoch",
     "pdb_validate_csr", "pdb_workspace_status", "pdb_transpose", "pdb_prev_writer",
-    "pdb_check_reciprocal",
+    "pdb_check_reciprocal", "pdb_batch_schedule", "pdb_batch_epoch",
 )
 
 
@@ -44,6 +44,11 @@ class PdbLevels(ctypes.Structure):
                 ("level_ptr", ctypes.c_void_p), ("n_levels", ctypes.c_void_p),
                 ("prev_nz", ctypes.c_void_p), ("L_host", ctypes.c_int64),
                 ("max_width_host", ctypes.c_int64)]
+
+
+class PdbBatches(ctypes.Structure):
+    _fields_ = [("bptr", ctypes.c_void_p), ("ucol", ctypes.c_void_p), ("uptr", ctypes.c_void_p),
+                ("occ", ctypes.c_void_p), ("occ_row", ctypes.c_void_p), ("U_host", ctypes.c_int64)]
 
 
 class PdbScheduleInfo(ctypes.Structure):
@@ -92,6 +97,11 @@ def load() -> ctypes.CDLL:
     lib.pdb_check_reciprocal.argtypes = [ctypes.c_uint32, ctypes.c_uint32,
                                          ctypes.POINTER(ctypes.c_uint64),
                                          ctypes.POINTER(ctypes.c_uint32), P, sz, P]
+    lib.pdb_batch_schedule.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, i64,
+                                       ctypes.POINTER(PdbBatches), ctypes.POINTER(PdbLevels),
+                                       ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, P]
+    lib.pdb_batch_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, i64, P, f32, ctypes.c_int,
+                                    ctypes.POINTER(PdbBatches), ctypes.POINTER(PdbLevels), P, sz, P]
     for name in EXPORTS:
         if name not in ("pdb_strerror",):
             getattr(lib, name).restype = ctypes.c_int
@@ -179,6 +189,26 @@ class Levels:
                          self.max_width_host)
 
 
+class Batches:
+    """Device output of pdb_batch_schedule: each batch's union of features and the
+    occurrence lists (sized for the worst case U = nnz)."""
+
+    def __init__(self, n: int, nnz: int, batch: int, device):
+        nb = (n + batch - 1) // batch
+        self.batch = batch
+        self.nb = nb
+        self.bptr = torch.empty(nb + 1, dtype=torch.int64, device=device)
+        self.ucol = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
+        self.uptr = torch.empty(nnz + 1, dtype=torch.int64, device=device)
+        self.occ = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
+        self.occ_row = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
+        self.U_host = 0
+
+    def c(self) -> PdbBatches:
+        return PdbBatches(_ptr(self.bptr), _ptr(self.ucol), _ptr(self.uptr), _ptr(self.occ),
+                          _ptr(self.occ_row), self.U_host)
+
+
 def pdb_strerror(code: int) -> str:
     return load().pdb_strerror(code).decode()
 
@@ -241,6 +271,41 @@ def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, r
                                _ptr(V), n_items, rank, ctypes.c_float(lr), ctypes.c_float(reg),
                                ctypes.byref(levels.c()), _ptr(ws), ws.numel(),
                                _stream(stream, U.device)), "pdb_mf_epoch")
+    return ws
+
+
+def pdb_batch_schedule(csr: Csr, n: int, d: int, batches: Batches, levels: Levels,
+                       method: int = PDB_SCHED_AUTO, ws: torch.Tensor | None = None,
+                       stream=None) -> dict:
+    """levels: a Levels for nb = ceil(n / batch) rows and (for prev_nz) nnz entries."""
+    if ws is None:
+        ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
+    bt = batches.c()
+    lv = levels.c()
+    info = PdbScheduleInfo()
+    _check(load().pdb_batch_schedule(ctypes.byref(csr.c()), n, d, batches.batch, ctypes.byref(bt),
+                                     ctypes.byref(lv), method, ctypes.byref(info), _ptr(ws),
+                                     ws.numel(), _stream(stream, csr.device)),
+           "pdb_batch_schedule")
+    batches.U_host = bt.U_host
+    levels.L_host, levels.max_width_host = lv.L_host, lv.max_width_host
+    return dict(method_used=info.method_used, rounds=info.rounds, n_levels=info.n_levels,
+                max_width=info.max_width)
+
+
+def pdb_batch_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor, lr: float,
+                    loss: int, batches: Batches, levels: Levels, ws: torch.Tensor | None = None,
+                    stream=None):
+    if w.dtype != torch.float32 or labels.dtype != torch.float32:
+        raise TypeError("w and labels must be float32")
+    if w.numel() < d or labels.numel() < n:
+        raise ValueError("w must hold d entries and labels n entries")
+    if ws is None:
+        ws = workspace(pdb_epoch_workspace_bytes(0), csr.device)
+    _check(load().pdb_batch_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, batches.batch, _ptr(w),
+                                  ctypes.c_float(lr), loss, ctypes.byref(batches.c()),
+                                  ctypes.byref(levels.c()), _ptr(ws), ws.numel(),
+                                  _stream(stream, csr.device)), "pdb_batch_epoch")
     return ws
 
 
