@@ -30,6 +30,25 @@ namespace {
 constexpr int kBB = 1024;                 // threads per batch block
 constexpr int kBWaves = kBB / kWave;
 constexpr int64_t kMaxBatch = 4096;       // examples per batch (LDS steps)
+constexpr int kG = 8;                     // examples a wave loads together in phase 1
+constexpr int kH = 8;                     // union features a thread takes in phase 2
+constexpr int64_t kCap = kBB * kH;        // entries of a batch staged in LDS (8192)
+
+// LDS of a batch block: steps by example; for staged batches the weights read
+// in phase 1 by entry, and per occurrence its example (relative to the
+// batch) and value
+struct BatchShared {
+    float s[kMaxBatch];
+    float w[kCap];
+    int32_t oi[kCap];
+    float ox[kCap];
+};
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)v >> 32), lane);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 
 // row of every stored entry, one wave per row
 __global__ __launch_bounds__(kBlock) void k_entry_row(const int64_t *__restrict__ row_ptr,
@@ -139,31 +158,118 @@ struct BatchOp {
     int64_t n, B;
     float lr;
 
-    // batch b with the whole block; s_step holds the batch's steps
-    __device__ __forceinline__ void run(int64_t b, float *s_step) const {
+    // Batch b with the whole block.  Sh holds the batch's steps and, when the
+    // batch has at most kCap entries, the weights phase 1 read (by entry) and
+    // each occurrence's example and value, so that phase 2 reads LDS only.
+    __device__ __forceinline__ void run(int64_t b, BatchShared &Sh) const {
         const int lane = lane_id();
         const int wave = (int)(threadIdx.x >> 6);
         const int64_t i0 = b * B, i1 = min(i0 + B, n);
-        // phase 1: every example against the batch-start weights
-        for (int64_t i = i0 + wave; i < i1; i += kBWaves) {
-            const int64_t p0 = row_ptr[i], m = row_ptr[i + 1] - p0;
-            float acc = 0.0f;
-            for (int64_t k = lane; k < m; k += kWave)
-                acc = __builtin_fmaf(w[col[p0 + k]], VAL ? val[p0 + k] : 1.0f, acc);
-            const float s = sgd_scale<LOSS>(wave_sum64(acc), y[i], lr);
-            if (lane == 0) s_step[i - i0] = s;
+        const int64_t pb = row_ptr[i0], pe = row_ptr[i1];   // the batch's entries
+        const int64_t ub = bptr[b], ue = bptr[b + 1];       // its union features
+        const bool staged = pe - pb <= kCap;
+        // union features this thread updates, and (staged) the entry of each
+        // one's first occurrence, whose weight phase 1 reads
+        // (positions fit in 32 bits: nnz < 2^31)
+        int32_t f[kH], q0[kH], q1[kH], pf[kH];
+        const int64_t u0 = ub + threadIdx.x;
+#pragma unroll
+        for (int h = 0; h < kH; ++h) {
+            const int64_t u = u0 + (int64_t)kBB * h;
+            const bool live = u < ue;
+            f[h] = live ? ucol[u] : 0;
+            q0[h] = live ? (int32_t)uptr[u] : 0;
+            q1[h] = live ? (int32_t)uptr[u + 1] : 0;
+        }
+        if (staged) {
+#pragma unroll
+            for (int h = 0; h < kH; ++h)
+                pf[h] = (u0 + (int64_t)kBB * h < ue) ? occ[q0[h]] - (int32_t)pb : 0;
+            // occurrences of the batch are its entries' positions [pb, pe)
+            for (int64_t q = pb + threadIdx.x; q < pe; q += kBB) {
+                Sh.oi[q - pb] = occ_row[q] - (int32_t)i0;
+                if (VAL) Sh.ox[q - pb] = val[occ[q]];
+            }
+        }
+        // phase 1: every example against the batch-start weights.  A wave
+        // takes kG examples at a time; every load is unconditional (indices
+        // clamped into the batch's entries), so all of them are in flight
+        // before the first use: row bounds (lane j for example j), two chunks
+        // of 64 columns per example, then the weights.
+        if (pe > pb) {
+            for (int64_t base = i0 + wave; base < i1; base += (int64_t)kBWaves * kG) {
+                const int64_t my_i = base + (int64_t)kBWaves * lane;
+                const bool has = lane < kG && my_i < i1;
+                const int64_t rb = row_ptr[has ? my_i : i0];
+                const int64_t re = has ? row_ptr[my_i + 1] : rb;
+                const float yv = y[has ? my_i : i0];
+                int64_t p[kG], m[kG];
+#pragma unroll
+                for (int j = 0; j < kG; ++j) {
+                    p[j] = readlane64(rb, j);
+                    m[j] = readlane64(re, j) - p[j];
+                }
+                int c[2 * kG];
+                float x[2 * kG], wv[2 * kG], acc[kG];
+#pragma unroll
+                for (int t = 0; t < 2 * kG; ++t) {
+                    const int64_t e = min(max(p[t >> 1] + (t & 1) * kWave + lane, pb), pe - 1);
+                    c[t] = col[e];
+                    x[t] = VAL ? val[e] : 1.0f;
+                }
+#pragma unroll
+                for (int t = 0; t < 2 * kG; ++t) wv[t] = w[c[t]];
+#pragma unroll
+                for (int j = 0; j < kG; ++j) {
+                    const int k0 = lane, k1 = kWave + lane;
+                    // lanes without an entry hold +0, as in the summation order
+                    acc[j] = k0 < m[j] ? __builtin_fmaf(wv[2 * j], x[2 * j], 0.0f) : 0.0f;
+                    if (k1 < m[j]) acc[j] = __builtin_fmaf(wv[2 * j + 1], x[2 * j + 1], acc[j]);
+                    if (staged) {
+                        if (k0 < m[j]) Sh.w[p[j] + k0 - pb] = wv[2 * j];
+                        if (k1 < m[j]) Sh.w[p[j] + k1 - pb] = wv[2 * j + 1];
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < kG; ++j) {
+                    if (base + (int64_t)kBWaves * j >= i1) break;  // wave-uniform
+                    for (int64_t k = 2 * kWave + lane; k < m[j]; k += kWave) {
+                        const float wk = w[col[p[j] + k]];
+                        acc[j] = __builtin_fmaf(wk, VAL ? val[p[j] + k] : 1.0f, acc[j]);
+                        if (staged) Sh.w[p[j] + k - pb] = wk;
+                    }
+                    const float yj =
+                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(yv), j));
+                    const float sj = sgd_scale<LOSS>(wave_sum64(acc[j]), yj, lr);
+                    if (lane == 0) Sh.s[base + (int64_t)kBWaves * j - i0] = sj;
+                }
+            }
+        } else {
+            // no entries: z = 0 for every example
+            for (int64_t i = i0 + threadIdx.x; i < i1; i += kBB)
+                Sh.s[i - i0] = sgd_scale<LOSS>(0.0f, y[i], lr);
         }
         __syncthreads();
         // phase 2: each union feature takes the batch's contributions in
         // example order; no other batch of the level touches it
-        const int64_t u1 = bptr[b + 1];
-        for (int64_t u = bptr[b] + threadIdx.x; u < u1; u += kBB) {
-            const int32_t f = ucol[u];
-            const int64_t q1 = uptr[u + 1];
-            float wv = w[f];
-            for (int64_t q = uptr[u]; q < q1; ++q)
-                wv = __builtin_fmaf(-s_step[occ_row[q] - i0], VAL ? val[occ[q]] : 1.0f, wv);
-            w[f] = wv;
+        if (staged) {
+#pragma unroll
+            for (int h = 0; h < kH; ++h) {
+                if (u0 + (int64_t)kBB * h >= ue) break;
+                float v = Sh.w[pf[h]];
+                for (int32_t q = q0[h] - (int32_t)pb; q < q1[h] - (int32_t)pb; ++q)
+                    v = __builtin_fmaf(-Sh.s[Sh.oi[q]], VAL ? Sh.ox[q] : 1.0f, v);
+                w[f[h]] = v;
+            }
+        } else {
+            for (int64_t u = u0; u < ue; u += kBB) {
+                const int32_t fu = ucol[u];
+                const int64_t qe = uptr[u + 1];
+                float v = w[fu];
+                for (int64_t q = uptr[u]; q < qe; ++q)
+                    v = __builtin_fmaf(-Sh.s[occ_row[q] - i0], VAL ? val[occ[q]] : 1.0f, v);
+                w[fu] = v;
+            }
         }
         __syncthreads();
     }
@@ -195,12 +301,12 @@ __global__ __launch_bounds__(kBB) void k_batch_levels(BatchOp<LOSS, VAL> op,
                                                      const int64_t *__restrict__ level_ptr,
                                                      const int32_t *__restrict__ n_levels,
                                                      int64_t thin, Ctrl *ctrl, int64_t timeout) {
-    __shared__ float s_step[kMaxBatch];
+    __shared__ BatchShared Sh;
     const int64_t L = *n_levels;
     if (gridDim.x == 1) {
         // one block: every batch in level order, one after another
         const int64_t nb = level_ptr[L];
-        for (int64_t e = 0; e < nb; ++e) op.run(perm[e], s_step);
+        for (int64_t e = 0; e < nb; ++e) op.run(perm[e], Sh);
         return;
     }
     int64_t l = 0;
@@ -209,10 +315,10 @@ __global__ __launch_bounds__(kBB) void k_batch_levels(BatchOp<LOSS, VAL> op,
         if (end - beg <= thin) {
             const int64_t l2 = batch_run_end(l, L, level_ptr, thin);
             if (blockIdx.x == 0)
-                for (int64_t e = beg; e < level_ptr[l2]; ++e) op.run(perm[e], s_step);
+                for (int64_t e = beg; e < level_ptr[l2]; ++e) op.run(perm[e], Sh);
             l = l2;
         } else {
-            for (int64_t e = beg + blockIdx.x; e < end; e += gridDim.x) op.run(perm[e], s_step);
+            for (int64_t e = beg + blockIdx.x; e < end; e += gridDim.x) op.run(perm[e], Sh);
             ++l;
         }
         if (l < L && !grid_barrier(ctrl, timeout)) return;

@@ -68,7 +68,7 @@ struct Ctrl {
     int spine_n_e;
     int spine_status;  // 0 solved, 1 too many exceptional rows or entries
     int spine_rounds;
-    int pad1;
+    int chain_breaks;  // rows that do not conflict with the row before them
     int pad[38];
     float sink[64];  // target of stores from lanes with nothing to store
 };

@@ -907,6 +907,43 @@ __global__ void k_level_ptr(const uint32_t *__restrict__ skeys, const uint32_t *
     }
 }
 
+// Chain check: counts the rows i >= 1 none of whose entries has row i-1 as
+// its previous writer.  An entry's previous writer lies in an earlier row, so
+// it is row i-1 exactly when the previous entry's index is at least
+// row_ptr[i-1].  One wave per row.
+__global__ __launch_bounds__(kBlock) void k_chain_check(const int64_t *__restrict__ row_ptr,
+                                                        int64_t n, const int32_t *__restrict__ pn,
+                                                        Ctrl *ctrl) {
+    const int lane = lane_id();
+    const int64_t nw = (int64_t)gridDim.x * (kBlock / kWave);
+    int breaks = 0;
+    for (int64_t i = 1 + blockIdx.x * (int64_t)(kBlock / kWave) + wave_in_block(); i < n; i += nw) {
+        const int64_t lo = row_ptr[i - 1], b = row_ptr[i], e = row_ptr[i + 1];
+        bool found = false;
+        for (int64_t p = b + lane; p < e && !found; p += kWave) found = pn[p] >= lo;
+        if (__ballot(found) == 0ull) ++breaks;
+    }
+    if (lane == 0 && breaks) atomicAdd(&ctrl->chain_breaks, breaks);
+}
+
+// Levels of a chain: every example conflicts with the one before it, so
+// levels increase strictly along the rows, the highest earlier conflicting
+// example is always the previous one, and level(i) = i + 1.
+__global__ __launch_bounds__(kBlock) void k_chain_levels(int64_t n, int32_t *__restrict__ level,
+                                                         int32_t *__restrict__ perm,
+                                                         int64_t *__restrict__ level_ptr,
+                                                         int32_t *__restrict__ n_levels) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i <= n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        if (i < n) {
+            level[i] = (int32_t)(i + 1);
+            perm[i] = (int32_t)i;
+        }
+        level_ptr[i] = i;
+        if (i == 0) *n_levels = (int32_t)n;
+    }
+}
+
 int bit_length(uint64_t x) {
     int b = 0;
     while (x) {
@@ -1066,7 +1103,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     if (rc != PDB_OK) return rc;
     if (!lv || !lv->level_ptr || !lv->n_levels || (n > 0 && (!lv->level || !lv->perm)))
         return PDB_ERR_INVALID_ARG;
-    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_SPINE) return PDB_ERR_INVALID_ARG;
+    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_CHAIN) return PDB_ERR_INVALID_ARG;
     const int64_t nnz = csr->nnz;
     Ctrl host{};
     k_ctrl_init<<<1, 64, 0, s>>>(w.ctrl);
@@ -1090,6 +1127,27 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     // the radix buffer pair that does not hold the sorted entries is free
     int32_t *free_k = reinterpret_cast<int32_t *>((sk == w.kA) ? w.kB : w.kA);
     const int64_t timeout = spin_timeout_ticks();
+
+    // a chain (every example conflicts with the one before it) is solved
+    // outright; auto tries it first
+    if (method == PDB_SCHED_AUTO || method == PDB_SCHED_CHAIN) {
+        k_chain_check<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n, pn,
+                                                                            w.ctrl);
+        PDB_LAUNCHED();
+        rc = read_ctrl(w.ctrl, &host, s);
+        if (rc != PDB_OK) return rc;
+        if (host.chain_breaks == 0) {
+            k_chain_levels<<<grid_for(n + 1, kBlock, 65536), kBlock, 0, s>>>(
+                n, lv->level, lv->perm, lv->level_ptr, lv->n_levels);
+            PDB_LAUNCHED();
+            PDB_HIP(hipStreamSynchronize(s));
+            lv->L_host = n;
+            lv->max_width_host = 1;
+            if (info) *info = pdb_schedule_info{PDB_SCHED_CHAIN, 0, n, 1};
+            return PDB_OK;
+        }
+        if (method == PDB_SCHED_CHAIN) method = PDB_SCHED_DATAFLOW;
+    }
 
     // which method: the spine when the most frequent feature misses at most
     // kSpineMaxE rows, else dataflow

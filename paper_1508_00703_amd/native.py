@@ -24,6 +24,7 @@ PDB_ERR_DEVICE = -5
 PDB_ERR_UNSUPPORTED = -6
 PDB_LOGISTIC, PDB_SQUARED = 0, 1
 PDB_SCHED_AUTO, PDB_SCHED_CHAINSCAN, PDB_SCHED_DATAFLOW, PDB_SCHED_SPINE = 0, 1, 2, 3
+PDB_SCHED_CHAIN = 4
 
 # every symbol declared in include/pdb.h
 EXPORTS = (

@@ -11,7 +11,7 @@ from pdbtest import check_mf, check_schedule, check_sgd, csr_from_rows, gpu_sche
 
 pytestmark = pytest.mark.gpu
 
-METHODS = [0, 1, 2, 3]  # auto, chain-scan, dataflow, spine
+METHODS = [0, 1, 2, 3, 4]  # auto, chain-scan, dataflow, spine, chain
 
 
 def native_mod():
@@ -350,9 +350,9 @@ def test_spine_selection_and_fallback(gpu):
     row_ptr, col = csr_from_rows(rows)
     d = int(col.max()) + 1
     _, info = check_schedule(native, gpu, row_ptr, col, d, 0)
-    assert info["method_used"] == 3 and info["rounds"] >= 1
+    assert info["method_used"] in (3, 4)   # the chain check runs first
     _, info = check_schedule(native, gpu, row_ptr, col, d, 3)
-    assert info["method_used"] == 3
+    assert info["method_used"] == 3 and info["rounds"] >= 1
     # 1500 exceptional rows
     rows = [{0, 1 + i % 5} if i % 2 else {6 + i % 9} for i in range(3000)]
     row_ptr, col = csr_from_rows(rows)
@@ -369,6 +369,35 @@ def test_spine_selection_and_fallback(gpu):
     assert info["method_used"] == 2
 
 
+def test_chain_selection_and_fallback(gpu):
+    """Auto takes the chain when every example conflicts with the one before
+    it (levels 1..n); when one does not, auto and an explicit chain request
+    both fall back.  Levels are exact each time."""
+    native = native_mod()
+    n = 4000
+    chain = [{i, i + 1, 5000 + i % 3} for i in range(n)]   # row i shares feature i with row i-1
+    row_ptr, col = csr_from_rows(chain)
+    d = int(col.max()) + 1
+    for method in (0, 4):
+        lv, info = check_schedule(native, gpu, row_ptr, col, d, method)
+        assert info["method_used"] == 4 and lv.L_host == n
+    # one example (row 2500) shares nothing with row 2499
+    broken = [set(r) for r in chain]
+    broken[2500] = {n + 10, 5003}
+    broken[2501] = {2501, 2502, 5000 + 2501 % 3}
+    row_ptr, col = csr_from_rows(broken)
+    d = int(col.max()) + 1
+    for method in (0, 4):
+        lv, info = check_schedule(native, gpu, row_ptr, col, d, method)
+        assert info["method_used"] != 4 and lv.L_host < n
+    # an empty row breaks the chain too
+    holed = [set(r) for r in chain]
+    holed[17] = set()
+    row_ptr, col = csr_from_rows(holed)
+    lv, info = check_schedule(native, gpu, row_ptr, col, int(col.max()) + 1, 4)
+    assert info["method_used"] != 4
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_spine_random_exceptions(gpu, seed):
     """Spine levels where exceptional rows feed the spine and each other:
@@ -383,7 +412,7 @@ def test_spine_random_exceptions(gpu, seed):
             r.add(0)
         rows.append(r)
     row_ptr, col = csr_from_rows(rows)
-    lv, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    lv, info = check_schedule(native, gpu, row_ptr, col, d, 3)
     assert info["method_used"] == 3
     # exceptional rows raised the spine above its own length
     assert lv.L_host > np.bincount(col).max()
