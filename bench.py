@@ -4,7 +4,8 @@
 A step is one pass of the whole path over the workload, inputs resident in
 HBM: conflict levels (pdb_schedule: transpose, previous writers, levels,
 grouping) and one SGD epoch (pdb_sgd_epoch / pdb_mf_epoch), weights reset to
-w0 at the start of the step.  `value` = stored entries updated per second
+w0 at the start of the step (--epochs E: E epochs on the step's schedule;
+--batch B: mini-batches of B examples).  `value` = stored entries updated per second
 over the K timed steps (ratings per second for matrix completion).
 
 Default workload: 10M examples x 1M features, 50 entries per example with
@@ -137,6 +138,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--epochs", type=int, default=1,
+                    help="epochs per step on the step's one schedule (the schedule is cached)")
     ap.add_argument("--batch", type=int, default=0,
                     help="mini-batch gradient descent with this many examples per batch "
                          "(pdb_batch_schedule + pdb_batch_epoch); 0 = SGD")
@@ -220,26 +223,25 @@ def main():
             info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s)
         s1.record(stream)
         sched_ms.append((s0, s1))
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         if mf:
             U.copy_(U0)
             V.copy_(V0)
-            a.record(stream)
-            native.pdb_mf_epoch(user, item, rating, n, U, g["n_users"], V, g["n_items"],
-                                g["rank"], float(g["lr"]), float(g["reg"]), lv, ws=ws_e)
-            b.record(stream)
-        elif batch:
-            w.copy_(w0)
-            a.record(stream)
-            native.pdb_batch_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], bt, lv, ws=ws_e)
-            b.record(stream)
         else:
             w.copy_(w0)
+        for _ in range(args.epochs):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], lv, ws=ws_e)
+            if mf:
+                native.pdb_mf_epoch(user, item, rating, n, U, g["n_users"], V, g["n_items"],
+                                    g["rank"], float(g["lr"]), float(g["reg"]), lv, ws=ws_e)
+            elif batch:
+                native.pdb_batch_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], bt, lv,
+                                       ws=ws_e)
+            else:
+                native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], lv, ws=ws_e)
             b.record(stream)
-        if timed:
-            ev.append((a, b))
+            if timed:
+                ev.append((a, b))
 
     for _ in range(args.warmup):
         step(False)
@@ -261,7 +263,7 @@ def main():
     ep = trimmed_mean(epoch_ms)
     L = lv.L_host
     units = n if mf else nnz
-    value = units * args.steps / elapsed
+    value = units * args.epochs * args.steps / elapsed
     abytes = (algorithmic_bytes(g, L, U=bt.U_host, nb=bt.nb) if batch
               else algorithmic_bytes(g, L, mf))
     achieved = abytes / (ep * 1e-3) / 1e9
@@ -283,6 +285,7 @@ def main():
         "unit": "ratings/s" if mf else "nnz-updates/s",
         "n_gpus": 1,
         "steps": args.steps,
+        "epochs_per_step": args.epochs,
         "warmup": args.warmup,
         "ms_per_step": elapsed * 1e3 / args.steps,
         "higher_is_better": True,
