@@ -190,13 +190,15 @@ int pdb_workspace_status(void *ws, hipStream_t stream);
  *                    (the first U entries are used);
  *   uptr    [nnz+1]  union entry u's occurrences are occ[uptr[u] .. uptr[u+1]);
  *   occ     [nnz]    CSR entry indices ordered by (batch, feature, index);
- *   occ_row [nnz]    the example of each of them. */
+ *   occ_row [nnz]    the example of each of them;
+ *   occ_u   [nnz]    the union entry of each of them. */
 typedef struct pdb_batches {
     int64_t *bptr;
     int32_t *ucol;
     int64_t *uptr;
     int32_t *occ;
     int32_t *occ_row;
+    int32_t *occ_u;
     int64_t U_host; /* union size U, written by pdb_batch_schedule */
 } pdb_batches;
 
@@ -220,7 +222,13 @@ int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int64_t batch,
  * order, w_f = fma(-s_i, x_if, w_f) -- the gradient step of Sec. 2 on the
  * sum of the batch's losses.  With batch = 1 this is pdb_sgd_epoch's
  * result.  batches and levels from pdb_batch_schedule with the same batch.
- * Batches of one level run concurrently (Theorem 2), one block per batch.
+ * Two executions, bitwise the same result, one block per batch:
+ *   - batch levels in order, a level's batches concurrently (Theorem 2);
+ *   - sync-free (the Read Protocol of Sec. 5 with a batch as the iteration):
+ *     batches in index order, each waiting only until each of its features
+ *     was written by its previous writer (levels->prev_nz over the union
+ *     entries), no barriers.  Chosen when levels->prev_nz is set and ws_bytes
+ *     covers pdb_epoch_workspace_bytes(d) (PDB_EPOCH_MODE=1 forces levels).
  * ws: at least pdb_epoch_workspace_bytes(0).  Asynchronous; a device error
  * (watchdog) is reported by pdb_workspace_status on ws. */
 int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, int64_t batch,

@@ -99,12 +99,15 @@ __global__ __launch_bounds__(kBlock) void k_union_write(
     const uint32_t *__restrict__ sk2, const uint32_t *__restrict__ sv2, int64_t nnz,
     const int32_t *__restrict__ col, const uint32_t *__restrict__ uidx,
     int32_t *__restrict__ ucol, int64_t *__restrict__ uptr, uint32_t *__restrict__ ubatch,
-    int64_t *__restrict__ u_total) {
+    int32_t *__restrict__ occ_u, int64_t *__restrict__ u_total) {
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
          q += (int64_t)gridDim.x * blockDim.x) {
         const uint32_t p = sv2[q];
         const bool head = q == 0 || sk2[q] != sk2[q - 1] || col[p] != col[sv2[q - 1]];
         const int64_t u = uidx[q];
+        // uidx counts the heads before q: q's own union entry is uidx[q] at a
+        // head, uidx[q] - 1 elsewhere
+        occ_u[q] = (int32_t)(head ? u : u - 1);
         if (head) {
             ucol[u] = col[p];
             uptr[u] = q;
@@ -155,6 +158,7 @@ struct BatchOp {
     const int64_t *uptr;
     const int32_t *occ;
     const int32_t *occ_row;
+    const int32_t *occ_u;
     int64_t n, B;
     float lr;
 
@@ -325,6 +329,284 @@ __global__ __launch_bounds__(kBB) void k_batch_levels(BatchOp<LOSS, VAL> op,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Sync-free mini-batch epoch (the Read Protocol of Sec. 5 at feature grain,
+// with a batch as the iteration): no batch levels, no barriers.  Each
+// feature's weight and the union entry that last wrote it share one 64-bit
+// word.  Blocks take batches in index order; a batch waits until each of its
+// union features' words carries that feature's previous union entry (the
+// schedule's prev_nz over the union CSR, -1 for none), runs both phases on
+// those values and publishes (new weight, its union entry).  The earliest
+// unfinished batch never waits for a later one, so the grid always makes
+// progress; batches that share no feature run concurrently on different CUs.
+
+__device__ __forceinline__ unsigned long long bw_pack(float w, int tag) {
+    return ((unsigned long long)(unsigned)tag << 32) | (unsigned long long)__float_as_uint(w);
+}
+__device__ __forceinline__ float bw_value(unsigned long long v) {
+    return __uint_as_float((unsigned)v);
+}
+// device-scope 64-bit accesses: single-copy atomic, so tag and value match
+__device__ __forceinline__ unsigned long long bw_get(unsigned long long *base, int64_t i) {
+    return __hip_atomic_load(&base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void bw_put(unsigned long long *base, int64_t i, unsigned long long v) {
+    __hip_atomic_store(&base[i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void k_bw_in(const float *__restrict__ w, unsigned long long *__restrict__ bw,
+                        int64_t d) {
+    for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
+         f += (int64_t)gridDim.x * blockDim.x)
+        bw[f] = bw_pack(w[f], -1);
+}
+
+__global__ void k_bw_out(const unsigned long long *__restrict__ bw, float *__restrict__ w,
+                         int64_t d) {
+    for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
+         f += (int64_t)gridDim.x * blockDim.x)
+        w[f] = bw_value(bw[f]);
+}
+
+// Sleeps about 2^min(round, 3) x 64 cycles.
+__device__ __forceinline__ void bw_backoff(int round) {
+    switch (round < 3 ? round : 3) {
+        case 0: __builtin_amdgcn_s_sleep(1); break;
+        case 1: __builtin_amdgcn_s_sleep(2); break;
+        case 2: __builtin_amdgcn_s_sleep(4); break;
+        default: __builtin_amdgcn_s_sleep(8); break;
+    }
+}
+
+// Polls word idx (one per lane; lanes with want = false only take part in
+// the rounds) until it carries tag.  False on timeout or abort.
+__device__ __forceinline__ bool bw_wait_wave(unsigned long long *base, bool want, int64_t idx,
+                                             int tag, unsigned long long *out, Ctrl *ctrl,
+                                             int64_t timeout) {
+    bool ready = !want;
+    int64_t t0 = 0;
+    for (int round = 0;; ++round) {
+        if (!ready) {
+            const unsigned long long v = bw_get(base, idx);
+            if ((int)(unsigned)(v >> 32) == tag) {
+                *out = v;
+                ready = true;
+            }
+        }
+        if (__ballot(!ready) == 0ull) return true;
+        if (round == 0) t0 = now_ticks();
+        if (aborted(ctrl)) return false;
+        if (now_ticks() - t0 > timeout) {
+            record_error(ctrl, DERR_WAIT_TIMEOUT);
+            return false;
+        }
+        bw_backoff(round);
+        __asm__ __volatile__("" ::: "memory");  // the next round loads again
+    }
+}
+
+// LDS of a sync-free batch block: steps; for staged batches the weights of
+// the union features, each entry's union feature, and per occurrence its
+// example and value
+struct SfShared {
+    float s[kMaxBatch];
+    float uw[kCap];
+    int32_t eu[kCap];
+    int32_t oi[kCap];
+    float ox[kCap];
+    int64_t ticket;
+    int ok;
+};
+
+// A batch of any size: wait for every union feature's previous writer, then
+// both phases on the words themselves (staged in LDS when they fit).  False
+// when a wait gave up; every thread of the block returns the same.
+template <int LOSS, bool VAL>
+__device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
+                              unsigned long long *bw, SfShared &Sh, int64_t i0, int64_t i1,
+                              int64_t pb, int64_t pe, int64_t ub, int64_t ue, Ctrl *ctrl,
+                              int64_t timeout) {
+    const int lane = lane_id();
+    const int wave = (int)(threadIdx.x >> 6);
+    const bool staged = pe - pb <= kCap;  // (ue - ub <= pe - pb)
+    bool ok = true;
+    for (int64_t u0 = ub + wave * kWave; u0 < ue; u0 += kBB) {
+        const int64_t u = u0 + lane;
+        const bool live = u < ue;
+        const int32_t f = live ? op.ucol[u] : 0;
+        const int tag = live ? uprev[u] : -1;
+        unsigned long long v = 0;
+        if (!bw_wait_wave(bw, live, f, tag, &v, ctrl, timeout)) {
+            ok = false;
+            break;
+        }
+        if (staged && live) {
+            Sh.uw[u - ub] = bw_value(v);
+            const int64_t q1 = op.uptr[u + 1];
+            for (int64_t q = op.uptr[u]; q < q1; ++q) {
+                const int32_t p = op.occ[q];
+                Sh.eu[p - pb] = (int32_t)(u - ub);
+                Sh.oi[q - pb] = op.occ_row[q] - (int32_t)i0;
+                if (VAL) Sh.ox[q - pb] = op.val[p];
+            }
+        }
+    }
+    if (!ok && lane == 0) Sh.ok = 0;
+    __syncthreads();
+    if (!Sh.ok) return false;
+    // phase 1: every example against the weights the batch read
+    for (int64_t i = i0 + wave; i < i1; i += kBWaves) {
+        const int64_t p0 = op.row_ptr[i], m = op.row_ptr[i + 1] - p0;
+        float acc = 0.0f;
+        for (int64_t k = lane; k < m; k += kWave) {
+            const int64_t p = p0 + k;
+            const float wk = staged ? Sh.uw[Sh.eu[p - pb]] : bw_value(bw_get(bw, op.col[p]));
+            acc = __builtin_fmaf(wk, VAL ? op.val[p] : 1.0f, acc);
+        }
+        const float s = sgd_scale<LOSS>(wave_sum64(acc), op.y[i], op.lr);
+        if (lane == 0) Sh.s[i - i0] = s;
+    }
+    __syncthreads();
+    // phase 2: contributions in example order, then publish
+    for (int64_t u = ub + threadIdx.x; u < ue; u += kBB) {
+        const int32_t f = op.ucol[u];
+        const int64_t qa = op.uptr[u], qe = op.uptr[u + 1];
+        float v = staged ? Sh.uw[u - ub] : bw_value(bw_get(bw, f));
+        if (staged) {
+            for (int64_t q = qa - pb; q < qe - pb; ++q)
+                v = __builtin_fmaf(-Sh.s[Sh.oi[q]], VAL ? Sh.ox[q] : 1.0f, v);
+        } else {
+            for (int64_t q = qa; q < qe; ++q)
+                v = __builtin_fmaf(-Sh.s[op.occ_row[q] - i0], VAL ? op.val[op.occ[q]] : 1.0f, v);
+        }
+        bw_put(bw, f, bw_pack(v, (int)u));
+    }
+    __syncthreads();
+    return true;
+}
+
+// A batch of at most kBWaves * kG examples and kCap entries.  Everything
+// that does not depend on other batches comes first -- each wave's example
+// bounds, labels and values in registers, every occurrence's example, value
+// and union feature in LDS, each thread's union features in registers --
+// then the words are read once and only those not yet written by their
+// previous writer are polled; after that both phases read LDS only.
+template <int LOSS, bool VAL>
+__device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
+                           unsigned long long *bw, SfShared &Sh, int64_t i0, int64_t i1,
+                           int64_t pb, int64_t pe, int64_t ub, int64_t ue, Ctrl *ctrl,
+                           int64_t timeout) {
+    const int lane = lane_id();
+    const int wave = (int)(threadIdx.x >> 6);
+    // this wave's examples i0 + wave + kBWaves * j, j < kG
+    const int64_t my_i = i0 + wave + (int64_t)kBWaves * lane;
+    const bool has = lane < kG && my_i < i1;
+    const int64_t rb = op.row_ptr[has ? my_i : i0];
+    const int64_t re = has ? op.row_ptr[my_i + 1] : rb;
+    const float yv = op.y[has ? my_i : i0];
+    int32_t p[kG], m[kG];  // first entry relative to pb, entry count
+#pragma unroll
+    for (int j = 0; j < kG; ++j) {
+        const int64_t r0 = readlane64(rb, j);
+        p[j] = (int32_t)(r0 - pb);
+        m[j] = (int32_t)(readlane64(re, j) - r0);
+    }
+    float x[2 * kG];
+#pragma unroll
+    for (int t = 0; t < 2 * kG; ++t) {
+        x[t] = 1.0f;
+        if (VAL && pe > pb)
+            x[t] = op.val[min(max(pb + p[t >> 1] + (t & 1) * kWave + lane, pb), pe - 1)];
+    }
+    for (int64_t q = pb + threadIdx.x; q < pe; q += kBB) {
+        const int32_t pq = op.occ[q];
+        Sh.oi[q - pb] = op.occ_row[q] - (int32_t)i0;
+        if (VAL) Sh.ox[q - pb] = op.val[pq];
+        Sh.eu[pq - pb] = op.occ_u[q] - (int32_t)ub;
+    }
+    int32_t f[kH], tag[kH], q0[kH], q1[kH];
+#pragma unroll
+    for (int h = 0; h < kH; ++h) {
+        const int64_t u = ub + threadIdx.x + (int64_t)kBB * h;
+        const bool live = u < ue;
+        f[h] = live ? op.ucol[u] : 0;
+        tag[h] = live ? uprev[u] : -1;
+        q0[h] = live ? (int32_t)(op.uptr[u] - pb) : 0;
+        q1[h] = live ? (int32_t)(op.uptr[u + 1] - pb) : 0;
+    }
+    // reads: every word once, then a wait for those not yet written
+    unsigned long long v[kH];
+    bool ready[kH];
+#pragma unroll
+    for (int h = 0; h < kH; ++h) {
+        const bool live = ub + threadIdx.x + (int64_t)kBB * h < ue;
+        v[h] = live ? bw_get(bw, f[h]) : 0ull;
+        ready[h] = !live || (int)(unsigned)(v[h] >> 32) == tag[h];
+    }
+    bool ok = true;
+#pragma unroll
+    for (int h = 0; h < kH; ++h) {
+        if (ok && __ballot(!ready[h]) != 0ull)
+            ok = bw_wait_wave(bw, !ready[h], f[h], tag[h], &v[h], ctrl, timeout);
+        if (ub + threadIdx.x + (int64_t)kBB * h < ue)
+            Sh.uw[threadIdx.x + kBB * h] = bw_value(v[h]);
+    }
+    if (!ok && lane == 0) Sh.ok = 0;
+    __syncthreads();
+    if (!Sh.ok) return false;
+    // phase 1 from LDS
+#pragma unroll
+    for (int j = 0; j < kG; ++j) {
+        if (i0 + wave + (int64_t)kBWaves * j >= i1) break;  // wave-uniform
+        const int k0 = lane, k1 = kWave + lane;
+        float acc = k0 < m[j] ? __builtin_fmaf(Sh.uw[Sh.eu[p[j] + k0]], x[2 * j], 0.0f) : 0.0f;
+        if (k1 < m[j]) acc = __builtin_fmaf(Sh.uw[Sh.eu[p[j] + k1]], x[2 * j + 1], acc);
+        for (int k = 2 * kWave + lane; k < m[j]; k += kWave)
+            acc = __builtin_fmaf(Sh.uw[Sh.eu[p[j] + k]], VAL ? op.val[pb + p[j] + k] : 1.0f, acc);
+        const float yj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(yv), j));
+        const float sj = sgd_scale<LOSS>(wave_sum64(acc), yj, op.lr);
+        if (lane == 0) Sh.s[wave + kBWaves * j] = sj;
+    }
+    __syncthreads();
+    // phase 2 from LDS, then publish
+#pragma unroll
+    for (int h = 0; h < kH; ++h) {
+        const int64_t u = ub + threadIdx.x + (int64_t)kBB * h;
+        if (u >= ue) break;
+        float val = Sh.uw[threadIdx.x + kBB * h];
+        for (int32_t q = q0[h]; q < q1[h]; ++q)
+            val = __builtin_fmaf(-Sh.s[Sh.oi[q]], VAL ? Sh.ox[q] : 1.0f, val);
+        bw_put(bw, f[h], bw_pack(val, (int)u));
+    }
+    __syncthreads();
+    return true;
+}
+
+template <int LOSS, bool VAL>
+__global__ __launch_bounds__(kBB) void k_batch_syncfree(BatchOp<LOSS, VAL> op,
+                                                       const int32_t *__restrict__ uprev,
+                                                       unsigned long long *bw, int64_t nb,
+                                                       Ctrl *ctrl, int64_t timeout) {
+    __shared__ SfShared Sh;
+    for (;;) {
+        if (threadIdx.x == 0) {
+            Sh.ticket = (int64_t)atomicAdd(&ctrl->ticket, 1ull);
+            Sh.ok = 1;
+        }
+        __syncthreads();
+        const int64_t b = Sh.ticket;
+        if (b >= nb) return;
+        const int64_t i0 = b * op.B, i1 = min(i0 + op.B, op.n);
+        const int64_t pb = op.row_ptr[i0], pe = op.row_ptr[i1];
+        const int64_t ub = op.bptr[b], ue = op.bptr[b + 1];
+        if (pe - pb <= kCap && i1 - i0 <= (int64_t)kBWaves * kG) {
+            if (!fast_batch(op, uprev, bw, Sh, i0, i1, pb, pe, ub, ue, ctrl, timeout)) return;
+        } else {
+            if (!general_batch(op, uprev, bw, Sh, i0, i1, pb, pe, ub, ue, ctrl, timeout)) return;
+        }
+    }
+}
+
 __global__ void k_batch_ctrl_zero(Ctrl *c) {
     int *w = reinterpret_cast<int *>(c);
     for (int i = threadIdx.x; i < (int)(sizeof(Ctrl) / sizeof(int)); i += blockDim.x) w[i] = 0;
@@ -365,6 +647,36 @@ int launch_batch(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, Ctrl *ctrl,
     return PDB_OK;
 }
 
+int64_t batch_sf_ws_bytes(int64_t d) { return (int64_t)sizeof(Ctrl) + align_up(8 * d); }
+
+template <int LOSS, bool VAL>
+int launch_batch_syncfree(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, int64_t d,
+                          int64_t nb, void *ws, hipStream_t s) {
+    Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    unsigned long long *bw =
+        reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
+    const int64_t timeout = spin_timeout_ticks();
+    k_batch_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
+    PDB_LAUNCHED();
+    if (d > 0) {
+        k_bw_in<<<grid_for(d, kBlock, 8192), kBlock, 0, s>>>(op.w, bw, d);
+        PDB_LAUNCHED();
+    }
+    // one block per CU (the LDS of a block fills most of a CU); blocks need
+    // not be co-resident: the earliest unfinished batch is always running
+    int dev = 0, cus = 0;
+    PDB_HIP(hipGetDevice(&dev));
+    PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cus, nb));
+    k_batch_syncfree<LOSS, VAL><<<grid, kBB, 0, s>>>(op, lv->prev_nz, bw, nb, ctrl, timeout);
+    PDB_LAUNCHED();
+    if (d > 0) {
+        k_bw_out<<<grid_for(d, kBlock, 8192), kBlock, 0, s>>>(bw, op.w, d);
+        PDB_LAUNCHED();
+    }
+    return PDB_OK;
+}
+
 int check_batch_sizes(int64_t n, int64_t d, int64_t nnz, int64_t B) {
     if (n < 0 || d < 0 || nnz < 0 || B < 1) return PDB_ERR_INVALID_ARG;
     if (B > kMaxBatch) return PDB_ERR_INVALID_ARG;
@@ -396,7 +708,8 @@ extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int6
     int rc = check_batch_sizes(n, d, nnz, batch);
     if (rc != PDB_OK) return rc;
     if (d == 0 && nnz > 0) return PDB_ERR_BAD_CSR;
-    if (!bt->bptr || !bt->uptr || (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row)))
+    if (!bt->bptr || !bt->uptr ||
+        (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row || !bt->occ_u)))
         return PDB_ERR_INVALID_ARG;
     SchedWs w = sched_ws_layout(ws, n, d, nnz);
     if (ws_bytes < w.total) return PDB_ERR_WORKSPACE;
@@ -431,7 +744,7 @@ extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int6
         PDB_LAUNCHED();
         PDB_HIP(exclusive_scan_u32(flag, flag, nnz, w.scan_tmp, s));
         k_union_write<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(
-            sk2, sv2, nnz, csr->col, flag, bt->ucol, bt->uptr, ubatch, bt->bptr + nb);
+            sk2, sv2, nnz, csr->col, flag, bt->ucol, bt->uptr, ubatch, bt->occ_u, bt->bptr + nb);
         PDB_LAUNCHED();
         if (nb > 0) {
             k_bptr<<<grid_for(nb, kBlock, 65536), kBlock, 0, s>>>(ubatch, nb, bt->bptr);
@@ -460,14 +773,29 @@ extern "C" int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t 
     if (loss != PDB_LOGISTIC && loss != PDB_SQUARED) return PDB_ERR_INVALID_ARG;
     if (ws_bytes < sizeof(Ctrl)) return PDB_ERR_WORKSPACE;
     if (n == 0) return PDB_OK;
-    if (!bt->bptr || !bt->uptr || (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row)))
+    if (!bt->bptr || !bt->uptr ||
+        (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row || !bt->occ_u)))
         return PDB_ERR_INVALID_ARG;
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    // sync-free when the previous writers over the union CSR are known and the
+    // workspace holds a word per feature; PDB_EPOCH_MODE 1 / 2 forces batch
+    // levels / sync-free
+    const char *me = getenv("PDB_EPOCH_MODE");
+    const int64_t mode = me ? atoll(me) : 0;
+    const bool sf_ok = lv->prev_nz != nullptr && (int64_t)ws_bytes >= batch_sf_ws_bytes(d);
+    const bool syncfree = sf_ok && mode != 1;
+    const int64_t nb = cdiv(n, batch);
 #define PDB_BATCH(LOSS, VAL)                                                                     \
-    launch_batch<LOSS, VAL>(BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w,      \
-                                               bt->bptr, bt->ucol, bt->uptr, bt->occ,           \
-                                               bt->occ_row, n, batch, lr},                      \
-                            lv, ctrl, s)
+    (syncfree ? launch_batch_syncfree<LOSS, VAL>(                                              \
+                    BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w, bt->bptr,   \
+                                       bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u, n, batch, \
+                                       lr}, \
+                    lv, d, nb, ws, s)                                                           \
+              : launch_batch<LOSS, VAL>(                                                       \
+                    BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w, bt->bptr,   \
+                                       bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u, n, batch, \
+                                       lr}, \
+                    lv, ctrl, s))
     if (loss == PDB_LOGISTIC) return csr->val ? PDB_BATCH(PDB_LOGISTIC, true) : PDB_BATCH(PDB_LOGISTIC, false);
     return csr->val ? PDB_BATCH(PDB_SQUARED, true) : PDB_BATCH(PDB_SQUARED, false);
 #undef PDB_BATCH

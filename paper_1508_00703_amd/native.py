@@ -49,7 +49,8 @@ class PdbLevels(ctypes.Structure):
 
 class PdbBatches(ctypes.Structure):
     _fields_ = [("bptr", ctypes.c_void_p), ("ucol", ctypes.c_void_p), ("uptr", ctypes.c_void_p),
-                ("occ", ctypes.c_void_p), ("occ_row", ctypes.c_void_p), ("U_host", ctypes.c_int64)]
+                ("occ", ctypes.c_void_p), ("occ_row", ctypes.c_void_p), ("occ_u", ctypes.c_void_p),
+                ("U_host", ctypes.c_int64)]
 
 
 class PdbScheduleInfo(ctypes.Structure):
@@ -203,11 +204,12 @@ class Batches:
         self.uptr = torch.empty(nnz + 1, dtype=torch.int64, device=device)
         self.occ = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
         self.occ_row = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
+        self.occ_u = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
         self.U_host = 0
 
     def c(self) -> PdbBatches:
         return PdbBatches(_ptr(self.bptr), _ptr(self.ucol), _ptr(self.uptr), _ptr(self.occ),
-                          _ptr(self.occ_row), self.U_host)
+                          _ptr(self.occ_row), _ptr(self.occ_u), self.U_host)
 
 
 def pdb_strerror(code: int) -> str:
@@ -302,7 +304,7 @@ def pdb_batch_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Ten
     if w.numel() < d or labels.numel() < n:
         raise ValueError("w must hold d entries and labels n entries")
     if ws is None:
-        ws = workspace(pdb_epoch_workspace_bytes(0), csr.device)
+        ws = workspace(pdb_epoch_workspace_bytes(d), csr.device)
     _check(load().pdb_batch_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, batches.batch, _ptr(w),
                                   ctypes.c_float(lr), loss, ctypes.byref(batches.c()),
                                   ctypes.byref(levels.c()), _ptr(ws), ws.numel(),

@@ -42,6 +42,7 @@ def check_batch_schedule(native, dev, row_ptr, col, d, B, method=0):
     assert np.array_equal(bt.occ.cpu().numpy()[:nnz], occ)
     row_of = np.repeat(np.arange(len(row_ptr) - 1), np.diff(row_ptr)).astype(np.int32)
     assert np.array_equal(bt.occ_row.cpu().numpy()[:nnz], row_of[occ])
+    assert np.array_equal(bt.occ_u.cpu().numpy()[:nnz], np.repeat(np.arange(U), np.diff(uptr)))
     level, perm, level_ptr, L = oracle.batch_schedule(row_ptr, col, d, B)
     assert lv.L_host == L
     assert np.array_equal(lv.level.cpu().numpy(), level)
@@ -65,6 +66,8 @@ def check_batch_epoch(native, dev, g, B, bt, lv, tol=1e-5):
     y = torch.from_numpy(g["y"]).to(dev)
     w = torch.zeros(g["d"], dtype=torch.float32, device=dev)
     ws = native.pdb_batch_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], bt, lv)
+    # (the default workspace holds a word per feature: sync-free unless
+    # PDB_EPOCH_MODE=1)
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     got = w.cpu().numpy()
@@ -110,11 +113,16 @@ def structured_problem(rows, loss, with_val, seed, B=1):
     return dict(row_ptr=row_ptr, col=col, val=val, y=y, n=n, d=d, lr=lr, loss=loss)
 
 
+EPOCH_MODES = ["1", "2"]  # batch levels, sync-free
+
+
 @pytest.mark.parametrize("name", sorted(structured_cases()))
 @pytest.mark.parametrize("loss", [0, 1])
 @pytest.mark.parametrize("with_val", [True, False])
 @pytest.mark.parametrize("B", [1, 3, 64])
-def test_structured_batch_epochs(gpu, name, loss, with_val, B):
+@pytest.mark.parametrize("mode", EPOCH_MODES)
+def test_structured_batch_epochs(gpu, name, loss, with_val, B, mode, monkeypatch):
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     g = structured_problem(structured_cases()[name], loss, with_val, B + loss, B)
     bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], B)
@@ -130,8 +138,10 @@ def batch_workload(g, B):
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
-@pytest.mark.parametrize("B", [1, 5, 100, 1000])
-def test_random_batch_epochs(gpu, cfg, B):
+@pytest.mark.parametrize("B", [1, 5, 100, 1000, 4096])
+@pytest.mark.parametrize("mode", EPOCH_MODES)
+def test_random_batch_epochs(gpu, cfg, B, mode, monkeypatch):
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     g = batch_workload(datagen.generate(cfg, n=6000, d=3000 if cfg == 4 else 500, seed=31 + B), B)
     bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], B)
@@ -144,6 +154,7 @@ def test_wide_and_narrow_batch_levels(gpu, thin, monkeypatch):
     # device barriers) and a chain of narrow ones (block 0), or everything in
     # one block
     monkeypatch.setenv("PDB_BATCH_THIN_MAX", thin)
+    monkeypatch.setenv("PDB_EPOCH_MODE", "1")
     native = native_mod()
     rows = [{2 * i, 2 * i + 1} for i in range(3000)] + [{0, 7 + i % 50} for i in range(500)]
     rows += [{10000 + i} for i in range(2000)]
@@ -184,10 +195,20 @@ def test_batch_errors(gpu):
 
 @pytest.mark.parametrize("cfg", [2, 3, 4])
 def test_full_size_batch(gpu, cfg):
-    # the launch configuration bench.py --batch 100 times
+    # the launch configuration bench.py --batch 100 times (sync-free)
     native = native_mod()
     g = batch_workload(datagen.generate(cfg), 100)
     bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 100)
     print("config %d, batches of 100: L=%d max width=%d U=%d" % (cfg, lv.L_host, lv.max_width_host,
                                                                  bt.U_host), flush=True)
+    check_batch_epoch(native, gpu, g, 100, bt, lv)
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_full_size_batch_levels(gpu, cfg, monkeypatch):
+    # the batch-level execution at full size
+    monkeypatch.setenv("PDB_EPOCH_MODE", "1")
+    native = native_mod()
+    g = batch_workload(datagen.generate(cfg), 100)
+    bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 100)
     check_batch_epoch(native, gpu, g, 100, bt, lv)

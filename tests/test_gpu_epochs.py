@@ -56,9 +56,11 @@ def test_sgd_epochs_on_a_cached_schedule(gpu, cfg, mode, monkeypatch):
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
-def test_batch_epochs_on_a_cached_schedule(gpu, cfg):
+@pytest.mark.parametrize("mode", ["1", "2"])
+def test_batch_epochs_on_a_cached_schedule(gpu, cfg, mode, monkeypatch):
     import torch
 
+    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     B = 100
     g = batch_workload(datagen.generate(cfg, n=20000, d=6000 if cfg == 4 else 1000, seed=10), B)
@@ -66,7 +68,7 @@ def test_batch_epochs_on_a_cached_schedule(gpu, cfg):
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], gpu)
     y = torch.from_numpy(g["y"]).to(gpu)
     w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
-    ws = native.workspace(native.pdb_epoch_workspace_bytes(0), gpu)
+    ws = native.workspace(native.pdb_epoch_workspace_bytes(g["d"]), gpu)
     for _ in range(EPOCHS):
         native.pdb_batch_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], bt, lv, ws=ws)
     torch.cuda.synchronize()
