@@ -191,7 +191,11 @@ int pdb_workspace_status(void *ws, hipStream_t stream);
  *   uptr    [nnz+1]  union entry u's occurrences are occ[uptr[u] .. uptr[u+1]);
  *   occ     [nnz]    CSR entry indices ordered by (batch, feature, index);
  *   occ_row [nnz]    the example of each of them;
- *   occ_u   [nnz]    the union entry of each of them. */
+ *   occ_u   [nnz]    the union entry of each of them;
+ *   unext   [nnz]    NULL, or the next union entry on the same feature (-1 if
+ *                    none; written when levels->prev_nz is set): the
+ *                    sync-free epoch publishes what the next batch needs
+ *                    first. */
 typedef struct pdb_batches {
     int64_t *bptr;
     int32_t *ucol;
@@ -199,6 +203,7 @@ typedef struct pdb_batches {
     int32_t *occ;
     int32_t *occ_row;
     int32_t *occ_u;
+    int32_t *unext;
     int64_t U_host; /* union size U, written by pdb_batch_schedule */
 } pdb_batches;
 

@@ -137,6 +137,21 @@ __global__ __launch_bounds__(kBlock) void k_bptr(const uint32_t *__restrict__ ub
     }
 }
 
+// next union entry on the same feature (the inverse of the previous-writer
+// relation over union entries), -1 if none
+__global__ __launch_bounds__(kBlock) void k_union_next(const int32_t *__restrict__ uprev,
+                                                       int64_t U, int32_t *__restrict__ unext) {
+    for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < U;
+         u += (int64_t)gridDim.x * blockDim.x)
+        if (uprev[u] >= 0) unext[uprev[u]] = (int32_t)u;
+}
+
+__global__ void k_fill32(int32_t *p, int64_t count, int32_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
 __global__ void k_fill64(int64_t *p, int64_t count, int64_t v) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
          i += (int64_t)gridDim.x * blockDim.x)
@@ -145,6 +160,32 @@ __global__ void k_fill64(int64_t *p, int64_t count, int64_t v) {
 
 // ---------------------------------------------------------------------------
 // epoch
+
+// oi[q] (an example relative to the batch) becomes that example's step,
+// stored in place as the float's bits; count occurrences, the whole block
+__device__ __forceinline__ void resolve_steps(int32_t *oi, const float *s, int64_t count) {
+    for (int64_t q = threadIdx.x; q < count; q += kBB) oi[q] = __float_as_int(s[oi[q]]);
+}
+
+// w after the contributions of occurrences [q0, q1): w = fma(-step, x, w)
+// in order; the loads of a group of 8 are issued before its fmas
+template <bool VAL>
+__device__ __forceinline__ float chain_apply(float w, const float *step, const float *x,
+                                             int32_t q0, int32_t q1) {
+    int32_t q = q0;
+    for (; q + 8 <= q1; q += 8) {
+        float sv[8], xv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            sv[k] = step[q + k];
+            xv[k] = VAL ? x[q + k] : 1.0f;
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) w = __builtin_fmaf(-sv[k], xv[k], w);
+    }
+    for (; q < q1; ++q) w = __builtin_fmaf(-step[q], VAL ? x[q] : 1.0f, w);
+    return w;
+}
 
 template <int LOSS, bool VAL>
 struct BatchOp {
@@ -159,6 +200,7 @@ struct BatchOp {
     const int32_t *occ;
     const int32_t *occ_row;
     const int32_t *occ_u;
+    const int32_t *unext;  // may be null
     int64_t n, B;
     float lr;
 
@@ -257,13 +299,13 @@ struct BatchOp {
         // phase 2: each union feature takes the batch's contributions in
         // example order; no other batch of the level touches it
         if (staged) {
+            resolve_steps(Sh.oi, Sh.s, pe - pb);
+            __syncthreads();
 #pragma unroll
             for (int h = 0; h < kH; ++h) {
                 if (u0 + (int64_t)kBB * h >= ue) break;
-                float v = Sh.w[pf[h]];
-                for (int32_t q = q0[h] - (int32_t)pb; q < q1[h] - (int32_t)pb; ++q)
-                    v = __builtin_fmaf(-Sh.s[Sh.oi[q]], VAL ? Sh.ox[q] : 1.0f, v);
-                w[f[h]] = v;
+                w[f[h]] = chain_apply<VAL>(Sh.w[pf[h]], reinterpret_cast<const float *>(Sh.oi),
+                                           Sh.ox, q0[h] - (int32_t)pb, q1[h] - (int32_t)pb);
             }
         } else {
             for (int64_t u = u0; u < ue; u += kBB) {
@@ -405,6 +447,41 @@ __device__ __forceinline__ bool bw_wait_wave(unsigned long long *base, bool want
     }
 }
 
+// Polls the words f[h] of the slots not yet ready until each carries tag[h];
+// every round reloads all of them at once, so a wave confirms several
+// arrivals in one round trip.  False on timeout or abort.
+template <int H>
+__device__ __forceinline__ bool bw_wait_slots(unsigned long long *base, const int32_t *f,
+                                              const int32_t *tag, bool *ready,
+                                              unsigned long long *v, Ctrl *ctrl,
+                                              int64_t timeout) {
+    int64_t t0 = 0;
+    for (int round = 0;; ++round) {
+        bool all = true;
+#pragma unroll
+        for (int h = 0; h < H; ++h) all = all && ready[h];
+        if (__ballot(!all) == 0ull) return true;
+        if (round == 0) {
+            t0 = now_ticks();
+        } else {
+            if (aborted(ctrl)) return false;
+            if (now_ticks() - t0 > timeout) {
+                record_error(ctrl, DERR_WAIT_TIMEOUT);
+                return false;
+            }
+        }
+        bw_backoff(round);
+        __asm__ __volatile__("" ::: "memory");  // the loads below are issued again
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+            if (!ready[h]) {
+                v[h] = bw_get(base, f[h]);
+                ready[h] = (int)(unsigned)(v[h] >> 32) == tag[h];
+            }
+        }
+    }
+}
+
 // LDS of a sync-free batch block: steps; for staged batches the weights of
 // the union features, each entry's union feature, and per occurrence its
 // example and value
@@ -467,14 +544,18 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
         if (lane == 0) Sh.s[i - i0] = s;
     }
     __syncthreads();
+    if (staged) {
+        resolve_steps(Sh.oi, Sh.s, pe - pb);
+        __syncthreads();
+    }
     // phase 2: contributions in example order, then publish
     for (int64_t u = ub + threadIdx.x; u < ue; u += kBB) {
         const int32_t f = op.ucol[u];
         const int64_t qa = op.uptr[u], qe = op.uptr[u + 1];
         float v = staged ? Sh.uw[u - ub] : bw_value(bw_get(bw, f));
         if (staged) {
-            for (int64_t q = qa - pb; q < qe - pb; ++q)
-                v = __builtin_fmaf(-Sh.s[Sh.oi[q]], VAL ? Sh.ox[q] : 1.0f, v);
+            v = chain_apply<VAL>(v, reinterpret_cast<const float *>(Sh.oi), Sh.ox,
+                                 (int32_t)(qa - pb), (int32_t)(qe - pb));
         } else {
             for (int64_t q = qa; q < qe; ++q)
                 v = __builtin_fmaf(-Sh.s[op.occ_row[q] - i0], VAL ? op.val[op.occ[q]] : 1.0f, v);
@@ -493,9 +574,9 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
 // previous writer are polled; after that both phases read LDS only.
 template <int LOSS, bool VAL>
 __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
-                           unsigned long long *bw, SfShared &Sh, int64_t i0, int64_t i1,
-                           int64_t pb, int64_t pe, int64_t ub, int64_t ue, Ctrl *ctrl,
-                           int64_t timeout) {
+                           unsigned long long *bw, SfShared &Sh, int64_t b, int64_t nb,
+                           int64_t i0, int64_t i1, int64_t pb, int64_t pe, int64_t ub,
+                           int64_t ue, Ctrl *ctrl, int64_t timeout) {
     const int lane = lane_id();
     const int wave = (int)(threadIdx.x >> 6);
     // this wave's examples i0 + wave + kBWaves * j, j < kG
@@ -525,6 +606,9 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
         Sh.eu[pq - pb] = op.occ_u[q] - (int32_t)ub;
     }
     int32_t f[kH], tag[kH], q0[kH], q1[kH];
+    bool urgent[kH];  // the next batch writes this feature too: publish it first
+    // union entries of the batches up to the next one end at soon_end
+    const int64_t soon_end = op.unext ? op.bptr[min(b + 2, nb)] : 0;
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
         const int64_t u = ub + threadIdx.x + (int64_t)kBB * h;
@@ -533,6 +617,8 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
         tag[h] = live ? uprev[u] : -1;
         q0[h] = live ? (int32_t)(op.uptr[u] - pb) : 0;
         q1[h] = live ? (int32_t)(op.uptr[u + 1] - pb) : 0;
+        const int32_t nx = (live && op.unext) ? op.unext[u] : -1;
+        urgent[h] = nx >= 0 && nx < soon_end;
     }
     // reads: every word once, then a wait for those not yet written
     unsigned long long v[kH];
@@ -543,14 +629,10 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
         v[h] = live ? bw_get(bw, f[h]) : 0ull;
         ready[h] = !live || (int)(unsigned)(v[h] >> 32) == tag[h];
     }
-    bool ok = true;
+    const bool ok = bw_wait_slots<kH>(bw, f, tag, ready, v, ctrl, timeout);
 #pragma unroll
-    for (int h = 0; h < kH; ++h) {
-        if (ok && __ballot(!ready[h]) != 0ull)
-            ok = bw_wait_wave(bw, !ready[h], f[h], tag[h], &v[h], ctrl, timeout);
-        if (ub + threadIdx.x + (int64_t)kBB * h < ue)
-            Sh.uw[threadIdx.x + kBB * h] = bw_value(v[h]);
-    }
+    for (int h = 0; h < kH; ++h)
+        if (ub + threadIdx.x + (int64_t)kBB * h < ue) Sh.uw[threadIdx.x + kBB * h] = bw_value(v[h]);
     if (!ok && lane == 0) Sh.ok = 0;
     __syncthreads();
     if (!Sh.ok) return false;
@@ -568,15 +650,28 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
         if (lane == 0) Sh.s[wave + kBWaves * j] = sj;
     }
     __syncthreads();
-    // phase 2 from LDS, then publish
+    // every occurrence's step, in parallel: the chains below then read one
+    // LDS word per fma, none of which depends on the chain
+    resolve_steps(Sh.oi, Sh.s, pe - pb);
+    __syncthreads();
+    // phase 2 from LDS; the features the next batch waits for are published
+    // before the others (one CU issues a batch's thousands of scattered
+    // stores, and the waiting batch needs only a few of them)
+    float val[kH];
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
-        const int64_t u = ub + threadIdx.x + (int64_t)kBB * h;
-        if (u >= ue) break;
-        float val = Sh.uw[threadIdx.x + kBB * h];
-        for (int32_t q = q0[h]; q < q1[h]; ++q)
-            val = __builtin_fmaf(-Sh.s[Sh.oi[q]], VAL ? Sh.ox[q] : 1.0f, val);
-        bw_put(bw, f[h], bw_pack(val, (int)u));
+        val[h] = 0.0f;
+        if (ub + threadIdx.x + (int64_t)kBB * h < ue)
+            val[h] = chain_apply<VAL>(Sh.uw[threadIdx.x + kBB * h],
+                                      reinterpret_cast<const float *>(Sh.oi), Sh.ox, q0[h], q1[h]);
+    }
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+        for (int h = 0; h < kH; ++h) {
+            const int64_t u = ub + threadIdx.x + (int64_t)kBB * h;
+            if (u < ue && urgent[h] == (pass == 0)) bw_put(bw, f[h], bw_pack(val[h], (int)u));
+        }
     }
     __syncthreads();
     return true;
@@ -600,7 +695,8 @@ __global__ __launch_bounds__(kBB) void k_batch_syncfree(BatchOp<LOSS, VAL> op,
         const int64_t pb = op.row_ptr[i0], pe = op.row_ptr[i1];
         const int64_t ub = op.bptr[b], ue = op.bptr[b + 1];
         if (pe - pb <= kCap && i1 - i0 <= (int64_t)kBWaves * kG) {
-            if (!fast_batch(op, uprev, bw, Sh, i0, i1, pb, pe, ub, ue, ctrl, timeout)) return;
+            if (!fast_batch(op, uprev, bw, Sh, b, nb, i0, i1, pb, pe, ub, ue, ctrl, timeout))
+                return;
         } else {
             if (!general_batch(op, uprev, bw, Sh, i0, i1, pb, pe, ub, ue, ctrl, timeout)) return;
         }
@@ -667,7 +763,11 @@ int launch_batch_syncfree(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, in
     int dev = 0, cus = 0;
     PDB_HIP(hipGetDevice(&dev));
     PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(cus, nb));
+    const char *ge = getenv("PDB_BATCH_SF_BLOCKS");
+    // at most 32 blocks by default: more batches in flight only add polls
+    // that slow the frontier's memory accesses
+    const int64_t cap = ge ? std::max<int64_t>(atoll(ge), 1) : 32;
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus, cap), nb));
     k_batch_syncfree<LOSS, VAL><<<grid, kBB, 0, s>>>(op, lv->prev_nz, bw, nb, ctrl, timeout);
     PDB_LAUNCHED();
     if (d > 0) {
@@ -757,7 +857,20 @@ extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int6
     }
     // the batch levels: conflict levels of the union CSR, whose rows are the batches
     const pdb_csr ucsr{bt->bptr, bt->ucol, nullptr, bt->U_host};
-    return pdb_schedule(&ucsr, nullptr, nb, d, lv, method, info, ws, ws_bytes, s);
+    rc = pdb_schedule(&ucsr, nullptr, nb, d, lv, method, info, ws, ws_bytes, s);
+    if (rc != PDB_OK) return rc;
+    // each union entry's next writer, when asked for and known
+    if (bt->unext && bt->U_host > 0) {
+        k_fill32<<<grid_for(bt->U_host, kBlock, 65536), kBlock, 0, s>>>(bt->unext, bt->U_host, -1);
+        PDB_LAUNCHED();
+        if (lv->prev_nz) {
+            k_union_next<<<grid_for(bt->U_host, kBlock, 65536), kBlock, 0, s>>>(
+                lv->prev_nz, bt->U_host, bt->unext);
+            PDB_LAUNCHED();
+        }
+        PDB_HIP(hipStreamSynchronize(s));
+    }
+    return PDB_OK;
 }
 
 extern "C" int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
@@ -788,13 +901,13 @@ extern "C" int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t 
 #define PDB_BATCH(LOSS, VAL)                                                                     \
     (syncfree ? launch_batch_syncfree<LOSS, VAL>(                                              \
                     BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w, bt->bptr,   \
-                                       bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u, n, batch, \
-                                       lr}, \
+                                       bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u,         \
+                                       bt->unext, n, batch, lr}, \
                     lv, d, nb, ws, s)                                                           \
               : launch_batch<LOSS, VAL>(                                                       \
                     BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w, bt->bptr,   \
-                                       bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u, n, batch, \
-                                       lr}, \
+                                       bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u,         \
+                                       bt->unext, n, batch, lr}, \
                     lv, ctrl, s))
     if (loss == PDB_LOGISTIC) return csr->val ? PDB_BATCH(PDB_LOGISTIC, true) : PDB_BATCH(PDB_LOGISTIC, false);
     return csr->val ? PDB_BATCH(PDB_SQUARED, true) : PDB_BATCH(PDB_SQUARED, false);

@@ -50,7 +50,7 @@ class PdbLevels(ctypes.Structure):
 class PdbBatches(ctypes.Structure):
     _fields_ = [("bptr", ctypes.c_void_p), ("ucol", ctypes.c_void_p), ("uptr", ctypes.c_void_p),
                 ("occ", ctypes.c_void_p), ("occ_row", ctypes.c_void_p), ("occ_u", ctypes.c_void_p),
-                ("U_host", ctypes.c_int64)]
+                ("unext", ctypes.c_void_p), ("U_host", ctypes.c_int64)]
 
 
 class PdbScheduleInfo(ctypes.Structure):
@@ -205,11 +205,12 @@ class Batches:
         self.occ = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
         self.occ_row = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
         self.occ_u = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
+        self.unext = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
         self.U_host = 0
 
     def c(self) -> PdbBatches:
         return PdbBatches(_ptr(self.bptr), _ptr(self.ucol), _ptr(self.uptr), _ptr(self.occ),
-                          _ptr(self.occ_row), _ptr(self.occ_u), self.U_host)
+                          _ptr(self.occ_row), _ptr(self.occ_u), _ptr(self.unext), self.U_host)
 
 
 def pdb_strerror(code: int) -> str:

@@ -51,6 +51,9 @@ def check_batch_schedule(native, dev, row_ptr, col, d, B, method=0):
     # previous writer over the union CSR: the union entry of the latest earlier
     # batch on the same feature
     pn = lv.prev_nz.cpu().numpy()[:U]
+    nxt = np.full(U, -1, np.int64)
+    nxt[pn[pn >= 0]] = np.nonzero(pn >= 0)[0]
+    assert np.array_equal(bt.unext.cpu().numpy()[:U], nxt)
     prev_batch = oracle.prev_writer(bptr, ucol, d)
     has = prev_batch >= 0
     assert np.array_equal(pn >= 0, has)
