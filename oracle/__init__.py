@@ -19,6 +19,10 @@ What it computes (all single-threaded, binary32 arithmetic, see oracle.c):
     (Sec. 6.3's mini-batch gradient descent): batch levels, each batch's
     union of features with its occurrences in example order, and the
     sequential mini-batch epoch.
+  * ``stale_epoch`` / ``stale_snapshot``: the bounded-delay relaxation of
+    Sec. 7, in the execution that reads as early as its read constraint
+    allows (example alpha computes z against the weights after examples
+    0 .. alpha - delay - 1; updates applied in example order).
   * ``history``: the execution-history predicates of Definition 4 and
     Sec. 4.3-4.4 (see ``oracle.history``).
 
@@ -84,6 +88,10 @@ def _load():
     lib.orc_batch_union.restype = i64
     lib.orc_batch_apply.argtypes = [i64, i64, P, P, P, P, P, P, f32, i32, i32, i64]
     lib.orc_batch_apply.restype = ctypes.c_int
+    lib.orc_stale_snapshot.argtypes = [i64, i64, P, P, P, P, P, f32, i32, i32, i64]
+    lib.orc_stale_snapshot.restype = ctypes.c_int
+    lib.orc_stale_apply.argtypes = [i64, i64, P, P, P, P, P, f32, i32, i32, i64]
+    lib.orc_stale_apply.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -275,3 +283,26 @@ def batch_epoch(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, B=100,
                                _ptr(w), np.float32(lr), loss, mode, B) != 0:
         raise MemoryError
     return w
+
+
+def _stale(fn, row_ptr, col, val, y, w, d, lr, loss, mode, delay):
+    row_ptr = _c(row_ptr, np.int64)
+    col = _c(col, np.int32)
+    val = None if val is None else _c(val, np.float32)
+    y = _c(y, np.float32)
+    w = np.array(w, dtype=np.float32, copy=True)
+    n = len(row_ptr) - 1
+    if fn(n, d, _ptr(row_ptr), _ptr(col), _ptr(val), _ptr(y), _ptr(w), np.float32(lr), loss, mode,
+          int(delay)) != 0:
+        raise MemoryError
+    return w
+
+
+def stale_epoch(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, delay=0):
+    """One epoch of delay-stale SGD (per-entry written values)."""
+    return _stale(_load().orc_stale_apply, row_ptr, col, val, y, w, len(w), lr, loss, mode, delay)
+
+
+def stale_snapshot(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, delay=0):
+    """The same from full weight snapshots after every example (tiny inputs)."""
+    return _stale(_load().orc_stale_snapshot, row_ptr, col, val, y, w, len(w), lr, loss, mode, delay)

@@ -417,3 +417,109 @@ int orc_batch_apply(int64_t n, int64_t count, const int32_t *order, const int64_
     free(s);
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Bounded delay (Sec. 7): an iteration may read a partition once the write
+ * of iteration alpha - 1 - delta to it is done (Asynchronous Read
+ * Constraint); it need not wait for the writes of the delta iterations before
+ * it.  The deterministic execution taken here reads as early as that allows:
+ * example alpha computes z against the weights as they were after examples
+ * 0 .. alpha - delta - 1, and every example's update is applied in example
+ * order to each of its features, w_f = fmaf(-s, x, w_f), so no update is
+ * lost.  delay = 0 is the sequential computation; delay >= n - 1 computes
+ * every z at the initial weights. */
+
+/* Literal form, tiny inputs: W[a] is the whole weight vector after examples
+ * 0 .. a-1 (W[0] = w0); z_a uses W[max(0, a - delay)].  Needs
+ * (n + 1) * d floats.  w receives W[n].  Returns 0, -1 on failure. */
+int orc_stale_snapshot(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                       const float *val, const float *y, float *w, float lr, int32_t loss,
+                       int32_t mode, int64_t delay) {
+    float *W = (float *)malloc((size_t)(n + 1) * (size_t)(d > 0 ? d : 1) * sizeof(float));
+    if (!W) return -1;
+    memcpy(W, w, (size_t)d * sizeof(float));
+    for (int64_t a = 0; a < n; ++a) {
+        const float *R = W + (size_t)(a - delay > 0 ? a - delay : 0) * (size_t)d;
+        float *cur = W + (size_t)a * (size_t)d, *nxt = W + (size_t)(a + 1) * (size_t)d;
+        int64_t p = row_ptr[a], m = row_ptr[a + 1] - p;
+        const float *v = val ? val + p : NULL;
+        float z = (mode == ORC_MATCHED) ? dot_matched(R, col + p, v, m) : dot_natural(R, col + p, v, m);
+        float g;
+        if (loss == ORC_LOGISTIC) {
+            float sig = (mode == ORC_MATCHED) ? orc_sigmoid(z) : 1.0f / (1.0f + expf(-z));
+            g = sig - ((y[a] > 0.0f) ? 1.0f : 0.0f);
+        } else {
+            g = z - y[a];
+        }
+        float s = lr * g;
+        memcpy(nxt, cur, (size_t)d * sizeof(float));
+        for (int64_t k = 0; k < m; ++k) nxt[col[p + k]] = fmaf(-s, v ? v[k] : 1.0f, cur[col[p + k]]);
+    }
+    memcpy(w, W + (size_t)n * (size_t)d, (size_t)d * sizeof(float));
+    free(W);
+    return 0;
+}
+
+/* The same with one written value per stored entry: V[q] is the value entry q
+ * wrote.  Entry q of example a reads the value of the latest earlier entry on
+ * its feature whose example is below a - delay (found by walking the
+ * previous-entry links back), w0 if there is none; it writes
+ * fmaf(-s, x_q, value of its previous entry, or w0).  w receives each
+ * feature's last written value.  Returns 0, -1 on failure. */
+int orc_stale_apply(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t *col,
+                    const float *val, const float *y, float *w, float lr, int32_t loss,
+                    int32_t mode, int64_t delay) {
+    int64_t nnz = row_ptr[n];
+    int64_t *prev = (int64_t *)malloc((size_t)(nnz > 0 ? nnz : 1) * sizeof(int64_t));
+    int64_t *last = (int64_t *)malloc((size_t)(d > 0 ? d : 1) * sizeof(int64_t));
+    float *V = (float *)malloc((size_t)(nnz > 0 ? nnz : 1) * sizeof(float));
+    float *rv = (float *)malloc((size_t)(nnz > 0 ? nnz : 1) * sizeof(float));
+    if (!prev || !last || !V || !rv) {
+        free(prev); free(last); free(V); free(rv);
+        return -1;
+    }
+    for (int64_t f = 0; f < d; ++f) last[f] = -1;
+    for (int64_t q = 0; q < nnz; ++q) {
+        prev[q] = last[col[q]];
+        last[col[q]] = q;
+    }
+    for (int64_t a = 0; a < n; ++a) {
+        int64_t p = row_ptr[a], m = row_ptr[a + 1] - p;
+        /* entries of examples a - delay .. a - 1 start at row_ptr[a - delay] */
+        int64_t lim = a - delay > 0 ? row_ptr[a - delay] : INT64_MAX;
+        for (int64_t k = 0; k < m; ++k) {
+            int64_t q = prev[p + k];
+            if (lim == INT64_MAX) q = -1;
+            while (q >= 0 && q >= lim) q = prev[q];
+            rv[k] = q >= 0 ? V[q] : w[col[p + k]];
+        }
+        /* the reads gathered, the dot product as for a weight vector */
+        float z = 0.0f;
+        if (mode == ORC_MATCHED) {
+            float acc[64];
+            for (int l = 0; l < 64; ++l) acc[l] = 0.0f;
+            for (int64_t k = 0; k < m; ++k)
+                acc[k & 63] = fmaf(rv[k], val ? val[p + k] : 1.0f, acc[k & 63]);
+            z = butterfly64(acc, 64);
+        } else {
+            for (int64_t k = 0; k < m; ++k) z = fmaf(rv[k], val ? val[p + k] : 1.0f, z);
+        }
+        float g;
+        if (loss == ORC_LOGISTIC) {
+            float sig = (mode == ORC_MATCHED) ? orc_sigmoid(z) : 1.0f / (1.0f + expf(-z));
+            g = sig - ((y[a] > 0.0f) ? 1.0f : 0.0f);
+        } else {
+            g = z - y[a];
+        }
+        float s = lr * g;
+        for (int64_t k = 0; k < m; ++k) {
+            int64_t q = prev[p + k];
+            float cur = q >= 0 ? V[q] : w[col[p + k]];
+            V[p + k] = fmaf(-s, val ? val[p + k] : 1.0f, cur);
+        }
+    }
+    for (int64_t f = 0; f < d; ++f)
+        if (last[f] >= 0) w[f] = V[last[f]];
+    free(prev); free(last); free(V); free(rv);
+    return 0;
+}
