@@ -49,11 +49,12 @@ def algorithmic_bytes(g, L, mf=False, U=None, nb=None):
     return g["nnz"] * per_nz + g["n"] * per_ex + L * 8
 
 
-def source_digest(batch=False):
+def source_digest(batch=False, stale=False):
     """Digest of the sources of the priced epoch kernel: a traffic record
     taken on other sources is not reported."""
     h = hashlib.sha256()
-    for f in ("batch.hip" if batch else "apply.hip", "pdb_math.h", "pdb_internal.h"):
+    main = "stale.hip" if stale else ("batch.hip" if batch else "apply.hip")
+    for f in (main, "pdb_math.h", "pdb_words.h", "pdb_internal.h"):
         with open(os.path.join(_ROOT, "paper_1508_00703_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -81,7 +82,7 @@ def trimmed_mean(xs):
     return sum(xs) / len(xs)
 
 
-def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0):
+def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0, delay=-1):
     """The oracle (one-pass levels + grouping + natural-order epoch), single
     thread, on the first rows of the same workload (with batch > 0: batch
     levels + grouping + the mini-batch epoch)."""
@@ -95,6 +96,12 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0):
         rp = g["row_ptr"][:rows + 1]
         col = g["col"][:rp[-1]]
         t0 = time.perf_counter()
+        if delay >= 0:
+            level, perm, level_ptr, L = oracle.schedule(rp, col, g["d"])
+            val = None if g["val"] is None else g["val"][:rp[-1]]
+            oracle.stale_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
+                               g["loss"], oracle.NATURAL, delay)
+            return time.perf_counter() - t0, int(rp[-1]), level
         if batch:
             level, perm, level_ptr, L = oracle.batch_schedule(rp, col, g["d"], batch)
             val = None if g["val"] is None else g["val"][:rp[-1]]
@@ -124,7 +131,9 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0):
            "sample": "first %d of %d %s (%d stored entries), one-pass %slevels + grouping + "
                      "natural-order %sepoch, %.1f s" % (
                          rows, n, "ratings" if mf else "examples", nnz_s,
-                         "batch " if batch else "", "mini-batch (B=%d) " % batch if batch else "", t),
+                         "batch " if batch else "",
+                         "mini-batch (B=%d) " % batch if batch else
+                         ("delay-%d " % delay if delay >= 0 else ""), t),
            "host_cpu": platform.processor() or platform.machine()}
     if gpu_levels is not None:
         k = len(level) if batch else rows
@@ -140,6 +149,8 @@ def main():
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--epochs", type=int, default=1,
                     help="epochs per step on the step's one schedule (the schedule is cached)")
+    ap.add_argument("--delay", type=int, default=-1,
+                    help="bounded-delay SGD (pdb_stale_epoch) with this delay; -1 = sequential")
     ap.add_argument("--batch", type=int, default=0,
                     help="mini-batch gradient descent with this many examples per batch "
                          "(pdb_batch_schedule + pdb_batch_epoch); 0 = SGD")
@@ -176,8 +187,11 @@ def main():
     cfg_id = args.config
     mf = cfg_id == 5
     batch = args.batch
-    if batch and mf:
-        raise SystemExit("--batch applies to the sparse SGD workloads (configs 1-4)")
+    delay = args.delay
+    if (batch or delay >= 0) and mf:
+        raise SystemExit("--batch and --delay apply to the sparse SGD workloads (configs 1-4)")
+    if batch and delay >= 0:
+        raise SystemExit("--batch and --delay are separate workloads")
     t0 = time.perf_counter()
     g = datagen.generate_mf(cfg_id) if mf else datagen.generate(cfg_id)
     t_gen = time.perf_counter() - t0
@@ -193,8 +207,9 @@ def main():
     bt = native.Batches(n, nnz, batch, dev) if batch else None
     lv = native.Levels(bt.nb if batch else n, nnz, dev)
     ws_s = native.workspace(native.pdb_schedule_workspace_bytes(n, d, nnz), dev)
-    ws_e = native.workspace(native.pdb_epoch_workspace_bytes(
-        (g["n_users"] + g["n_items"]) * g["rank"] if mf else d), dev)
+    ws_e = native.workspace(
+        native.pdb_stale_workspace_bytes(nnz) if delay >= 0 else native.pdb_epoch_workspace_bytes(
+            (g["n_users"] + g["n_items"]) * g["rank"] if mf else d), dev)
     if mf:
         user = torch.from_numpy(g["user"]).to(dev)
         item = torch.from_numpy(g["item"]).to(dev)
@@ -237,6 +252,9 @@ def main():
             elif batch:
                 native.pdb_batch_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], bt, lv,
                                        ws=ws_e)
+            elif delay >= 0:
+                native.pdb_stale_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], delay, lv,
+                                       ws=ws_e)
             else:
                 native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], lv, ws=ws_e)
             b.record(stream)
@@ -267,17 +285,21 @@ def main():
     abytes = (algorithmic_bytes(g, L, U=bt.U_host, nb=bt.nb) if batch
               else algorithmic_bytes(g, L, mf))
     achieved = abytes / (ep * 1e-3) / 1e9
-    workload = "c%d" % cfg_id + ("-b%d" % batch if batch else "")
+    workload = "c%d" % cfg_id + ("-b%d" % batch if batch else "") + \
+        ("-d%d" % delay if delay >= 0 else "")
     # the epoch kernel the library runs (the rule of pdb_sgd_epoch / pdb_mf_epoch)
     mode = int(os.environ.get("PDB_EPOCH_MODE", "0"))
     syncfree = mode == 2 or (mode == 0 and L > 0 and n >= 8 * L)
     if batch:
-        kernel = "k_batch_levels (mini-batch epoch)"
+        kernel = "k_batch_syncfree (mini-batch epoch)" if mode != 1 else \
+            "k_batch_levels (mini-batch epoch)"
+    elif delay >= 0:
+        kernel = "k_stale_epoch (bounded-delay epoch)"
     elif syncfree:
         kernel = "k_mf_syncfree (epoch)" if mf else "k_sgd_syncfree (epoch)"
     else:
         kernel = "k_levels_apply (epoch)"
-    digest = source_digest(bool(batch))
+    digest = source_digest(bool(batch), delay >= 0)
     traffic = read_traffic(workload, digest)
     out = {
         "metric": METRIC,
@@ -293,8 +315,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "%s: %s%s" % (workload, g["name"],
-                                              ", mini-batches of %d" % batch if batch else ""),
+        "config": {"workload": "%s: %s%s%s" % (workload, g["name"],
+                                                ", mini-batches of %d" % batch if batch else "",
+                                                ", delay %d" % delay if delay >= 0 else ""),
                    "n": n, "d": d, "nnz": nnz,
                    "seed": g["seed"], "levels": L, "max_level_width": lv.max_width_host,
                    "schedule_method": info.get("method_used"),
@@ -312,7 +335,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget, lv.level.cpu().numpy(),
-                                           batch)
+                                           batch, delay)
     print(json.dumps(out))
 
 

@@ -240,6 +240,29 @@ int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t 
                     float *w, float lr, int loss, const pdb_batches *batches,
                     const pdb_levels *levels, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Device workspace (bytes) for pdb_stale_epoch: the control block, one
+ * 64-bit word and two ints per stored entry.  Host-only arithmetic. */
+int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes);
+
+/* One epoch of bounded-delay SGD (Sec. 7: the Asynchronous Read Constraint
+ * lets iteration alpha read a partition once the write of iteration
+ * alpha - 1 - delay is done), in the execution that reads as early as that
+ * allows: example alpha computes z, with the per-example arithmetic at the
+ * top of this header, from the values its features had after examples
+ * 0 .. alpha - delay - 1 (the initial w where no such example wrote them);
+ * each example's update is then applied in example order to each of its
+ * features, w_f = fma(-s, x, w_f), on the value the previous writer left.
+ * delay = 0 is pdb_sgd_epoch's result; delay >= n - 1 reads the initial
+ * weights everywhere (pdb_batch_epoch with batch = n).  prev_nz: device,
+ * [nnz], from pdb_schedule on the same CSR.  Sync-free over examples in index
+ * order; finding each entry's read source takes up to `delay` steps back
+ * along its feature.  ws: at least pdb_stale_workspace_bytes(nnz).
+ * Asynchronous; a device error (watchdog) is reported by
+ * pdb_workspace_status on ws. */
+int pdb_stale_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
+                    float lr, int loss, int64_t delay, const int32_t *prev_nz, void *ws,
+                    size_t ws_bytes, hipStream_t stream);
+
 /* Per-feature occurrence lists (the transpose that exposes which examples
  * share a feature): col_ptr (device, [d+1]) and csc_row (device, [nnz],
  * rows ascending within a feature).  ws as for pdb_schedule.  Synchronous. */

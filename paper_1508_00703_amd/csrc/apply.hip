@@ -34,6 +34,7 @@
 #include <cstdlib>
 
 #include "pdb_math.h"
+#include "pdb_words.h"
 
 namespace pdbk {
 
@@ -792,76 +793,18 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
 // always makes progress.
 constexpr int kSyncB = 4;  // examples per ticket, run in order by one wave
 
-__device__ __forceinline__ unsigned long long wv_pack(float w, int tag) {
-    return ((unsigned long long)(unsigned)tag << 32) | (unsigned long long)__float_as_uint(w);
-}
-__device__ __forceinline__ float wv_value(unsigned long long v) {
-    return __uint_as_float((unsigned)v);
-}
-
 __global__ void k_wv_in(const float *__restrict__ w, unsigned long long *__restrict__ wv,
                         int64_t d) {
     for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
          f += (int64_t)gridDim.x * blockDim.x)
-        wv[f] = wv_pack(w[f], -1);
+        wv[f] = word_pack(w[f], -1);
 }
 
 __global__ void k_wv_out(const unsigned long long *__restrict__ wv, float *__restrict__ w,
                          int64_t d) {
     for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
          f += (int64_t)gridDim.x * blockDim.x)
-        w[f] = wv_value(wv[f]);
-}
-
-// Access to the packed words: device-scope atomics (a relaxed 64-bit load or
-// store is single-copy atomic, so the tag and the value always match).
-__device__ __forceinline__ unsigned long long wv_get(unsigned long long *base, int64_t i) {
-    return __hip_atomic_load(&base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void wv_put(unsigned long long *base, int64_t i, unsigned long long v) {
-    __hip_atomic_store(&base[i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Sleeps about 2^min(round, 3) x 64 cycles (s_sleep takes a constant).
-__device__ __forceinline__ void wave_backoff(int round) {
-    switch (round < 3 ? round : 3) {
-        case 0: __builtin_amdgcn_s_sleep(1); break;
-        case 1: __builtin_amdgcn_s_sleep(2); break;
-        case 2: __builtin_amdgcn_s_sleep(4); break;
-        case 3: __builtin_amdgcn_s_sleep(8); break;
-        case 4: __builtin_amdgcn_s_sleep(16); break;
-        case 5: __builtin_amdgcn_s_sleep(32); break;
-        default: __builtin_amdgcn_s_sleep(64); break;
-    }
-}
-
-// Polls words idx (one per lane; lanes with want = false take part in the
-// rounds only) until each carries tag; the whole wave backs off while
-// nothing arrives, so waves far from the frontier barely load the memory
-// system.  False on timeout or abort.
-__device__ __forceinline__ bool wv_wait_wave(unsigned long long *base, bool want, int64_t idx, int tag,
-                                             unsigned long long *out, Ctrl *ctrl,
-                                             int64_t timeout) {
-    bool ready = !want;
-    int64_t t0 = 0;
-    for (int round = 0;; ++round) {
-        if (!ready) {
-            const unsigned long long v = wv_get(base, idx);
-            if ((int)(unsigned)(v >> 32) == tag) {
-                *out = v;
-                ready = true;
-            }
-        }
-        if (__ballot(!ready) == 0ull) return true;
-        if (round == 0) t0 = now_ticks();
-        if (aborted(ctrl)) return false;
-        if (now_ticks() - t0 > timeout) {
-            record_error(ctrl, DERR_WAIT_TIMEOUT);
-            return false;
-        }
-        wave_backoff(round);
-        compiler_fence();  // the next round loads again
-    }
+        w[f] = word_value(wv[f]);
 }
 
 template <int LOSS, bool VAL>
@@ -889,12 +832,12 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
                     if (VAL) x = op.val[b + lane];
                 }
                 unsigned long long v = 0;
-                if (!wv_wait_wave(wv, lane < m, c, pn, &v, ctrl, timeout)) return;
-                const float wold = wv_value(v);
+                if (!word_wait_wave(wv, lane < m, c, pn, &v, ctrl, timeout)) return;
+                const float wold = word_value(v);
                 const float acc = lane < m ? __builtin_fmaf(wold, x, 0.0f) : 0.0f;
                 const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
                 if (lane < m)
-                    wv_put(wv, c, wv_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)));
+                    word_put(wv, c, word_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)));
             } else {
                 float acc = 0.0f;
                 for (int k0 = 0; k0 < m; k0 += kWave) {
@@ -903,16 +846,16 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
                     const int c = live ? op.col[b + k] : 0;
                     const int pn = live ? op.prev_nz[b + k] : -1;
                     unsigned long long v = 0;
-                    if (!wv_wait_wave(wv, live, c, pn, &v, ctrl, timeout)) return;
-                    if (live) acc = __builtin_fmaf(wv_value(v), VAL ? op.val[b + k] : 1.0f, acc);
+                    if (!word_wait_wave(wv, live, c, pn, &v, ctrl, timeout)) return;
+                    if (live) acc = __builtin_fmaf(word_value(v), VAL ? op.val[b + k] : 1.0f, acc);
                 }
                 const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
                 // nothing else writes these features before this example does
                 for (int k = lane; k < m; k += kWave) {
                     const int c = op.col[b + k];
-                    const float wold = wv_value(wv_get(wv, c));
-                    wv_put(wv, c,
-                               wv_pack(__builtin_fmaf(-s, VAL ? op.val[b + k] : 1.0f, wold),
+                    const float wold = word_value(word_get(wv, c));
+                    word_put(wv, c,
+                               word_pack(__builtin_fmaf(-s, VAL ? op.val[b + k] : 1.0f, wold),
                                        (int)(b + k)));
                 }
             }
@@ -966,15 +909,15 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
                 r = rating[tt];
             }
             unsigned long long u = 0, v = 0;
-            if (!wv_wait_wave(uvw, valid, uo, tu, &u, ctrl, timeout)) return;
-            if (!wv_wait_wave(uvw, valid, vo, ti, &v, ctrl, timeout)) return;
-            const float uj = valid ? wv_value(u) : 0.0f, vj = valid ? wv_value(v) : 0.0f;
+            if (!word_wait_wave(uvw, valid, uo, tu, &u, ctrl, timeout)) return;
+            if (!word_wait_wave(uvw, valid, vo, ti, &v, ctrl, timeout)) return;
+            const float uj = valid ? word_value(u) : 0.0f, vj = valid ? word_value(v) : 0.0f;
             const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
             if (valid) {
                 const float a = err * vj, b = reg * uj;
                 const float a2 = err * uj, b2 = reg * vj;
-                wv_put(uvw, uo, wv_pack(__builtin_fmaf(lr, a - b, uj), (int)tt));
-                wv_put(uvw, vo, wv_pack(__builtin_fmaf(lr, a2 - b2, vj), (int)tt));
+                word_put(uvw, uo, word_pack(__builtin_fmaf(lr, a - b, uj), (int)tt));
+                word_put(uvw, vo, word_pack(__builtin_fmaf(lr, a2 - b2, vj), (int)tt));
             }
             t += count;
         }

@@ -22,6 +22,7 @@
 #include <climits>
 
 #include "pdb_math.h"
+#include "pdb_words.h"
 
 namespace pdbk {
 
@@ -382,69 +383,18 @@ __global__ __launch_bounds__(kBB) void k_batch_levels(BatchOp<LOSS, VAL> op,
 // unfinished batch never waits for a later one, so the grid always makes
 // progress; batches that share no feature run concurrently on different CUs.
 
-__device__ __forceinline__ unsigned long long bw_pack(float w, int tag) {
-    return ((unsigned long long)(unsigned)tag << 32) | (unsigned long long)__float_as_uint(w);
-}
-__device__ __forceinline__ float bw_value(unsigned long long v) {
-    return __uint_as_float((unsigned)v);
-}
-// device-scope 64-bit accesses: single-copy atomic, so tag and value match
-__device__ __forceinline__ unsigned long long bw_get(unsigned long long *base, int64_t i) {
-    return __hip_atomic_load(&base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void bw_put(unsigned long long *base, int64_t i, unsigned long long v) {
-    __hip_atomic_store(&base[i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 __global__ void k_bw_in(const float *__restrict__ w, unsigned long long *__restrict__ bw,
                         int64_t d) {
     for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
          f += (int64_t)gridDim.x * blockDim.x)
-        bw[f] = bw_pack(w[f], -1);
+        bw[f] = word_pack(w[f], -1);
 }
 
 __global__ void k_bw_out(const unsigned long long *__restrict__ bw, float *__restrict__ w,
                          int64_t d) {
     for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < d;
          f += (int64_t)gridDim.x * blockDim.x)
-        w[f] = bw_value(bw[f]);
-}
-
-// Sleeps about 2^min(round, 3) x 64 cycles.
-__device__ __forceinline__ void bw_backoff(int round) {
-    switch (round < 3 ? round : 3) {
-        case 0: __builtin_amdgcn_s_sleep(1); break;
-        case 1: __builtin_amdgcn_s_sleep(2); break;
-        case 2: __builtin_amdgcn_s_sleep(4); break;
-        default: __builtin_amdgcn_s_sleep(8); break;
-    }
-}
-
-// Polls word idx (one per lane; lanes with want = false only take part in
-// the rounds) until it carries tag.  False on timeout or abort.
-__device__ __forceinline__ bool bw_wait_wave(unsigned long long *base, bool want, int64_t idx,
-                                             int tag, unsigned long long *out, Ctrl *ctrl,
-                                             int64_t timeout) {
-    bool ready = !want;
-    int64_t t0 = 0;
-    for (int round = 0;; ++round) {
-        if (!ready) {
-            const unsigned long long v = bw_get(base, idx);
-            if ((int)(unsigned)(v >> 32) == tag) {
-                *out = v;
-                ready = true;
-            }
-        }
-        if (__ballot(!ready) == 0ull) return true;
-        if (round == 0) t0 = now_ticks();
-        if (aborted(ctrl)) return false;
-        if (now_ticks() - t0 > timeout) {
-            record_error(ctrl, DERR_WAIT_TIMEOUT);
-            return false;
-        }
-        bw_backoff(round);
-        __asm__ __volatile__("" ::: "memory");  // the next round loads again
-    }
+        w[f] = word_value(bw[f]);
 }
 
 // Polls the words f[h] of the slots not yet ready until each carries tag[h];
@@ -470,12 +420,12 @@ __device__ __forceinline__ bool bw_wait_slots(unsigned long long *base, const in
                 return false;
             }
         }
-        bw_backoff(round);
+        word_backoff(round);
         __asm__ __volatile__("" ::: "memory");  // the loads below are issued again
 #pragma unroll
         for (int h = 0; h < H; ++h) {
             if (!ready[h]) {
-                v[h] = bw_get(base, f[h]);
+                v[h] = word_get(base, f[h]);
                 ready[h] = (int)(unsigned)(v[h] >> 32) == tag[h];
             }
         }
@@ -513,12 +463,12 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
         const int32_t f = live ? op.ucol[u] : 0;
         const int tag = live ? uprev[u] : -1;
         unsigned long long v = 0;
-        if (!bw_wait_wave(bw, live, f, tag, &v, ctrl, timeout)) {
+        if (!word_wait_wave(bw, live, f, tag, &v, ctrl, timeout)) {
             ok = false;
             break;
         }
         if (staged && live) {
-            Sh.uw[u - ub] = bw_value(v);
+            Sh.uw[u - ub] = word_value(v);
             const int64_t q1 = op.uptr[u + 1];
             for (int64_t q = op.uptr[u]; q < q1; ++q) {
                 const int32_t p = op.occ[q];
@@ -537,7 +487,7 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
         float acc = 0.0f;
         for (int64_t k = lane; k < m; k += kWave) {
             const int64_t p = p0 + k;
-            const float wk = staged ? Sh.uw[Sh.eu[p - pb]] : bw_value(bw_get(bw, op.col[p]));
+            const float wk = staged ? Sh.uw[Sh.eu[p - pb]] : word_value(word_get(bw, op.col[p]));
             acc = __builtin_fmaf(wk, VAL ? op.val[p] : 1.0f, acc);
         }
         const float s = sgd_scale<LOSS>(wave_sum64(acc), op.y[i], op.lr);
@@ -552,7 +502,7 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
     for (int64_t u = ub + threadIdx.x; u < ue; u += kBB) {
         const int32_t f = op.ucol[u];
         const int64_t qa = op.uptr[u], qe = op.uptr[u + 1];
-        float v = staged ? Sh.uw[u - ub] : bw_value(bw_get(bw, f));
+        float v = staged ? Sh.uw[u - ub] : word_value(word_get(bw, f));
         if (staged) {
             v = chain_apply<VAL>(v, reinterpret_cast<const float *>(Sh.oi), Sh.ox,
                                  (int32_t)(qa - pb), (int32_t)(qe - pb));
@@ -560,7 +510,7 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
             for (int64_t q = qa; q < qe; ++q)
                 v = __builtin_fmaf(-Sh.s[op.occ_row[q] - i0], VAL ? op.val[op.occ[q]] : 1.0f, v);
         }
-        bw_put(bw, f, bw_pack(v, (int)u));
+        word_put(bw, f, word_pack(v, (int)u));
     }
     __syncthreads();
     return true;
@@ -626,13 +576,13 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
         const bool live = ub + threadIdx.x + (int64_t)kBB * h < ue;
-        v[h] = live ? bw_get(bw, f[h]) : 0ull;
+        v[h] = live ? word_get(bw, f[h]) : 0ull;
         ready[h] = !live || (int)(unsigned)(v[h] >> 32) == tag[h];
     }
     const bool ok = bw_wait_slots<kH>(bw, f, tag, ready, v, ctrl, timeout);
 #pragma unroll
     for (int h = 0; h < kH; ++h)
-        if (ub + threadIdx.x + (int64_t)kBB * h < ue) Sh.uw[threadIdx.x + kBB * h] = bw_value(v[h]);
+        if (ub + threadIdx.x + (int64_t)kBB * h < ue) Sh.uw[threadIdx.x + kBB * h] = word_value(v[h]);
     if (!ok && lane == 0) Sh.ok = 0;
     __syncthreads();
     if (!Sh.ok) return false;
@@ -670,7 +620,7 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
 #pragma unroll
         for (int h = 0; h < kH; ++h) {
             const int64_t u = ub + threadIdx.x + (int64_t)kBB * h;
-            if (u < ue && urgent[h] == (pass == 0)) bw_put(bw, f[h], bw_pack(val[h], (int)u));
+            if (u < ue && urgent[h] == (pass == 0)) word_put(bw, f[h], word_pack(val[h], (int)u));
         }
     }
     __syncthreads();

@@ -1,0 +1,67 @@
+// Packed (value, tag) words of the sync-free kernels (gfx950, wave64): a
+// binary32 value and the 32-bit tag of the writer that produced it share one
+// 64-bit word, so a single device-scope access reads or publishes both and
+// a reader never sees a value with another writer's tag.  Internal header,
+// not installed.
+#pragma once
+
+#include "pdb_internal.h"
+
+namespace pdbk {
+
+__device__ __forceinline__ unsigned long long word_pack(float v, int tag) {
+    return ((unsigned long long)(unsigned)tag << 32) | (unsigned long long)__float_as_uint(v);
+}
+__device__ __forceinline__ float word_value(unsigned long long w) {
+    return __uint_as_float((unsigned)w);
+}
+__device__ __forceinline__ int word_tag(unsigned long long w) { return (int)(unsigned)(w >> 32); }
+
+// device-scope 64-bit accesses: single-copy atomic
+__device__ __forceinline__ unsigned long long word_get(unsigned long long *base, int64_t i) {
+    return __hip_atomic_load(&base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void word_put(unsigned long long *base, int64_t i,
+                                         unsigned long long w) {
+    __hip_atomic_store(&base[i], w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Sleeps about 2^min(round, 3) x 64 cycles (s_sleep takes a constant).
+__device__ __forceinline__ void word_backoff(int round) {
+    switch (round < 3 ? round : 3) {
+        case 0: __builtin_amdgcn_s_sleep(1); break;
+        case 1: __builtin_amdgcn_s_sleep(2); break;
+        case 2: __builtin_amdgcn_s_sleep(4); break;
+        default: __builtin_amdgcn_s_sleep(8); break;
+    }
+}
+
+// Polls word idx (one per lane; lanes with want = false only take part in
+// the rounds) until it carries tag; the whole wave backs off while nothing
+// arrives.  False on timeout or abort.
+__device__ __forceinline__ bool word_wait_wave(unsigned long long *base, bool want, int64_t idx,
+                                               int tag, unsigned long long *out, Ctrl *ctrl,
+                                               int64_t timeout) {
+    bool ready = !want;
+    int64_t t0 = 0;
+    for (int round = 0;; ++round) {
+        if (!ready) {
+            const unsigned long long v = word_get(base, idx);
+            if (word_tag(v) == tag) {
+                *out = v;
+                ready = true;
+            }
+        }
+        if (__ballot(!ready) == 0ull) return true;
+        if (round == 0) t0 = now_ticks();
+        if (aborted(ctrl)) return false;
+        if (now_ticks() - t0 > timeout) {
+            record_error(ctrl, DERR_WAIT_TIMEOUT);
+            return false;
+        }
+        word_backoff(round);
+        __asm__ __volatile__("" ::: "memory");  // the next round loads again
+    }
+}
+
+}  // namespace pdbk

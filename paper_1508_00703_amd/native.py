@@ -32,6 +32,7 @@ EXPORTS = (
     "pdb_epoch_workspace_bytes", "pdb_schedule", "pdb_sgd_epoch", "pdb_mf_epoch",
     "pdb_validate_csr", "pdb_workspace_status", "pdb_transpose", "pdb_prev_writer",
     "pdb_check_reciprocal", "pdb_batch_schedule", "pdb_batch_epoch",
+    "pdb_stale_workspace_bytes", "pdb_stale_epoch",
 )
 
 
@@ -104,6 +105,9 @@ def load() -> ctypes.CDLL:
                                        ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, P]
     lib.pdb_batch_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, i64, P, f32, ctypes.c_int,
                                     ctypes.POINTER(PdbBatches), ctypes.POINTER(PdbLevels), P, sz, P]
+    lib.pdb_stale_workspace_bytes.argtypes = [i64, ctypes.POINTER(sz)]
+    lib.pdb_stale_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int, i64,
+                                    P, P, sz, P]
     for name in EXPORTS:
         if name not in ("pdb_strerror",):
             getattr(lib, name).restype = ctypes.c_int
@@ -310,6 +314,30 @@ def pdb_batch_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Ten
                                   ctypes.c_float(lr), loss, ctypes.byref(batches.c()),
                                   ctypes.byref(levels.c()), _ptr(ws), ws.numel(),
                                   _stream(stream, csr.device)), "pdb_batch_epoch")
+    return ws
+
+
+def pdb_stale_workspace_bytes(nnz: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().pdb_stale_workspace_bytes(nnz, ctypes.byref(out)), "pdb_stale_workspace_bytes")
+    return out.value
+
+
+def pdb_stale_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor, lr: float,
+                    loss: int, delay: int, levels: Levels, ws: torch.Tensor | None = None,
+                    stream=None):
+    """levels: from pdb_schedule on the same CSR (its prev_nz is used)."""
+    if w.dtype != torch.float32 or labels.dtype != torch.float32:
+        raise TypeError("w and labels must be float32")
+    if w.numel() < d or labels.numel() < n:
+        raise ValueError("w must hold d entries and labels n entries")
+    if levels.prev_nz is None and csr.nnz > 0:
+        raise ValueError("the levels must carry prev_nz")
+    if ws is None:
+        ws = workspace(pdb_stale_workspace_bytes(csr.nnz), csr.device)
+    _check(load().pdb_stale_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
+                                  ctypes.c_float(lr), loss, delay, _ptr(levels.prev_nz), _ptr(ws),
+                                  ws.numel(), _stream(stream, csr.device)), "pdb_stale_epoch")
     return ws
 
 
