@@ -58,6 +58,8 @@ def _load():
     lib.gen_zipf_sample.argtypes = [u64, i64, f64, i64, P]
     lib.gen_poisson_sample.argtypes = [u64, f64, i64, P]
     lib.gen_wstar.argtypes = [u64, i64, P, ctypes.c_int]
+    lib.gen_dense.argtypes = [u64, i64, i64, i64, i32, f64, P, P, ctypes.c_int]
+    lib.gen_dense.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -122,6 +124,29 @@ CONFIGS = {
                     0.0, 1, 0.1, SQUARED, 0.001),
     5: MFConfig("mf-20m-1mx200k-r32", 20_000_000, 1_000_000, 200_000, 1.0, 1.0, 32,
                 1.0 / np.sqrt(32.0), 0.5, 0.005, 0.02),
+}
+
+
+@dataclass(frozen=True)
+class DenseConfig:
+    name: str
+    n: int
+    d: int
+    label_kind: int        # 0 sign with flips, 1 linear + noise
+    label_p: float
+    loss: int
+    lr: float
+    iters: int
+
+
+# Dense full-batch gradient descent (the linear-regression experiments of
+# Sec. 6.1-6.2): 960 numerical features over 5000 examples, and the widest of
+# a sweep over the number of features at 500 examples.  The step sizes keep
+# the summed-gradient iteration contractive: lr times the largest eigenvalue
+# of X^T X, about (sqrt(n) + sqrt(d))^2, stays near 1.
+DENSE = {
+    1: DenseConfig("lsq-dense-5000x960", 5000, 960, 1, 0.1, SQUARED, 1e-4, 200),
+    2: DenseConfig("lsq-dense-500x1m", 500, 1_000_000, 1, 0.1, SQUARED, 1e-6, 50),
 }
 
 
@@ -199,6 +224,29 @@ def generate_mf(cfg_id: int = 5, n: int | None = None, n_users: int | None = Non
     return dict(user=user, item=item, rating=rating, U0=U0, V0=V0, n=n, n_users=nu, n_items=ni,
                 rank=cfg.rank, lr=np.float32(cfg.lr), reg=np.float32(cfg.reg), row_ptr=row_ptr,
                 col=col, d=nu + ni, nnz=2 * n, name=cfg.name, seed=seed, cfg=cfg_id)
+
+
+def generate_dense(cfg_id: int, n: int | None = None, d: int | None = None,
+                   seed: int | None = None, loss: int | None = None, ldx: int | None = None,
+                   nthreads: int | None = None) -> dict:
+    """Dense workload: X (float32, n x d, row stride ldx >= d; the view of the
+    first d columns), y (float32[n]), and the config's loss, lr, iters."""
+    cfg = DENSE[cfg_id]
+    n = cfg.n if n is None else int(n)
+    d = cfg.d if d is None else int(d)
+    loss = cfg.loss if loss is None else int(loss)
+    ldx = d if ldx is None else int(ldx)
+    if ldx < d:
+        raise ValueError("row stride below the row length")
+    seed = 2000 + cfg_id if seed is None else int(seed)
+    label_kind, label_p = (cfg.label_kind, cfg.label_p) if loss == SQUARED else (0, 0.05)
+    buf = np.zeros((n, ldx), dtype=np.float32)
+    y = np.empty(n, dtype=np.float32)
+    if _load().gen_dense(seed, n, d, ldx, label_kind, label_p, buf.ctypes.data, y.ctypes.data,
+                         _threads(nthreads)) != 0:
+        raise MemoryError("generator failed")
+    return dict(X=buf[:, :d], y=y, n=n, d=d, ldx=ldx, loss=loss, lr=np.float32(cfg.lr),
+                iters=cfg.iters, name=cfg.name, seed=seed)
 
 
 def philox_block(ctr, key):

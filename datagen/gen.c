@@ -68,7 +68,7 @@ typedef struct {
 enum {
     ST_NNZ = 1, ST_COL = 2, ST_VAL = 3, ST_WSTAR = 4, ST_LABEL = 5,
     ST_USER = 6, ST_ITEM = 7, ST_USTAR = 8, ST_VSTAR = 9, ST_NOISE = 10,
-    ST_U0 = 11, ST_V0 = 12
+    ST_U0 = 11, ST_V0 = 12, ST_DENSE = 13
 };
 
 static inline void rng_init(rng_t *r, uint64_t seed, uint32_t stream, uint64_t index) {
@@ -347,6 +347,43 @@ int gen_mf(uint64_t seed, int64_t n_ratings, int64_t n_users, int64_t n_items, d
         rating[i] = (float)(dot + noise_sd * rng_normal(&rn));
     }
     free(cu); free(ci); free(us); free(vs);
+    return 0;
+}
+
+/* ---------------- dense examples ---------------- */
+/* X (n x d, row stride ldx) with N(0,1) entries, drawn row by row; labels
+ * from the hidden model w* (gen_wstar) through dot = <X_i, w*> / sqrt(d):
+ * label_kind 0: sign(dot), flipped with probability label_p;
+ * label_kind 1: dot + label_p * N(0,1). */
+int gen_dense(uint64_t seed, int64_t n, int64_t d, int64_t ldx, int32_t label_kind,
+              double label_p, float *X, float *y, int nthreads) {
+    double *wstar = (double *)malloc((size_t)(d > 0 ? d : 1) * sizeof(double));
+    if (!wstar) return -1;
+    gen_wstar(seed, d, wstar, nthreads);
+    const double scale = d > 0 ? 1.0 / sqrt((double)d) : 0.0;
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t i = 0; i < n; ++i) {
+        rng_t r;
+        rng_init(&r, seed, ST_DENSE, (uint64_t)i);
+        float *x = X + i * ldx;
+        double dot = 0.0;
+        for (int64_t j = 0; j < d; ++j) {
+            x[j] = (float)rng_normal(&r);
+            dot += (double)x[j] * wstar[j];
+        }
+        dot *= scale;
+        rng_t rl;
+        rng_init(&rl, seed, ST_LABEL, (uint64_t)i);
+        if (label_kind == 0) {
+            float sg = (dot >= 0.0) ? 1.0f : -1.0f;
+            if (rng_unif(&rl) < label_p) sg = -sg;
+            y[i] = sg;
+        } else {
+            y[i] = (float)(dot + label_p * rng_normal(&rl));
+        }
+    }
+    free(wstar);
     return 0;
 }
 

@@ -23,6 +23,9 @@ What it computes (all single-threaded, binary32 arithmetic, see oracle.c):
     Sec. 7, in the execution that reads as early as its read constraint
     allows (example alpha computes z against the weights after examples
     0 .. alpha - delay - 1; updates applied in example order).
+  * ``dense_gd``: full-batch gradient descent on a dense example matrix
+    (every example in every iteration, the update of Sec. 2 as in the dense
+    workloads of Sec. 6.1-6.2).
   * ``history``: the execution-history predicates of Definition 4 and
     Sec. 4.3-4.4 (see ``oracle.history``).
 
@@ -91,6 +94,8 @@ def _load():
     lib.orc_stale_snapshot.argtypes = [i64, i64, P, P, P, P, P, f32, i32, i32, i64]
     lib.orc_stale_snapshot.restype = ctypes.c_int
     lib.orc_stale_apply.argtypes = [i64, i64, P, P, P, P, P, f32, i32, i32, i64]
+    lib.orc_dense_gd.argtypes = [i64, i64, P, i64, P, P, f32, i32, i32, i64, i64, i64]
+    lib.orc_dense_gd.restype = ctypes.c_int
     lib.orc_stale_apply.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -306,3 +311,22 @@ def stale_epoch(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, delay=
 def stale_snapshot(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, delay=0):
     """The same from full weight snapshots after every example (tiny inputs)."""
     return _stale(_load().orc_stale_snapshot, row_ptr, col, val, y, w, len(w), lr, loss, mode, delay)
+
+
+def dense_gd(X, y, w, lr, loss=SQUARED, mode=MATCHED, iters=1, row_block=None, col_block=None):
+    """Full-batch gradient descent on the rows of X (n x d, float32), iters
+    iterations, on a copy of w.  Matched mode sums in the blocked order given
+    by row_block and col_block (default: one block each way)."""
+    X = np.asarray(X, dtype=np.float32)
+    if X.ndim != 2 or X.strides[1] != 4 or X.strides[0] % 4:
+        X = np.ascontiguousarray(X)
+    n, d = X.shape
+    ldx = X.strides[0] // 4 if n > 0 else d
+    y = _c(y, np.float32)
+    w = np.array(w, dtype=np.float32, copy=True)
+    rb = max(n, 1) if row_block is None else int(row_block)
+    cb = max(d, 1) if col_block is None else int(col_block)
+    if _load().orc_dense_gd(n, d, X.ctypes.data, ldx, _ptr(y), _ptr(w), np.float32(lr), loss, mode,
+                            int(iters), rb, cb) != 0:
+        raise ValueError("bad blocking or out of memory")
+    return w

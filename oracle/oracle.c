@@ -523,3 +523,77 @@ int orc_stale_apply(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t 
     free(prev); free(last); free(V); free(rv);
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Dense full-batch gradient descent: the update of Sec. 2 with every
+ * example in every iteration (the dense linear-regression workloads of
+ * Sec. 6.1-6.2).  X is n x d, row-major with row stride ldx.  One iteration,
+ * all reads from the weights before it (the scalar form of Sec. 2):
+ *   z_i = <X_i, w>;  s_i = lr * g(z_i, y_i);  G_j = sum_i s_i X_ij;
+ *   w_j <- w_j - G_j.
+ * natural: z_i = fmaf(X_ij, w_j, z) over j = 0..d-1 from 0, and
+ *          G_j = fmaf(s_i, X_ij, G) over i = 0..n-1 from 0.
+ * matched: rows in blocks of row_block, columns in blocks of col_block.
+ *   The partial dot of a column block has 64 partial sums; column k of the
+ *   block (k from 0) goes into sum (k / 4) mod 64, in increasing k, then the
+ *   butterfly; z_i adds the blocks' partials in block order, starting from
+ *   block 0's.  A row block's partial of G_j is fmaf over its rows in order
+ *   from 0; G_j adds the row blocks' partials in block order, starting from
+ *   block 0's.
+ * Returns 0, -1 on failure (bad blocking or no memory). */
+static float residual(float z, float y, int32_t loss, int32_t mode) {
+    if (loss == ORC_LOGISTIC) {
+        float sig = (mode == ORC_MATCHED) ? orc_sigmoid(z) : 1.0f / (1.0f + expf(-z));
+        return sig - ((y > 0.0f) ? 1.0f : 0.0f);
+    }
+    return z - y;
+}
+
+int orc_dense_gd(int64_t n, int64_t d, const float *X, int64_t ldx, const float *y, float *w,
+                 float lr, int32_t loss, int32_t mode, int64_t iters, int64_t row_block,
+                 int64_t col_block) {
+    if (mode == ORC_MATCHED && (row_block < 1 || col_block < 1)) return -1;
+    float *s = (float *)malloc((size_t)(n > 0 ? n : 1) * sizeof(float));
+    float *G = (float *)malloc((size_t)(d > 0 ? d : 1) * sizeof(float));
+    if (!s || !G) {
+        free(s); free(G);
+        return -1;
+    }
+    for (int64_t t = 0; t < iters; ++t) {
+        for (int64_t i = 0; i < n; ++i) {
+            const float *x = X + i * ldx;
+            float z = 0.0f;
+            if (mode == ORC_MATCHED) {
+                for (int64_t c0 = 0; c0 < d; c0 += col_block) {
+                    int64_t c1 = c0 + col_block < d ? c0 + col_block : d;
+                    float acc[64];
+                    for (int l = 0; l < 64; ++l) acc[l] = 0.0f;
+                    for (int64_t k = 0; k < c1 - c0; ++k)
+                        acc[(k >> 2) & 63] = fmaf(x[c0 + k], w[c0 + k], acc[(k >> 2) & 63]);
+                    float part = butterfly64(acc, 64);
+                    z = (c0 == 0) ? part : z + part;
+                }
+            } else {
+                for (int64_t j = 0; j < d; ++j) z = fmaf(x[j], w[j], z);
+            }
+            s[i] = lr * residual(z, y[i], loss, mode);
+        }
+        for (int64_t j = 0; j < d; ++j) {
+            float g = 0.0f;
+            if (mode == ORC_MATCHED) {
+                for (int64_t r0 = 0; r0 < n; r0 += row_block) {
+                    int64_t r1 = r0 + row_block < n ? r0 + row_block : n;
+                    float part = 0.0f;
+                    for (int64_t i = r0; i < r1; ++i) part = fmaf(s[i], X[i * ldx + j], part);
+                    g = (r0 == 0) ? part : g + part;
+                }
+            } else {
+                for (int64_t i = 0; i < n; ++i) g = fmaf(s[i], X[i * ldx + j], g);
+            }
+            G[j] = g;
+        }
+        for (int64_t j = 0; j < d; ++j) w[j] = w[j] - G[j];
+    }
+    free(s); free(G);
+    return 0;
+}

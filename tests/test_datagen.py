@@ -117,3 +117,17 @@ def test_matrix_completion_shapes_and_scale():
     assert abs(g["rating"].var() - (1 / 32 + 0.25)) < 0.02
     assert np.array_equal(g["col"][0::2], g["user"])
     assert np.array_equal(g["col"][1::2], g["item"] + 20000)
+
+
+def test_dense_examples():
+    a = datagen.generate_dense(1, n=300, d=200, nthreads=1)
+    b = datagen.generate_dense(1, n=300, d=200, nthreads=7, ldx=203)
+    assert a["X"].shape == (300, 200) and b["X"].strides == (203 * 4, 4)
+    assert np.array_equal(a["X"], b["X"]) and np.array_equal(a["y"], b["y"])
+    assert abs(a["X"].mean()) < 0.02 and abs(a["X"].std() - 1.0) < 0.02
+    # least squares: y = <x, w*> / sqrt(d) + 0.1 N(0,1), so var(y) ~ |w*|^2 / d + 0.01
+    assert 0.7 < a["y"].var() < 1.3
+    c = datagen.generate_dense(1, n=300, d=200, loss=datagen.LOGISTIC)
+    assert set(np.unique(c["y"])) <= {-1.0, 1.0}
+    full = datagen.DENSE[1]
+    assert (full.n, full.d) == (5000, 960)
