@@ -263,6 +263,47 @@ int pdb_stale_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t 
                     float lr, int loss, int64_t delay, const int32_t *prev_nz, void *ws,
                     size_t ws_bytes, hipStream_t stream);
 
+/* Dense full-batch gradient descent (the update of Sec. 2 with every example
+ * in every iteration; the dense linear-regression workloads of Sec. 6.1-6.2).
+ *
+ * The work is split over an R x C grid of workers: rows in blocks of
+ * row_block, columns in blocks of col_block (a multiple of 4), R =
+ * ceil(n / row_block), C = ceil(d / col_block).  The blocking fixes the
+ * summation order, so pdb_dense_plan is deterministic: it picks the blocks
+ * for `workers` workers (<= 0: the current device's compute units), with
+ * C / R near sqrt(d / n).  Host-only arithmetic apart from the device query.
+ * PDB_ERR_UNSUPPORTED when a block would exceed 4096 rows or 16384 columns. */
+int pdb_dense_plan(int64_t n, int64_t d, int workers, int64_t *row_block, int64_t *col_block);
+
+/* Device workspace (bytes) for pdb_dense_gd: the control block and two
+ * buffers of 64-bit words, 2 C n partial dot products and 2 R d partial
+ * gradients.  Host-only arithmetic. */
+int pdb_dense_workspace_bytes(int64_t n, int64_t d, int64_t row_block, int64_t col_block,
+                              size_t *bytes);
+
+/* `iters` iterations of full-batch gradient descent in place on w (device,
+ * [d]).  X: device, n x d, row-major with row stride ldx >= d (16-byte
+ * alignment and ldx % 4 == 0 take the vector loads; any layout works).
+ * labels: device, [n].  One iteration, every z_i from the weights before it:
+ *   z_i = <X_i, w>;  s_i = lr * g(z_i, y_i) with g as at the top of this
+ *   header;  G_j = sum_i s_i X_ij;  w_j = w_j - G_j.
+ * Summation order: within a column block, column k (k from 0 at the block
+ * start) goes to partial sum floor(k / 4) mod 64 as fma(X_ik, w_k, p), then
+ * the butterfly as at the top of this header; z_i adds the column blocks'
+ * results in block order (starting from block 0's).  Within a row block, the
+ * partial of G_j is fma(s_i, X_ij, p) over its rows in order from 0; G_j adds
+ * the row blocks' partials in block order.  Worker (r, c) waits only for the
+ * partials of its row group and of its column group (the read constraint of
+ * Sec. 4.4 per partition), never on a grid-wide barrier; the R C workers
+ * must be resident at once (one per compute unit; PDB_ERR_UNSUPPORTED
+ * otherwise).  Nothing changes when n, d or iters is 0.
+ * ws: at least pdb_dense_workspace_bytes(n, d, row_block, col_block).
+ * Asynchronous; a device error (watchdog) is reported by pdb_workspace_status
+ * on ws. */
+int pdb_dense_gd(const float *X, int64_t ldx, const float *labels, int64_t n, int64_t d,
+                 float *w, float lr, int loss, int64_t iters, int64_t row_block,
+                 int64_t col_block, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Per-feature occurrence lists (the transpose that exposes which examples
  * share a feature): col_ptr (device, [d+1]) and csc_row (device, [nnz],
  * rows ascending within a feature).  ws as for pdb_schedule.  Synchronous. */

@@ -32,7 +32,8 @@ EXPORTS = (
     "pdb_epoch_workspace_bytes", "pdb_schedule", "pdb_sgd_epoch", "pdb_mf_epoch",
     "pdb_validate_csr", "pdb_workspace_status", "pdb_transpose", "pdb_prev_writer",
     "pdb_check_reciprocal", "pdb_batch_schedule", "pdb_batch_epoch",
-    "pdb_stale_workspace_bytes", "pdb_stale_epoch",
+    "pdb_stale_workspace_bytes", "pdb_stale_epoch", "pdb_dense_plan",
+    "pdb_dense_workspace_bytes", "pdb_dense_gd",
 )
 
 
@@ -108,6 +109,9 @@ def load() -> ctypes.CDLL:
     lib.pdb_stale_workspace_bytes.argtypes = [i64, ctypes.POINTER(sz)]
     lib.pdb_stale_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int, i64,
                                     P, P, sz, P]
+    lib.pdb_dense_plan.argtypes = [i64, i64, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.pdb_dense_workspace_bytes.argtypes = [i64, i64, i64, i64, ctypes.POINTER(sz)]
+    lib.pdb_dense_gd.argtypes = [P, i64, P, i64, i64, P, f32, ctypes.c_int, i64, i64, i64, P, sz, P]
     for name in EXPORTS:
         if name not in ("pdb_strerror",):
             getattr(lib, name).restype = ctypes.c_int
@@ -338,6 +342,46 @@ def pdb_stale_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Ten
     _check(load().pdb_stale_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
                                   ctypes.c_float(lr), loss, delay, _ptr(levels.prev_nz), _ptr(ws),
                                   ws.numel(), _stream(stream, csr.device)), "pdb_stale_epoch")
+    return ws
+
+
+def pdb_dense_plan(n: int, d: int, workers: int = 0) -> tuple[int, int]:
+    """(row_block, col_block) for n x d on `workers` workers (0: the device's CUs)."""
+    rb, cb = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(load().pdb_dense_plan(n, d, workers, ctypes.byref(rb), ctypes.byref(cb)),
+           "pdb_dense_plan")
+    return rb.value, cb.value
+
+
+def pdb_dense_workspace_bytes(n: int, d: int, row_block: int, col_block: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().pdb_dense_workspace_bytes(n, d, row_block, col_block, ctypes.byref(out)),
+           "pdb_dense_workspace_bytes")
+    return out.value
+
+
+def pdb_dense_gd(X: torch.Tensor, labels: torch.Tensor, w: torch.Tensor, lr: float, loss: int,
+                 iters: int, row_block: int = 0, col_block: int = 0,
+                 ws: torch.Tensor | None = None, stream=None):
+    """X: float32 device matrix n x d with unit column stride (any row stride
+    >= d).  row_block = col_block = 0 takes pdb_dense_plan's blocking."""
+    if X.dtype != torch.float32 or w.dtype != torch.float32 or labels.dtype != torch.float32:
+        raise TypeError("X, w and labels must be float32")
+    if X.dim() != 2 or (X.shape[0] > 1 and X.shape[1] > 0 and X.stride(1) != 1):
+        raise ValueError("X must be a matrix with unit column stride")
+    n, d = X.shape
+    ldx = X.stride(0) if n > 1 else d
+    if w.numel() < d or labels.numel() < n:
+        raise ValueError("w must hold d entries and labels n entries")
+    if row_block == 0 and col_block == 0:
+        row_block, col_block = pdb_dense_plan(n, d)
+    if ws is None:
+        ws = workspace(pdb_dense_workspace_bytes(n, d, row_block, col_block), X.device)
+    if not X.is_cuda:
+        raise ValueError("expected a device tensor")
+    _check(load().pdb_dense_gd(X.data_ptr() if X.numel() else None, ldx, _ptr(labels), n, d, _ptr(w), ctypes.c_float(lr), loss,
+                               iters, row_block, col_block, _ptr(ws), ws.numel(),
+                               _stream(stream, X.device)), "pdb_dense_gd")
     return ws
 
 

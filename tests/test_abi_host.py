@@ -70,3 +70,30 @@ def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
     monkeypatch.setattr(native, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         native.load()
+
+
+def test_dense_plan_and_workspace(lib):
+    # host-only arithmetic when the worker count is given
+    from paper_1508_00703_amd import native
+
+    rb, cb = ctypes.c_int64(0), ctypes.c_int64(0)
+    sz = ctypes.c_size_t(0)
+    for n, d, workers in [(5000, 960, 256), (500, 10 ** 6, 256), (37, 301, 256), (1, 1, 256),
+                          (10 ** 6, 10, 256), (7, 5, 3), (0, 10, 256), (10, 0, 256)]:
+        assert lib.pdb_dense_plan(n, d, workers, ctypes.byref(rb), ctypes.byref(cb)) == 0
+        R = -(-max(n, 1) // rb.value)
+        C = -(-max(d, 1) // cb.value)
+        assert cb.value % 4 == 0 and rb.value >= 1
+        assert R * C <= workers, (n, d, rb.value, cb.value)
+        assert lib.pdb_dense_workspace_bytes(n, d, rb.value, cb.value, ctypes.byref(sz)) == 0
+        assert sz.value >= 512 + 16 * (C * n + R * d)
+    assert lib.pdb_dense_plan(5000, 960, 256, ctypes.byref(rb), ctypes.byref(cb)) == 0
+    assert (rb.value, cb.value) == (209, 96)
+    bad = native.PDB_ERR_INVALID_ARG
+    assert lib.pdb_dense_plan(-1, 4, 8, ctypes.byref(rb), ctypes.byref(cb)) == bad
+    assert lib.pdb_dense_workspace_bytes(10, 10, 4, 6, ctypes.byref(sz)) == bad   # cb % 4
+    assert lib.pdb_dense_workspace_bytes(10, 10, 0, 4, ctypes.byref(sz)) == bad
+    assert (lib.pdb_dense_workspace_bytes(10, 10, 5000, 4, ctypes.byref(sz))
+            == native.PDB_ERR_UNSUPPORTED)
+    assert (lib.pdb_dense_plan(10 ** 7, 1, 256, ctypes.byref(rb), ctypes.byref(cb))
+            == native.PDB_ERR_UNSUPPORTED)
