@@ -5,8 +5,11 @@ A step is one pass of the whole path over the workload, inputs resident in
 HBM: conflict levels (pdb_schedule: transpose, previous writers, levels,
 grouping) and one SGD epoch (pdb_sgd_epoch / pdb_mf_epoch), weights reset to
 w0 at the start of the step (--epochs E: E epochs on the step's schedule;
---batch B: mini-batches of B examples).  `value` = stored entries updated per second
-over the K timed steps (ratings per second for matrix completion).
+--batch B: mini-batches of B examples; --delay D: bounded-delay SGD; --dense W:
+full-batch gradient descent on dense workload W, one step = the workload's
+iterations).  `value` = stored entries updated per second over the K timed
+steps (ratings per second for matrix completion; example-feature pairs times
+iterations for dense gradient descent).
 
 Default workload: 10M examples x 1M features, 50 entries per example with
 Zipf(1.2) feature ids, binary values, logistic loss, lr 0.01.
@@ -49,11 +52,11 @@ def algorithmic_bytes(g, L, mf=False, U=None, nb=None):
     return g["nnz"] * per_nz + g["n"] * per_ex + L * 8
 
 
-def source_digest(batch=False, stale=False):
+def source_digest(batch=False, stale=False, dense=False):
     """Digest of the sources of the priced epoch kernel: a traffic record
     taken on other sources is not reported."""
     h = hashlib.sha256()
-    main = "stale.hip" if stale else ("batch.hip" if batch else "apply.hip")
+    main = "dense.hip" if dense else ("stale.hip" if stale else ("batch.hip" if batch else "apply.hip"))
     for f in (main, "pdb_math.h", "pdb_words.h", "pdb_internal.h"):
         with open(os.path.join(_ROOT, "paper_1508_00703_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
@@ -141,6 +144,114 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0, delay=-1):
     return res
 
 
+DENSE_LDS_FLOATS = 36864  # the tile stays in LDS when cb + rb (rounded to 4) + rb cb fit
+
+
+def dense_cpu_baseline(g, budget_s):
+    """The oracle's natural-order full-batch gradient descent, single thread,
+    on the whole matrix for as many iterations as fit the budget."""
+    import numpy as np
+
+    import oracle
+
+    w0 = np.zeros(g["d"], np.float32)
+    t0 = time.perf_counter()
+    oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.NATURAL, 1)
+    t1 = time.perf_counter() - t0
+    iters = int(max(1, min(g["iters"], budget_s / max(t1, 1e-6))))
+    t0 = time.perf_counter()
+    oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.NATURAL, iters)
+    t = time.perf_counter() - t0
+    return {"value": g["n"] * g["d"] * iters / t, "unit": "nnz-updates/s", "cores": 1,
+            "kind": "oracle",
+            "sample": "all %d x %d entries, %d of %d iterations, natural order, %.1f s" % (
+                g["n"], g["d"], iters, g["iters"], t),
+            "host_cpu": platform.processor() or platform.machine()}
+
+
+def run_dense(args):
+    """Dense full-batch gradient descent: a step is one pdb_dense_gd call of
+    the workload's iterations from w = 0."""
+    import numpy as np
+    import torch
+
+    import datagen
+    from paper_1508_00703_amd import native
+
+    native.load()
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    g = datagen.generate_dense(args.dense)
+    print("generated %s: %d x %d in %.1f s" % (g["name"], g["n"], g["d"], time.perf_counter() - t0),
+          file=sys.stderr, flush=True)
+    n, d, iters = g["n"], g["d"], g["iters"]
+    X = torch.from_numpy(np.ascontiguousarray(g["X"])).to(dev)
+    y = torch.from_numpy(g["y"]).to(dev)
+    w = torch.zeros(d, dtype=torch.float32, device=dev)
+    rb, cb = native.pdb_dense_plan(n, d)
+    ws = native.workspace(native.pdb_dense_workspace_bytes(n, d, rb, cb), dev)
+    resident = cb + ((rb + 3) // 4) * 4 + rb * cb <= DENSE_LDS_FLOATS
+    stream = torch.cuda.current_stream(dev)
+    ev = []
+
+    def step(timed):
+        w.zero_()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        native.pdb_dense_gd(X, y, w, float(g["lr"]), g["loss"], iters, rb, cb, ws=ws)
+        b.record(stream)
+        if timed:
+            ev.append((a, b))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    if native.pdb_workspace_status(ws) != native.PDB_OK:
+        raise SystemExit("device-side failure during warmup")
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(True)
+        print("step %d done" % k, file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    if native.pdb_workspace_status(ws) != native.PDB_OK:
+        raise SystemExit("device-side failure during the timed steps")
+    call_ms = [a.elapsed_time(b) for a, b in ev]
+    ms = trimmed_mean(call_ms)
+    # bytes the algorithm must move per call: X once when its tiles stay on
+    # chip, else X twice per iteration (the dot products need every column of
+    # the new weights, the gradient every row's step); y once, w read + written
+    xbytes = 4 * n * d * (1 if resident else 2 * iters)
+    abytes = xbytes + 4 * n + 8 * d
+    achieved = abytes / (ms * 1e-3) / 1e9
+    workload = "dense%d" % args.dense
+    digest = source_digest(dense=True)
+    out = {
+        "metric": METRIC,
+        "value": n * d * iters * args.steps / elapsed,
+        "unit": "nnz-updates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "%s: %s, %d iterations of full-batch gradient descent" % (
+                       workload, g["name"], iters),
+                   "n": n, "d": d, "iters": iters, "seed": g["seed"], "row_block": rb,
+                   "col_block": cb, "workers": -(-n // rb) * -(-d // cb),
+                   "tile": "resident in LDS" if resident else "streamed every iteration"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": read_traffic(workload, digest),
+                     "kernel": "k_dense_gd (all iterations)", "algorithmic_bytes": abytes,
+                     "call_ms": ms, "call_ms_all": call_ms, "source_digest": digest,
+                     "us_per_iteration": ms * 1e3 / max(iters, 1)},
+        "epoch_ms": ms,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = dense_cpu_baseline(g, args.cpu_budget)
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -154,6 +265,9 @@ def main():
     ap.add_argument("--batch", type=int, default=0,
                     help="mini-batch gradient descent with this many examples per batch "
                          "(pdb_batch_schedule + pdb_batch_epoch); 0 = SGD")
+    ap.add_argument("--dense", type=int, default=0, choices=[0, 1, 2],
+                    help="full-batch gradient descent on dense workload 1 (5000 x 960, "
+                         "200 iterations) or 2 (500 x 1M, 50 iterations); 0 = sparse")
     ap.add_argument("--method", type=int, default=0,
                     help="0 auto, 1 chain-scan, 2 dataflow, 3 spine")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -177,6 +291,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copied_bytes": src.numel() * 4}))
+        return
+
+    if args.dense:
+        run_dense(args)
         return
 
     import datagen

@@ -290,9 +290,13 @@ int pdb_dense_workspace_bytes(int64_t n, int64_t d, int64_t row_block, int64_t c
  * Summation order: within a column block, column k (k from 0 at the block
  * start) goes to partial sum floor(k / 4) mod 64 as fma(X_ik, w_k, p), then
  * the butterfly as at the top of this header; z_i adds the column blocks'
- * results in block order (starting from block 0's).  Within a row block, the
- * partial of G_j is fma(s_i, X_ij, p) over its rows in order from 0; G_j adds
- * the row blocks' partials in block order.  Worker (r, c) waits only for the
+ * results in block order (starting from block 0's).  A row block's partial
+ * of G_j adds, in order (starting from the first's), the partials of its
+ * chunks of 32 rows, each fma(s_i, X_ij, p) over the chunk's rows in order
+ * from 0; G_j adds the row blocks' partials in block order.  The tile of a
+ * worker stays in LDS across iterations when col_block + row_block (rounded
+ * up to 4) + row_block col_block floats, plus room for its staged partials,
+ * fit 36864 floats; otherwise it is read from memory twice per iteration.  Worker (r, c) waits only for the
  * partials of its row group and of its column group (the read constraint of
  * Sec. 4.4 per partition), never on a grid-wide barrier; the R C workers
  * must be resident at once (one per compute unit; PDB_ERR_UNSUPPORTED

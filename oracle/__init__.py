@@ -94,7 +94,7 @@ def _load():
     lib.orc_stale_snapshot.argtypes = [i64, i64, P, P, P, P, P, f32, i32, i32, i64]
     lib.orc_stale_snapshot.restype = ctypes.c_int
     lib.orc_stale_apply.argtypes = [i64, i64, P, P, P, P, P, f32, i32, i32, i64]
-    lib.orc_dense_gd.argtypes = [i64, i64, P, i64, P, P, f32, i32, i32, i64, i64, i64]
+    lib.orc_dense_gd.argtypes = [i64, i64, P, i64, P, P, f32, i32, i32, i64, i64, i64, i64]
     lib.orc_dense_gd.restype = ctypes.c_int
     lib.orc_stale_apply.restype = ctypes.c_int
     _lib = lib
@@ -313,10 +313,12 @@ def stale_snapshot(row_ptr, col, val, y, w, lr, loss=LOGISTIC, mode=MATCHED, del
     return _stale(_load().orc_stale_snapshot, row_ptr, col, val, y, w, len(w), lr, loss, mode, delay)
 
 
-def dense_gd(X, y, w, lr, loss=SQUARED, mode=MATCHED, iters=1, row_block=None, col_block=None):
+def dense_gd(X, y, w, lr, loss=SQUARED, mode=MATCHED, iters=1, row_block=None, col_block=None,
+             row_chunk=None):
     """Full-batch gradient descent on the rows of X (n x d, float32), iters
     iterations, on a copy of w.  Matched mode sums in the blocked order given
-    by row_block and col_block (default: one block each way)."""
+    by row_block, col_block and row_chunk (default: one block each way, one
+    chunk per row block)."""
     X = np.asarray(X, dtype=np.float32)
     if X.ndim != 2 or X.strides[1] != 4 or X.strides[0] % 4:
         X = np.ascontiguousarray(X)
@@ -326,7 +328,8 @@ def dense_gd(X, y, w, lr, loss=SQUARED, mode=MATCHED, iters=1, row_block=None, c
     w = np.array(w, dtype=np.float32, copy=True)
     rb = max(n, 1) if row_block is None else int(row_block)
     cb = max(d, 1) if col_block is None else int(col_block)
+    rc = rb if row_chunk is None else int(row_chunk)
     if _load().orc_dense_gd(n, d, X.ctypes.data, ldx, _ptr(y), _ptr(w), np.float32(lr), loss, mode,
-                            int(iters), rb, cb) != 0:
+                            int(iters), rb, cb, rc) != 0:
         raise ValueError("bad blocking or out of memory")
     return w

@@ -537,9 +537,11 @@ int orc_stale_apply(int64_t n, int64_t d, const int64_t *row_ptr, const int32_t 
  *   The partial dot of a column block has 64 partial sums; column k of the
  *   block (k from 0) goes into sum (k / 4) mod 64, in increasing k, then the
  *   butterfly; z_i adds the blocks' partials in block order, starting from
- *   block 0's.  A row block's partial of G_j is fmaf over its rows in order
- *   from 0; G_j adds the row blocks' partials in block order, starting from
- *   block 0's.
+ *   block 0's.  A row block is cut into chunks of row_chunk rows; a chunk's
+ *   partial of G_j is fmaf over its rows in order from 0, the row block's
+ *   partial adds its chunks' partials in order (starting from the first's),
+ *   and G_j adds the row blocks' partials in block order (starting from
+ *   block 0's).
  * Returns 0, -1 on failure (bad blocking or no memory). */
 static float residual(float z, float y, int32_t loss, int32_t mode) {
     if (loss == ORC_LOGISTIC) {
@@ -551,8 +553,8 @@ static float residual(float z, float y, int32_t loss, int32_t mode) {
 
 int orc_dense_gd(int64_t n, int64_t d, const float *X, int64_t ldx, const float *y, float *w,
                  float lr, int32_t loss, int32_t mode, int64_t iters, int64_t row_block,
-                 int64_t col_block) {
-    if (mode == ORC_MATCHED && (row_block < 1 || col_block < 1)) return -1;
+                 int64_t col_block, int64_t row_chunk) {
+    if (mode == ORC_MATCHED && (row_block < 1 || col_block < 1 || row_chunk < 1)) return -1;
     float *s = (float *)malloc((size_t)(n > 0 ? n : 1) * sizeof(float));
     float *G = (float *)malloc((size_t)(d > 0 ? d : 1) * sizeof(float));
     if (!s || !G) {
@@ -584,7 +586,12 @@ int orc_dense_gd(int64_t n, int64_t d, const float *X, int64_t ldx, const float 
                 for (int64_t r0 = 0; r0 < n; r0 += row_block) {
                     int64_t r1 = r0 + row_block < n ? r0 + row_block : n;
                     float part = 0.0f;
-                    for (int64_t i = r0; i < r1; ++i) part = fmaf(s[i], X[i * ldx + j], part);
+                    for (int64_t h0 = r0; h0 < r1; h0 += row_chunk) {
+                        int64_t h1 = h0 + row_chunk < r1 ? h0 + row_chunk : r1;
+                        float chunk = 0.0f;
+                        for (int64_t i = h0; i < h1; ++i) chunk = fmaf(s[i], X[i * ldx + j], chunk);
+                        part = (h0 == r0) ? chunk : part + chunk;
+                    }
                     g = (r0 == 0) ? part : g + part;
                 }
             } else {

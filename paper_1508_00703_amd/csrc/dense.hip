@@ -26,12 +26,16 @@
 // Summation order (reproduced by the oracle's matched mode): a partial dot
 // product has 64 running sums, column k of the block (k from 0) in sum
 // (k / 4) mod 64 -- lane k / 4 mod 64 takes four consecutive columns -- then
-// the wave sum; z_i adds the column blocks' partials in block order.  A
-// partial gradient is an fma chain over the block's rows in order; G_j adds
-// the row blocks' partials in block order.
+// the wave sum; z_i adds the column blocks' partials in block order.  A row
+// block's partial gradient adds, in order, the partials of its chunks of 32
+// rows, each an fma chain over the chunk's rows in order; G_j adds the row
+// blocks' partials in block order.
 //
-// The tile stays in LDS across iterations when it fits (resident variant);
-// otherwise both passes stream it from memory every iteration.
+// Waiting: a worker loads all the partial words it needs at once, many per
+// thread, into LDS, and re-polls only those not yet written; the ordered sums
+// then run from LDS.  The tile stays in LDS across iterations when it fits
+// (resident variant); otherwise both passes stream it from memory every
+// iteration.
 #include <cmath>
 
 #include "pdb_math.h"
@@ -45,7 +49,8 @@ constexpr int kDThreads = 1024;
 constexpr int kDWaves = kDThreads / kWave;
 constexpr int kZRows = 4;               // rows per wave step of the dot-product pass
 constexpr int kGRows = 8;               // rows per step of the gradient pass (streaming)
-constexpr int kWaitBatch = 8;           // partial words loaded before checking their tags
+constexpr int kWaitBatch = 8;           // partial words per thread loaded before checking tags
+constexpr int kRowChunk = 32;           // rows per fma chain of a partial gradient
 constexpr int64_t kMaxRowBlock = 4096;
 constexpr int64_t kMaxColBlock = 16384;
 constexpr int kLdsFloats = 36864;       // 144 KB: w_c, s and (resident) the tile
@@ -86,9 +91,17 @@ struct DenseArgs {
     int64_t timeout;
 };
 
-// floats of LDS a worker needs: w_c, s, and the tile when resident
-inline int64_t lds_floats(int64_t rb, int64_t cb, bool resident) {
+// floats of LDS a worker needs: w_c, s, and the tile when resident; the
+// rest stages partial words and chunk partials
+__host__ __device__ inline int64_t lds_floats(int64_t rb, int64_t cb, bool resident) {
     return cb + ((rb + 3) & ~int64_t(3)) + (resident ? rb * cb : 0);
+}
+
+// the resident variant also needs room to stage one row's or one column's
+// partials and the chunk partials of its gradient pass
+inline bool fits_resident(int64_t rb, int64_t cb, int64_t R, int64_t C) {
+    const int64_t stage = std::max({R, C, cb * cdiv(rb, kRowChunk)});
+    return lds_floats(rb, cb, true) + stage <= kLdsFloats;
 }
 
 __global__ void k_dense_clear(unsigned long long *__restrict__ a, int64_t count, Ctrl *ctrl) {
@@ -118,31 +131,31 @@ __device__ __noinline__ unsigned long long word_wait_one(unsigned long long *bas
     }
 }
 
-// Sum, in order p = 0..count-1, of the values of words base[first + p *
-// stride] once each carries tag; loads kWaitBatch words before checking.
-__device__ __forceinline__ bool ordered_sum(unsigned long long *base, int64_t first,
-                                            int64_t stride, int count, int tag, float *sum,
-                                            Ctrl *ctrl, int64_t timeout) {
-    float acc = 0.0f;
-    for (int p0 = 0; p0 < count; p0 += kWaitBatch) {
+// Loads count words into stage[0..count), word e from base[idx(e)], once
+// each carries tag.  Thread tid takes e = tid + m kDThreads, kWaitBatch loads
+// in flight before the first check.  False on timeout or abort.
+template <class Idx>
+__device__ __forceinline__ bool gather_words(unsigned long long *base, Idx idx, int count, int tag,
+                                             float *stage, Ctrl *ctrl, int64_t timeout) {
+    for (int e0 = threadIdx.x; e0 < count; e0 += kDThreads * kWaitBatch) {
         unsigned long long v[kWaitBatch];
 #pragma unroll
-        for (int u = 0; u < kWaitBatch; ++u)
-            if (p0 + u < count) v[u] = word_get(base, first + (int64_t)(p0 + u) * stride);
+        for (int u = 0; u < kWaitBatch; ++u) {
+            const int e = e0 + u * kDThreads;
+            if (e < count) v[u] = word_get(base, idx(e));
+        }
 #pragma unroll
         for (int u = 0; u < kWaitBatch; ++u) {
-            if (p0 + u < count) {
+            const int e = e0 + u * kDThreads;
+            if (e < count) {
                 if (word_tag(v[u]) != tag) {
-                    v[u] = word_wait_one(base, first + (int64_t)(p0 + u) * stride, tag, ctrl,
-                                         timeout);
+                    v[u] = word_wait_one(base, idx(e), tag, ctrl, timeout);
                     if (word_tag(v[u]) != tag) return false;
                 }
-                const float x = word_value(v[u]);
-                acc = (p0 + u == 0) ? x : acc + x;
+                stage[e] = word_value(v[u]);
             }
         }
     }
-    *sum = acc;
     return true;
 }
 
@@ -164,6 +177,9 @@ __global__ __launch_bounds__(kDThreads) void k_dense_gd(DenseArgs a) {
     float *sw = lds;                     // [cb] this worker's copy of w_c
     float *ss = lds + a.cb;              // [rb] steps s_i of the row block
     float *tile = ss + ((a.rb + 3) & ~3);  // [rb][cb] resident tile
+    const int used = (int)lds_floats(a.rb, a.cb, RES);
+    float *stage = lds + used;              // staged partials
+    const int cap = kLdsFloats - used;
     const float *xt = a.X + row0 * a.ldx + col0;
 
     for (int k = tid; k < cols; k += kDThreads) sw[k] = a.w[col0 + k];
@@ -226,70 +242,113 @@ __global__ __launch_bounds__(kDThreads) void k_dense_gd(DenseArgs a) {
 
     dot_pass(0);
     for (int t = 0; t < a.iters; ++t) {
-        // steps of this row block: the C column blocks' partials in order
-        bool ok = true;
-        for (int i = tid; i < rows && ok; i += kDThreads) {
-            float z = 0.0f;
-            ok = ordered_sum(a.zw, (int64_t)(t & 1) * a.C * a.n + row0 + i, a.n, a.C, t, &z,
-                             a.ctrl, a.timeout);
-            ss[i] = sgd_scale<LOSS>(z, a.y[row0 + i], a.lr);
+        // steps of this row block: the C column blocks' partials in order,
+        // rows in chunks whose C partials fit the stage
+        {
+            const int chunk = std::max(1, std::min(rows, cap / a.C));
+            for (int i0 = 0; i0 < rows; i0 += chunk) {
+                const int nr = std::min(chunk, rows - i0);
+                const int64_t base = (int64_t)(t & 1) * a.C * a.n + row0 + i0;
+                const int64_t n = a.n;
+                const bool ok = gather_words(
+                    a.zw, [=](int e) { const int p = e / nr; return base + p * n + (e - p * nr); },
+                    nr * a.C, t, stage, a.ctrl, a.timeout);
+                if (__syncthreads_or(!ok)) return;
+                for (int i = tid; i < nr; i += kDThreads) {
+                    float z = stage[i];
+                    for (int p = 1; p < a.C; ++p) z = z + stage[p * nr + i];
+                    ss[i0 + i] = sgd_scale<LOSS>(z, a.y[row0 + i0 + i], a.lr);
+                }
+                __syncthreads();
+            }
         }
-        if (__syncthreads_or(!ok)) return;
 
         // partial gradients of this worker's columns over its rows
         unsigned long long *gw = a.gw + ((int64_t)(t & 1) * a.R + r) * a.d + col0;
         if (RES) {
-            for (int k = tid; k < cols; k += kDThreads) {
+            // one thread per (chunk, column), then the chunks added in order
+            const int nch = (rows + kRowChunk - 1) / kRowChunk;
+            for (int e = tid; e < nch * cols; e += kDThreads) {
+                const int h = e / cols, k = e - h * cols;
+                const int i1 = std::min(rows, (h + 1) * kRowChunk);
                 float acc = 0.0f;
-                for (int i = 0; i < rows; ++i) acc = __builtin_fmaf(ss[i], tile[i * a.cb + k], acc);
-                word_put(gw, k, word_pack(acc, t));
+                for (int i = h * kRowChunk; i < i1; ++i)
+                    acc = __builtin_fmaf(ss[i], tile[i * a.cb + k], acc);
+                stage[e] = acc;
             }
+            __syncthreads();
+            for (int k = tid; k < cols; k += kDThreads) {
+                float part = stage[k];
+                for (int h = 1; h < nch; ++h) part = part + stage[h * cols + k];
+                word_put(gw, k, word_pack(part, t));
+            }
+            __syncthreads();
         } else {
             for (int g = tid; g < groups; g += kDThreads) {
-                float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                float tot[4] = {0.0f, 0.0f, 0.0f, 0.0f};
                 const float *xg = xt + 4 * g;
-                if (4 * g + 3 < cols) {
-                    int i = 0;
-                    for (; i + kGRows <= rows; i += kGRows) {
-                        float4 x[kGRows];
+                const bool full = 4 * g + 3 < cols;
+                for (int h0 = 0; h0 < rows; h0 += kRowChunk) {
+                    const int h1 = std::min(rows, h0 + kRowChunk);
+                    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if (full) {
+                        int i = h0;
+                        for (; i + kGRows <= h1; i += kGRows) {
+                            float4 x[kGRows];
 #pragma unroll
-                        for (int u = 0; u < kGRows; ++u) x[u] = load4<VEC>(xg + (int64_t)(i + u) * a.ldx);
+                            for (int u = 0; u < kGRows; ++u)
+                                x[u] = load4<VEC>(xg + (int64_t)(i + u) * a.ldx);
 #pragma unroll
-                        for (int u = 0; u < kGRows; ++u) {
-                            const float s = ss[i + u];
-                            acc[0] = __builtin_fmaf(s, x[u].x, acc[0]);
-                            acc[1] = __builtin_fmaf(s, x[u].y, acc[1]);
-                            acc[2] = __builtin_fmaf(s, x[u].z, acc[2]);
-                            acc[3] = __builtin_fmaf(s, x[u].w, acc[3]);
+                            for (int u = 0; u < kGRows; ++u) {
+                                const float s = ss[i + u];
+                                acc[0] = __builtin_fmaf(s, x[u].x, acc[0]);
+                                acc[1] = __builtin_fmaf(s, x[u].y, acc[1]);
+                                acc[2] = __builtin_fmaf(s, x[u].z, acc[2]);
+                                acc[3] = __builtin_fmaf(s, x[u].w, acc[3]);
+                            }
                         }
+                        for (; i < h1; ++i) {
+                            const float4 x = load4<VEC>(xg + (int64_t)i * a.ldx);
+                            const float s = ss[i];
+                            acc[0] = __builtin_fmaf(s, x.x, acc[0]);
+                            acc[1] = __builtin_fmaf(s, x.y, acc[1]);
+                            acc[2] = __builtin_fmaf(s, x.z, acc[2]);
+                            acc[3] = __builtin_fmaf(s, x.w, acc[3]);
+                        }
+                    } else {
+                        for (int i = h0; i < h1; ++i)
+                            for (int k = 0; k < 4; ++k)
+                                if (4 * g + k < cols)
+                                    acc[k] = __builtin_fmaf(ss[i], xg[(int64_t)i * a.ldx + k], acc[k]);
                     }
-                    for (; i < rows; ++i) {
-                        const float4 x = load4<VEC>(xg + (int64_t)i * a.ldx);
-                        const float s = ss[i];
-                        acc[0] = __builtin_fmaf(s, x.x, acc[0]);
-                        acc[1] = __builtin_fmaf(s, x.y, acc[1]);
-                        acc[2] = __builtin_fmaf(s, x.z, acc[2]);
-                        acc[3] = __builtin_fmaf(s, x.w, acc[3]);
-                    }
-                } else {
-                    for (int i = 0; i < rows; ++i)
-                        for (int k = 0; k < 4; ++k)
-                            if (4 * g + k < cols)
-                                acc[k] = __builtin_fmaf(ss[i], xg[(int64_t)i * a.ldx + k], acc[k]);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) tot[k] = (h0 == 0) ? acc[k] : tot[k] + acc[k];
                 }
                 for (int k = 0; k < 4; ++k)
-                    if (4 * g + k < cols) word_put(gw, 4 * g + k, word_pack(acc[k], t));
+                    if (4 * g + k < cols) word_put(gw, 4 * g + k, word_pack(tot[k], t));
             }
         }
 
-        // the step of w_c: the R row blocks' partials in order
-        for (int k = tid; k < cols && ok; k += kDThreads) {
-            float G = 0.0f;
-            ok = ordered_sum(a.gw, (int64_t)(t & 1) * a.R * a.d + col0 + k, a.d, a.R, t, &G,
-                             a.ctrl, a.timeout);
-            sw[k] = sw[k] - G;
+        // the step of w_c: the R row blocks' partials in order, columns in
+        // chunks whose R partials fit the stage
+        {
+            const int chunk = std::max(1, std::min(cols, cap / a.R));
+            for (int k0 = 0; k0 < cols; k0 += chunk) {
+                const int nc = std::min(chunk, cols - k0);
+                const int64_t base = (int64_t)(t & 1) * a.R * a.d + col0 + k0;
+                const int64_t d = a.d;
+                const bool ok = gather_words(
+                    a.gw, [=](int e) { const int p = e / nc; return base + p * d + (e - p * nc); },
+                    nc * a.R, t, stage, a.ctrl, a.timeout);
+                if (__syncthreads_or(!ok)) return;
+                for (int k = tid; k < nc; k += kDThreads) {
+                    float G = stage[k];
+                    for (int p = 1; p < a.R; ++p) G = G + stage[p * nc + k];
+                    sw[k0 + k] = sw[k0 + k] - G;
+                }
+                __syncthreads();
+            }
         }
-        if (__syncthreads_or(!ok)) return;
         if (t + 1 < a.iters) dot_pass(t + 1);
     }
     if (r == 0)
@@ -406,7 +465,7 @@ extern "C" int pdb_dense_gd(const float *X, int64_t ldx, const float *labels, in
     PDB_LAUNCHED();
     if (idle) return PDB_OK;
     const char *e = getenv("PDB_DENSE_STREAM");
-    const bool res = !(e && atoi(e) != 0) && lds_floats(p.rb, p.cb, true) <= kLdsFloats;
+    const bool res = !(e && atoi(e) != 0) && fits_resident(p.rb, p.cb, p.R, p.C);
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) && (ldx % 4 == 0);
     DenseArgs a{X, ldx, labels, w, n, d, iters, lr, (int)p.rb, (int)p.cb, (int)p.R, (int)p.C,
                 lay.zw, lay.gw, lay.ctrl, spin_timeout_ticks()};

@@ -14,6 +14,8 @@ import oracle
 
 pytestmark = pytest.mark.gpu
 
+ROW_CHUNK = 32  # rows per fma chain of a partial gradient (the documented order)
+
 
 def native_mod():
     from paper_1508_00703_amd import native
@@ -44,7 +46,7 @@ def check_dense(native, dev, X, y, w0, lr, loss, iters, rb=0, cb=0, natural=True
     if rb == 0 and cb == 0:
         rb, cb = native.pdb_dense_plan(n, d)
     got, _ = run_gpu(native, dev, X, y, w0, lr, loss, iters, rb, cb)
-    ref = oracle.dense_gd(X, y, w0, lr, loss, oracle.MATCHED, iters, rb, cb)
+    ref = oracle.dense_gd(X, y, w0, lr, loss, oracle.MATCHED, iters, rb, cb, ROW_CHUNK)
     bad = np.nonzero(got.view(np.int32) != ref.view(np.int32))[0]
     assert len(bad) == 0, "blocks %dx%d, first mismatches %s: gpu %s oracle %s" % (
         rb, cb, bad[:5], got[bad[:5]], ref[bad[:5]])
@@ -66,6 +68,7 @@ CASES = [
     (37, 301, 0, 0), (37, 301, 5, 16), (37, 301, 37, 304), (37, 301, 1, 64),
     (5, 4, 0, 0), (1, 1, 0, 0), (1, 1, 1, 4), (64, 3, 8, 4), (300, 1000, 0, 0),
     (300, 1000, 20, 256), (1000, 257, 70, 32), (4096, 8, 4096, 8), (3, 20000, 1, 16384),
+    (2000, 40, 100, 8), (130, 64, 130, 64),
 ]
 
 
@@ -114,7 +117,7 @@ def test_calls_compose(gpu):
     w33, _ = run_gpu(native, gpu, X, y, w3, lr, oracle.SQUARED, 3, rb, cb, ws=ws)
     w6, _ = run_gpu(native, gpu, X, y, w0, lr, oracle.SQUARED, 6, rb, cb)
     assert np.array_equal(w33.view(np.int32), w6.view(np.int32))
-    ref = oracle.dense_gd(X, y, w0, lr, oracle.SQUARED, oracle.MATCHED, 6, rb, cb)
+    ref = oracle.dense_gd(X, y, w0, lr, oracle.SQUARED, oracle.MATCHED, 6, rb, cb, ROW_CHUNK)
     assert np.array_equal(w6.view(np.int32), ref.view(np.int32))
 
 

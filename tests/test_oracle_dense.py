@@ -12,7 +12,8 @@ import pytest
 
 import oracle
 
-BLOCKINGS = [(None, None), (1, 4), (2, 8), (3, 1), (5, 64), (1000, 3)]
+BLOCKINGS = [(None, None, None), (1, 4, None), (2, 8, None), (3, 1, 1), (5, 64, 2), (1000, 3, None),
+             (1000, 3, 32), (11, 8, 4)]
 
 
 def exact_gd(X, y, w, lr, iters):
@@ -46,9 +47,9 @@ def test_exact_integer_iterations(seed, iters):
     want = np.array([float(v) for v in want], np.float32)
     got = oracle.dense_gd(X, y, w, lr, oracle.SQUARED, oracle.NATURAL, iters)
     assert np.array_equal(got, want)
-    for rb, cb in BLOCKINGS:
-        got = oracle.dense_gd(X, y, w, lr, oracle.SQUARED, oracle.MATCHED, iters, rb, cb)
-        assert np.array_equal(got, want), (rb, cb)
+    for rb, cb, rc in BLOCKINGS:
+        got = oracle.dense_gd(X, y, w, lr, oracle.SQUARED, oracle.MATCHED, iters, rb, cb, rc)
+        assert np.array_equal(got, want), (rb, cb, rc)
 
 
 def closed_form_lsq(X, y, w0, lr, T):
@@ -145,9 +146,9 @@ def test_blockings_agree_with_natural(loss):
          else rng.normal(size=n)).astype(np.float32)
     lr = np.float32(0.5 / (n + d))
     nat = oracle.dense_gd(X, y, np.zeros(d), lr, loss, oracle.NATURAL, 5)
-    for rb, cb in BLOCKINGS + [(37, 512), (36, 300)]:
-        got = oracle.dense_gd(X, y, np.zeros(d), lr, loss, oracle.MATCHED, 5, rb, cb)
-        assert np.max(np.abs(got - nat)) <= 1e-6, (rb, cb)
+    for rb, cb, rc in BLOCKINGS + [(37, 512, None), (36, 300, 32), (37, 300, 5)]:
+        got = oracle.dense_gd(X, y, np.zeros(d), lr, loss, oracle.MATCHED, 5, rb, cb, rc)
+        assert np.max(np.abs(got - nat)) <= 1e-6, (rb, cb, rc)
 
 
 def test_equals_one_batch_of_all_examples():
@@ -196,3 +197,20 @@ def test_degenerate_cases():
         assert np.array_equal(oracle.dense_gd(X, y, w0, 0.0, oracle.SQUARED, mode, 2), w0)
     with pytest.raises(ValueError):
         oracle.dense_gd(X, y, w0, 0.1, oracle.SQUARED, oracle.MATCHED, 1, 0, 4)
+    with pytest.raises(ValueError):
+        oracle.dense_gd(X, y, w0, 0.1, oracle.SQUARED, oracle.MATCHED, 1, 2, 4, 0)
+
+
+def test_row_chunks_split_the_gradient_chain():
+    # a chunk as long as the row block is the single chain; shorter chunks
+    # regroup the same sum (equal here up to rounding, and bitwise when the
+    # data make every partial exact)
+    rng = np.random.default_rng(17)
+    X = rng.normal(size=(64, 10)).astype(np.float32)
+    y = rng.normal(size=64).astype(np.float32)
+    w0 = rng.normal(size=10).astype(np.float32)
+    a = oracle.dense_gd(X, y, w0, 0.01, oracle.SQUARED, oracle.MATCHED, 2, 64, 12)
+    b = oracle.dense_gd(X, y, w0, 0.01, oracle.SQUARED, oracle.MATCHED, 2, 64, 12, 64)
+    c = oracle.dense_gd(X, y, w0, 0.01, oracle.SQUARED, oracle.MATCHED, 2, 64, 12, 7)
+    assert np.array_equal(a, b)
+    assert np.max(np.abs(a - c)) <= 1e-5 and not np.array_equal(a, c)
