@@ -47,10 +47,12 @@ namespace {
 
 constexpr int kDThreads = 1024;
 constexpr int kDWaves = kDThreads / kWave;
-constexpr int kZRows = 4;               // rows per wave step of the dot-product pass
-constexpr int kGRows = 8;               // rows per step of the gradient pass (streaming)
+constexpr int kZRowsRes = 8;            // rows per wave step of the dot-product pass (LDS tile)
+constexpr int kGRows = 4;               // rows per step of the gradient pass (streaming)
+constexpr int kGUnroll = 4;             // groups per lane in flight in the dot-product pass (streaming)
 constexpr int kWaitBatch = 8;           // partial words per thread loaded before checking tags
 constexpr int kRowChunk = 32;           // rows per fma chain of a partial gradient
+constexpr int kLaneStride = kWave + 4;  // LDS floats per row of lane sums (b128 reads spread over the banks)
 constexpr int64_t kMaxRowBlock = 4096;
 constexpr int64_t kMaxColBlock = 16384;
 constexpr int kLdsFloats = 36864;       // 144 KB: w_c, s and (resident) the tile
@@ -100,7 +102,7 @@ __host__ __device__ inline int64_t lds_floats(int64_t rb, int64_t cb, bool resid
 // the resident variant also needs room to stage one row's or one column's
 // partials and the chunk partials of its gradient pass
 inline bool fits_resident(int64_t rb, int64_t cb, int64_t R, int64_t C) {
-    const int64_t stage = std::max({R, C, cb * cdiv(rb, kRowChunk)});
+    const int64_t stage = std::max({R, C, cb * cdiv(rb, kRowChunk), (int64_t)kLaneStride});
     return lds_floats(rb, cb, true) + stage <= kLdsFloats;
 }
 
@@ -114,31 +116,16 @@ __global__ void k_dense_clear(unsigned long long *__restrict__ a, int64_t count,
     }
 }
 
-// one thread polls one word until it carries tag; returns the last word
-// read, whose tag differs from tag on timeout or abort
-__device__ __noinline__ unsigned long long word_wait_one(unsigned long long *base, int64_t idx,
-                                                         int tag, Ctrl *ctrl, int64_t timeout) {
-    const int64_t t0 = now_ticks();
-    for (int round = 0;; ++round) {
-        const unsigned long long v = word_get(base, idx);
-        if (word_tag(v) == tag || aborted(ctrl)) return v;
-        if (now_ticks() - t0 > timeout) {
-            record_error(ctrl, DERR_WAIT_TIMEOUT);
-            return v;
-        }
-        word_backoff(round);
-        __asm__ __volatile__("" ::: "memory");
-    }
-}
-
 // Loads count words into stage[0..count), word e from base[idx(e)], once
-// each carries tag.  Thread tid takes e = tid + m kDThreads, kWaitBatch loads
-// in flight before the first check.  False on timeout or abort.
+// each carries tag.  Thread tid takes e = tid + m kDThreads, kWaitBatch words
+// at a time; the words not yet written are polled again together, all their
+// loads in flight at once.  False on timeout or abort.
 template <class Idx>
 __device__ __forceinline__ bool gather_words(unsigned long long *base, Idx idx, int count, int tag,
                                              float *stage, Ctrl *ctrl, int64_t timeout) {
     for (int e0 = threadIdx.x; e0 < count; e0 += kDThreads * kWaitBatch) {
         unsigned long long v[kWaitBatch];
+        unsigned pending = 0;
 #pragma unroll
         for (int u = 0; u < kWaitBatch; ++u) {
             const int e = e0 + u * kDThreads;
@@ -147,13 +134,32 @@ __device__ __forceinline__ bool gather_words(unsigned long long *base, Idx idx, 
 #pragma unroll
         for (int u = 0; u < kWaitBatch; ++u) {
             const int e = e0 + u * kDThreads;
-            if (e < count) {
-                if (word_tag(v[u]) != tag) {
-                    v[u] = word_wait_one(base, idx(e), tag, ctrl, timeout);
-                    if (word_tag(v[u]) != tag) return false;
+            if (e < count && word_tag(v[u]) != tag) pending |= 1u << u;
+        }
+        int64_t t0 = 0;
+        for (int round = 0; pending != 0; ++round) {
+            if (round == 0) {
+                t0 = now_ticks();
+            } else {
+                if (aborted(ctrl)) return false;
+                if (now_ticks() - t0 > timeout) {
+                    record_error(ctrl, DERR_WAIT_TIMEOUT);
+                    return false;
                 }
-                stage[e] = word_value(v[u]);
             }
+            word_backoff(round);
+            __asm__ __volatile__("" ::: "memory");
+#pragma unroll
+            for (int u = 0; u < kWaitBatch; ++u)
+                if (pending & (1u << u)) v[u] = word_get(base, idx(e0 + u * kDThreads));
+#pragma unroll
+            for (int u = 0; u < kWaitBatch; ++u)
+                if ((pending & (1u << u)) && word_tag(v[u]) == tag) pending &= ~(1u << u);
+        }
+#pragma unroll
+        for (int u = 0; u < kWaitBatch; ++u) {
+            const int e = e0 + u * kDThreads;
+            if (e < count) stage[e] = word_value(v[u]);
         }
     }
     return true;
@@ -198,46 +204,124 @@ __global__ __launch_bounds__(kDThreads) void k_dense_gd(DenseArgs a) {
     }
     __syncthreads();
 
-    // partial dot products of this worker's rows over its columns, tag t
+    // Partial dot products of this worker's rows over its columns, tag t.
+    // Each lane keeps the running sums of its four-column groups.  Streamed:
+    // a wave takes a row, kGUnroll groups per lane in flight, and sums the
+    // lanes across the wave.  Resident: a wave takes kZRowsRes rows at once
+    // and writes its lanes' sums to LDS; then a thread per row adds the 64 in
+    // the butterfly's pairing (adjacent pairs, then pairs of pairs, ...) --
+    // the value every lane of the butterfly ends with.  Rows past the end are
+    // clamped (computed, not published) and columns past the end masked by a
+    // select, so the loads of a step issue together.
     auto dot_pass = [&](int t) {
         unsigned long long *zw = a.zw + ((int64_t)(t & 1) * a.C + c) * a.n + row0;
-        for (int i0 = wave * kZRows; i0 < rows; i0 += kDWaves * kZRows) {
-            float acc[kZRows];
+        if constexpr (RES) {
+            const int chunk = std::min(rows, std::max(1, cap / kLaneStride));
+            for (int h0 = 0; h0 < rows; h0 += chunk) {
+                const int nr = std::min(chunk, rows - h0);
+                for (int i0 = wave * kZRowsRes; i0 < nr; i0 += kDWaves * kZRowsRes) {
+                    float acc[kZRowsRes];
 #pragma unroll
-            for (int u = 0; u < kZRows; ++u) acc[u] = 0.0f;
-            for (int g = lane; g < groups; g += kWave) {
-                const float4 wv = *reinterpret_cast<const float4 *>(sw + 4 * g);
-                const bool full = 4 * g + 3 < cols;
+                    for (int u = 0; u < kZRowsRes; ++u) acc[u] = 0.0f;
+                    for (int g = lane; g < groups; g += kWave) {
+                        const int kk = 4 * g;
+                        // w_c and the tile rows are padded to cb: in bounds
+                        const float4 wv = *reinterpret_cast<const float4 *>(sw + kk);
+                        float4 x[kZRowsRes];
 #pragma unroll
-                for (int u = 0; u < kZRows; ++u) {
-                    const int i = i0 + u;
-                    if (i < rows) {
-                        if (full) {
-                            const float4 x = RES ? *reinterpret_cast<const float4 *>(tile + i * a.cb + 4 * g)
-                                                 : load4<VEC>(xt + (int64_t)i * a.ldx + 4 * g);
-                            acc[u] = __builtin_fmaf(x.x, wv.x, acc[u]);
-                            acc[u] = __builtin_fmaf(x.y, wv.y, acc[u]);
-                            acc[u] = __builtin_fmaf(x.z, wv.z, acc[u]);
-                            acc[u] = __builtin_fmaf(x.w, wv.w, acc[u]);
-                        } else {
-                            const float *x = RES ? tile + i * a.cb + 4 * g
-                                                 : xt + (int64_t)i * a.ldx + 4 * g;
-                            for (int k = 0; k < 4; ++k)
-                                if (4 * g + k < cols)
-                                    acc[u] = __builtin_fmaf(x[k], sw[4 * g + k], acc[u]);
+                        for (int u = 0; u < kZRowsRes; ++u) {
+                            const int i = h0 + std::min(i0 + u, nr - 1);
+                            x[u] = *reinterpret_cast<const float4 *>(tile + i * a.cb + kk);
+                        }
+                        const bool c1 = kk + 1 < cols, c2 = kk + 2 < cols, c3 = kk + 3 < cols;
+#pragma unroll
+                        for (int u = 0; u < kZRowsRes; ++u) {
+                            float v = __builtin_fmaf(x[u].x, wv.x, acc[u]);
+                            const float v1 = __builtin_fmaf(x[u].y, wv.y, v);
+                            v = c1 ? v1 : v;
+                            const float v2 = __builtin_fmaf(x[u].z, wv.z, v);
+                            v = c2 ? v2 : v;
+                            const float v3 = __builtin_fmaf(x[u].w, wv.w, v);
+                            acc[u] = c3 ? v3 : v;
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < kZRowsRes; ++u)
+                        if (i0 + u < nr) stage[(i0 + u) * kLaneStride + lane] = acc[u];
+                }
+                __syncthreads();
+                for (int i = tid; i < nr; i += kDThreads) {
+                    float v[kWave];
+#pragma unroll
+                    for (int q = 0; q < kWave; q += 4) {
+                        const float4 p4 = *reinterpret_cast<const float4 *>(stage + i * kLaneStride + q);
+                        v[q] = p4.x;
+                        v[q + 1] = p4.y;
+                        v[q + 2] = p4.z;
+                        v[q + 3] = p4.w;
+                    }
+#pragma unroll
+                    for (int span = 1; span < kWave; span *= 2)
+#pragma unroll
+                        for (int q = 0; q < kWave; q += 2 * span) v[q] = v[q] + v[q + span];
+                    word_put(zw, h0 + i, word_pack(v[0], t));
+                }
+                __syncthreads();
+            }
+        } else {
+            for (int i = wave; i < rows; i += kDWaves) {
+                const float *row = xt + (int64_t)i * a.ldx;
+                float acc = 0.0f;
+                for (int g0 = lane; g0 < groups; g0 += kWave * kGUnroll) {
+                    float4 x[kGUnroll], wv[kGUnroll];
+#pragma unroll
+                    for (int q = 0; q < kGUnroll; ++q) {
+                        const int kk = 4 * (g0 + q * kWave);
+                        if (kk < cols) {
+                            wv[q] = *reinterpret_cast<const float4 *>(sw + kk);
+                            if (kk + 3 < cols) {
+                                x[q] = load4<VEC>(row + kk);
+                            } else {
+                                x[q] = make_float4(row[kk], row[std::min(kk + 1, cols - 1)],
+                                                   row[std::min(kk + 2, cols - 1)],
+                                                   row[std::min(kk + 3, cols - 1)]);
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int q = 0; q < kGUnroll; ++q) {
+                        const int kk = 4 * (g0 + q * kWave);
+                        if (kk < cols) {
+                            const bool c1 = kk + 1 < cols, c2 = kk + 2 < cols, c3 = kk + 3 < cols;
+                            float v = __builtin_fmaf(x[q].x, wv[q].x, acc);
+                            const float v1 = __builtin_fmaf(x[q].y, wv[q].y, v);
+                            v = c1 ? v1 : v;
+                            const float v2 = __builtin_fmaf(x[q].z, wv[q].z, v);
+                            v = c2 ? v2 : v;
+                            const float v3 = __builtin_fmaf(x[q].w, wv[q].w, v);
+                            acc = c3 ? v3 : v;
                         }
                     }
                 }
-            }
-#pragma unroll
-            for (int u = 0; u < kZRows; ++u) {
-                const int i = i0 + u;
-                if (i < rows) {  // uniform across the wave
-                    const float z = wave_sum64(acc[u]);
-                    if (lane == 0) word_put(zw, i, word_pack(z, t));
-                }
+                const float z = wave_sum64(acc);
+                if (lane == 0) word_put(zw, i, word_pack(z, t));
             }
         }
+    };
+
+    // in-order sum p = 0..count-1 of stage[p * stride + j], loads in batches
+    auto ordered_sum = [&](int j, int count, int stride) {
+        float acc = stage[j];
+        int p = 1;
+        for (; p + 8 <= count; p += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = stage[(p + u) * stride + j];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc = acc + v[u];
+        }
+        for (; p < count; ++p) acc = acc + stage[p * stride + j];
+        return acc;
     };
 
     dot_pass(0);
@@ -254,11 +338,8 @@ __global__ __launch_bounds__(kDThreads) void k_dense_gd(DenseArgs a) {
                     a.zw, [=](int e) { const int p = e / nr; return base + p * n + (e - p * nr); },
                     nr * a.C, t, stage, a.ctrl, a.timeout);
                 if (__syncthreads_or(!ok)) return;
-                for (int i = tid; i < nr; i += kDThreads) {
-                    float z = stage[i];
-                    for (int p = 1; p < a.C; ++p) z = z + stage[p * nr + i];
-                    ss[i0 + i] = sgd_scale<LOSS>(z, a.y[row0 + i0 + i], a.lr);
-                }
+                for (int i = tid; i < nr; i += kDThreads)
+                    ss[i0 + i] = sgd_scale<LOSS>(ordered_sum(i, a.C, nr), a.y[row0 + i0 + i], a.lr);
                 __syncthreads();
             }
         }
@@ -271,17 +352,25 @@ __global__ __launch_bounds__(kDThreads) void k_dense_gd(DenseArgs a) {
             for (int e = tid; e < nch * cols; e += kDThreads) {
                 const int h = e / cols, k = e - h * cols;
                 const int i1 = std::min(rows, (h + 1) * kRowChunk);
+                const float *xc = tile + k;
                 float acc = 0.0f;
-                for (int i = h * kRowChunk; i < i1; ++i)
-                    acc = __builtin_fmaf(ss[i], tile[i * a.cb + k], acc);
+                int i = h * kRowChunk;
+                for (; i + 8 <= i1; i += 8) {
+                    float x[8], sv[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        x[u] = xc[(i + u) * a.cb];
+                        sv[u] = ss[i + u];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) acc = __builtin_fmaf(sv[u], x[u], acc);
+                }
+                for (; i < i1; ++i) acc = __builtin_fmaf(ss[i], xc[i * a.cb], acc);
                 stage[e] = acc;
             }
             __syncthreads();
-            for (int k = tid; k < cols; k += kDThreads) {
-                float part = stage[k];
-                for (int h = 1; h < nch; ++h) part = part + stage[h * cols + k];
-                word_put(gw, k, word_pack(part, t));
-            }
+            for (int k = tid; k < cols; k += kDThreads)
+                word_put(gw, k, word_pack(ordered_sum(k, nch, cols), t));
             __syncthreads();
         } else {
             for (int g = tid; g < groups; g += kDThreads) {
@@ -341,11 +430,8 @@ __global__ __launch_bounds__(kDThreads) void k_dense_gd(DenseArgs a) {
                     a.gw, [=](int e) { const int p = e / nc; return base + p * d + (e - p * nc); },
                     nc * a.R, t, stage, a.ctrl, a.timeout);
                 if (__syncthreads_or(!ok)) return;
-                for (int k = tid; k < nc; k += kDThreads) {
-                    float G = stage[k];
-                    for (int p = 1; p < a.R; ++p) G = G + stage[p * nc + k];
-                    sw[k0 + k] = sw[k0 + k] - G;
-                }
+                for (int k = tid; k < nc; k += kDThreads)
+                    sw[k0 + k] = sw[k0 + k] - ordered_sum(k, a.R, nc);
                 __syncthreads();
             }
         }
