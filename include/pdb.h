@@ -241,7 +241,7 @@ int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t 
                     const pdb_levels *levels, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Device workspace (bytes) for pdb_stale_epoch: the control block, one
- * 64-bit word and two ints per stored entry.  Host-only arithmetic. */
+ * 64-bit word and three ints per stored entry.  Host-only arithmetic. */
 int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes);
 
 /* One epoch of bounded-delay SGD (Sec. 7: the Asynchronous Read Constraint
@@ -254,11 +254,19 @@ int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes);
  * features, w_f = fma(-s, x, w_f), on the value the previous writer left.
  * delay = 0 is pdb_sgd_epoch's result; delay >= n - 1 reads the initial
  * weights everywhere (pdb_batch_epoch with batch = n).  prev_nz: device,
- * [nnz], from pdb_schedule on the same CSR.  Sync-free over examples in index
- * order; finding each entry's read source takes up to `delay` steps back
- * along its feature.  ws: at least pdb_stale_workspace_bytes(nnz).
- * Asynchronous; a device error (watchdog) is reported by
- * pdb_workspace_status on ws. */
+ * [nnz], from pdb_schedule on the same CSR.  Finding each entry's read
+ * source takes up to `delay` steps back along its feature.  Two executions,
+ * bitwise the same result:
+ *   - windowed, one block: examples in windows of delay + 1, whose reads all
+ *     come from earlier windows; chosen when every window holds at most 2048
+ *     examples and 2048 stored entries and at most a quarter of the examples
+ *     share no feature with the example before them (PDB_STALE_MODE=1 forces
+ *     the sync-free execution, 2 the windowed one where windows fit);
+ *   - sync-free: examples in index order, each waiting on the words of its
+ *     read sources and previous writers.
+ * ws: at least pdb_stale_workspace_bytes(nnz).  Synchronous: it reads back
+ * the largest window's size to choose; a device error (watchdog) is reported
+ * by pdb_workspace_status on ws. */
 int pdb_stale_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
                     float lr, int loss, int64_t delay, const int32_t *prev_nz, void *ws,
                     size_t ws_bytes, hipStream_t stream);

@@ -59,11 +59,16 @@ def structured_problem(rows, loss, with_val, seed):
     return dict(row_ptr=row_ptr, col=col, val=val, y=y, n=n, d=d, lr=lr, loss=loss)
 
 
+STALE_MODES = ["2", "1"]  # windowed where the windows fit, sync-free
+
+
 @pytest.mark.parametrize("name", sorted(structured_cases()))
 @pytest.mark.parametrize("loss", [0, 1])
 @pytest.mark.parametrize("with_val", [True, False])
 @pytest.mark.parametrize("delay", [0, 1, 3, 17, 1000])
-def test_structured_stale_epochs(gpu, name, loss, with_val, delay):
+@pytest.mark.parametrize("mode", STALE_MODES)
+def test_structured_stale_epochs(gpu, name, loss, with_val, delay, mode, monkeypatch):
+    monkeypatch.setenv("PDB_STALE_MODE", mode)
     native = native_mod()
     g = structured_problem(structured_cases()[name], loss, with_val, delay + 7 * loss)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
@@ -72,7 +77,9 @@ def test_structured_stale_epochs(gpu, name, loss, with_val, delay):
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
 @pytest.mark.parametrize("delay", [0, 2, 8, 64])
-def test_random_stale_epochs(gpu, cfg, delay):
+@pytest.mark.parametrize("mode", STALE_MODES)
+def test_random_stale_epochs(gpu, cfg, delay, mode, monkeypatch):
+    monkeypatch.setenv("PDB_STALE_MODE", mode)
     native = native_mod()
     g = datagen.generate(cfg, n=8000, d=4000 if cfg == 4 else 500, seed=40 + delay)
     g["lr"] = np.float32(g["lr"] / 4)
@@ -111,8 +118,37 @@ def test_stale_errors(gpu):
     check_stale(native, gpu, g, lv, 1)
 
 
+def test_windows_too_large_fall_back(gpu, monkeypatch):
+    monkeypatch.setenv("PDB_STALE_MODE", "2")
+    # 60 entries per example: windows of 40 examples hold 2400 entries, over
+    # the block's 2048, so the sync-free execution runs; 30 fit
+    native = native_mod()
+    rows = [set(range(i % 7, i % 7 + 60)) for i in range(500)]
+    g = structured_problem(rows, 1, True, 3)
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    for delay in (29, 39):
+        check_stale(native, gpu, g, lv, delay)
+
+
+@pytest.mark.parametrize("mode", ["0", "2"])
+def test_empty_rows_and_window_edges(gpu, mode, monkeypatch):
+    monkeypatch.setenv("PDB_STALE_MODE", mode)
+    # empty examples, a last window shorter than delay + 1, one example
+    native = native_mod()
+    rows = [set(), {0, 1}, set(), {1, 2}, {2}, set(), {0, 2, 3}, {3}, set(), {1}, {0}]
+    for delay in (0, 1, 2, 3, 4, 10, 11, 50):
+        g = structured_problem(rows, 0, True, delay)
+        lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+        check_stale(native, gpu, g, lv, delay)
+    g = structured_problem([{5}], 1, False, 2)
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    check_stale(native, gpu, g, lv, 3)
+
+
 @pytest.mark.parametrize("cfg,delay", [(2, 8), (4, 8)])
 def test_full_size_stale(gpu, cfg, delay):
+    # the executions bench.py --delay 8 times (windowed on config 2, sync-free
+    # on config 4)
     native = native_mod()
     g = datagen.generate(cfg)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
