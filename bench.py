@@ -100,11 +100,11 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0, delay=-1):
         col = g["col"][:rp[-1]]
         t0 = time.perf_counter()
         if delay >= 0:
-            level, perm, level_ptr, L = oracle.schedule(rp, col, g["d"])
+            oracle.prev_writer(rp, col, g["d"])
             val = None if g["val"] is None else g["val"][:rp[-1]]
             oracle.stale_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
                                g["loss"], oracle.NATURAL, delay)
-            return time.perf_counter() - t0, int(rp[-1]), level
+            return time.perf_counter() - t0, int(rp[-1]), None
         if batch:
             level, perm, level_ptr, L = oracle.batch_schedule(rp, col, g["d"], batch)
             val = None if g["val"] is None else g["val"][:rp[-1]]
@@ -131,14 +131,15 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0, delay=-1):
     units = rows if mf else nnz_s
     res = {"value": units / t, "unit": "ratings/s" if mf else "nnz-updates/s", "cores": 1,
            "kind": "oracle",
-           "sample": "first %d of %d %s (%d stored entries), one-pass %slevels + grouping + "
-                     "natural-order %sepoch, %.1f s" % (
+           "sample": "first %d of %d %s (%d stored entries), %s + natural-order %sepoch, "
+                     "%.1f s" % (
                          rows, n, "ratings" if mf else "examples", nnz_s,
-                         "batch " if batch else "",
+                         "previous writers" if delay >= 0 else
+                         "one-pass %slevels + grouping" % ("batch " if batch else ""),
                          "mini-batch (B=%d) " % batch if batch else
                          ("delay-%d " % delay if delay >= 0 else ""), t),
            "host_cpu": platform.processor() or platform.machine()}
-    if gpu_levels is not None:
+    if gpu_levels is not None and level is not None:
         k = len(level) if batch else rows
         res["sample_levels_equal_gpu"] = bool(np.array_equal(gpu_levels[:k], level[:k]))
     return res
@@ -323,6 +324,7 @@ def main():
     n, d, nnz = g["n"], g["d"], g["nnz"]
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None if mf else g["val"], dev)
     bt = native.Batches(n, nnz, batch, dev) if batch else None
+    prev_row = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev) if delay >= 0 else None
     lv = native.Levels(bt.nb if batch else n, nnz, dev)
     ws_s = native.workspace(native.pdb_schedule_workspace_bytes(n, d, nnz), dev)
     ws_e = native.workspace(
@@ -352,6 +354,9 @@ def main():
         s0.record(stream)
         if batch:
             info = native.pdb_batch_schedule(csr, n, d, bt, lv, args.method, ws=ws_s)
+        elif delay >= 0:
+            # bounded delay needs only each entry's previous writer
+            native.pdb_prev_writer(csr, n, d, prev_row, lv.prev_nz, ws=ws_s)
         else:
             info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s)
         s1.record(stream)
@@ -412,7 +417,8 @@ def main():
         kernel = "k_batch_syncfree (mini-batch epoch)" if mode != 1 else \
             "k_batch_levels (mini-batch epoch)"
     elif delay >= 0:
-        kernel = "k_stale_epoch (bounded-delay epoch)"
+        kernel = ("k_stale_window or k_stale_epoch (bounded-delay epoch; the library picks "
+                  "per call, windowed on chain-like inputs)")
     elif syncfree:
         kernel = "k_mf_syncfree (epoch)" if mf else "k_sgd_syncfree (epoch)"
     else:
@@ -437,7 +443,8 @@ def main():
                                                 ", mini-batches of %d" % batch if batch else "",
                                                 ", delay %d" % delay if delay >= 0 else ""),
                    "n": n, "d": d, "nnz": nnz,
-                   "seed": g["seed"], "levels": L, "max_level_width": lv.max_width_host,
+                   "seed": g["seed"], "levels": None if delay >= 0 else L,
+                   "max_level_width": None if delay >= 0 else lv.max_width_host,
                    "schedule_method": info.get("method_used"),
                    "schedule_rounds": info.get("rounds")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -447,12 +454,13 @@ def main():
                      # levels run one after another: the epoch is a dependent
                      # chain of L levels, so the time per level is the figure
                      # that bounds it when levels are narrow
-                     "levels": L, "ns_per_level": ep * 1e6 / max(L, 1)},
+                     **({"levels": L, "ns_per_level": ep * 1e6 / max(L, 1)} if delay < 0 else {})},
         "schedule_ms": trimmed_mean([a.elapsed_time(b) for a, b in sched_ms]),
         "epoch_ms": ep,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget, lv.level.cpu().numpy(),
+        out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget,
+                                           None if delay >= 0 else lv.level.cpu().numpy(),
                                            batch, delay)
     print(json.dumps(out))
 
