@@ -72,15 +72,20 @@ typedef enum pdb_status {
 typedef enum pdb_loss { PDB_LOGISTIC = 0, PDB_SQUARED = 1 } pdb_loss;
 
 typedef enum pdb_sched_method {
-    PDB_SCHED_AUTO = 0,      /* chain, else spine when it applies, else dataflow */
+    PDB_SCHED_AUTO = 0,      /* chain, else spine when it applies, else the walk on chain-like
+                                inputs (at most a quarter of the examples share no feature
+                                with the one before them), else dataflow */
     PDB_SCHED_CHAINSCAN = 1, /* chain-scan relaxation until the fixed point */
     PDB_SCHED_DATAFLOW = 2,  /* each example waits for its previous writers' levels */
     PDB_SCHED_SPINE = 3,     /* the most frequent feature's rows as a spine: applies when that
                                 feature misses at most 1024 rows whose entries number at most
                                 4096; otherwise dataflow runs (method_used says which) */
-    PDB_SCHED_CHAIN = 4      /* every example conflicts with the one before it: levels are
+    PDB_SCHED_CHAIN = 4,     /* every example conflicts with the one before it: levels are
                                 1..n, checked in one pass over the previous writers; otherwise
                                 dataflow runs.  Auto tries this first. */
+    PDB_SCHED_WALK = 5       /* one block walks the rows in order, windows of rows staged in
+                                LDS; dataflow runs instead when a row holds more than 16384
+                                entries */
 } pdb_sched_method;
 
 /* Sparse examples in CSR form (Definition 1: the immutable data set D). */

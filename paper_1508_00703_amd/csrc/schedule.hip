@@ -570,6 +570,147 @@ __global__ __launch_bounds__(kBlock) void k_max_level(const int32_t *__restrict_
     if (lane_id() == 0 && m > 0) atomicMax(&ctrl->max_level, m);
 }
 
+// ---- K3 walk ---------------------------------------------------------------
+// Chain-like inputs, where most examples share a feature with the one before
+// them: the dependency chain is about as long as the data, so one block
+// walks the rows in order instead of crossing CUs per row.  Rows go in
+// windows of at most kWalkRows rows and kWalkEnt entries.
+//
+// A run is a maximal stretch of rows each of which has the row before it as
+// a previous writer.  Along a run levels rise by at least one per row, so a
+// writer inside the run other than the row just before can never set a
+// level: for row i of a run starting at a, with M_i the largest level among
+// its writers before a,
+//   level(a) = 1 + M_a,  level(i) = max(level(i-1), M_i) + 1,
+// that is level(i) = i + 1 + max over a <= t <= i of (M_t - t): a prefix
+// maximum.  The block stages a window (per entry: a writer before the window
+// is folded into its row's M at once, from the levels already written or,
+// for the window before, from LDS; a writer in the window is kept as a row
+// index; the writer just before marks the row as continuing a run).  Then
+// the window's runs go in order: the block folds the levels of writers in
+// earlier runs into the run's M (one thread per entry), and wave 0 turns
+// them into levels by a prefix maximum over 64 rows at a time.
+constexpr int kWalkRows = 512;
+constexpr int kWalkEnt = 16384;
+constexpr int kWalkThreads = 1024;
+
+struct WalkShared {
+    int16_t ref[kWalkEnt];   // a writer in the window: its row; -1: none or already folded
+    int16_t row[kWalkEnt];   // the entry's row in the window
+    int16_t runs[kWalkRows + 1];  // first rows of the runs, then nr
+    int nruns;
+    int m[kWalkRows];        // largest level among the row's writers before the window
+    int chain[kWalkRows];    // 1 when the row just before is one of the row's writers
+    int rp[kWalkRows + 1];   // row bounds relative to the window's first entry
+    int lvl[2][kWalkRows];   // levels of this window and the previous one
+    int nrows;
+};
+
+__device__ __forceinline__ int wave_prefix_max(int v) {
+    const int l = lane_id();
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int t = __shfl_up(v, off);
+        if (l >= off) v = max(v, t);
+    }
+    return v;
+}
+
+__global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__restrict__ row_ptr,
+                                                              int64_t n,
+                                                              const int32_t *__restrict__ prow,
+                                                              const int32_t *__restrict__ row_idx,
+                                                              int32_t *__restrict__ level,
+                                                              Ctrl *ctrl) {
+    __shared__ WalkShared S;
+    const int tid = threadIdx.x, lane = lane_id();
+    constexpr int kNone = INT_MIN / 2;
+    int64_t r0 = 0, r0p = 0;  // first rows of this and the previous window
+    int cur = 0;
+    while (r0 < n) {
+        // the window: as many rows (up to kWalkRows) as fit kWalkEnt entries
+        const int64_t q0 = row_ptr[r0];
+        if (tid == 0) S.nrows = 0;
+        __syncthreads();
+        for (int t = tid; t <= kWalkRows; t += kWalkThreads) {
+            const int64_t rel = row_ptr[min(r0 + t, n)] - q0;
+            S.rp[t] = (int)min<int64_t>(rel, INT_MAX);
+            if (t >= 1 && r0 + t <= n && rel <= kWalkEnt) atomicMax(&S.nrows, t);
+            if (t < kWalkRows) {
+                S.m[t] = 0;
+                S.chain[t] = 0;
+            }
+        }
+        __syncthreads();
+        const int nr = S.nrows;
+        if (nr == 0) {  // one row longer than a window: the caller uses another method
+            if (tid == 0) ctrl->bad = 1;
+            return;
+        }
+        const int E = S.rp[nr];
+        int *lc = S.lvl[cur];
+        const int *lp = S.lvl[cur ^ 1];
+        // stage the window's entries
+        for (int e = tid; e < E; e += kWalkThreads) {
+            const int32_t pr = prow[q0 + e];
+            int16_t ref = -1;
+            const int row = (int)(row_idx[q0 + e] - r0);
+            S.row[e] = (int16_t)row;
+            if (pr >= 0) {
+                if (pr >= r0) {
+                    if (pr == r0 + row - 1) S.chain[row] = 1;
+                    else ref = (int16_t)(pr - r0);
+                } else {
+                    atomicMax(&S.m[row], pr >= r0p ? lp[pr - r0p] : level[pr]);
+                }
+            }
+            S.ref[e] = ref;
+        }
+        __syncthreads();
+        // the runs' first rows (wave 0)
+        if (tid < kWave) {
+            int cnt = 0;
+            for (int c0 = 0; c0 < nr; c0 += kWave) {
+                const int j = c0 + lane;
+                const bool st = j < nr && S.chain[j] == 0;
+                const unsigned long long m = __ballot(st);
+                if (st) S.runs[cnt + (int)lanes_below(m)] = (int16_t)j;
+                cnt += __popcll(m);
+            }
+            if (lane == 0) {
+                S.runs[cnt] = (int16_t)nr;
+                S.nruns = cnt;
+            }
+        }
+        __syncthreads();
+        const int nruns = S.nruns;
+        for (int k = 0; k < nruns; ++k) {
+            const int a = S.runs[k], b = S.runs[k + 1];
+            // writers in earlier runs of the window
+            for (int e = S.rp[a] + tid; e < S.rp[b]; e += kWalkThreads) {
+                const int r = S.ref[e];
+                if (r >= 0 && r < a) atomicMax(&S.m[S.row[e]], lc[r]);
+            }
+            __syncthreads();
+            // level(j) = j + 1 + max over a <= t <= j of (M_t - t)
+            if (tid < kWave) {
+                int carry = kNone;
+                for (int c0 = a; c0 < b; c0 += kWave) {
+                    const int j = c0 + lane;
+                    const int pm = max(wave_prefix_max(j < b ? S.m[j] - j : kNone), carry);
+                    if (j < b) lc[j] = j + 1 + pm;
+                    carry = __shfl(pm, kWave - 1);
+                }
+            }
+            __syncthreads();
+        }
+        for (int i = tid; i < nr; i += kWalkThreads) level[r0 + i] = lc[i];
+        r0p = r0;
+        r0 += nr;
+        cur ^= 1;
+    }
+}
+
 // ---- K3 spine --------------------------------------------------------------
 // When one feature f* is held by all rows but a few (the exceptional rows E),
 // the rows holding it form a spine c_0 < c_1 < ... < c_{K-1}.  Consecutive
@@ -1103,7 +1244,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     if (rc != PDB_OK) return rc;
     if (!lv || !lv->level_ptr || !lv->n_levels || (n > 0 && (!lv->level || !lv->perm)))
         return PDB_ERR_INVALID_ARG;
-    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_CHAIN) return PDB_ERR_INVALID_ARG;
+    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_WALK) return PDB_ERR_INVALID_ARG;
     const int64_t nnz = csr->nnz;
     Ctrl host{};
     k_ctrl_init<<<1, 64, 0, s>>>(w.ctrl);
@@ -1130,6 +1271,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
 
     // a chain (every example conflicts with the one before it) is solved
     // outright; auto tries it first
+    bool chain_like = false;
     if (method == PDB_SCHED_AUTO || method == PDB_SCHED_CHAIN) {
         k_chain_check<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n, pn,
                                                                             w.ctrl);
@@ -1147,10 +1289,12 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
             return PDB_OK;
         }
         if (method == PDB_SCHED_CHAIN) method = PDB_SCHED_DATAFLOW;
+        // most examples conflict with their predecessor: the walk pays
+        chain_like = 4 * (int64_t)host.chain_breaks <= n;
     }
 
     // which method: the spine when the most frequent feature misses at most
-    // kSpineMaxE rows, else dataflow
+    // kSpineMaxE rows, else the walk on chain-like inputs, else dataflow
     int use = method;
     int rounds = 0;
     int64_t top_count = 0, top_f = 0;
@@ -1162,7 +1306,8 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         top_count = (int64_t)(host.top_feature >> 32);
         top_f = (int64_t)(0xFFFFFFFFull - (host.top_feature & 0xFFFFFFFFull));
         const bool fits = top_count > 0 && n - top_count <= kSpineMaxE;
-        use = fits ? PDB_SCHED_SPINE : PDB_SCHED_DATAFLOW;
+        use = fits ? PDB_SCHED_SPINE
+                   : ((method == PDB_SCHED_AUTO && chain_like) ? PDB_SCHED_WALK : PDB_SCHED_DATAFLOW);
     }
 
     if (use == PDB_SCHED_SPINE) {
@@ -1191,6 +1336,20 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         } else {
             use = PDB_SCHED_DATAFLOW;  // too many exceptional rows or entries
         }
+    }
+
+    if (use == PDB_SCHED_WALK) {
+        if (nnz > 0) {
+            k_prev_row<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(pn, nnz, w.row_idx,
+                                                                        w.cand);
+            PDB_LAUNCHED();
+        }
+        k_levels_walk<<<1, kWalkThreads, 0, s>>>(csr->row_ptr, n, w.cand, w.row_idx, lv->level,
+                                                 w.ctrl);
+        PDB_LAUNCHED();
+        rc = read_ctrl(w.ctrl, &host, s);
+        if (rc != PDB_OK) return rc;
+        if (host.bad) use = PDB_SCHED_DATAFLOW;  // a row longer than a window
     }
 
     if (use == PDB_SCHED_CHAINSCAN) {

@@ -11,7 +11,7 @@ from pdbtest import check_mf, check_schedule, check_sgd, csr_from_rows, gpu_sche
 
 pytestmark = pytest.mark.gpu
 
-METHODS = [0, 1, 2, 3, 4]  # auto, chain-scan, dataflow, spine, chain
+METHODS = [0, 1, 2, 3, 4, 5]  # auto, chain-scan, dataflow, spine, chain, walk
 
 
 def native_mod():
@@ -366,6 +366,41 @@ def test_spine_selection_and_fallback(gpu):
     row_ptr, col = csr_from_rows(rows)
     d = int(col.max()) + 1
     _, info = check_schedule(native, gpu, row_ptr, col, d, 3)
+    assert info["method_used"] == 2
+
+
+def test_walk_selection_windows_and_fallback(gpu):
+    """Auto walks chain-like inputs (a few examples share nothing with their
+    predecessor); the walk's windows of 512 rows see writers in the same
+    window, the one before and further back.  A row longer than a window
+    falls back to dataflow.  Levels are exact each time."""
+    native = native_mod()
+    rng = np.random.default_rng(3)
+    n = 5000
+    rows = []
+    for i in range(n):
+        # features 0 and 1 take turns chaining runs of 700 rows, so no one
+        # feature covers all rows but a few (no spine)
+        r = {(i // 700) % 2} if i % 97 else {2 + i % 5}
+        r |= {10 + int(x) for x in rng.integers(0, 3000, size=rng.integers(0, 6))}
+        if i % 700 == 3:
+            r.add(5000)                                # a writer many windows back
+        rows.append(r)
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1
+    lv, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert info["method_used"] == 5
+    lv, info = check_schedule(native, gpu, row_ptr, col, d, 5)
+    assert info["method_used"] == 5
+    # windows cut by entries, not rows: rows of 100 entries (163 per window)
+    wide = [set(range(i % 3, i % 3 + 100)) | {1000 + i} for i in range(1200)]
+    row_ptr, col = csr_from_rows(wide)
+    lv, info = check_schedule(native, gpu, row_ptr, col, int(col.max()) + 1, 5)
+    assert info["method_used"] == 5
+    # a row of 20000 entries does not fit a window
+    big = [{0, 1}, set(range(2, 20002)), {1, 3}, {3, 7}]
+    row_ptr, col = csr_from_rows(big)
+    lv, info = check_schedule(native, gpu, row_ptr, col, int(col.max()) + 1, 5)
     assert info["method_used"] == 2
 
 
