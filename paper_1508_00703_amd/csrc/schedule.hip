@@ -593,6 +593,7 @@ __global__ __launch_bounds__(kBlock) void k_max_level(const int32_t *__restrict_
 constexpr int kWalkRows = 512;
 constexpr int kWalkEnt = 16384;
 constexpr int kWalkThreads = 1024;
+constexpr int kWalkPer = kWalkEnt / kWalkThreads;  // entries per thread
 
 struct WalkShared {
     int16_t ref[kWalkEnt];   // a writer in the window: its row; -1: none or already folded
@@ -650,21 +651,36 @@ __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__r
         const int E = S.rp[nr];
         int *lc = S.lvl[cur];
         const int *lp = S.lvl[cur ^ 1];
-        // stage the window's entries
-        for (int e = tid; e < E; e += kWalkThreads) {
-            const int32_t pr = prow[q0 + e];
-            int16_t ref = -1;
-            const int row = (int)(row_idx[q0 + e] - r0);
-            S.row[e] = (int16_t)row;
-            if (pr >= 0) {
-                if (pr >= r0) {
-                    if (pr == r0 + row - 1) S.chain[row] = 1;
-                    else ref = (int16_t)(pr - r0);
-                } else {
-                    atomicMax(&S.m[row], pr >= r0p ? lp[pr - r0p] : level[pr]);
+        // stage the window's entries: every thread's loads in flight at once
+        // (writers, rows, then the levels of writers before the window)
+        {
+            int32_t pr[kWalkPer], row[kWalkPer], lvf[kWalkPer];
+#pragma unroll
+            for (int u = 0; u < kWalkPer; ++u) {
+                const int e = tid + u * kWalkThreads;
+                const int64_t q = q0 + min(e, max(E - 1, 0));
+                pr[u] = e < E ? prow[q] : -1;
+                row[u] = e < E ? (int)(row_idx[q] - r0) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kWalkPer; ++u)
+                lvf[u] = (pr[u] >= 0 && pr[u] < r0p) ? level[pr[u]] : 0;
+#pragma unroll
+            for (int u = 0; u < kWalkPer; ++u) {
+                const int e = tid + u * kWalkThreads;
+                if (e < E) {
+                    int16_t ref = -1;
+                    S.row[e] = (int16_t)row[u];
+                    const int32_t p = pr[u];
+                    if (p >= r0) {
+                        if (p == r0 + row[u] - 1) S.chain[row[u]] = 1;
+                        else ref = (int16_t)(p - r0);
+                    } else if (p >= 0) {
+                        atomicMax(&S.m[row[u]], p >= r0p ? lp[p - r0p] : lvf[u]);
+                    }
+                    S.ref[e] = ref;
                 }
             }
-            S.ref[e] = ref;
         }
         __syncthreads();
         // the runs' first rows (wave 0)
