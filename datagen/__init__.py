@@ -140,7 +140,7 @@ class DenseConfig:
 
 
 # Dense full-batch gradient descent (the linear-regression experiments of
-# Sec. 6.1-6.2): 960 numerical features over 5000 examples, and the widest of
+# Sec. 6.1-6.2): 960 features over 5000 examples, and the widest of
 # a sweep over the number of features at 500 examples.  The step sizes keep
 # the summed-gradient iteration contractive: lr times the largest eigenvalue
 # of X^T X, about (sqrt(n) + sqrt(d))^2, stays near 1.
