@@ -20,7 +20,10 @@
 // levels, while the other blocks wait at the next device barrier.
 //
 // Runs of width-1 levels are a dependent chain: example t+1 reads what
-// example t wrote.  There one wave runs the chain and the three other waves
+// example t wrote.  Runs of levels at most `chain_width` wide (default 4) go
+// the same way, their examples one after another in level order, which is a
+// sequential order of them (Theorem 2).  There one wave runs the chain and
+// the three other waves
 // of the block stage upcoming examples (columns, values, and the CSR index
 // of each entry's previous writer) into LDS.  Weights of features below
 // `hot` live in LDS for the whole run; a feature that example t just wrote is
@@ -578,10 +581,12 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
     return stop;
 }
 
-// Runs perm[e_beg .. e_end) (consecutive width-1 levels) with the whole block.
+// Runs perm[e_beg .. e_end) (consecutive narrow levels, in level order: a
+// sequential order of their examples) with the whole block.  width1: every
+// level of the run has one example, so the examples have increasing indices.
 template <int LOSS, bool VAL>
 __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_end, int hot,
-                          int64_t d, Ctrl *ctrl) {
+                          int64_t d, Ctrl *ctrl, bool width1) {
     __shared__ ChainShared S;
     __shared__ int64_t s_done;
     const int wave = wave_in_block();
@@ -590,7 +595,7 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
         // examples of a width-1 run have increasing indices: the run is a range
         // of consecutive examples exactly when its ends differ by its length - 1
         const int64_t r_first = op.perm[pos], r_last = op.perm[e_end - 1];
-        const int64_t dense_r0 = (r_last - r_first == e_end - 1 - pos) ? r_first : -1;
+        const int64_t dense_r0 = (width1 && r_last - r_first == e_end - 1 - pos) ? r_first : -1;
         for (int i = threadIdx.x; i < hot; i += kBlock) g_wcache[i] = op.w[i];
         for (int i = threadIdx.x; i < kRB; i += kBlock) S.seq[i] = INT_MIN;
         if (threadIdx.x < 4) {
@@ -640,11 +645,45 @@ __device__ int64_t find_run_end(int64_t l, int64_t L, const int64_t *level_ptr,
     return L;
 }
 
+// first level after l that is wider than cw or starts kChainMin levels of
+// width 1 (L if none); block-uniform.  Bit i of a wave's 128-bit mask is the
+// width-1 test of level base + i; after the shifts it says whether the 32
+// levels from base + i all have width 1.
+static_assert(kChainMin == 32, "narrow_run_end tests runs of 32 levels");
+__device__ int64_t narrow_run_end(int64_t l, int64_t L, const int64_t *level_ptr, int64_t cw) {
+    __shared__ int64_t s_w[kWavesPerBlock];
+    const int wave = wave_in_block();
+    for (int64_t start = l + 1; start < L; start += kBlock) {
+        const int64_t c = start + threadIdx.x;
+        const int64_t w0 = c < L ? level_ptr[c + 1] - level_ptr[c] : 0;
+        const int64_t c1 = c + kWave;
+        const int64_t w1 = c1 < L ? level_ptr[c1 + 1] - level_ptr[c1] : 0;
+        const unsigned long long wide = __ballot(c < L && w0 > cw);
+        unsigned __int128 m = ((unsigned __int128)__ballot(w1 == 1) << 64) | __ballot(w0 == 1);
+        m &= m >> 1;
+        m &= m >> 2;
+        m &= m >> 4;
+        m &= m >> 8;
+        m &= m >> 16;
+        const unsigned long long hit = wide | (unsigned long long)m;
+        if (lane_id() == 0)
+            s_w[wave] = hit ? start + wave * kWave + (__ffsll(hit) - 1) : INT64_MAX;
+        __syncthreads();
+        int64_t mn = INT64_MAX;
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) mn = min(mn, s_w[w]);
+        __syncthreads();
+        if (mn != INT64_MAX) return min(mn, L);
+    }
+    return L;
+}
+
 template <class Op>
 __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *level_ptr,
                                                          const int32_t *n_levels,
                                                          int64_t thin_max, int hot, int64_t d,
-                                                         Ctrl *ctrl, int64_t timeout) {
+                                                         Ctrl *ctrl, int64_t timeout,
+                                                         int64_t chain_width) {
     constexpr int U = Op::kUnits;
     const int64_t L = *n_levels;
     const int wave = wave_in_block();
@@ -663,14 +702,29 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
                     end = level_ptr[l2 + 1];
                     if (!single && end - beg > thin_max) break;
                     if constexpr (Op::kChain) {
-                        if (hot >= 0 && end - beg == 1 && l2 >= no_chain_before) {
+                        // a run of narrow levels goes through the pipeline one
+                        // example after another (a sequential order of them)
+                        // when it holds enough examples
+                        if (hot >= 0 && end - beg <= chain_width && l2 >= no_chain_before) {
+                            // a long run of width-1 levels first (its examples
+                            // may be consecutive rows); else narrow levels up
+                            // to the next such run or wider level
                             const int64_t l3 = find_run_end(l2, L, level_ptr, 1);
                             if (l3 - l2 >= kChainMin) {
-                                chain_run(op, beg, level_ptr[l3], hot, d, ctrl);
+                                chain_run(op, beg, level_ptr[l3], hot, d, ctrl, true);
                                 l2 = l3;
                                 continue;
                             }
-                            no_chain_before = l3;
+                            int64_t l4 = l3;
+                            if (chain_width > 1) {
+                                l4 = narrow_run_end(l2, L, level_ptr, chain_width);
+                                if (level_ptr[l4] - beg >= kChainMin) {
+                                    chain_run(op, beg, level_ptr[l4], hot, d, ctrl, false);
+                                    l2 = l4;
+                                    continue;
+                                }
+                            }
+                            no_chain_before = max(l3, l4);
                         }
                     }
                     if (end - beg <= U) {
@@ -735,6 +789,10 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
     // cap on the number of weights cached in LDS by the width-1 pipeline
     const int64_t thin = std::max<int64_t>(env_setting("PDB_THIN_MAX", 16), 1);
     const int64_t hot_cap = env_setting("PDB_HOT_FEATURES", -1);
+    // widest level a pipeline run may include: a level of w examples costs w
+    // pipeline steps (about 140 ns each) instead of one block-barrier level
+    // (about 650 ns)
+    const int64_t chain_width = std::max<int64_t>(env_setting("PDB_CHAIN_WIDTH", 4), 1);
     const int64_t timeout = spin_timeout_ticks();
     k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
     PDB_LAUNCHED();
@@ -770,13 +828,13 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
     const int32_t *n_levels = lv->n_levels;
     if (grid == 1) {
         k_levels_apply<Op><<<1, kBlock, lds, s>>>(o, level_ptr, n_levels, thin, hot, d, ctrl,
-                                                  timeout);
+                                                  timeout, chain_width);
         PDB_LAUNCHED();
     } else {
-        int64_t thin_arg = thin, to = timeout;
+        int64_t thin_arg = thin, to = timeout, cw = chain_width;
         int hot_arg = hot;
         int64_t d_arg = d;
-        void *args[] = {&o, &level_ptr, &n_levels, &thin_arg, &hot_arg, &d_arg, &ctrl, &to};
+        void *args[] = {&o, &level_ptr, &n_levels, &thin_arg, &hot_arg, &d_arg, &ctrl, &to, &cw};
         PDB_HIP(hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBlock), args, lds, s));
     }
     return PDB_OK;

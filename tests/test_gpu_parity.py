@@ -214,16 +214,50 @@ def test_bad_csr_and_arguments(gpu):
 
 @pytest.mark.parametrize("hot", ["0", "5", "64", None])
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_width1_pipeline_hot_and_cold(gpu, cfg, hot, monkeypatch):
-    """Runs of width-1 levels through the staged pipeline, with the LDS weight
-    cache shrunk so that cold features (ring, prefetch, forwarding) appear."""
+@pytest.mark.parametrize("width", ["1", "4", "16"])
+def test_width1_pipeline_hot_and_cold(gpu, cfg, hot, width, monkeypatch):
+    """Runs of narrow levels (at most `width` examples each) through the
+    staged pipeline, with the LDS weight cache shrunk so that cold features
+    (ring, prefetch, forwarding) appear."""
     if hot is not None:
         monkeypatch.setenv("PDB_HOT_FEATURES", hot)
+    monkeypatch.setenv("PDB_CHAIN_WIDTH", width)
     native = native_mod()
     g = datagen.generate(cfg, **SCALED[cfg])
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
     assert lv.prev_nz is not None
     check_sgd(native, gpu, g, lv)
+
+
+@pytest.mark.parametrize("width", ["2", "4", "8"])
+@pytest.mark.parametrize("hot", ["0", None])
+def test_pipeline_runs_of_narrow_levels(gpu, width, hot, monkeypatch):
+    """Levels of 1 to 5 examples (disjoint pairs and triples between shared
+    features), with consecutive rows and without: the pipeline takes the
+    examples of a run in level order, and the result is the sequential one."""
+    if hot is not None:
+        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
+    monkeypatch.setenv("PDB_CHAIN_WIDTH", width)
+    native = native_mod()
+    rng = np.random.default_rng(int(width))
+    rows = []
+    for b in range(150):
+        base, m = 100 * b + 10, 1 + b % 5
+        rows.append({0, base})                                  # width 1
+        rows.append({0} | {base + 1 + j for j in range(m)})     # width 1
+        rows += [{base + 1 + j, base + 50 + j} for j in range(m)]  # one level of m
+        rows.append({0, base + 50, base + 50 + m - 1})          # width 1
+        if b % 7 == 3:
+            rows = rows[:-1] + [set()] + rows[-1:]              # an empty example (level 1)
+    row_ptr, col = csr_from_rows(rows)
+    n, d = len(rows), int(col.max()) + 1
+    val = (0.5 * rng.normal(size=len(col))).astype(np.float32)
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=0, lr=np.float32(0.05), val=val,
+             y=np.sign(rng.normal(size=n)).astype(np.float32))
+    lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
+    widths = set(np.diff(lv.level_ptr.cpu().numpy()[:lv.L_host + 1]).tolist())
+    assert {1, 2, 3, 4, 5} <= widths
+    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
 
 
 def test_plain_path_matches_pipeline(gpu, monkeypatch):
