@@ -401,7 +401,7 @@ int launch_stale(const pdb_csr *csr, const float *labels, int64_t n, float *w, f
     // examples at once.  Read back: this call synchronises the stream.
     const char *mode_env = getenv("PDB_STALE_MODE");
     const int mode = mode_env ? atoi(mode_env) : 0;
-    const int64_t W = std::min<int64_t>(delay + 1, std::max<int64_t>(n, 1));
+    const int64_t W = delay >= n ? std::max<int64_t>(n, 1) : delay + 1;  // no overflow at huge delays
     bool windowed = false;
     if (mode != 1 && W <= kWinCap) {
         k_window_max<<<grid_for(cdiv(n, W), kBlock, 4096), kBlock, 0, s>>>(csr->row_ptr, n, W,

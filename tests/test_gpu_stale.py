@@ -143,6 +143,10 @@ def test_empty_rows_and_window_edges(gpu, mode, monkeypatch):
     g = structured_problem([{5}], 1, False, 2)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
     check_stale(native, gpu, g, lv, 3)
+    # the largest delay: every read at the initial weights
+    g = structured_problem(rows, 0, True, 9)
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    check_stale(native, gpu, g, lv, 2 ** 63 - 1)
 
 
 @pytest.mark.parametrize("cfg,delay", [(2, 8), (4, 8)])
