@@ -849,6 +849,39 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
 // One word carries both, so a single 64-bit access is the whole handshake.
 // The earliest unfinished example never waits for a later one, so the grid
 // always makes progress.
+
+// Polls two words per lane as word_wait_wave does one (want0/want1 say which
+// this lane needs); both polls are in flight together every round.
+__device__ __forceinline__ bool word_wait_wave2(unsigned long long *base, bool want0, int64_t idx0,
+                                                int tag0, unsigned long long *out0, bool want1,
+                                                int64_t idx1, int tag1, unsigned long long *out1,
+                                                Ctrl *ctrl, int64_t timeout) {
+    bool ready0 = !want0, ready1 = !want1;
+    int64_t t0 = 0;
+    for (int round = 0;; ++round) {
+        unsigned long long v0 = 0, v1 = 0;
+        if (!ready0) v0 = word_get(base, idx0);
+        if (!ready1) v1 = word_get(base, idx1);
+        if (!ready0 && word_tag(v0) == tag0) {
+            *out0 = v0;
+            ready0 = true;
+        }
+        if (!ready1 && word_tag(v1) == tag1) {
+            *out1 = v1;
+            ready1 = true;
+        }
+        if (__ballot(!(ready0 && ready1)) == 0ull) return true;
+        if (round == 0) t0 = now_ticks();
+        if (aborted(ctrl)) return false;
+        if (now_ticks() - t0 > timeout) {
+            record_error(ctrl, DERR_WAIT_TIMEOUT);
+            return false;
+        }
+        word_backoff(round);
+        __asm__ __volatile__("" ::: "memory");  // the next round loads again
+    }
+}
+
 constexpr int kSyncB = 4;  // examples per ticket, run in order by one wave
 
 __global__ void k_wv_in(const float *__restrict__ w, unsigned long long *__restrict__ wv,
@@ -896,6 +929,25 @@ __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
                 const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
                 if (lane < m)
                     word_put(wv, c, word_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)));
+            } else if (m <= 2 * kWave) {
+                // two entries per lane: every load, and every poll, in flight
+                // together; the new weights come from the values the wait read
+                // (nothing else writes these features before this example does)
+                const int k1 = kWave + lane;
+                const bool l1 = k1 < m;
+                const int c0 = op.col[b + lane], pn0 = op.prev_nz[b + lane];
+                const int c1 = l1 ? op.col[b + k1] : 0, pn1 = l1 ? op.prev_nz[b + k1] : -1;
+                const float x0 = VAL ? op.val[b + lane] : 1.0f;
+                const float x1 = (VAL && l1) ? op.val[b + k1] : 1.0f;
+                unsigned long long v0 = 0, v1 = 0;
+                if (!word_wait_wave2(wv, true, c0, pn0, &v0, l1, c1, pn1, &v1, ctrl, timeout))
+                    return;
+                const float w0 = word_value(v0), w1 = word_value(v1);
+                float acc = __builtin_fmaf(w0, x0, 0.0f);
+                if (l1) acc = __builtin_fmaf(w1, x1, acc);
+                const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
+                word_put(wv, c0, word_pack(__builtin_fmaf(-s, x0, w0), (int)(b + lane)));
+                if (l1) word_put(wv, c1, word_pack(__builtin_fmaf(-s, x1, w1), (int)(b + k1)));
             } else {
                 float acc = 0.0f;
                 for (int k0 = 0; k0 < m; k0 += kWave) {
