@@ -882,7 +882,7 @@ __device__ __forceinline__ bool word_wait_wave2(unsigned long long *base, bool w
     }
 }
 
-constexpr int kSyncB = 4;  // examples per ticket, run in order by one wave
+constexpr int kSyncB = 1;  // consecutive examples per ticket, run in order by one wave
 
 __global__ void k_wv_in(const float *__restrict__ w, unsigned long long *__restrict__ wv,
                         int64_t d) {
@@ -898,56 +898,73 @@ __global__ void k_wv_out(const unsigned long long *__restrict__ wv, float *__res
         w[f] = word_value(wv[f]);
 }
 
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)v, l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)((uint64_t)v >> 32), l);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Examples are dealt to the waves in turn: with W waves in the grid, wave k
+// runs tickets k, k + W, k + 2W, ... of kSyncB consecutive examples each, in
+// order.  The grid is launched cooperatively (all of it resident), so the
+// earliest unfinished example is always the one its wave is working on, and
+// it waits only on earlier examples, all finished: the grid always makes
+// progress.  No shared counter hands out the work: requests to one
+// contended device-scope counter are served about 200 ns apart, which would
+// bound the epoch at that much per ticket.  Everything of a ticket that does
+// not depend on earlier examples is loaded when it starts: row bounds,
+// labels, and the entries (column, previous writer, value) of every example
+// of up to 2 x 64 entries.
 template <int LOSS, bool VAL>
 __global__ __launch_bounds__(kBlock) void k_sgd_syncfree(SgdOp<LOSS, VAL> op,
                                                          unsigned long long *wv, int64_t d,
                                                          int64_t n, Ctrl *ctrl, int64_t timeout) {
     (void)d;
     const int lane = lane_id();
-    for (;;) {
-        long long tk = 0;
-        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kSyncB);
-        tk = __shfl(tk, 0);
-        if (tk >= n) return;
-        const int64_t stop = min((int64_t)tk + kSyncB, n);
-        for (int64_t i = tk; i < stop; ++i) {
-            const int64_t b = op.row_ptr[i];
-            const int m = (int)(op.row_ptr[i + 1] - b);
-            const float yi = op.y[i];
-            if (m <= kWave) {
-                int c = 0, pn = -1;
-                float x = 1.0f;
-                if (lane < m) {
-                    c = op.col[b + lane];
-                    pn = op.prev_nz[b + lane];
-                    if (VAL) x = op.val[b + lane];
-                }
-                unsigned long long v = 0;
-                if (!word_wait_wave(wv, lane < m, c, pn, &v, ctrl, timeout)) return;
-                const float wold = word_value(v);
-                const float acc = lane < m ? __builtin_fmaf(wold, x, 0.0f) : 0.0f;
-                const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
-                if (lane < m)
-                    word_put(wv, c, word_pack(__builtin_fmaf(-s, x, wold), (int)(b + lane)));
-            } else if (m <= 2 * kWave) {
-                // two entries per lane: every load, and every poll, in flight
-                // together; the new weights come from the values the wait read
-                // (nothing else writes these features before this example does)
-                const int k1 = kWave + lane;
-                const bool l1 = k1 < m;
-                const int c0 = op.col[b + lane], pn0 = op.prev_nz[b + lane];
-                const int c1 = l1 ? op.col[b + k1] : 0, pn1 = l1 ? op.prev_nz[b + k1] : -1;
-                const float x0 = VAL ? op.val[b + lane] : 1.0f;
-                const float x1 = (VAL && l1) ? op.val[b + k1] : 1.0f;
+    const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock * kSyncB;
+    for (int64_t tk = ((int64_t)blockIdx.x * kWavesPerBlock + wave_in_block()) * kSyncB; tk < n;
+         tk += stride) {
+        // lanes 0 .. kSyncB: row bounds of the ticket's examples (clamped at n)
+        const int64_t rp = lane <= kSyncB ? op.row_ptr[min(tk + lane, n)] : 0;
+        const float yv = lane < kSyncB ? op.y[min(tk + lane, n - 1)] : 0.0f;
+        int c0[kSyncB], pn0[kSyncB], c1[kSyncB], pn1[kSyncB];
+        float x0[kSyncB], x1[kSyncB];
+#pragma unroll
+        for (int j = 0; j < kSyncB; ++j) {
+            const int64_t b = readlane64(rp, j);
+            const int m = (int)(readlane64(rp, j + 1) - b);  // 0 past n
+            const bool short_row = m <= 2 * kWave;
+            const bool l0 = short_row && lane < m, l1 = short_row && kWave + lane < m;
+            c0[j] = l0 ? op.col[b + lane] : 0;
+            pn0[j] = l0 ? op.prev_nz[b + lane] : -1;
+            x0[j] = (VAL && l0) ? op.val[b + lane] : 1.0f;
+            c1[j] = l1 ? op.col[b + kWave + lane] : 0;
+            pn1[j] = l1 ? op.prev_nz[b + kWave + lane] : -1;
+            x1[j] = (VAL && l1) ? op.val[b + kWave + lane] : 1.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < kSyncB; ++j) {
+            if (tk + j >= n) break;
+            const int64_t b = readlane64(rp, j);
+            const int m = (int)(readlane64(rp, j + 1) - b);
+            const float yi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(yv), j));
+            if (m <= 2 * kWave) {
+                // every poll of the example in flight together; the new
+                // weights come from the values the wait read (nothing else
+                // writes these features before this example does)
+                const bool l0 = lane < m, l1 = kWave + lane < m;
                 unsigned long long v0 = 0, v1 = 0;
-                if (!word_wait_wave2(wv, true, c0, pn0, &v0, l1, c1, pn1, &v1, ctrl, timeout))
+                if (!word_wait_wave2(wv, l0, c0[j], pn0[j], &v0, l1, c1[j], pn1[j], &v1, ctrl,
+                                     timeout))
                     return;
                 const float w0 = word_value(v0), w1 = word_value(v1);
-                float acc = __builtin_fmaf(w0, x0, 0.0f);
-                if (l1) acc = __builtin_fmaf(w1, x1, acc);
+                float acc = l0 ? __builtin_fmaf(w0, x0[j], 0.0f) : 0.0f;
+                if (l1) acc = __builtin_fmaf(w1, x1[j], acc);
                 const float s = sgd_scale<LOSS>(wave_sum64(acc), yi, op.lr);
-                word_put(wv, c0, word_pack(__builtin_fmaf(-s, x0, w0), (int)(b + lane)));
-                if (l1) word_put(wv, c1, word_pack(__builtin_fmaf(-s, x1, w1), (int)(b + k1)));
+                if (l0) word_put(wv, c0[j], word_pack(__builtin_fmaf(-s, x0[j], w0), (int)(b + lane)));
+                if (l1)
+                    word_put(wv, c1[j],
+                             word_pack(__builtin_fmaf(-s, x1[j], w1), (int)(b + kWave + lane)));
             } else {
                 float acc = 0.0f;
                 for (int k0 = 0; k0 < m; k0 += kWave) {
@@ -981,7 +998,7 @@ int64_t syncfree_ws_bytes(int64_t d) { return (int64_t)sizeof(Ctrl) + align_up(8
 // previous rating on that item (prev_nz[2t + 1] / 2), then writes both rows
 // tagged t.  Two ratings per wave, one per 32-lane half, unless the second
 // depends on the first.
-constexpr int kSyncMfB = 8;  // ratings per ticket
+constexpr int kSyncMfB = 2;  // consecutive ratings per ticket (a pair when independent)
 
 __device__ __forceinline__ int prev_rating(const int32_t *prev_nz, int64_t e) {
     const int32_t q = prev_nz[e];
@@ -996,37 +1013,39 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
     (void)n_items;
     const int lane = lane_id();
     const int h = lane >> 5, j = lane & 31;  // user rows first, then item rows, 32 words each
-    for (;;) {
-        long long tk = 0;
-        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kSyncMfB);
-        tk = __shfl(tk, 0);
-        if (tk >= n) return;
-        const int64_t stop = min((int64_t)tk + kSyncMfB, n);
+    // tickets of kSyncMfB consecutive ratings dealt to the waves in turn, as
+    // in k_sgd_syncfree (lane k < kSyncMfB holds rating tk + k)
+    const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock * kSyncMfB;
+    for (int64_t tk = ((int64_t)blockIdx.x * kWavesPerBlock + wave_in_block()) * kSyncMfB; tk < n;
+         tk += stride) {
+        const int64_t stop = min(tk + kSyncMfB, n);
+        const bool mine = lane < kSyncMfB && tk + lane < n;
+        const int64_t q = mine ? tk + lane : 0;
+        const int mu = mine ? user[q] : 0, mi = mine ? item[q] : 0;
+        const float mr = mine ? rating[q] : 0.0f;
+        const int mpu = mine ? prev_rating(prev_nz, 2 * q) : -1;
+        const int mpi = mine ? prev_rating(prev_nz, 2 * q + 1) : -1;
         for (int64_t t = tk; t < stop;) {
-            const bool pair = t + 1 < stop && prev_rating(prev_nz, 2 * (t + 1)) != t &&
-                              prev_rating(prev_nz, 2 * (t + 1) + 1) != t;
+            const int a = (int)(t - tk);
+            const bool pair = t + 1 < stop && __builtin_amdgcn_readlane(mpu, a + 1) != (int)t &&
+                              __builtin_amdgcn_readlane(mpi, a + 1) != (int)t;
             const int count = pair ? 2 : 1;
             const int64_t tt = t + h;
             const bool valid = h < count;
-            int64_t uo = 0, vo = 0;
-            int tu = -1, ti = -1;
-            float r = 0.0f;
-            if (valid) {
-                uo = (int64_t)user[tt] * 32 + j;
-                vo = (n_users + (int64_t)item[tt]) * 32 + j;
-                tu = prev_rating(prev_nz, 2 * tt);
-                ti = prev_rating(prev_nz, 2 * tt + 1);
-                r = rating[tt];
-            }
+            const int src = a + (valid ? h : 0);  // a lane of the ticket: a + 1 < kSyncMfB if valid
+            const int su = __shfl(mu, src), si = __shfl(mi, src);
+            const int tu = __shfl(mpu, src), ti = __shfl(mpi, src);
+            const float r = __shfl(mr, src);
+            const int64_t uo = valid ? (int64_t)su * 32 + j : 0;
+            const int64_t vo = valid ? (n_users + (int64_t)si) * 32 + j : 0;
             unsigned long long u = 0, v = 0;
-            if (!word_wait_wave(uvw, valid, uo, tu, &u, ctrl, timeout)) return;
-            if (!word_wait_wave(uvw, valid, vo, ti, &v, ctrl, timeout)) return;
+            if (!word_wait_wave2(uvw, valid, uo, tu, &u, valid, vo, ti, &v, ctrl, timeout)) return;
             const float uj = valid ? word_value(u) : 0.0f, vj = valid ? word_value(v) : 0.0f;
             const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
             if (valid) {
-                const float a = err * vj, b = reg * uj;
+                const float ea = err * vj, eb = reg * uj;
                 const float a2 = err * uj, b2 = reg * vj;
-                word_put(uvw, uo, word_pack(__builtin_fmaf(lr, a - b, uj), (int)tt));
+                word_put(uvw, uo, word_pack(__builtin_fmaf(lr, ea - eb, uj), (int)tt));
                 word_put(uvw, vo, word_pack(__builtin_fmaf(lr, a2 - b2, vj), (int)tt));
             }
             t += count;
@@ -1034,9 +1053,10 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
     }
 }
 
-// Grid of a sync-free kernel: every block resident (a wave spinning on a
-// writer never keeps that writer's wave from running) and about 8 levels'
-// worth of examples in flight (more only adds waiting waves).
+// Grid of a sync-free kernel: no more blocks than can be resident at once
+// (the launch is cooperative: a wave spinning on a writer never keeps that
+// writer's wave from running) and about 8 levels' worth of examples in
+// flight (more only adds waiting waves).
 int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *grid) {
     int dev = 0, cus = 0, per_cu = 0;
     PDB_HIP(hipGetDevice(&dev));
@@ -1067,10 +1087,13 @@ int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_
     int64_t grid = 1;
     int rc = syncfree_grid(fn, n, L, 2 * kWavesPerBlock, &grid);
     if (rc != PDB_OK) return rc;
-    k_mf_syncfree<<<(unsigned)grid, kBlock, 0, s>>>(op.user, op.item, op.rating, prev_nz, uvw,
-                                                    n_users, n_items, n, op.lr, op.reg, ctrl,
-                                                    timeout);
-    PDB_LAUNCHED();
+    // cooperative: the whole grid resident (the waves wait on each other)
+    const int32_t *a_user = op.user, *a_item = op.item;
+    const float *a_rating = op.rating;
+    float a_lr = op.lr, a_reg = op.reg;
+    void *args[] = {&a_user, &a_item, &a_rating, &prev_nz, &uvw, &n_users, &n_items, &n,
+                    &a_lr, &a_reg, &ctrl, const_cast<int64_t *>(&timeout)};
+    PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, s));
     if (n_users > 0)
         k_wv_out<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(uvw, op.U, n_users * 32);
     if (n_items > 0)
@@ -1097,8 +1120,10 @@ int launch_syncfree(const SgdOp<LOSS, VAL> &op, int64_t n, int64_t d, int64_t L,
     int64_t grid = 1;
     int rc = syncfree_grid(fn, n, L, kSyncB * kWavesPerBlock, &grid);
     if (rc != PDB_OK) return rc;
-    k_sgd_syncfree<LOSS, VAL><<<(unsigned)grid, kBlock, 0, s>>>(op, wv, d, n, ctrl, timeout);
-    PDB_LAUNCHED();
+    // cooperative: the whole grid resident (the waves wait on each other)
+    SgdOp<LOSS, VAL> a_op = op;
+    void *args[] = {&a_op, &wv, &d, &n, &ctrl, const_cast<int64_t *>(&timeout)};
+    PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, s));
     if (d > 0) {
         k_wv_out<<<grid_for(d, kBlock, 8192), kBlock, 0, s>>>(wv, op.w, d);
         PDB_LAUNCHED();
