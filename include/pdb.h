@@ -74,7 +74,8 @@ typedef enum pdb_loss { PDB_LOGISTIC = 0, PDB_SQUARED = 1 } pdb_loss;
 typedef enum pdb_sched_method {
     PDB_SCHED_AUTO = 0,      /* chain, else spine when it applies, else the walk on chain-like
                                 inputs (at most a quarter of the examples share no feature
-                                with the one before them), else dataflow */
+                                with the one before them), else the short-row walk when no row
+                                holds more than 4 entries, else dataflow */
     PDB_SCHED_CHAINSCAN = 1, /* chain-scan relaxation until the fixed point */
     PDB_SCHED_DATAFLOW = 2,  /* each example waits for its previous writers' levels */
     PDB_SCHED_SPINE = 3,     /* the most frequent feature's rows as a spine: applies when that
@@ -83,9 +84,12 @@ typedef enum pdb_sched_method {
     PDB_SCHED_CHAIN = 4,     /* every example conflicts with the one before it: levels are
                                 1..n, checked in one pass over the previous writers; otherwise
                                 dataflow runs.  Auto tries this first. */
-    PDB_SCHED_WALK = 5       /* one block walks the rows in order, windows of rows staged in
+    PDB_SCHED_WALK = 5,      /* one block walks the rows in order, windows of rows staged in
                                 LDS; dataflow runs instead when a row holds more than 16384
                                 entries */
+    PDB_SCHED_SHORT = 6      /* short rows (matrix completion): one block walks chunks of 1024
+                                consecutive rows, each chunk's levels settled by rounds in LDS;
+                                dataflow runs instead when a row holds more than 4 entries */
 } pdb_sched_method;
 
 /* Sparse examples in CSR form (Definition 1: the immutable data set D). */

@@ -560,6 +560,153 @@ __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__res
     }
 }
 
+// ---- K3s short-row walk --------------------------------------------------
+// One block walks the examples in sub-chunks of 64 consecutive rows, one row
+// per lane, for inputs whose rows hold at most kShortR entries (matrix
+// completion: a user and an item).  Sub-chunk q belongs to wave q mod
+// kShortWaves; the sub-chunks are settled strictly in order, handed on by an
+// LDS counter (s_done = number of settled sub-chunks).  Settling q:
+//   known(i) = max level of i's writers before q (the last kShortRing
+//              sub-chunks from an LDS ring, older ones loaded from global
+//              memory sixteen sub-chunks ahead);
+//   level(i) = 1 + max(known(i), level(in-q writers)), the fixed point of
+//              Jacobi rounds across the wave's lanes (one round per link of
+//              the longest chain inside q, plus one).
+// A round is a lane shuffle, where waiting on another workgroup's published
+// level costs a device-scope round trip.  Visibility of the global levels:
+// a wave waits for its own earlier stores (a workgroup-scope release) before
+// it settles a sub-chunk, so when a wave observes s_done past q + 16 the
+// stores of every sub-chunk up to q are complete; it loads only writers
+// kShortRing sub-chunks back, long past that.  A row with more than kShortR
+// entries sets ctrl->bad and stops the block (the host then runs dataflow);
+// every wait is bounded by the spin budget.
+constexpr int kShortWaves = 16;
+constexpr int kShortThreads = kShortWaves * 64;
+constexpr int kShortR = 4;
+constexpr int kShortRing = 64;  // sub-chunks whose levels stay in LDS
+
+template <int R>
+struct ShortRow {
+    int m;        // entries (R + 1 stands for more)
+    int pr[R];    // previous-writer rows, -1 none
+    int v[R];     // levels of writers before row `old`, else 0
+};
+
+// row r0 + lane; levels of writers before `old` are final and visible
+template <int R>
+__device__ __forceinline__ ShortRow<R> short_fetch(const int64_t *__restrict__ row_ptr,
+                                                const int32_t *__restrict__ prev_row,
+                                                const int32_t *level, int64_t n, int64_t r0,
+                                                int64_t old) {
+    ShortRow<R> r;
+    const int64_t i = r0 + lane_id();
+    int64_t b0 = 0, b1 = 0;
+    if (i < n) {
+        b0 = row_ptr[i];
+        b1 = row_ptr[i + 1];
+    }
+    r.m = (int)min(b1 - b0, (int64_t)R + 1);
+#pragma unroll
+    for (int k = 0; k < R; ++k) r.pr[k] = k < r.m ? prev_row[b0 + k] : -1;
+#pragma unroll
+    for (int k = 0; k < R; ++k) r.v[k] = (r.pr[k] >= 0 && r.pr[k] < old) ? level[r.pr[k]] : 0;
+    return r;
+}
+
+template <int R>
+__global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *__restrict__ row_ptr,
+                                                                const int32_t *__restrict__ prev_row,
+                                                                int64_t n, int32_t *level,
+                                                                Ctrl *ctrl, int64_t timeout) {
+    __shared__ int s_ring[kShortRing][64];
+    __shared__ int s_done, s_stop;
+    const int lane = lane_id(), wave = wave_in_block();
+    if (threadIdx.x == 0) {
+        s_done = 0;
+        s_stop = 0;
+    }
+    __syncthreads();
+    const int64_t nsub = (n + 63) / 64;
+    int64_t q = wave;
+    if (q >= nsub) return;
+    ShortRow<R> cur = short_fetch<R>(row_ptr, prev_row, level, n, 64 * q, 64 * (q - kShortRing));
+    for (; q < nsub; q += kShortWaves) {
+        // this wave's earlier stores complete before it settles q (see above)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        if (__ballot(cur.m > R) != 0ull) {
+            if (lane == 0) {
+                ctrl->bad = 1;
+                __hip_atomic_store(&s_stop, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+            return;
+        }
+        // wait for the sub-chunks before q: far from its turn a wave sleeps
+        // between polls; the next in line polls s_done alone, and looks at
+        // the stop flag and the clock every 32nd poll
+        const int64_t t0 = now_ticks();
+        for (int it = 1;; ++it) {
+            const int dn = __hip_atomic_load(&s_done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            if (dn == (int)q) break;
+            if ((int)q - dn > 1) {
+                __builtin_amdgcn_s_sleep(8);
+                it = 0;
+            }
+            if ((it & 31) == 0) {
+                if (__hip_atomic_load(&s_stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) return;
+                if (now_ticks() - t0 > timeout) {
+                    if (lane == 0) {
+                        record_error(ctrl, DERR_WAIT_TIMEOUT);
+                        __hip_atomic_store(&s_stop, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    }
+                    return;
+                }
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        __builtin_amdgcn_s_setprio(3);  // the block waits on this wave: issue it first
+        const int64_t r0 = 64 * q, ring0 = r0 - 64 * kShortRing;
+        // every ring read issued at once (lanes without one read slot 0 and
+        // ignore it), then the bounds folded in
+        int known = 0, rv[R], pin[R];
+        bool in_ring[R];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int p = cur.pr[k];  // -1: no writer, or past the row's end
+            in_ring[k] = p >= 0 && p >= ring0 && p < r0;
+            rv[k] = s_ring[in_ring[k] ? (p >> 6) & (kShortRing - 1) : 0][in_ring[k] ? p & 63 : 0];
+            pin[k] = p >= r0 ? (int)(p - r0) : -1;
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int p = cur.pr[k];
+            if (p >= 0 && p < ring0) known = max(known, cur.v[k]);
+            if (in_ring[k]) known = max(known, rv[k]);
+        }
+        const bool live = r0 + lane < n;
+        int lv = known + 1;
+        for (;;) {
+            int nl = known + 1;
+#pragma unroll
+            for (int k = 0; k < R; ++k) {
+                const int o = __shfl(lv, pin[k] < 0 ? lane : pin[k]);
+                if (pin[k] >= 0) nl = max(nl, o + 1);
+            }
+            const bool ch = live && nl != lv;
+            lv = nl;
+            if (__ballot(ch) == 0ull) break;
+        }
+        s_ring[q & (kShortRing - 1)][lane] = lv;
+        __asm__ __volatile__("" ::: "memory");  // one wave's LDS operations run in order
+        if (lane == 0) __hip_atomic_store(&s_done, (int)q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __builtin_amdgcn_s_setprio(0);
+        if (live) level[r0 + lane] = lv;
+        // the wave's next sub-chunk: writers before its ring window were
+        // settled at least kShortRing - kShortWaves sub-chunks before q
+        const int64_t qn = q + kShortWaves;
+        if (qn < nsub) cur = short_fetch<R>(row_ptr, prev_row, level, n, 64 * qn, 64 * (qn - kShortRing));
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_max_level(const int32_t *__restrict__ level,
                                                       int64_t n, Ctrl *ctrl) {
     int m = 0;
@@ -1260,7 +1407,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     if (rc != PDB_OK) return rc;
     if (!lv || !lv->level_ptr || !lv->n_levels || (n > 0 && (!lv->level || !lv->perm)))
         return PDB_ERR_INVALID_ARG;
-    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_WALK) return PDB_ERR_INVALID_ARG;
+    if (method < PDB_SCHED_AUTO || method > PDB_SCHED_SHORT) return PDB_ERR_INVALID_ARG;
     const int64_t nnz = csr->nnz;
     Ctrl host{};
     k_ctrl_init<<<1, 64, 0, s>>>(w.ctrl);
@@ -1326,6 +1473,17 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
                    : ((method == PDB_SCHED_AUTO && chain_like) ? PDB_SCHED_WALK : PDB_SCHED_DATAFLOW);
     }
 
+    // rows of at most kShortR entries (matrix completion), where dataflow
+    // would run: the short-row walk
+    if ((method == PDB_SCHED_AUTO && use == PDB_SCHED_DATAFLOW) || method == PDB_SCHED_SHORT) {
+        k_fill_i32<<<1, 64, 0, s>>>(reinterpret_cast<int32_t *>(&w.ctrl->max_width), 2, 0);
+        k_max_diff<<<grid_for(n, kBlock, 4096), kBlock, 0, s>>>(csr->row_ptr, n, w.ctrl);
+        PDB_LAUNCHED();
+        rc = read_ctrl(w.ctrl, &host, s);
+        if (rc != PDB_OK) return rc;
+        use = host.max_width <= kShortR ? PDB_SCHED_SHORT : PDB_SCHED_DATAFLOW;
+    }
+
     if (use == PDB_SCHED_SPINE) {
         SpineWs *sp = static_cast<SpineWs *>(w.spine);
         int32_t *rows = free_k;  // the spine rows, ascending
@@ -1366,6 +1524,26 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
         if (host.bad) use = PDB_SCHED_DATAFLOW;  // a row longer than a window
+    }
+
+    if (use == PDB_SCHED_SHORT) {
+        if (n > kFlowMaxN) return PDB_ERR_UNSUPPORTED;
+        if (nnz > 0) {
+            k_prev_row<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(pn, nnz, w.row_idx,
+                                                                        w.cand);
+            PDB_LAUNCHED();
+        }
+        // rows of at most two entries (matrix completion) need half the lane shuffles
+        if (host.max_width <= 2)
+            k_levels_short<2><<<1, kShortThreads, 0, s>>>(csr->row_ptr, w.cand, n, lv->level,
+                                                          w.ctrl, timeout);
+        else
+            k_levels_short<kShortR><<<1, kShortThreads, 0, s>>>(csr->row_ptr, w.cand, n, lv->level,
+                                                                w.ctrl, timeout);
+        PDB_LAUNCHED();
+        rc = read_ctrl(w.ctrl, &host, s);
+        if (rc != PDB_OK) return rc;
+        if (host.bad) use = PDB_SCHED_DATAFLOW;  // a row longer than kShortR
     }
 
     if (use == PDB_SCHED_CHAINSCAN) {

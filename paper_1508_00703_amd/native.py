@@ -26,6 +26,7 @@ PDB_LOGISTIC, PDB_SQUARED = 0, 1
 PDB_SCHED_AUTO, PDB_SCHED_CHAINSCAN, PDB_SCHED_DATAFLOW, PDB_SCHED_SPINE = 0, 1, 2, 3
 PDB_SCHED_CHAIN = 4
 PDB_SCHED_WALK = 5
+PDB_SCHED_SHORT = 6
 
 # every symbol declared in include/pdb.h
 EXPORTS = (

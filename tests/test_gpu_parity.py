@@ -11,7 +11,7 @@ from pdbtest import check_mf, check_schedule, check_sgd, csr_from_rows, gpu_sche
 
 pytestmark = pytest.mark.gpu
 
-METHODS = [0, 1, 2, 3, 4, 5]  # auto, chain-scan, dataflow, spine, chain, walk
+METHODS = [0, 1, 2, 3, 4, 5, 6]  # auto, chain-scan, dataflow, spine, chain, walk, short
 
 
 def native_mod():
@@ -392,7 +392,7 @@ def test_spine_selection_and_fallback(gpu):
     row_ptr, col = csr_from_rows(rows)
     d = int(col.max()) + 1
     _, info = check_schedule(native, gpu, row_ptr, col, d, 0)
-    assert info["method_used"] == 2
+    assert info["method_used"] == 6        # rows of at most 4 entries: the short-row walk
     _, info = check_schedule(native, gpu, row_ptr, col, d, 3)
     assert info["method_used"] == 2
     # 100 exceptional rows with 60 entries each
@@ -435,6 +435,36 @@ def test_walk_selection_windows_and_fallback(gpu):
     big = [{0, 1}, set(range(2, 20002)), {1, 3}, {3, 7}]
     row_ptr, col = csr_from_rows(big)
     lv, info = check_schedule(native, gpu, row_ptr, col, int(col.max()) + 1, 5)
+    assert info["method_used"] == 2
+
+
+@pytest.mark.parametrize("n", [1, 1023, 1024, 1025, 5000])
+def test_short_selection_chunks_and_fallback(gpu, n):
+    """Rows of at most 4 entries take the short-row walk under auto: one block
+    settles chunks of 1024 rows by rounds in LDS, with writers in the same
+    chunk, the previous one (LDS) and older ones (loaded a chunk ahead).  Hot
+    features make long chains inside a chunk; empty rows and ragged chunk
+    ends are included.  A row of 5 entries falls back to dataflow."""
+    native = native_mod()
+    rng = np.random.default_rng(n)
+    rows = []
+    for i in range(n):
+        k = int(rng.integers(0, 5))                   # 0..4 entries
+        r = set()
+        for _ in range(k):
+            u = rng.random()
+            # a hot feature (long chains), a warm one, or one of many cold ones
+            r.add(0 if u < 0.08 else (1 + int(rng.integers(0, 50)) if u < 0.4
+                                      else 100 + int(rng.integers(0, 20000))))
+        rows.append(r)
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1 if len(col) else 1
+    for method in (0, 6):
+        lv, info = check_schedule(native, gpu, row_ptr, col, d, method)
+        assert info["method_used"] in ((6, 4, 3) if method == 0 else (6,))
+    rows[n // 2] = {0, 1, 2, 3, 4}
+    row_ptr, col = csr_from_rows(rows)
+    _, info = check_schedule(native, gpu, row_ptr, col, max(d, 5), 6)
     assert info["method_used"] == 2
 
 
