@@ -850,38 +850,6 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
 // The earliest unfinished example never waits for a later one, so the grid
 // always makes progress.
 
-// Polls two words per lane as word_wait_wave does one (want0/want1 say which
-// this lane needs); both polls are in flight together every round.
-__device__ __forceinline__ bool word_wait_wave2(unsigned long long *base, bool want0, int64_t idx0,
-                                                int tag0, unsigned long long *out0, bool want1,
-                                                int64_t idx1, int tag1, unsigned long long *out1,
-                                                Ctrl *ctrl, int64_t timeout) {
-    bool ready0 = !want0, ready1 = !want1;
-    int64_t t0 = 0;
-    for (int round = 0;; ++round) {
-        unsigned long long v0 = 0, v1 = 0;
-        if (!ready0) v0 = word_get(base, idx0);
-        if (!ready1) v1 = word_get(base, idx1);
-        if (!ready0 && word_tag(v0) == tag0) {
-            *out0 = v0;
-            ready0 = true;
-        }
-        if (!ready1 && word_tag(v1) == tag1) {
-            *out1 = v1;
-            ready1 = true;
-        }
-        if (__ballot(!(ready0 && ready1)) == 0ull) return true;
-        if (round == 0) t0 = now_ticks();
-        if (aborted(ctrl)) return false;
-        if (now_ticks() - t0 > timeout) {
-            record_error(ctrl, DERR_WAIT_TIMEOUT);
-            return false;
-        }
-        word_backoff(round);
-        __asm__ __volatile__("" ::: "memory");  // the next round loads again
-    }
-}
-
 constexpr int kSyncB = 1;  // consecutive examples per ticket, run in order by one wave
 
 __global__ void k_wv_in(const float *__restrict__ w, unsigned long long *__restrict__ wv,

@@ -25,9 +25,12 @@
 //         the exact level).  Rounds = 1 + chain switches on the critical
 //         path: few when one feature dominates every example;
 //         dataflow: every example waits for its previous writers' levels
-//         (published with device-scope atomics) and publishes its own; waves
-//         take batches of consecutive examples by ticket, so the smallest
-//         unfinished example always runs.  Time ~ critical path length;
+//         (published with device-scope atomics) and publishes its own;
+//         batches of consecutive examples are dealt to the resident waves
+//         in turn, so the smallest unfinished example always runs.  Time ~
+//         critical path length;
+//         short-row walk (rows of at most four entries): one block settles
+//         64-row sub-chunks in order, each by Jacobi rounds across a wave;
 //   K4  stable radix sort of examples by level -> perm, level_ptr.
 #include <climits>
 #include <cstdlib>
@@ -248,8 +251,9 @@ __global__ __launch_bounds__(kBlock) void k_cs_rows(const int64_t *__restrict__ 
 
 // ---- K3 dataflow ---------------------------------------------------------
 // Every example waits for its previous writers' levels and publishes its own.
-// Waves take batches of kFlowB consecutive examples by ticket, so the
-// smallest unfinished example always runs.  Per batch:
+// Batches of kFlowB consecutive examples are dealt to the waves in turn
+// (wave k of W runs batches k, k + W, ...), and the whole grid is resident,
+// so the smallest unfinished example always runs.  Per batch:
 //   1. the batch's row bounds and the previous-writer rows of all its
 //      entries go to LDS, with the levels of previous writers outside the
 //      batch loaded at the same time (device-scope loads, as levels are
@@ -314,12 +318,13 @@ __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__res
     int *src = g_flow + wave * kFlowWaveLds;
     int *lvb = src + kFlowEnt;
     int *pend = lvb + kFlowB;
+    // batches dealt to the waves in turn (the launch is cooperative)
+    const int64_t fstride = (int64_t)gridDim.x * (kBlock / kWave) * kFlowB;
+    int64_t fnext = ((int64_t)blockIdx.x * (kBlock / kWave) + wave) * kFlowB;
     for (;;) {
-        long long tk = 0;
-        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kFlowB);
-        tk = __shfl(tk, 0);
-        if (tk >= n) return;
-        const int64_t base = tk;
+        const int64_t base = fnext;
+        fnext += fstride;
+        if (base >= n) return;
         const int cnt = (int)min((int64_t)kFlowB, n - base);
         const bool mine_ok = lane < cnt;
         const int64_t r0 = row_ptr[base + min(lane, cnt)];
@@ -1581,7 +1586,6 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
             PDB_LAUNCHED();
         }
         k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 0);
-        k_fill_i32<<<1, 64, 0, s>>>(reinterpret_cast<int32_t *>(&w.ctrl->ticket), 2, 0);
         PDB_LAUNCHED();
         if (n > kFlowMaxN) return PDB_ERR_UNSUPPORTED;
         const size_t lds = (size_t)kFlowWaveLds * 4 * (kBlock / kWave);
@@ -1591,9 +1595,17 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, lds));
         const int64_t grid = std::min<int64_t>((int64_t)device_cus() * std::max(per_cu, 1),
                                                cdiv(n, (int64_t)kFlowB * (kBlock / kWave)));
-        k_levels_dataflow<<<(unsigned)std::max<int64_t>(grid, 1), kBlock, lds, s>>>(
-            csr->row_ptr, w.cand, n, lv->level, w.ctrl, timeout);
-        PDB_LAUNCHED();
+        {
+            // cooperative: the whole grid resident (the waves wait on each other)
+            const int64_t *a_rp = csr->row_ptr;
+            const int32_t *a_prev = w.cand;
+            int32_t *a_level = lv->level;
+            Ctrl *a_ctrl = w.ctrl;
+            int64_t a_n = n, a_timeout = timeout;
+            void *args[] = {&a_rp, &a_prev, &a_n, &a_level, &a_ctrl, &a_timeout};
+            PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)std::max<int64_t>(grid, 1)),
+                                               dim3(kBlock), args, lds, s));
+        }
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
         if (host.err) return PDB_ERR_DEVICE;

@@ -35,7 +35,6 @@ namespace pdbk {
 
 namespace {
 
-constexpr int kStaleB = 4;  // examples per ticket, run in order by one wave
 constexpr int kSWaves = kBlock / kWave;
 constexpr int kWinCap = 2048;          // entries (and examples) of a window held in LDS
 constexpr int kWinThreads = 1024;
@@ -151,6 +150,11 @@ __global__ __launch_bounds__(kBlock) void k_stale_sources(const int64_t *__restr
     }
 }
 
+// Examples are dealt to the waves in turn (wave k of W runs examples k,
+// k + W, ...); the grid is launched cooperatively, so the earliest
+// unfinished example is always being worked on.  A shared ticket counter
+// would serve one request about every 200 ns.  An example of up to 2 x 64
+// entries issues the loads and polls of both chunks together.
 template <int LOSS, bool VAL>
 __global__ __launch_bounds__(kBlock) void k_stale_epoch(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
@@ -158,41 +162,62 @@ __global__ __launch_bounds__(kBlock) void k_stale_epoch(
     const int32_t *__restrict__ prev, const int32_t *__restrict__ rd, unsigned long long *words,
     int64_t n, float lr, Ctrl *ctrl, int64_t timeout) {
     const int lane = lane_id();
-    for (;;) {
-        long long tk = 0;
-        if (lane == 0) tk = (long long)atomicAdd(&ctrl->ticket, (unsigned long long)kStaleB);
-        tk = __shfl(tk, 0);
-        if (tk >= n) return;
-        const int64_t stop = min((int64_t)tk + kStaleB, n);
-        for (int64_t a = tk; a < stop; ++a) {
-            const int64_t b = row_ptr[a];
-            const int64_t m = row_ptr[a + 1] - b;
+    const int64_t nw = (int64_t)gridDim.x * kSWaves;
+    for (int64_t a = (int64_t)blockIdx.x * kSWaves + wave_in_block(); a < n; a += nw) {
+        const int64_t b = row_ptr[a];
+        const int64_t m = row_ptr[a + 1] - b;
+        if (m <= 2 * kWave) {
+            const bool l0 = lane < m, l1 = kWave + lane < m;
+            const int64_t q0 = b + lane, q1 = b + kWave + lane;
+            const int32_t s0 = l0 ? rd[q0] : -1, s1 = l1 ? rd[q1] : -1;
+            const int32_t p0 = l0 ? prev[q0] : -1, p1 = l1 ? prev[q1] : -1;
+            const int32_t c0 = l0 ? col[q0] : 0, c1 = l1 ? col[q1] : 0;
+            const float x0 = (VAL && l0) ? val[q0] : 1.0f, x1 = (VAL && l1) ? val[q1] : 1.0f;
+            const float i0 = l0 ? w0[c0] : 0.0f, i1 = l1 ? w0[c1] : 0.0f;
             // reads: the value of each entry's read source (waits for it)
+            unsigned long long v0 = 0, v1 = 0;
+            if (!word_wait_wave2(words, s0 >= 0, s0, s0, &v0, s1 >= 0, s1, s1, &v1, ctrl, timeout))
+                return;
             float acc = 0.0f;
-            for (int64_t k0 = 0; k0 < m; k0 += kWave) {
-                const int64_t k = k0 + lane;
-                const bool live = k < m;
-                const int32_t src = live ? rd[b + k] : -1;
-                unsigned long long v = 0;
-                if (!word_wait_wave(words, src >= 0, src, src, &v, ctrl, timeout)) return;
-                if (live) {
-                    const float r = src >= 0 ? word_value(v) : w0[col[b + k]];
-                    acc = __builtin_fmaf(r, VAL ? val[b + k] : 1.0f, acc);
-                }
-            }
-            const float s = sgd_scale<LOSS>(wave_sum64(acc), y[a], lr);
+            if (l0) acc = __builtin_fmaf(s0 >= 0 ? word_value(v0) : i0, x0, acc);
+            if (l1) acc = __builtin_fmaf(s1 >= 0 ? word_value(v1) : i1, x1, acc);
+            const float st = sgd_scale<LOSS>(wave_sum64(acc), y[a], lr);
             // writes: onto the value of each entry's previous writer
-            for (int64_t k0 = 0; k0 < m; k0 += kWave) {
-                const int64_t k = k0 + lane;
-                const bool live = k < m;
-                const int32_t pq = live ? prev[b + k] : -1;
-                unsigned long long v = 0;
-                if (!word_wait_wave(words, pq >= 0, pq, pq, &v, ctrl, timeout)) return;
-                if (live) {
-                    const float cur = pq >= 0 ? word_value(v) : w0[col[b + k]];
-                    const float nv = __builtin_fmaf(-s, VAL ? val[b + k] : 1.0f, cur);
-                    word_put(words, b + k, word_pack(nv, (int)(b + k)));
-                }
+            if (!word_wait_wave2(words, p0 >= 0, p0, p0, &v0, p1 >= 0, p1, p1, &v1, ctrl, timeout))
+                return;
+            if (l0)
+                word_put(words, q0,
+                         word_pack(__builtin_fmaf(-st, x0, p0 >= 0 ? word_value(v0) : i0), (int)q0));
+            if (l1)
+                word_put(words, q1,
+                         word_pack(__builtin_fmaf(-st, x1, p1 >= 0 ? word_value(v1) : i1), (int)q1));
+            continue;
+        }
+        // reads: the value of each entry's read source (waits for it)
+        float acc = 0.0f;
+        for (int64_t k0 = 0; k0 < m; k0 += kWave) {
+            const int64_t k = k0 + lane;
+            const bool live = k < m;
+            const int32_t src = live ? rd[b + k] : -1;
+            unsigned long long v = 0;
+            if (!word_wait_wave(words, src >= 0, src, src, &v, ctrl, timeout)) return;
+            if (live) {
+                const float r = src >= 0 ? word_value(v) : w0[col[b + k]];
+                acc = __builtin_fmaf(r, VAL ? val[b + k] : 1.0f, acc);
+            }
+        }
+        const float st = sgd_scale<LOSS>(wave_sum64(acc), y[a], lr);
+        // writes: onto the value of each entry's previous writer
+        for (int64_t k0 = 0; k0 < m; k0 += kWave) {
+            const int64_t k = k0 + lane;
+            const bool live = k < m;
+            const int32_t pq = live ? prev[b + k] : -1;
+            unsigned long long v = 0;
+            if (!word_wait_wave(words, pq >= 0, pq, pq, &v, ctrl, timeout)) return;
+            if (live) {
+                const float cur = pq >= 0 ? word_value(v) : w0[col[b + k]];
+                const float nv = __builtin_fmaf(-st, VAL ? val[b + k] : 1.0f, cur);
+                word_put(words, b + k, word_pack(nv, (int)(b + k)));
             }
         }
     }
@@ -425,19 +450,28 @@ int launch_stale(const pdb_csr *csr, const float *labels, int64_t n, float *w, f
         PDB_LAUNCHED();
         return PDB_OK;
     }
-    // every block resident; about as many waves as there are examples in
-    // flight (tickets of kStaleB examples)
+    // every block resident (a cooperative launch: the waves wait on each
+    // other), at most one wave per example
     const void *fn = reinterpret_cast<const void *>(&k_stale_epoch<LOSS, VAL>);
     int dev = 0, cus = 0, per_cu = 0;
     PDB_HIP(hipGetDevice(&dev));
     PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
     PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0));
     const int64_t grid = std::max<int64_t>(
-        1, std::min<int64_t>((int64_t)cus * std::max(per_cu, 1), cdiv(n, (int64_t)kStaleB * kSWaves)));
-    k_stale_epoch<LOSS, VAL><<<(unsigned)grid, kBlock, 0, s>>>(
-        csr->row_ptr, csr->col, csr->val, labels, w, prev, ws.rd, ws.words, n, lr, ws.ctrl,
-        timeout);
-    PDB_LAUNCHED();
+        1, std::min<int64_t>((int64_t)cus * std::max(per_cu, 1), cdiv(n, (int64_t)kSWaves)));
+    {
+        const int64_t *a_rp = csr->row_ptr;
+        const int32_t *a_col = csr->col, *a_rd = ws.rd;
+        const float *a_val = csr->val, *a_y = labels, *a_w0 = w;
+        const int32_t *a_prev = prev;
+        unsigned long long *a_words = ws.words;
+        Ctrl *a_ctrl = ws.ctrl;
+        int64_t a_n = n, a_timeout = timeout;
+        float a_lr = lr;
+        void *args[] = {&a_rp, &a_col, &a_val, &a_y, &a_w0, &a_prev, &a_rd, &a_words,
+                        &a_n, &a_lr, &a_ctrl, &a_timeout};
+        PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, s));
+    }
     if (nnz > 0) {
         k_stale_final<<<grid_for(nnz, kBlock, 8192), kBlock, 0, s>>>(csr->col, ws.words,
                                                                     ws.overwritten, nnz, w);
