@@ -565,7 +565,7 @@ __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__res
     }
 }
 
-// ---- K3s short-row walk --------------------------------------------------
+// ---- K3r short-row walk --------------------------------------------------
 // One block walks the examples in sub-chunks of 64 consecutive rows, one row
 // per lane, for inputs whose rows hold at most kShortR entries (matrix
 // completion: a user and an item).  Sub-chunk q belongs to wave q mod
