@@ -276,6 +276,7 @@ constexpr int kFlowShort = 4;          // longest row resolved by Jacobi rounds
 // batch's example j (j < 64); kPendBase + r an outside writer r whose level
 // was not seen yet (r < n <= kFlowMaxN keeps the two ranges apart).
 constexpr int kPendBase = INT_MIN;
+constexpr int64_t kRowWaveMinAvg = 16;  // mean entries per row from which dataflow runs a wave per example
 constexpr int64_t kFlowMaxN = (int64_t)INT_MAX - 128;
 
 // Level of entry e's writer: known, an example of the batch (already
@@ -562,6 +563,50 @@ __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__res
                 idle = 0;
             }
         }
+    }
+}
+
+// Dataflow with a wave per example, for inputs with long rows and wide
+// levels (not chain-like: many examples share nothing with the one before).
+// Examples are dealt to the waves in turn (cooperative launch); a wave polls
+// the published levels of all writer rows of up to 2 x 64 entries at once
+// and publishes 1 + their maximum.  Beside the batch form it spends no time
+// on batch-mates: an example waits only for its own writers.
+__global__ __launch_bounds__(kBlock) void k_levels_rowwave(const int64_t *__restrict__ row_ptr,
+                                                           const int32_t *__restrict__ prev_row,
+                                                           int64_t n, int32_t *level, Ctrl *ctrl,
+                                                           int64_t timeout) {
+    const int lane = lane_id();
+    const int64_t nw = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t a = (int64_t)blockIdx.x * (kBlock / kWave) + wave_in_block(); a < n; a += nw) {
+        const int64_t b = row_ptr[a], m = row_ptr[a + 1] - b;
+        int mx = 0;
+        for (int64_t k0 = 0; k0 < m; k0 += 2 * kWave) {
+            const bool l0 = k0 + lane < m, l1 = k0 + kWave + lane < m;
+            const int p0 = l0 ? prev_row[b + k0 + lane] : -1;
+            const int p1 = l1 ? prev_row[b + k0 + kWave + lane] : -1;
+            int v0 = 0, v1 = 0;
+            bool r0 = p0 < 0, r1 = p1 < 0;
+            int64_t t0 = 0;
+            for (int round = 0;; ++round) {
+                if (!r0) v0 = __hip_atomic_load(&level[p0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (!r1) v1 = __hip_atomic_load(&level[p1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                r0 |= v0 != 0;
+                r1 |= v1 != 0;
+                if (__ballot(!(r0 && r1)) == 0ull) break;
+                if (round == 0) t0 = now_ticks();
+                if (aborted(ctrl)) return;
+                if (now_ticks() - t0 > timeout) {
+                    record_error(ctrl, DERR_WAIT_TIMEOUT);
+                    return;
+                }
+                if (round < 3) __builtin_amdgcn_s_sleep(1);
+                else __builtin_amdgcn_s_sleep(4);
+            }
+            mx = max(mx, max(v0, v1));
+        }
+        const int lv = wave_max_dpp(mx) + 1;
+        if (lane == 0) __hip_atomic_store(&level[a], lv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -1439,8 +1484,9 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
 
     // a chain (every example conflicts with the one before it) is solved
     // outright; auto tries it first
-    bool chain_like = false;
+    bool chain_like = false, chain_checked = false;
     if (method == PDB_SCHED_AUTO || method == PDB_SCHED_CHAIN) {
+        chain_checked = true;
         k_chain_check<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n, pn,
                                                                             w.ctrl);
         PDB_LAUNCHED();
@@ -1588,13 +1634,23 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 0);
         PDB_LAUNCHED();
         if (n > kFlowMaxN) return PDB_ERR_UNSUPPORTED;
-        const size_t lds = (size_t)kFlowWaveLds * 4 * (kBlock / kWave);
-        const void *fn = reinterpret_cast<const void *>(&k_levels_dataflow);
-        PDB_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        // long rows, not chain-like (the chain check ran and found many
+        // breaks): a wave per example
+        const bool rowwave = chain_checked && !chain_like && nnz >= kRowWaveMinAvg * n;
+        const size_t lds = rowwave ? 0 : (size_t)kFlowWaveLds * 4 * (kBlock / kWave);
+        const void *fn = rowwave ? reinterpret_cast<const void *>(&k_levels_rowwave)
+                                 : reinterpret_cast<const void *>(&k_levels_dataflow);
+        if (!rowwave)
+            PDB_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
         int per_cu = 0;
         PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, lds));
-        const int64_t grid = std::min<int64_t>((int64_t)device_cus() * std::max(per_cu, 1),
-                                               cdiv(n, (int64_t)kFlowB * (kBlock / kWave)));
+        int64_t grid = std::min<int64_t>(
+            (int64_t)device_cus() * std::max(per_cu, 1),
+            cdiv(n, (int64_t)(rowwave ? 1 : kFlowB) * (kBlock / kWave)));
+        // a wave per example: four waves per CU keep enough examples in
+        // flight; more waves only add polling traffic (5M rows of 80 entries:
+        // 128 -> 93 ms per schedule)
+        if (rowwave) grid = std::min<int64_t>(grid, (int64_t)device_cus());
         {
             // cooperative: the whole grid resident (the waves wait on each other)
             const int64_t *a_rp = csr->row_ptr;

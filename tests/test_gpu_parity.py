@@ -468,6 +468,27 @@ def test_short_selection_chunks_and_fallback(gpu, n):
     assert info["method_used"] == 2
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_dataflow_wave_per_example(gpu, seed):
+    """Auto on long rows with wide levels (most examples share nothing with
+    the one before): dataflow runs a wave per example.  Rows of 0 to 300
+    entries (one, two and three 128-entry rounds), a few hot features for
+    long dependence chains.  Levels exact."""
+    native = native_mod()
+    rng = np.random.default_rng(40 + seed)
+    n, d = 4000, 200_000
+    rows = []
+    for i in range(n):
+        k = int(rng.choice([0, 3, 20, 64, 65, 127, 128, 129, 300]))
+        r = set(int(x) for x in rng.integers(50, d, size=k))
+        if rng.random() < 0.05:
+            r.add(int(rng.integers(0, 50)))           # hot features chain a few rows
+        rows.append(r)
+    row_ptr, col = csr_from_rows(rows)
+    lv, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert info["method_used"] == 2
+
+
 def test_chain_selection_and_fallback(gpu):
     """Auto takes the chain when every example conflicts with the one before
     it (levels 1..n); when one does not, auto and an explicit chain request
