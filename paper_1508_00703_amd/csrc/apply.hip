@@ -1024,7 +1024,8 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
 // Grid of a sync-free kernel: no more blocks than can be resident at once
 // (the launch is cooperative: a wave spinning on a writer never keeps that
 // writer's wave from running) and about 8 levels' worth of examples in
-// flight (more only adds waiting waves).
+// flight, at least a block per four CUs (more only adds waiting waves and
+// polling traffic).
 int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *grid) {
     int dev = 0, cus = 0, per_cu = 0;
     PDB_HIP(hipGetDevice(&dev));
@@ -1032,7 +1033,7 @@ int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *
     PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0));
     const int64_t width = L > 0 ? cdiv(n, L) : n;
     int64_t g = std::min<int64_t>((int64_t)cus * std::max(per_cu, 1), cdiv(n, per_block));
-    g = std::min<int64_t>(g, std::max<int64_t>(cdiv(8 * width, per_block), cus));
+    g = std::min<int64_t>(g, std::max<int64_t>(cdiv(8 * width, per_block), cus / 4));
     *grid = std::max<int64_t>(g, 1);
     return PDB_OK;
 }
