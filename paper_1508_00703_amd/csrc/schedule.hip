@@ -799,9 +799,9 @@ struct WalkShared {
     int nruns;
     int m[kWalkRows];        // largest level among the row's writers before the window
     int chain[kWalkRows];    // 1 when the row just before is one of the row's writers
-    int rp[kWalkRows + 1];   // row bounds relative to the window's first entry
+    int rp[2][kWalkRows + 1];  // row bounds relative to a window's first entry (this, next)
     int lvl[2][kWalkRows];   // levels of this window and the previous one
-    int nrows;
+    int nrows;               // rows of the next window
 };
 
 __device__ __forceinline__ int wave_prefix_max(int v) {
@@ -814,6 +814,30 @@ __device__ __forceinline__ int wave_prefix_max(int v) {
     return v;
 }
 
+// Row bounds of the window starting at row r0 into S.rp[slot] (relative to
+// its first entry), and its row count (as many rows as fit kWalkEnt
+// entries) into S.nrows; S.nrows must be 0 beforehand.  One load per thread.
+__device__ __forceinline__ void walk_bounds(const int64_t *__restrict__ row_ptr, int64_t n,
+                                            int64_t r0, int64_t q0, int64_t rpt, WalkShared &S,
+                                            int slot) {
+    // the rows that fit are a prefix (row bounds never decrease): count them
+    const int t = threadIdx.x;
+    const int64_t rel = rpt - q0;
+    const bool fits = t >= 1 && t <= kWalkRows && r0 + t <= n && rel <= kWalkEnt;
+    if (t <= kWalkRows) S.rp[slot][t] = (int)min<int64_t>(rel, INT_MAX);
+    const int c = __popcll(__ballot(fits));
+    if (lane_id() == 0 && c > 0) atomicAdd(&S.nrows, c);
+}
+
+// A block barrier for LDS only: global loads may stay in flight across it
+// (__syncthreads would wait for them).
+__device__ __forceinline__ void lds_barrier() {
+    __asm__ __volatile__("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __asm__ __volatile__("" ::: "memory");
+}
+
 __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__restrict__ row_ptr,
                                                               int64_t n,
                                                               const int32_t *__restrict__ prow,
@@ -823,63 +847,74 @@ __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__r
     __shared__ WalkShared S;
     const int tid = threadIdx.x, lane = lane_id();
     constexpr int kNone = INT_MIN / 2;
+    // The next window's row bounds and entries are loaded while the current
+    // one is staged and solved: what a window loads does not depend on
+    // earlier windows' levels, only the levels of writers before it do.
     int64_t r0 = 0, r0p = 0;  // first rows of this and the previous window
-    int cur = 0;
-    while (r0 < n) {
-        // the window: as many rows (up to kWalkRows) as fit kWalkEnt entries
-        const int64_t q0 = row_ptr[r0];
-        if (tid == 0) S.nrows = 0;
-        __syncthreads();
-        for (int t = tid; t <= kWalkRows; t += kWalkThreads) {
-            const int64_t rel = row_ptr[min(r0 + t, n)] - q0;
-            S.rp[t] = (int)min<int64_t>(rel, INT_MAX);
-            if (t >= 1 && r0 + t <= n && rel <= kWalkEnt) atomicMax(&S.nrows, t);
-            if (t < kWalkRows) {
-                S.m[t] = 0;
-                S.chain[t] = 0;
-            }
+    int cur = 0, cb = 0;      // level buffer, row-bound buffer of this window
+    if (tid == 0) S.nrows = 0;
+    __syncthreads();
+    int64_t q0 = row_ptr[0];
+    walk_bounds(row_ptr, n, 0, q0, tid <= kWalkRows ? row_ptr[min((int64_t)tid, n)] : 0, S, 0);
+    __syncthreads();
+    int nr = S.nrows;
+    int32_t pr[kWalkPer], row[kWalkPer], lvf[kWalkPer];
+    auto load_entries = [&](int64_t wr0, int64_t wq0, int wE) {
+#pragma unroll
+        for (int u = 0; u < kWalkPer; ++u) {
+            const int e = tid + u * kWalkThreads;
+            const int64_t q = wq0 + min(e, max(wE - 1, 0));
+            // raw rows: subtracting the window's first row here would wait
+            // for the load; the staging does it
+            pr[u] = e < wE ? prow[q] : -1;
+            row[u] = e < wE ? row_idx[q] : (int32_t)wr0;
         }
-        __syncthreads();
-        const int nr = S.nrows;
+    };
+    if (nr > 0) load_entries(0, q0, S.rp[0][nr]);
+#pragma unroll
+    for (int u = 0; u < kWalkPer; ++u) lvf[u] = 0;  // no writers before the first window
+    while (r0 < n) {
         if (nr == 0) {  // one row longer than a window: the caller uses another method
             if (tid == 0) ctrl->bad = 1;
             return;
         }
-        const int E = S.rp[nr];
+        const int E = S.rp[cb][nr];
         int *lc = S.lvl[cur];
         const int *lp = S.lvl[cur ^ 1];
-        // stage the window's entries: every thread's loads in flight at once
-        // (writers, rows, then the levels of writers before the window)
-        {
-            int32_t pr[kWalkPer], row[kWalkPer], lvf[kWalkPer];
+        // lvf: levels of writers before the previous window, loaded during
+        // the previous window; now the next window's row bounds
+        const int64_t r0n = r0 + nr;
+        const int64_t q0n = q0 + E;
+        const int64_t rpn = tid <= kWalkRows ? row_ptr[min(r0n + tid, n)] : 0;
+        if (tid < kWalkRows) {
+            S.m[tid] = 0;
+            S.chain[tid] = 0;
+        }
+        if (tid == 0) S.nrows = 0;
+        lds_barrier();
+        // stage this window
 #pragma unroll
-            for (int u = 0; u < kWalkPer; ++u) {
-                const int e = tid + u * kWalkThreads;
-                const int64_t q = q0 + min(e, max(E - 1, 0));
-                pr[u] = e < E ? prow[q] : -1;
-                row[u] = e < E ? (int)(row_idx[q] - r0) : 0;
-            }
-#pragma unroll
-            for (int u = 0; u < kWalkPer; ++u)
-                lvf[u] = (pr[u] >= 0 && pr[u] < r0p) ? level[pr[u]] : 0;
-#pragma unroll
-            for (int u = 0; u < kWalkPer; ++u) {
-                const int e = tid + u * kWalkThreads;
-                if (e < E) {
-                    int16_t ref = -1;
-                    S.row[e] = (int16_t)row[u];
-                    const int32_t p = pr[u];
-                    if (p >= r0) {
-                        if (p == r0 + row[u] - 1) S.chain[row[u]] = 1;
-                        else ref = (int16_t)(p - r0);
-                    } else if (p >= 0) {
-                        atomicMax(&S.m[row[u]], p >= r0p ? lp[p - r0p] : lvf[u]);
-                    }
-                    S.ref[e] = ref;
+        for (int u = 0; u < kWalkPer; ++u) {
+            const int e = tid + u * kWalkThreads;
+            if (e < E) {
+                int16_t ref = -1;
+                const int rw = row[u] - (int32_t)r0;  // the entry's row in the window
+                S.row[e] = (int16_t)rw;
+                const int32_t p = pr[u];
+                if (p >= r0) {
+                    if (p == r0 + rw - 1) S.chain[rw] = 1;
+                    else ref = (int16_t)(p - r0);
+                } else if (p >= 0) {
+                    atomicMax(&S.m[rw], p >= r0p ? lp[p - r0p] : lvf[u]);
                 }
+                S.ref[e] = ref;
             }
         }
-        __syncthreads();
+        walk_bounds(row_ptr, n, r0n, q0n, rpn, S, cb ^ 1);
+        lds_barrier();
+        // the next window's entries, in flight while this one is solved
+        const int nrn = S.nrows;
+        if (r0n < n && nrn > 0) load_entries(r0n, q0n, S.rp[cb ^ 1][nrn]);
         // the runs' first rows (wave 0)
         if (tid < kWave) {
             int cnt = 0;
@@ -895,16 +930,16 @@ __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__r
                 S.nruns = cnt;
             }
         }
-        __syncthreads();
+        lds_barrier();
         const int nruns = S.nruns;
         for (int k = 0; k < nruns; ++k) {
             const int a = S.runs[k], b = S.runs[k + 1];
             // writers in earlier runs of the window
-            for (int e = S.rp[a] + tid; e < S.rp[b]; e += kWalkThreads) {
+            for (int e = S.rp[cb][a] + tid; e < S.rp[cb][b]; e += kWalkThreads) {
                 const int r = S.ref[e];
                 if (r >= 0 && r < a) atomicMax(&S.m[S.row[e]], lc[r]);
             }
-            __syncthreads();
+            lds_barrier();
             // level(j) = j + 1 + max over a <= t <= j of (M_t - t)
             if (tid < kWave) {
                 int carry = kNone;
@@ -915,11 +950,21 @@ __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__r
                     carry = __shfl(pm, kWave - 1);
                 }
             }
-            __syncthreads();
+            lds_barrier();
         }
+        // every load and store of the block done: the next window's
+        // entries are in registers, the levels of earlier windows in memory
+        __syncthreads();
+        // the next window's writers before this window: their levels are
+        // final (stored by this block before at least one barrier)
+#pragma unroll
+        for (int u = 0; u < kWalkPer; ++u) lvf[u] = (pr[u] >= 0 && pr[u] < r0) ? level[pr[u]] : 0;
         for (int i = tid; i < nr; i += kWalkThreads) level[r0 + i] = lc[i];
         r0p = r0;
-        r0 += nr;
+        r0 = r0n;
+        q0 = q0n;
+        nr = nrn;
+        cb ^= 1;
         cur ^= 1;
     }
 }
