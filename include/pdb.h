@@ -159,7 +159,10 @@ int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
  *   - level by level (narrow levels: a width-1 run is one dependent chain);
  *   - sync-free, the Read Protocol of Sec. 5 at feature grain: examples in
  *     index order, each entry waiting only until its feature was written by
- *     its previous writer (levels->prev_nz), no barriers.  Chosen when
+ *     its previous writer (levels->prev_nz), no barriers.  The examples are
+ *     dealt to the waves of a cooperatively launched grid in turn (every
+ *     block resident, so the earliest unfinished example always runs; a
+ *     refused launch returns PDB_ERR_HIP).  Chosen when
  *     n >= 8 L, levels->prev_nz is set and ws_bytes covers
  *     pdb_epoch_workspace_bytes(d) (environment PDB_EPOCH_MODE=1 or 2 forces
  *     levels or sync-free).
@@ -272,7 +275,8 @@ int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes);
  *     share no feature with the example before them (PDB_STALE_MODE=1 forces
  *     the sync-free execution, 2 the windowed one where windows fit);
  *   - sync-free: examples in index order, each waiting on the words of its
- *     read sources and previous writers.
+ *     read sources and previous writers (dealt to the waves of a
+ *     cooperatively launched grid in turn, as in pdb_sgd_epoch).
  * ws: at least pdb_stale_workspace_bytes(nnz).  Synchronous: it reads back
  * the largest window's size to choose; a device error (watchdog) is reported
  * by pdb_workspace_status on ws. */
