@@ -438,7 +438,7 @@ def test_walk_selection_windows_and_fallback(gpu):
     assert info["method_used"] == 2
 
 
-@pytest.mark.parametrize("n", [1, 1023, 1024, 1025, 5000])
+@pytest.mark.parametrize("n", [1, 1023, 1024, 1025, 5000, 12295])
 def test_short_selection_chunks_and_fallback(gpu, n):
     """Rows of at most 4 entries take the short-row walk under auto: one block
     settles chunks of 1024 rows by rounds in LDS, with writers in the same
