@@ -572,8 +572,12 @@ __global__ __launch_bounds__(kBlock) void k_levels_dataflow(const int64_t *__res
 // the published levels of all writer rows of up to 2 x 64 entries at once
 // and publishes 1 + their maximum.  Beside the batch form it spends no time
 // on batch-mates: an example waits only for its own writers.
+// Writer rows are looked up here (row_idx of the previous-writer entry)
+// rather than gathered by a pass of their own: an example's lookups happen
+// while it waits for its turn, off the dependence chain.
 __global__ __launch_bounds__(kBlock) void k_levels_rowwave(const int64_t *__restrict__ row_ptr,
-                                                           const int32_t *__restrict__ prev_row,
+                                                           const int32_t *__restrict__ prev_nz,
+                                                           const int32_t *__restrict__ row_idx,
                                                            int64_t n, int32_t *level, Ctrl *ctrl,
                                                            int64_t timeout) {
     const int lane = lane_id();
@@ -583,8 +587,10 @@ __global__ __launch_bounds__(kBlock) void k_levels_rowwave(const int64_t *__rest
         int mx = 0;
         for (int64_t k0 = 0; k0 < m; k0 += 2 * kWave) {
             const bool l0 = k0 + lane < m, l1 = k0 + kWave + lane < m;
-            const int p0 = l0 ? prev_row[b + k0 + lane] : -1;
-            const int p1 = l1 ? prev_row[b + k0 + kWave + lane] : -1;
+            const int e0 = l0 ? prev_nz[b + k0 + lane] : -1;
+            const int e1 = l1 ? prev_nz[b + k0 + kWave + lane] : -1;
+            const int p0 = e0 >= 0 ? row_idx[e0] : -1;
+            const int p1 = e1 >= 0 ? row_idx[e1] : -1;
             int v0 = 0, v1 = 0;
             bool r0 = p0 < 0, r1 = p1 < 0;
             int64_t t0 = 0;
@@ -1670,8 +1676,12 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         }
     }
     if (use == PDB_SCHED_DATAFLOW) {
-        // previous-writer rows into cand
-        if (nnz > 0) {
+        // long rows, not chain-like (the chain check ran and found many
+        // breaks): a wave per example
+        const bool rowwave = chain_checked && !chain_like && nnz >= kRowWaveMinAvg * n;
+        // previous-writer rows into cand (the wave-per-example form looks
+        // them up itself)
+        if (nnz > 0 && !rowwave) {
             k_prev_row<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(pn, nnz, w.row_idx,
                                                                         w.cand);
             PDB_LAUNCHED();
@@ -1679,9 +1689,6 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 0);
         PDB_LAUNCHED();
         if (n > kFlowMaxN) return PDB_ERR_UNSUPPORTED;
-        // long rows, not chain-like (the chain check ran and found many
-        // breaks): a wave per example
-        const bool rowwave = chain_checked && !chain_like && nnz >= kRowWaveMinAvg * n;
         const size_t lds = rowwave ? 0 : (size_t)kFlowWaveLds * 4 * (kBlock / kWave);
         const void *fn = rowwave ? reinterpret_cast<const void *>(&k_levels_rowwave)
                                  : reinterpret_cast<const void *>(&k_levels_dataflow);
@@ -1699,13 +1706,16 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         {
             // cooperative: the whole grid resident (the waves wait on each other)
             const int64_t *a_rp = csr->row_ptr;
-            const int32_t *a_prev = w.cand;
+            const int32_t *a_prev = rowwave ? pn : w.cand;
+            const int32_t *a_rows = w.row_idx;
             int32_t *a_level = lv->level;
             Ctrl *a_ctrl = w.ctrl;
             int64_t a_n = n, a_timeout = timeout;
-            void *args[] = {&a_rp, &a_prev, &a_n, &a_level, &a_ctrl, &a_timeout};
+            void *args_flow[] = {&a_rp, &a_prev, &a_n, &a_level, &a_ctrl, &a_timeout};
+            void *args_row[] = {&a_rp, &a_prev, &a_rows, &a_n, &a_level, &a_ctrl, &a_timeout};
             PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)std::max<int64_t>(grid, 1)),
-                                               dim3(kBlock), args, lds, s));
+                                               dim3(kBlock), rowwave ? args_row : args_flow, lds,
+                                               s));
         }
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
