@@ -14,9 +14,14 @@ iterations for dense gradient descent).
 Default workload: 10M examples x 1M features, 50 entries per example with
 Zipf(1.2) feature ids, binary values, logistic loss, lr 0.01.
 
-Prints one JSON line.  `roofline` prices the dominant kernel (the epoch)
-against HBM bandwidth with its algorithmic bytes; `cpu_baseline` times the
-CPU oracle on a bounded prefix of the same workload.
+Prints one JSON line.  `parity` compares the last step's result with the CPU
+oracle on the whole workload (levels bit-exact, weights within 1e-5 of the
+natural summation order and bitwise equal to the matched one); `value` is
+0 and `invalid` says why when any of them fails.  `roofline` prices the
+dominant kernel (the epoch) against HBM bandwidth with its algorithmic
+bytes, next to the copy rate the library's stream kernel reaches on the same
+GPU; `cpu_baseline` times the CPU oracle on a bounded prefix of the same
+workload.  --microbench prints the copy, hand-over and barrier figures alone.
 """
 from __future__ import annotations
 
@@ -33,6 +38,7 @@ sys.path.insert(0, _ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "sequentially-correct nnz-updates/sec per epoch + achieved HBM GB/s fraction"
+NATURAL_TOL = 1e-5
 
 
 def algorithmic_bytes(g, L, mf=False, U=None, nb=None):
@@ -53,7 +59,7 @@ def algorithmic_bytes(g, L, mf=False, U=None, nb=None):
 
 
 def source_digest(batch=False, stale=False, dense=False):
-    """Digest of the sources of the priced epoch kernel: a traffic record
+    """Digest of the sources of the priced epoch kernel: a counter record
     taken on other sources is not reported."""
     h = hashlib.sha256()
     main = "dense.hip" if dense else ("stale.hip" if stale else ("batch.hip" if batch else "apply.hip"))
@@ -63,19 +69,34 @@ def source_digest(batch=False, stale=False, dense=False):
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload, digest):
-    """HBM bytes per epoch launch from the committed counter summary, if it was
-    taken on the current kernel source; else None."""
-    path = os.path.join(_ROOT, "profiles", "traffic_%s.md" % workload)
+def read_profile(kind, workload, digest):
+    """The JSON record of profiles/<kind>_<workload>.md (a line starting with
+    '<kind>_json:'), if it was taken on the current kernel source; else None."""
+    path = os.path.join(_ROOT, "profiles", "%s_%s.md" % (kind, workload))
     if not os.path.exists(path):
         return None
     vals = {}
     for line in open(path):
-        if line.startswith("traffic_json:"):
+        if line.startswith("%s_json:" % kind):
             vals = json.loads(line.split(":", 1)[1])
     if vals.get("source_digest") != digest:
         return None
-    return vals.get("hbm_bytes_per_launch")
+    return vals
+
+
+def read_traffic(workload, digest):
+    """HBM bytes per epoch launch from the committed counter summary."""
+    rec = read_profile("traffic", workload, digest)
+    return None if rec is None else rec.get("hbm_bytes_per_launch")
+
+
+def read_l2(workload, digest):
+    """L2 hits, misses and hit rate of the epoch kernel per launch."""
+    rec = read_profile("l2", workload, digest)
+    if rec is None:
+        return None
+    return {k: rec[k] for k in ("hit_rate", "hits_per_launch", "misses_per_launch", "kernel")
+            if k in rec}
 
 
 def trimmed_mean(xs):
@@ -85,10 +106,80 @@ def trimmed_mean(xs):
     return sum(xs) / len(xs)
 
 
-def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0, delay=-1):
+def host_cpu():
+    """lscpu's model name and the host threads this process may use."""
+    model = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count()
+    return {"model": model, "nproc": nproc, "threads_in_host": os.cpu_count()}
+
+
+def copy_peak(dev, nbytes=1 << 30, reps=10):
+    """The library's streaming copy of nbytes, timed with events: read plus
+    written bytes per second (GB/s), trimmed mean of reps runs."""
+    import torch
+
+    from paper_1508_00703_amd import native
+
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(2):
+        native.pdb_mb_copy(src, dst)
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        native.pdb_mb_copy(src, dst)
+        b.record(stream)
+        times.append((a, b))
+    torch.cuda.synchronize()
+    ms = trimmed_mean([a.elapsed_time(b) for a, b in times])
+    del src, dst
+    return 2.0 * nbytes / (ms * 1e-3) / 1e9
+
+
+def microbench(args):
+    """Copy rate, device-scope hand-over latency and grid-barrier cost."""
+    import torch
+
+    from paper_1508_00703_amd import native
+
+    native.load()
+    dev = torch.device("cuda:0")
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    out = {"microbench": True, "device": torch.cuda.get_device_name(dev), "compute_units": cus,
+           "copy_gbs": {}, "hop_ns": {}, "barrier_ns": {}}
+    for gib in (1, 4):
+        out["copy_gbs"]["%d GiB" % gib] = copy_peak(dev, gib << 30)
+        print("copy %d GiB done" % gib, file=sys.stderr, flush=True)
+    for partner in (1, 8, 9, 255):
+        ns, xa, xb = native.pdb_mb_hop(20000, partner, dev)
+        out["hop_ns"]["block 0 (XCD %d) <-> block %d (XCD %d)" % (xa, partner, xb)] = ns
+        print("hop %d done" % partner, file=sys.stderr, flush=True)
+    for blocks in (8, 64, cus):
+        out["barrier_ns"]["%d blocks" % blocks] = native.pdb_mb_barrier(5000, blocks, dev)
+        print("barrier %d done" % blocks, file=sys.stderr, flush=True)
+    print(json.dumps(out))
+
+
+def cpu_baseline(g, cfg_id, budget_s, batch=0, delay=-1, epochs=1):
     """The oracle (one-pass levels + grouping + natural-order epoch), single
     thread, on the first rows of the same workload (with batch > 0: batch
-    levels + grouping + the mini-batch epoch)."""
+    levels + grouping + the mini-batch epoch; with delay >= 0: previous
+    writers + the bounded-delay epoch).  Returns the record and, when the
+    prefix is the whole workload, the oracle's schedule and natural result
+    (reused by the parity check)."""
     import numpy as np
 
     import oracle
@@ -98,51 +189,106 @@ def cpu_baseline(g, cfg_id, budget_s, gpu_levels=None, batch=0, delay=-1):
     def run(rows):
         rp = g["row_ptr"][:rows + 1]
         col = g["col"][:rp[-1]]
+        val = None if mf or g["val"] is None else g["val"][:rp[-1]]
         t0 = time.perf_counter()
         if delay >= 0:
             oracle.prev_writer(rp, col, g["d"])
-            val = None if g["val"] is None else g["val"][:rp[-1]]
-            oracle.stale_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
-                               g["loss"], oracle.NATURAL, delay)
-            return time.perf_counter() - t0, int(rp[-1]), None
+            res = oracle.stale_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32),
+                                     g["lr"], g["loss"], oracle.NATURAL, delay)
+            return time.perf_counter() - t0, int(rp[-1]), None, res
         if batch:
-            level, perm, level_ptr, L = oracle.batch_schedule(rp, col, g["d"], batch)
-            val = None if g["val"] is None else g["val"][:rp[-1]]
-            oracle.batch_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
-                               g["loss"], oracle.NATURAL, batch)
-            return time.perf_counter() - t0, int(rp[-1]), level
-        level, perm, level_ptr, L = oracle.schedule(rp, col, g["d"])
+            sched = oracle.batch_schedule(rp, col, g["d"], batch)
+            res = oracle.batch_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32),
+                                     g["lr"], g["loss"], oracle.NATURAL, batch)
+            return time.perf_counter() - t0, int(rp[-1]), sched, res
+        sched = oracle.schedule(rp, col, g["d"])
         if mf:
-            oracle.mf_epoch(g["user"][:rows], g["item"][:rows], g["rating"][:rows], g["U0"],
-                            g["V0"], g["lr"], g["reg"], oracle.NATURAL)
+            res = oracle.mf_epoch(g["user"][:rows], g["item"][:rows], g["rating"][:rows], g["U0"],
+                                  g["V0"], g["lr"], g["reg"], oracle.NATURAL)
         else:
-            val = None if g["val"] is None else g["val"][:rp[-1]]
-            oracle.sgd_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32), g["lr"],
-                             g["loss"], oracle.NATURAL)
-        return time.perf_counter() - t0, int(rp[-1]), level
+            res = oracle.sgd_epoch(rp, col, val, g["y"][:rows], np.zeros(g["d"], np.float32),
+                                   g["lr"], g["loss"], oracle.NATURAL)
+        return time.perf_counter() - t0, int(rp[-1]), sched, res
 
     n = g["n"]
     probe = min(n, 20000)
-    t, _, _ = run(probe)
+    t, _, _, _ = run(probe)
     rows = int(min(n, max(probe, probe * budget_s / max(t, 1e-6))))
     if batch:
         rows = min(n, max(batch, rows // batch * batch))  # whole batches
-    t, nnz_s, level = run(rows)
+    t, nnz_s, sched, res = run(rows)
     units = rows if mf else nnz_s
-    res = {"value": units / t, "unit": "ratings/s" if mf else "nnz-updates/s", "cores": 1,
+    cpu = host_cpu()
+    rec = {"value": units / t, "unit": "ratings/s" if mf else "nnz-updates/s", "cores": 1,
            "kind": "oracle",
            "sample": "first %d of %d %s (%d stored entries), %s + natural-order %sepoch, "
-                     "%.1f s" % (
+                     "%.1f s, one thread" % (
                          rows, n, "ratings" if mf else "examples", nnz_s,
                          "previous writers" if delay >= 0 else
                          "one-pass %slevels + grouping" % ("batch " if batch else ""),
                          "mini-batch (B=%d) " % batch if batch else
                          ("delay-%d " % delay if delay >= 0 else ""), t),
-           "host_cpu": platform.processor() or platform.machine()}
-    if gpu_levels is not None and level is not None:
-        k = len(level) if batch else rows
-        res["sample_levels_equal_gpu"] = bool(np.array_equal(gpu_levels[:k], level[:k]))
-    return res
+           "host_cpu": cpu["model"], "host_nproc": cpu["nproc"],
+           "host_threads": cpu["threads_in_host"]}
+    whole = rows == n and epochs == 1
+    return rec, (sched if whole else None), (res if whole else None)
+
+
+def parity_check(g, cfg_id, gpu_levels, gpu_result, sched=None, natural=None, batch=0, delay=-1,
+                 epochs=1):
+    """The last step's result against the oracle on the whole workload:
+    levels (and grouping) bit-exact, weights within NATURAL_TOL of the natural
+    summation order and bitwise equal to the matched one (the summation order
+    the kernels use).  sched / natural: the oracle's schedule and natural
+    result when already computed on the whole workload."""
+    import numpy as np
+
+    import oracle
+
+    t0 = time.perf_counter()
+    mf = cfg_id == 5
+    out = {"scope": "whole workload", "tol_natural": NATURAL_TOL}
+    if delay < 0 and gpu_levels is not None:
+        if sched is None:
+            sched = (oracle.batch_schedule(g["row_ptr"], g["col"], g["d"], batch) if batch
+                     else oracle.schedule(g["row_ptr"], g["col"], g["d"]))
+        level, perm, level_ptr, L = sched
+        lv_level, lv_perm, lv_ptr, lv_L = gpu_levels
+        out["levels_equal"] = bool(lv_L == L and np.array_equal(lv_level, level) and
+                                   np.array_equal(lv_perm, perm) and
+                                   np.array_equal(lv_ptr[:L + 1], level_ptr))
+    else:
+        out["levels_equal"] = None  # bounded delay runs on previous writers, not levels
+
+    def epochs_of(mode):
+        if mf:
+            U, V = g["U0"], g["V0"]
+            for _ in range(epochs):
+                U, V = oracle.mf_epoch(g["user"], g["item"], g["rating"], U, V, g["lr"], g["reg"],
+                                       mode)
+            return [U, V]
+        w = np.zeros(g["d"], np.float32)
+        args = (g["row_ptr"], g["col"], g["val"], g["y"])
+        for _ in range(epochs):
+            if batch:
+                w = oracle.batch_epoch(*args, w, g["lr"], g["loss"], mode, batch)
+            elif delay >= 0:
+                w = oracle.stale_epoch(*args, w, g["lr"], g["loss"], mode, delay)
+            else:
+                w = oracle.sgd_epoch(*args, w, g["lr"], g["loss"], mode)
+        return [w]
+
+    nat = ([natural] if not mf else list(natural)) if natural is not None else epochs_of(
+        oracle.NATURAL)
+    mat = epochs_of(oracle.MATCHED)
+    out["max_abs_dw_natural"] = float(max(np.max(np.abs(a - b), initial=0.0)
+                                          for a, b in zip(gpu_result, nat)))
+    out["bitwise_matched"] = bool(all(np.array_equal(a.view(np.int32), b.view(np.int32))
+                                      for a, b in zip(gpu_result, mat)))
+    out["ok"] = bool(out["levels_equal"] is not False and out["bitwise_matched"] and
+                     out["max_abs_dw_natural"] <= NATURAL_TOL)
+    out["oracle_s"] = time.perf_counter() - t0
+    return out
 
 
 DENSE_LDS_FLOATS = 36864  # the tile stays in LDS when cb + rb (rounded to 4) + rb cb fit
@@ -163,11 +309,13 @@ def dense_cpu_baseline(g, budget_s):
     t0 = time.perf_counter()
     oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.NATURAL, iters)
     t = time.perf_counter() - t0
+    cpu = host_cpu()
     return {"value": g["n"] * g["d"] * iters / t, "unit": "nnz-updates/s", "cores": 1,
             "kind": "oracle",
-            "sample": "all %d x %d entries, %d of %d iterations, natural order, %.1f s" % (
-                g["n"], g["d"], iters, g["iters"], t),
-            "host_cpu": platform.processor() or platform.machine()}
+            "sample": "all %d x %d entries, %d of %d iterations, natural order, %.1f s, "
+                      "one thread" % (g["n"], g["d"], iters, g["iters"], t),
+            "host_cpu": cpu["model"], "host_nproc": cpu["nproc"],
+            "host_threads": cpu["threads_in_host"]}
 
 
 def run_dense(args):
@@ -227,9 +375,24 @@ def run_dense(args):
     achieved = abytes / (ms * 1e-3) / 1e9
     workload = "dense%d" % args.dense
     digest = source_digest(dense=True)
+    got = w.cpu().numpy()
+    import oracle
+
+    t0 = time.perf_counter()
+    w0 = np.zeros(d, np.float32)
+    nat = oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.NATURAL, iters)
+    mat = oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.MATCHED, iters, rb, cb, 32)
+    tol = 1e-4 * float(np.abs(nat).max(initial=0.0)) + 1e-6
+    parity = {"scope": "whole workload", "levels_equal": None,
+              "max_abs_dw_natural": float(np.max(np.abs(got - nat), initial=0.0)),
+              "tol_natural": tol,
+              "bitwise_matched": bool(np.array_equal(got.view(np.int32), mat.view(np.int32))),
+              "oracle_s": time.perf_counter() - t0}
+    parity["ok"] = parity["bitwise_matched"] and parity["max_abs_dw_natural"] <= tol
+    peak = copy_peak(dev)
     out = {
         "metric": METRIC,
-        "value": n * d * iters * args.steps / elapsed,
+        "value": n * d * iters * args.steps / elapsed if parity["ok"] else 0.0,
         "unit": "nnz-updates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": elapsed * 1e3 / args.steps,
@@ -240,14 +403,19 @@ def run_dense(args):
                    "n": n, "d": d, "iters": iters, "seed": g["seed"], "row_block": rb,
                    "col_block": cb, "workers": -(-n // rb) * -(-d // cb),
                    "tile": "resident in LDS" if resident else "streamed every iteration"},
+        "parity": parity,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": read_traffic(workload, digest),
+                     "l2": read_l2(workload, digest),
+                     "peak_measured": peak, "frac_of_measured": achieved / peak,
                      "kernel": "k_dense_gd (all iterations)", "algorithmic_bytes": abytes,
                      "call_ms": ms, "call_ms_all": call_ms, "source_digest": digest,
                      "us_per_iteration": ms * 1e3 / max(iters, 1)},
         "epoch_ms": ms,
     }
+    if not parity["ok"]:
+        out["invalid"] = "parity with the oracle failed: the value is not counted"
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = dense_cpu_baseline(g, args.cpu_budget)
     print(json.dumps(out))
@@ -270,12 +438,19 @@ def main():
                     help="full-batch gradient descent on dense workload 1 (5000 x 960, "
                          "200 iterations) or 2 (500 x 1M, 50 iterations); 0 = sparse")
     ap.add_argument("--method", type=int, default=0,
-                    help="0 auto, 1 chain-scan, 2 dataflow, 3 spine")
+                    help="schedule method: 0 auto, 1 chain-scan, 2 dataflow, 3 spine, 4 chain, "
+                         "5 walk, 6 short-row walk")
+    ap.add_argument("--epoch-mode", type=int, default=0, choices=[0, 1, 2],
+                    help="epoch execution: 0 auto, 1 level by level, 2 sync-free")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true",
+                    help="skip the oracle comparison (the value is then reported as unchecked)")
+    ap.add_argument("--microbench", action="store_true",
+                    help="only the copy rate, device-scope hand-over and grid-barrier figures")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
-                    help="only copy BYTES of device memory once (a plain copy kernel of known "
-                         "size, for scaling HBM traffic counters) and exit")
+                    help="only copy BYTES of device memory once with the library's copy kernel "
+                         "(a plain copy of known size, for scaling HBM traffic counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: the path does not shard across GPUs "
@@ -286,12 +461,20 @@ def main():
     import torch
 
     if args.calibrate_copy:
-        src = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device="cuda:0")
+        from paper_1508_00703_amd import native
+
+        native.load()
+        nbytes = args.calibrate_copy // 16 * 16
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        native.pdb_mb_copy(src, dst)
         torch.cuda.synchronize()
-        print(json.dumps({"copied_bytes": src.numel() * 4}))
+        print(json.dumps({"copied_bytes": nbytes, "kernel": "k_mb_copy"}))
+        return
+
+    if args.microbench:
+        microbench(args)
         return
 
     if args.dense:
@@ -322,6 +505,7 @@ def main():
         g = dict(g)
         g["lr"] = np.float32(g["lr"] / batch)
     n, d, nnz = g["n"], g["d"], g["nnz"]
+    opt = native.options(epoch_mode=args.epoch_mode)
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None if mf else g["val"], dev)
     bt = native.Batches(n, nnz, batch, dev) if batch else None
     prev_row = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev) if delay >= 0 else None
@@ -353,12 +537,12 @@ def main():
         s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s0.record(stream)
         if batch:
-            info = native.pdb_batch_schedule(csr, n, d, bt, lv, args.method, ws=ws_s)
+            info = native.pdb_batch_schedule(csr, n, d, bt, lv, args.method, ws=ws_s, opt=opt)
         elif delay >= 0:
             # bounded delay needs only each entry's previous writer
             native.pdb_prev_writer(csr, n, d, prev_row, lv.prev_nz, ws=ws_s)
         else:
-            info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s)
+            info = native.pdb_schedule(csr, None, n, d, lv, args.method, ws=ws_s, opt=opt)
         s1.record(stream)
         sched_ms.append((s0, s1))
         if mf:
@@ -371,15 +555,17 @@ def main():
             a.record(stream)
             if mf:
                 native.pdb_mf_epoch(user, item, rating, n, U, g["n_users"], V, g["n_items"],
-                                    g["rank"], float(g["lr"]), float(g["reg"]), lv, ws=ws_e)
+                                    g["rank"], float(g["lr"]), float(g["reg"]), lv, ws=ws_e,
+                                    opt=opt)
             elif batch:
                 native.pdb_batch_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], bt, lv,
-                                       ws=ws_e)
+                                       ws=ws_e, opt=opt)
             elif delay >= 0:
                 native.pdb_stale_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], delay, lv,
-                                       ws=ws_e)
+                                       ws=ws_e, opt=opt)
             else:
-                native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], lv, ws=ws_e)
+                native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], lv, ws=ws_e,
+                                     opt=opt)
             b.record(stream)
             if timed:
                 ev.append((a, b))
@@ -411,7 +597,7 @@ def main():
     workload = "c%d" % cfg_id + ("-b%d" % batch if batch else "") + \
         ("-d%d" % delay if delay >= 0 else "")
     # the epoch kernel the library runs (the rule of pdb_sgd_epoch / pdb_mf_epoch)
-    mode = int(os.environ.get("PDB_EPOCH_MODE", "0"))
+    mode = args.epoch_mode
     syncfree = mode == 2 or (mode == 0 and L > 0 and n >= 8 * L)
     if batch:
         kernel = "k_batch_syncfree (mini-batch epoch)" if mode != 1 else \
@@ -424,7 +610,14 @@ def main():
     else:
         kernel = "k_levels_apply (epoch)"
     digest = source_digest(bool(batch), delay >= 0)
-    traffic = read_traffic(workload, digest)
+
+    # the last step's result and levels, copied out after the timed region
+    gpu_result = [U.cpu().numpy(), V.cpu().numpy()] if mf else [w.cpu().numpy()]
+    gpu_levels = None
+    if delay < 0:
+        gpu_levels = (lv.level.cpu().numpy(), lv.perm.cpu().numpy(), lv.level_ptr.cpu().numpy(),
+                      L)
+    peak = copy_peak(dev)
     out = {
         "metric": METRIC,
         "value": value,
@@ -446,9 +639,12 @@ def main():
                    "seed": g["seed"], "levels": None if delay >= 0 else L,
                    "max_level_width": None if delay >= 0 else lv.max_width_host,
                    "schedule_method": info.get("method_used"),
-                   "schedule_rounds": info.get("rounds")},
+                   "schedule_rounds": info.get("rounds"), "epoch_mode": args.epoch_mode},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": read_traffic(workload, digest),
+                     "l2": read_l2(workload, digest),
+                     "peak_measured": peak, "frac_of_measured": achieved / peak,
                      "kernel": kernel, "algorithmic_bytes": abytes,
                      "epoch_ms": ep, "epoch_ms_all": epoch_ms, "source_digest": digest,
                      # levels run one after another: the epoch is a dependent
@@ -458,10 +654,22 @@ def main():
         "schedule_ms": trimmed_mean([a.elapsed_time(b) for a, b in sched_ms]),
         "epoch_ms": ep,
     }
+    sched = natural = None
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(g, cfg_id, args.cpu_budget,
-                                           None if delay >= 0 else lv.level.cpu().numpy(),
-                                           batch, delay)
+        out["cpu_baseline"], sched, natural = cpu_baseline(g, cfg_id, args.cpu_budget, batch,
+                                                           delay, args.epochs)
+        print("cpu baseline done", file=sys.stderr, flush=True)
+    if args.no_parity:
+        out["parity"] = None
+        out["invalid"] = "parity not checked (--no-parity): the value is not counted"
+        out["value"] = 0.0
+    else:
+        out["parity"] = parity_check(g, cfg_id, gpu_levels, gpu_result, sched, natural, batch,
+                                     delay, args.epochs)
+        print("parity check done", file=sys.stderr, flush=True)
+        if not out["parity"]["ok"]:
+            out["invalid"] = "parity with the oracle failed: the value is not counted"
+            out["value"] = 0.0
     print(json.dumps(out))
 
 

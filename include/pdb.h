@@ -66,7 +66,7 @@ typedef enum pdb_status {
     PDB_ERR_WORKSPACE = -3,   /* workspace pointer NULL or smaller than required */
     PDB_ERR_HIP = -4,         /* a HIP runtime call failed; pdb_last_hip_error() has the code */
     PDB_ERR_DEVICE = -5,      /* a device-side check failed (spin-wait watchdog, inconsistent schedule) */
-    PDB_ERR_UNSUPPORTED = -6  /* sizes beyond 2^31 - 1 */
+    PDB_ERR_UNSUPPORTED = -6  /* sizes beyond 2^31 - 1, or beyond a limit an entry point states */
 } pdb_status;
 
 typedef enum pdb_loss { PDB_LOGISTIC = 0, PDB_SQUARED = 1 } pdb_loss;
@@ -87,10 +87,65 @@ typedef enum pdb_sched_method {
     PDB_SCHED_WALK = 5,      /* one block walks the rows in order, windows of rows staged in
                                 LDS; dataflow runs instead when a row holds more than 16384
                                 entries */
-    PDB_SCHED_SHORT = 6      /* short rows (matrix completion): one block walks chunks of 1024
-                                consecutive rows, each chunk's levels settled by rounds in LDS;
-                                dataflow runs instead when a row holds more than 4 entries */
+    PDB_SCHED_SHORT = 6      /* short rows (matrix completion): one block settles sub-chunks of
+                                64 consecutive rows strictly in order, one wave per sub-chunk in
+                                turn, each by rounds of lane shuffles, with the levels of the
+                                last 64 sub-chunks kept in an LDS ring; dataflow runs instead
+                                when a row holds more than 4 entries */
 } pdb_sched_method;
+/* Two dataflow forms.  The wave-per-example form runs when the chain check
+ * ran (PDB_SCHED_AUTO or PDB_SCHED_CHAIN), found the input not chain-like
+ * (more than a quarter of the examples share no feature with the one before
+ * them) and rows hold at least 16 entries on average.  Every other dataflow
+ * run, an explicit PDB_SCHED_DATAFLOW request among them, uses the batch form
+ * (64-example batches per wave). */
+
+/* Which execution pdb_sgd_epoch, pdb_mf_epoch and pdb_batch_epoch use. */
+typedef enum pdb_epoch_mode {
+    PDB_EPOCH_AUTO = 0,     /* sync-free when it is possible and levels are wide on average
+                               (n >= 8 L, L from pdb_levels.L_host), else level by level;
+                               mini-batches: sync-free whenever it is possible */
+    PDB_EPOCH_LEVELS = 1,   /* level by level */
+    PDB_EPOCH_SYNCFREE = 2  /* sync-free when possible (prev_nz set, workspace large enough) */
+} pdb_epoch_mode;
+
+/* Which execution pdb_stale_epoch uses. */
+typedef enum pdb_stale_mode {
+    PDB_STALE_AUTO = 0,      /* windowed on chain-like inputs whose windows fit, else sync-free */
+    PDB_STALE_SYNCFREE = 1,
+    PDB_STALE_WINDOWED = 2   /* windowed wherever the windows fit */
+} pdb_stale_mode;
+
+/* Execution options.  Every option selects among executions that give
+ * bitwise the same result, or bounds a device-side wait; none changes what is
+ * computed.  A NULL pointer means all defaults; otherwise fill the struct with
+ * pdb_options_init and change fields.  Options act only on the call they are
+ * passed to: the library keeps no configuration between calls and reads no
+ * environment variables. */
+typedef struct pdb_options {
+    int32_t epoch_mode;            /* pdb_epoch_mode (default PDB_EPOCH_AUTO) */
+    int32_t pipeline;              /* level-by-level epoch: 1 runs of narrow levels go through the
+                                      one-block pipeline (default), 0 every level on the plain path */
+    int32_t pipeline_width;        /* widest level a pipeline run may include (>= 1, default 4) */
+    int32_t thin_max;              /* widest level run by one block alone (>= 1, default 16) */
+    int64_t hot_features;          /* cap on the weights the pipeline caches in LDS; -1 (default)
+                                      all that fit */
+    int64_t spin_timeout_us;       /* watchdog of every device-side wait, in microseconds (default
+                                      20,000,000): a wait that lasts longer gives up, every kernel
+                                      of the call exits, and the call (or pdb_workspace_status)
+                                      reports PDB_ERR_DEVICE.  0 gives up on any wait not met
+                                      within a few polls, which exercises that path */
+    int32_t batch_thin_max;        /* level-by-level mini-batch epoch: widest batch level run by
+                                      one block alone (>= 1, default 2) */
+    int32_t batch_syncfree_blocks; /* sync-free mini-batch epoch: blocks in flight (>= 1,
+                                      default 32; at most one per compute unit) */
+    int32_t stale_mode;            /* pdb_stale_mode (default PDB_STALE_AUTO) */
+    int32_t dense_stream;          /* pdb_dense_gd: 1 streams the tiles from memory even when they
+                                      fit in LDS, 0 (default) keeps them resident when they fit */
+} pdb_options;
+
+/* Fills *opt with the defaults above.  Host only. */
+int pdb_options_init(pdb_options *opt);
 
 /* Sparse examples in CSR form (Definition 1: the immutable data set D). */
 typedef struct pdb_csr {
@@ -143,11 +198,13 @@ int pdb_epoch_workspace_bytes(int64_t d, size_t *bytes);
  * not NULL) and the host fields L_host, max_width_host.  labels is accepted
  * for symmetry with pdb_sgd_epoch and ignored: conflicts depend only on the
  * sparsity pattern.  ws: device workspace of at least
- * pdb_schedule_workspace_bytes().  Synchronous (it waits for the stream).
+ * pdb_schedule_workspace_bytes().  opt: only spin_timeout_us applies (the
+ * dataflow and short-row methods wait on device).  Synchronous (it waits
+ * for the stream); a device-side wait that gave up returns PDB_ERR_DEVICE.
  * Does not check the CSR: call pdb_validate_csr first on untrusted input. */
 int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
                  pdb_levels *levels, int method, pdb_schedule_info *info, void *ws,
-                 size_t ws_bytes, hipStream_t stream);
+                 size_t ws_bytes, const pdb_options *opt, hipStream_t stream);
 
 /* One SGD epoch over all n examples in place on w (device, [d]), with the
  * per-example arithmetic stated at the top of this header, for loss
@@ -164,30 +221,54 @@ int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
  *     block resident, so the earliest unfinished example always runs; a
  *     refused launch returns PDB_ERR_HIP).  Chosen when
  *     n >= 8 L, levels->prev_nz is set and ws_bytes covers
- *     pdb_epoch_workspace_bytes(d) (environment PDB_EPOCH_MODE=1 or 2 forces
- *     levels or sync-free).
+ *     pdb_epoch_workspace_bytes(d) (opt->epoch_mode forces levels or, where
+ *     possible, sync-free).
  * ws: at least pdb_epoch_workspace_bytes(0).  Asynchronous; a device error
  * (watchdog) is reported by pdb_workspace_status on ws. */
 int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
                   float lr, int loss, const pdb_levels *levels, void *ws, size_t ws_bytes,
-                  hipStream_t stream);
+                  const pdb_options *opt, hipStream_t stream);
 
-/* One matrix-completion SGD epoch (rank 32): rating t touches user row
- * U[user[t]] (device [n_users*32]) and item row V[item[t]] (device
- * [n_items*32]); levels from pdb_schedule on the CSR whose row t is
- * {user[t], n_users + item[t]}.  Runs level by level or sync-free under the
+/* One matrix-completion SGD epoch (rank 32).  Rating t's loss is Eq. 2's
+ * squared error with its L2 regulariser on the two factor rows it touches,
+ * (r_t - <U_u, V_i>)^2 / 2 + reg (|U_u|^2 + |V_i|^2) / 2, and its update is
+ * the gradient step of Sec. 2 on that loss (the per-rating arithmetic at the
+ * top of this header; both rows from their values before the step).  Rating
+ * t touches user row U[user[t]] (device [n_users*32]) and item row
+ * V[item[t]] (device [n_items*32]); levels from pdb_schedule on the CSR whose
+ * row t is {user[t], n_users + item[t]}.  Runs level by level or sync-free under the
  * rule of pdb_sgd_epoch (the sync-free run needs levels->prev_nz and
  * pdb_epoch_workspace_bytes((n_users + n_items) * 32)).  Asynchronous. */
 int pdb_mf_epoch(const int32_t *user, const int32_t *item, const float *rating, int64_t n,
                  float *U, int64_t n_users, float *V, int64_t n_items, int32_t rank, float lr,
                  float reg, const pdb_levels *levels, void *ws, size_t ws_bytes,
-                 hipStream_t stream);
+                 const pdb_options *opt, hipStream_t stream);
 
 /* Checks row_ptr[0] == 0, row_ptr non-decreasing, row_ptr[n] == nnz, every
  * column in [0, d) and strictly increasing within its row.  Synchronous.
  * Returns PDB_OK or PDB_ERR_BAD_CSR.  ws: pdb_epoch_workspace_bytes(). */
 int pdb_validate_csr(const pdb_csr *csr, int64_t n, int64_t d, void *ws, size_t ws_bytes,
                      hipStream_t stream);
+
+/* Checks that levels are a schedule the epoch may run (Theorem 2 with the
+ * read/write constraints of Sec. 4.4 at feature grain):
+ *   - level_ptr[0] = 0, non-decreasing, level_ptr[L] = n with L = *n_levels
+ *     (1 <= L <= n when n > 0), and perm a permutation of 0..n-1 with
+ *     level[perm[e]] = l for every e in [level_ptr[l-1], level_ptr[l]);
+ *   - along every feature's occurrences in example order the levels strictly
+ *     increase: each example's level exceeds that of the latest earlier
+ *     example sharing a feature with it.  That makes every level's examples
+ *     pairwise feature-disjoint and puts every conflicting earlier example in
+ *     a lower level;
+ *   - when levels->prev_nz is set, it equals the previous writers computed
+ *     here from the CSR.
+ * The previous writers are recomputed from the CSR (the transpose of
+ * pdb_schedule), so nothing in levels is trusted.  ws: at least
+ * pdb_schedule_workspace_bytes(n, d, nnz).  Synchronous.  Returns PDB_OK, or
+ * PDB_ERR_DEVICE when a check fails (and writes nothing).  Does not check the
+ * CSR: call pdb_validate_csr first on untrusted input. */
+int pdb_validate_schedule(const pdb_csr *csr, int64_t n, int64_t d, const pdb_levels *levels,
+                          void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Waits for the stream, then returns PDB_ERR_DEVICE if a kernel that used
  * ws recorded a device-side failure (and clears it), else PDB_OK. */
@@ -229,7 +310,8 @@ typedef struct pdb_batches {
  * ws: at least pdb_schedule_workspace_bytes(n, d, nnz).  Synchronous. */
 int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int64_t batch,
                        pdb_batches *batches, pdb_levels *levels, int method,
-                       pdb_schedule_info *info, void *ws, size_t ws_bytes, hipStream_t stream);
+                       pdb_schedule_info *info, void *ws, size_t ws_bytes,
+                       const pdb_options *opt, hipStream_t stream);
 
 /* One epoch of mini-batch gradient descent in place on w (device, [d]).
  * Batch b, in the sequential order of batches: every example i of b computes
@@ -245,12 +327,14 @@ int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int64_t batch,
  *     batches in index order, each waiting only until each of its features
  *     was written by its previous writer (levels->prev_nz over the union
  *     entries), no barriers.  Chosen when levels->prev_nz is set and ws_bytes
- *     covers pdb_epoch_workspace_bytes(d) (PDB_EPOCH_MODE=1 forces levels).
+ *     covers pdb_epoch_workspace_bytes(d) (opt->epoch_mode = PDB_EPOCH_LEVELS forces
+ *     batch levels).
  * ws: at least pdb_epoch_workspace_bytes(0).  Asynchronous; a device error
  * (watchdog) is reported by pdb_workspace_status on ws. */
 int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, int64_t batch,
                     float *w, float lr, int loss, const pdb_batches *batches,
-                    const pdb_levels *levels, void *ws, size_t ws_bytes, hipStream_t stream);
+                    const pdb_levels *levels, void *ws, size_t ws_bytes,
+                    const pdb_options *opt, hipStream_t stream);
 
 /* Device workspace (bytes) for pdb_stale_epoch: the control block, one
  * 64-bit word and three ints per stored entry.  Host-only arithmetic. */
@@ -272,8 +356,8 @@ int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes);
  *   - windowed, one block: examples in windows of delay + 1, whose reads all
  *     come from earlier windows; chosen when every window holds at most 2048
  *     examples and 2048 stored entries and at most a quarter of the examples
- *     share no feature with the example before them (PDB_STALE_MODE=1 forces
- *     the sync-free execution, 2 the windowed one where windows fit);
+ *     share no feature with the example before them (opt->stale_mode forces
+ *     the sync-free execution, or the windowed one where windows fit);
  *   - sync-free: examples in index order, each waiting on the words of its
  *     read sources and previous writers (dealt to the waves of a
  *     cooperatively launched grid in turn, as in pdb_sgd_epoch).
@@ -282,7 +366,7 @@ int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes);
  * by pdb_workspace_status on ws. */
 int pdb_stale_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
                     float lr, int loss, int64_t delay, const int32_t *prev_nz, void *ws,
-                    size_t ws_bytes, hipStream_t stream);
+                    size_t ws_bytes, const pdb_options *opt, hipStream_t stream);
 
 /* Dense full-batch gradient descent (the update of Sec. 2 with every example
  * in every iteration; the dense linear-regression workloads of Sec. 6.1-6.2).
@@ -317,7 +401,8 @@ int pdb_dense_workspace_bytes(int64_t n, int64_t d, int64_t row_block, int64_t c
  * from 0; G_j adds the row blocks' partials in block order.  The tile of a
  * worker stays in LDS across iterations when col_block + row_block (rounded
  * up to 4) + row_block col_block floats, plus room for its staged partials,
- * fit 36864 floats; otherwise it is read from memory twice per iteration.  Worker (r, c) waits only for the
+ * fit 36864 floats (unless opt->dense_stream is set); otherwise it is read
+ * from memory twice per iteration.  Worker (r, c) waits only for the
  * partials of its row group and of its column group (the read constraint of
  * Sec. 4.4 per partition), never on a grid-wide barrier; the R C workers
  * must be resident at once (one per compute unit; PDB_ERR_UNSUPPORTED
@@ -327,7 +412,8 @@ int pdb_dense_workspace_bytes(int64_t n, int64_t d, int64_t row_block, int64_t c
  * on ws. */
 int pdb_dense_gd(const float *X, int64_t ldx, const float *labels, int64_t n, int64_t d,
                  float *w, float lr, int loss, int64_t iters, int64_t row_block,
-                 int64_t col_block, void *ws, size_t ws_bytes, hipStream_t stream);
+                 int64_t col_block, void *ws, size_t ws_bytes, const pdb_options *opt,
+                 hipStream_t stream);
 
 /* Per-feature occurrence lists (the transpose that exposes which examples
  * share a feature): col_ptr (device, [d+1]) and csc_row (device, [nnz],

@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libpdb.so")
-SOURCES = ["radix.hip", "schedule.hip", "apply.hip", "batch.hip", "stale.hip", "dense.hip", "abi.hip"]
+SOURCES = ["radix.hip", "schedule.hip", "apply.hip", "batch.hip", "stale.hip", "dense.hip", "abi.hip",
+           "mb.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

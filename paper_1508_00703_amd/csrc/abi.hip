@@ -1,6 +1,6 @@
 // C-ABI plumbing: error strings, HIP error capture, CSR validation, device
 // status word, spin-wait budget.
-#include <cstdlib>
+#include <atomic>
 
 #include "pdb_internal.h"
 
@@ -43,19 +43,52 @@ __global__ void k_ctrl_clear(Ctrl *c) {
 
 void set_hip_error(hipError_t e) { g_last_hip_error = (int)e; }
 
-int64_t spin_timeout_ticks() {
-    static int64_t ticks = -1;
-    if (ticks < 0) {
-        const char *s = getenv("PDB_SPIN_TIMEOUT_MS");
-        const int64_t ms = s ? atoll(s) : 20000;
-        int dev = 0, khz = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
-            khz <= 0)
-            khz = 100000;
-        ticks = (ms > 0 ? ms : 1) * (int64_t)khz;
-    }
-    return ticks;
+namespace {
+// constant-clock rate (kHz) per device, queried once; 0 = not yet known.
+// Concurrent first calls may both query: they store the same value.
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_clock_khz[kMaxDevices];
+
+int clock_khz() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 100000;
+    std::atomic<int> *slot = dev < kMaxDevices ? &g_clock_khz[dev] : nullptr;
+    int khz = slot ? slot->load(std::memory_order_relaxed) : 0;
+    if (khz > 0) return khz;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+        khz <= 0)
+        khz = 100000;  // the gfx9 constant clock runs at 100 MHz
+    if (slot) slot->store(khz, std::memory_order_relaxed);
+    return khz;
+}
+}  // namespace
+
+int resolve_opts(const pdb_options *o, Opts *out) {
+    pdb_options d;
+    pdb_options_init(&d);
+    if (!o) o = &d;
+    if (o->epoch_mode < PDB_EPOCH_AUTO || o->epoch_mode > PDB_EPOCH_SYNCFREE)
+        return PDB_ERR_INVALID_ARG;
+    if (o->stale_mode < PDB_STALE_AUTO || o->stale_mode > PDB_STALE_WINDOWED)
+        return PDB_ERR_INVALID_ARG;
+    if ((o->pipeline != 0 && o->pipeline != 1) || (o->dense_stream != 0 && o->dense_stream != 1))
+        return PDB_ERR_INVALID_ARG;
+    if (o->pipeline_width < 1 || o->thin_max < 1 || o->batch_thin_max < 1 ||
+        o->batch_syncfree_blocks < 1 || o->hot_features < -1 || o->spin_timeout_us < 0)
+        return PDB_ERR_INVALID_ARG;
+    // at most about 10^5 s, so the tick count stays far from overflow
+    if (o->spin_timeout_us > (int64_t)100000 * 1000000) return PDB_ERR_INVALID_ARG;
+    out->epoch_mode = o->epoch_mode;
+    out->pipeline = o->pipeline != 0;
+    out->pipeline_width = o->pipeline_width;
+    out->thin_max = o->thin_max;
+    out->hot_cap = o->hot_features;
+    out->timeout = o->spin_timeout_us * (int64_t)clock_khz() / 1000;
+    out->batch_thin_max = o->batch_thin_max;
+    out->batch_sf_blocks = o->batch_syncfree_blocks;
+    out->stale_mode = o->stale_mode;
+    out->dense_stream = o->dense_stream != 0;
+    return PDB_OK;
 }
 
 }  // namespace pdbk
@@ -69,13 +102,28 @@ extern "C" const char *pdb_strerror(int status) {
     case PDB_ERR_BAD_CSR: return "malformed CSR (row_ptr not monotone / not ending at nnz, column out of range, columns not strictly increasing in a row)";
     case PDB_ERR_WORKSPACE: return "workspace missing or smaller than the size query returned";
     case PDB_ERR_HIP: return "a HIP runtime call failed (see pdb_last_hip_error)";
-    case PDB_ERR_DEVICE: return "device-side failure (spin-wait watchdog expired or inconsistent schedule)";
-    case PDB_ERR_UNSUPPORTED: return "size beyond 2^31-1 entries";
+    case PDB_ERR_DEVICE: return "device-side failure (spin-wait watchdog expired, or the schedule check failed)";
+    case PDB_ERR_UNSUPPORTED: return "size beyond 2^31-1 entries, or beyond the limit the entry point states";
     default: return "unknown pdb status";
     }
 }
 
 extern "C" int pdb_last_hip_error(void) { return g_last_hip_error; }
+
+extern "C" int pdb_options_init(pdb_options *o) {
+    if (!o) return PDB_ERR_INVALID_ARG;
+    o->epoch_mode = PDB_EPOCH_AUTO;
+    o->pipeline = 1;
+    o->pipeline_width = 4;
+    o->thin_max = 16;
+    o->hot_features = -1;
+    o->spin_timeout_us = 20000000;
+    o->batch_thin_max = 2;
+    o->batch_syncfree_blocks = 32;
+    o->stale_mode = PDB_STALE_AUTO;
+    o->dense_stream = 0;
+    return PDB_OK;
+}
 
 extern "C" int pdb_validate_csr(const pdb_csr *csr, int64_t n, int64_t d, void *ws,
                                 size_t ws_bytes, hipStream_t s) {

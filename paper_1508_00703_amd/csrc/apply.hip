@@ -34,7 +34,6 @@
 // from a small LDS ring; all other cold features are prefetched from global
 // memory kD examples ahead (their last writer finished before the prefetch).
 #include <climits>
-#include <cstdlib>
 
 #include "pdb_math.h"
 #include "pdb_words.h"
@@ -777,23 +776,18 @@ __global__ void k_ctrl_zero(Ctrl *c) {
     for (int i = threadIdx.x; i < (int)(sizeof(Ctrl) / sizeof(int)); i += blockDim.x) w[i] = 0;
 }
 
-int64_t env_setting(const char *name, int64_t dflt) {
-    const char *s = getenv(name);
-    return s ? atoll(s) : dflt;
-}
-
 template <class Op>
 int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, Ctrl *ctrl,
-                  hipStream_t s) {
-    // tuning knobs, read per call: widest level run by block 0 alone, and a
-    // cap on the number of weights cached in LDS by the width-1 pipeline
-    const int64_t thin = std::max<int64_t>(env_setting("PDB_THIN_MAX", 16), 1);
-    const int64_t hot_cap = env_setting("PDB_HOT_FEATURES", -1);
-    // widest level a pipeline run may include: a level of w examples costs w
-    // pipeline steps (about 140 ns each) instead of one block-barrier level
-    // (about 650 ns)
-    const int64_t chain_width = std::max<int64_t>(env_setting("PDB_CHAIN_WIDTH", 4), 1);
-    const int64_t timeout = spin_timeout_ticks();
+                  const Opts &opt, hipStream_t s) {
+    // the caller's options: widest level run by block 0 alone, a cap on the
+    // number of weights cached in LDS by the width-1 pipeline, and the
+    // widest level a pipeline run may include (a level of w examples costs
+    // w pipeline steps, about 140 ns each, instead of one block-barrier
+    // level, about 650 ns)
+    const int64_t thin = opt.thin_max;
+    const int64_t hot_cap = opt.hot_cap;
+    const int64_t chain_width = opt.pipeline_width;
+    const int64_t timeout = opt.timeout;
     k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
     PDB_LAUNCHED();
     const void *fn = reinterpret_cast<const void *>(&k_levels_apply<Op>);
@@ -1039,11 +1033,10 @@ int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *
 }
 
 int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_t n_users,
-                       int64_t n_items, int64_t L, void *ws, hipStream_t s) {
+                       int64_t n_items, int64_t L, void *ws, int64_t timeout, hipStream_t s) {
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
     unsigned long long *uvw =
         reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
-    const int64_t timeout = spin_timeout_ticks();
     k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
     PDB_LAUNCHED();
     if (n_users > 0)
@@ -1074,11 +1067,10 @@ int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_
 
 template <int LOSS, bool VAL>
 int launch_syncfree(const SgdOp<LOSS, VAL> &op, int64_t n, int64_t d, int64_t L, void *ws,
-                    hipStream_t s) {
+                    int64_t timeout, hipStream_t s) {
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
     unsigned long long *wv = reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) +
                                                                     sizeof(Ctrl));
-    const int64_t timeout = spin_timeout_ticks();
     k_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
     PDB_LAUNCHED();
     if (d > 0) {
@@ -1121,10 +1113,14 @@ extern "C" int pdb_epoch_workspace_bytes(int64_t d, size_t *bytes) {
     return PDB_OK;
 }
 
-extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
-                             float *w, float lr, int loss, const pdb_levels *lv, void *ws,
-                             size_t ws_bytes, hipStream_t s) {
+namespace {
+int sgd_epoch_impl(const pdb_csr *csr, const float *labels, int64_t n, int64_t d, float *w,
+                   float lr, int loss, const pdb_levels *lv, void *ws, size_t ws_bytes,
+                   const pdb_options *opt, hipStream_t s) {
     int rc = epoch_checks(lv, n, ws, ws_bytes);
+    if (rc != PDB_OK) return rc;
+    Opts o;
+    rc = resolve_opts(opt, &o);
     if (rc != PDB_OK) return rc;
     if (!csr || (n > 0 && (!csr->row_ptr || !labels || !w)) || (csr->nnz > 0 && !csr->col))
         return PDB_ERR_INVALID_ARG;
@@ -1134,22 +1130,21 @@ extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n,
     if (n == 0) return PDB_OK;
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
     const bool has_val = csr->val != nullptr;
-    const bool chain_env = env_setting("PDB_CHAIN", 1) != 0;
     // the width-1 pipeline addresses weights with 32-bit buffer offsets
-    const bool chain_ok = chain_env && lv->prev_nz != nullptr && d < (int64_t(1) << 29);
+    const bool chain_ok = o.pipeline && lv->prev_nz != nullptr && d < (int64_t(1) << 29);
     // sync-free when the levels are wide on average (a barrier per level
     // would cost more than a wait per feature), the previous writers are
-    // known and the workspace holds the packed words; PDB_EPOCH_MODE 1 / 2
-    // forces levels / sync-free
-    const int64_t mode = env_setting("PDB_EPOCH_MODE", 0);
+    // known and the workspace holds the packed words; the epoch mode option
+    // forces levels or sync-free
     const bool sf_ok = lv->prev_nz != nullptr && (int64_t)ws_bytes >= syncfree_ws_bytes(d);
     const bool wide = lv->L_host > 0 && n >= 8 * lv->L_host;
-    const bool syncfree = sf_ok && (mode == 2 || (mode == 0 && wide));
+    const bool syncfree =
+        sf_ok && (o.epoch_mode == PDB_EPOCH_SYNCFREE || (o.epoch_mode == PDB_EPOCH_AUTO && wide));
 #define PDB_SGD_CASE(LS, HV)                                                                 \
     if (loss == LS && has_val == HV) {                                                       \
         SgdOp<LS, HV> op{csr->row_ptr, csr->col, csr->val, labels, w, lv->perm, lv->prev_nz, lr}; \
-        if (syncfree) return launch_syncfree(op, n, d, lv->L_host, ws, s);                    \
-        return launch_levels(op, lv, d, chain_ok, ctrl, s);                                  \
+        if (syncfree) return launch_syncfree(op, n, d, lv->L_host, ws, o.timeout, s);         \
+        return launch_levels(op, lv, d, chain_ok, ctrl, o, s);                               \
     }
     PDB_SGD_CASE(PDB_LOGISTIC, true)
     PDB_SGD_CASE(PDB_LOGISTIC, false)
@@ -1159,11 +1154,22 @@ extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n,
     return PDB_ERR_INVALID_ARG;
 }
 
+}  // namespace
+
+extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
+                             float *w, float lr, int loss, const pdb_levels *lv, void *ws,
+                             size_t ws_bytes, const pdb_options *opt, hipStream_t s) {
+    return sgd_epoch_impl(csr, labels, n, d, w, lr, loss, lv, ws, ws_bytes, opt, s);
+}
+
 extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const float *rating,
                             int64_t n, float *U, int64_t n_users, float *V, int64_t n_items,
                             int32_t rank, float lr, float reg, const pdb_levels *lv, void *ws,
-                            size_t ws_bytes, hipStream_t s) {
+                            size_t ws_bytes, const pdb_options *opt, hipStream_t s) {
     int rc = epoch_checks(lv, n, ws, ws_bytes);
+    if (rc != PDB_OK) return rc;
+    Opts o;
+    rc = resolve_opts(opt, &o);
     if (rc != PDB_OK) return rc;
     if (rank != 32) return PDB_ERR_INVALID_ARG;
     if (n_users < 0 || n_items < 0) return PDB_ERR_INVALID_ARG;
@@ -1172,14 +1178,15 @@ extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const floa
     MfOp op{user, item, rating, U, V, lv->perm, lr, reg};
     // sync-free under the same rule as pdb_sgd_epoch; the packed words need
     // pdb_epoch_workspace_bytes((n_users + n_items) * 32)
-    const int64_t mode = env_setting("PDB_EPOCH_MODE", 0);
     const bool sf_ok = lv->prev_nz != nullptr &&
                        (int64_t)ws_bytes >= syncfree_ws_bytes((n_users + n_items) * 32) &&
                        n < INT32_MAX / 2;
     const bool wide = lv->L_host > 0 && n >= 8 * lv->L_host;
-    if (sf_ok && (mode == 2 || (mode == 0 && wide)))
-        return launch_mf_syncfree(op, lv->prev_nz, n, n_users, n_items, lv->L_host, ws, s);
-    return launch_levels(op, lv, n_users + n_items, false, static_cast<Ctrl *>(ws), s);
+    if (sf_ok &&
+        (o.epoch_mode == PDB_EPOCH_SYNCFREE || (o.epoch_mode == PDB_EPOCH_AUTO && wide)))
+        return launch_mf_syncfree(op, lv->prev_nz, n, n_users, n_items, lv->L_host, ws, o.timeout,
+                                  s);
+    return launch_levels(op, lv, n_users + n_items, false, static_cast<Ctrl *>(ws), o, s);
 }
 
 extern "C" int pdb_check_reciprocal(uint32_t lo_bits, uint32_t hi_bits, uint64_t *mismatches,

@@ -659,10 +659,10 @@ __global__ void k_batch_ctrl_zero(Ctrl *c) {
 }
 
 template <int LOSS, bool VAL>
-int launch_batch(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, Ctrl *ctrl, hipStream_t s) {
-    const char *e = getenv("PDB_BATCH_THIN_MAX");
-    const int64_t thin = std::max<int64_t>(e ? atoll(e) : 2, 1);
-    const int64_t timeout = spin_timeout_ticks();
+int launch_batch(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, Ctrl *ctrl, const Opts &opt,
+                 hipStream_t s) {
+    const int64_t thin = opt.batch_thin_max;
+    const int64_t timeout = opt.timeout;
     k_batch_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
     PDB_LAUNCHED();
     const void *fn = reinterpret_cast<const void *>(&k_batch_levels<LOSS, VAL>);
@@ -697,11 +697,11 @@ int64_t batch_sf_ws_bytes(int64_t d) { return (int64_t)sizeof(Ctrl) + align_up(8
 
 template <int LOSS, bool VAL>
 int launch_batch_syncfree(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, int64_t d,
-                          int64_t nb, void *ws, hipStream_t s) {
+                          int64_t nb, void *ws, const Opts &opt, hipStream_t s) {
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
     unsigned long long *bw =
         reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
-    const int64_t timeout = spin_timeout_ticks();
+    const int64_t timeout = opt.timeout;
     k_batch_ctrl_zero<<<1, 64, 0, s>>>(ctrl);
     PDB_LAUNCHED();
     if (d > 0) {
@@ -713,10 +713,9 @@ int launch_batch_syncfree(const BatchOp<LOSS, VAL> &op, const pdb_levels *lv, in
     int dev = 0, cus = 0;
     PDB_HIP(hipGetDevice(&dev));
     PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    const char *ge = getenv("PDB_BATCH_SF_BLOCKS");
     // at most 32 blocks by default: more batches in flight only add polls
     // that slow the frontier's memory accesses
-    const int64_t cap = ge ? std::max<int64_t>(atoll(ge), 1) : 32;
+    const int64_t cap = opt.batch_sf_blocks;
     const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus, cap), nb));
     k_batch_syncfree<LOSS, VAL><<<grid, kBB, 0, s>>>(op, lv->prev_nz, bw, nb, ctrl, timeout);
     PDB_LAUNCHED();
@@ -751,12 +750,17 @@ using namespace pdbk;
 extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int64_t batch,
                                   pdb_batches *bt, pdb_levels *lv, int method,
                                   pdb_schedule_info *info, void *ws, size_t ws_bytes,
-                                  hipStream_t s) {
+                                  const pdb_options *opt, hipStream_t s) {
     if (!csr || !bt || !lv || !ws || (n > 0 && !csr->row_ptr) || (csr->nnz > 0 && !csr->col))
         return PDB_ERR_INVALID_ARG;
     const int64_t nnz = csr->nnz;
     int rc = check_batch_sizes(n, d, nnz, batch);
     if (rc != PDB_OK) return rc;
+    {
+        Opts o;
+        rc = resolve_opts(opt, &o);  // checked here, applied by pdb_schedule
+        if (rc != PDB_OK) return rc;
+    }
     if (d == 0 && nnz > 0) return PDB_ERR_BAD_CSR;
     if (!bt->bptr || !bt->uptr ||
         (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row || !bt->occ_u)))
@@ -807,7 +811,7 @@ extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int6
     }
     // the batch levels: conflict levels of the union CSR, whose rows are the batches
     const pdb_csr ucsr{bt->bptr, bt->ucol, nullptr, bt->U_host};
-    rc = pdb_schedule(&ucsr, nullptr, nb, d, lv, method, info, ws, ws_bytes, s);
+    rc = pdb_schedule(&ucsr, nullptr, nb, d, lv, method, info, ws, ws_bytes, opt, s);
     if (rc != PDB_OK) return rc;
     // each union entry's next writer, when asked for and known
     if (bt->unext && bt->U_host > 0) {
@@ -826,7 +830,7 @@ extern "C" int pdb_batch_schedule(const pdb_csr *csr, int64_t n, int64_t d, int6
 extern "C" int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
                                int64_t batch, float *w, float lr, int loss,
                                const pdb_batches *bt, const pdb_levels *lv, void *ws,
-                               size_t ws_bytes, hipStream_t s) {
+                               size_t ws_bytes, const pdb_options *opt, hipStream_t s) {
     if (!csr || !labels || !w || !bt || !lv || !ws || !lv->perm || !lv->level_ptr ||
         !lv->n_levels)
         return PDB_ERR_INVALID_ARG;
@@ -840,25 +844,26 @@ extern "C" int pdb_batch_epoch(const pdb_csr *csr, const float *labels, int64_t 
         (nnz > 0 && (!bt->ucol || !bt->occ || !bt->occ_row || !bt->occ_u)))
         return PDB_ERR_INVALID_ARG;
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
+    Opts o;
+    rc = resolve_opts(opt, &o);
+    if (rc != PDB_OK) return rc;
     // sync-free when the previous writers over the union CSR are known and the
-    // workspace holds a word per feature; PDB_EPOCH_MODE 1 / 2 forces batch
-    // levels / sync-free
-    const char *me = getenv("PDB_EPOCH_MODE");
-    const int64_t mode = me ? atoll(me) : 0;
+    // workspace holds a word per feature, unless the epoch mode option asks
+    // for batch levels
     const bool sf_ok = lv->prev_nz != nullptr && (int64_t)ws_bytes >= batch_sf_ws_bytes(d);
-    const bool syncfree = sf_ok && mode != 1;
+    const bool syncfree = sf_ok && o.epoch_mode != PDB_EPOCH_LEVELS;
     const int64_t nb = cdiv(n, batch);
 #define PDB_BATCH(LOSS, VAL)                                                                     \
     (syncfree ? launch_batch_syncfree<LOSS, VAL>(                                              \
                     BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w, bt->bptr,   \
                                        bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u,         \
                                        bt->unext, n, batch, lr}, \
-                    lv, d, nb, ws, s)                                                           \
+                    lv, d, nb, ws, o, s)                                                        \
               : launch_batch<LOSS, VAL>(                                                       \
                     BatchOp<LOSS, VAL>{csr->row_ptr, csr->col, csr->val, labels, w, bt->bptr,   \
                                        bt->ucol, bt->uptr, bt->occ, bt->occ_row, bt->occ_u,         \
                                        bt->unext, n, batch, lr}, \
-                    lv, ctrl, s))
+                    lv, ctrl, o, s))
     if (loss == PDB_LOGISTIC) return csr->val ? PDB_BATCH(PDB_LOGISTIC, true) : PDB_BATCH(PDB_LOGISTIC, false);
     return csr->val ? PDB_BATCH(PDB_SQUARED, true) : PDB_BATCH(PDB_SQUARED, false);
 #undef PDB_BATCH

@@ -532,8 +532,11 @@ extern "C" int pdb_dense_workspace_bytes(int64_t n, int64_t d, int64_t row_block
 extern "C" int pdb_dense_gd(const float *X, int64_t ldx, const float *labels, int64_t n,
                             int64_t d, float *w, float lr, int loss, int64_t iters,
                             int64_t row_block, int64_t col_block, void *ws, size_t ws_bytes,
-                            hipStream_t s) {
+                            const pdb_options *opt, hipStream_t s) {
     if (!ws || n < 0 || d < 0 || iters < 0 || ldx < d) return PDB_ERR_INVALID_ARG;
+    Opts o;
+    const int orc = resolve_opts(opt, &o);
+    if (orc != PDB_OK) return orc;
     if (loss != PDB_LOGISTIC && loss != PDB_SQUARED) return PDB_ERR_INVALID_ARG;
     if (n >= INT32_MAX || d >= INT32_MAX || iters >= INT32_MAX) return PDB_ERR_UNSUPPORTED;
     if (n > 0 && d > 0 && (!X || !labels)) return PDB_ERR_INVALID_ARG;
@@ -550,11 +553,10 @@ extern "C" int pdb_dense_gd(const float *X, int64_t ldx, const float *labels, in
     k_dense_clear<<<grid_for(words, 256, 4096), 256, 0, s>>>(lay.zw, words, lay.ctrl);
     PDB_LAUNCHED();
     if (idle) return PDB_OK;
-    const char *e = getenv("PDB_DENSE_STREAM");
-    const bool res = !(e && atoi(e) != 0) && fits_resident(p.rb, p.cb, p.R, p.C);
+    const bool res = !o.dense_stream && fits_resident(p.rb, p.cb, p.R, p.C);
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) && (ldx % 4 == 0);
     DenseArgs a{X, ldx, labels, w, n, d, iters, lr, (int)p.rb, (int)p.cb, (int)p.R, (int)p.C,
-                lay.zw, lay.gw, lay.ctrl, spin_timeout_ticks()};
+                lay.zw, lay.gw, lay.ctrl, o.timeout};
     return loss == PDB_LOGISTIC ? dispatch_dense<PDB_LOGISTIC>(a, vec, res, s)
                                 : dispatch_dense<PDB_SQUARED>(a, vec, res, s);
 }

@@ -76,8 +76,22 @@ static_assert(sizeof(Ctrl) == 512, "Ctrl is two 256-byte lines");
 
 enum DeviceErr { DERR_NONE = 0, DERR_BARRIER_TIMEOUT = 1, DERR_WAIT_TIMEOUT = 2 };
 
-// Spin-wait budget in ticks of the 100 MHz constant clock (s_memrealtime).
-int64_t spin_timeout_ticks();
+// The caller's pdb_options, checked, with the watchdog converted to ticks of
+// the constant clock the kernels read (s_memrealtime) on the current device.
+struct Opts {
+    int epoch_mode;          // pdb_epoch_mode
+    bool pipeline;           // runs of narrow levels through the one-block pipeline
+    int64_t pipeline_width;  // widest level a pipeline run may include
+    int64_t thin_max;        // widest level run by one block alone
+    int64_t hot_cap;         // cap on weights cached in LDS, -1 none
+    int64_t timeout;         // watchdog of device-side waits, in clock ticks
+    int64_t batch_thin_max;
+    int64_t batch_sf_blocks;
+    int stale_mode;          // pdb_stale_mode
+    bool dense_stream;
+};
+// PDB_ERR_INVALID_ARG for out-of-range fields; NULL gives the defaults.
+int resolve_opts(const pdb_options *o, Opts *out);
 
 // ----------------------------------------------------------------------------
 // schedule workspace layout

@@ -1349,6 +1349,66 @@ __global__ __launch_bounds__(kBlock) void k_chain_levels(int64_t n, int32_t *__r
     }
 }
 
+// Schedule check, part 1: level_ptr non-decreasing from 0 to n, and every
+// position e of level l (level_ptr[l-1] <= e < level_ptr[l]) holding an
+// example p = perm[e] in [0, n) with level[p] = l, counted in seen[p] (a
+// permutation leaves every count at 1).  The level of e by binary search.
+__global__ __launch_bounds__(kBlock) void k_val_levels(const int32_t *__restrict__ level,
+                                                       const int32_t *__restrict__ perm,
+                                                       const int64_t *__restrict__ level_ptr,
+                                                       int64_t n, int64_t L,
+                                                       uint32_t *__restrict__ seen, Ctrl *ctrl) {
+    int bad = 0;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e <= n;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        if (e <= L) {
+            const int64_t v = level_ptr[e];
+            if (e == 0 && v != 0) bad = 1;
+            if (e == L && v != n) bad = 1;
+            if (e > 0 && v < level_ptr[e - 1]) bad = 1;
+        }
+        if (e == n) continue;
+        // the last l in [0, L) with level_ptr[l] <= e: position e is in level l + 1
+        int64_t lo = 0, hi = L;
+        while (hi - lo > 1) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (level_ptr[mid] <= e) lo = mid; else hi = mid;
+        }
+        const int32_t p = perm[e];
+        if (p < 0 || (int64_t)p >= n) {
+            bad = 1;
+            continue;
+        }
+        if ((int64_t)level[p] != lo + 1) bad = 1;
+        atomicAdd(&seen[p], 1u);
+    }
+    if (__ballot(bad) != 0ull && lane_id() == 0)
+        __hip_atomic_store(&ctrl->bad, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Schedule check, part 2: every example seen once; every stored entry's
+// example has a level above that of the example owning its previous entry on
+// the same feature (pn, recomputed from the CSR), and the caller's prev_nz,
+// when given, equals pn.
+__global__ __launch_bounds__(kBlock) void k_val_order(const int32_t *__restrict__ level,
+                                                      const uint32_t *__restrict__ seen, int64_t n,
+                                                      const int32_t *__restrict__ pn,
+                                                      const int32_t *__restrict__ row_idx,
+                                                      const int32_t *__restrict__ prev_nz,
+                                                      int64_t nnz, Ctrl *ctrl) {
+    int bad = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += stride)
+        if (seen[i] != 1u) bad = 1;
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < nnz; p += stride) {
+        const int32_t q = pn[p];
+        if (prev_nz && prev_nz[p] != q) bad = 1;
+        if (q >= 0 && level[row_idx[q]] >= level[row_idx[p]]) bad = 1;
+    }
+    if (__ballot(bad) != 0ull && lane_id() == 0)
+        __hip_atomic_store(&ctrl->bad, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 int bit_length(uint64_t x) {
     int b = 0;
     while (x) {
@@ -1358,15 +1418,13 @@ int bit_length(uint64_t x) {
     return b;
 }
 
+// compute units of the current device (queried per call: no cached state)
 int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-    }
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
     return cus;
 }
 
@@ -1501,10 +1559,13 @@ extern "C" int pdb_prev_writer(const pdb_csr *csr, int64_t n, int64_t d, int32_t
 
 extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
                             pdb_levels *lv, int method, pdb_schedule_info *info, void *ws,
-                            size_t ws_bytes, hipStream_t s) {
+                            size_t ws_bytes, const pdb_options *opt, hipStream_t s) {
     (void)labels;
     SchedWs w;
     int rc = sched_common_checks(csr, n, d, ws, ws_bytes, &w);
+    if (rc != PDB_OK) return rc;
+    Opts o;
+    rc = resolve_opts(opt, &o);
     if (rc != PDB_OK) return rc;
     if (!lv || !lv->level_ptr || !lv->n_levels || (n > 0 && (!lv->level || !lv->perm)))
         return PDB_ERR_INVALID_ARG;
@@ -1531,7 +1592,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     if (rc != PDB_OK) return rc;
     // the radix buffer pair that does not hold the sorted entries is free
     int32_t *free_k = reinterpret_cast<int32_t *>((sk == w.kA) ? w.kB : w.kA);
-    const int64_t timeout = spin_timeout_ticks();
+    const int64_t timeout = o.timeout;
 
     // a chain (every example conflicts with the one before it) is solved
     // outright; auto tries it first
@@ -1630,6 +1691,10 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
 
     if (use == PDB_SCHED_SHORT) {
         if (n > kFlowMaxN) return PDB_ERR_UNSUPPORTED;
+        // every row gets its level from the walk; zeros until then, so a walk
+        // that stops early leaves no stale levels behind
+        k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, 0);
+        PDB_LAUNCHED();
         if (nnz > 0) {
             k_prev_row<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(pn, nnz, w.row_idx,
                                                                         w.cand);
@@ -1645,6 +1710,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         PDB_LAUNCHED();
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
+        if (host.err) return PDB_ERR_DEVICE;      // a wave's wait gave up
         if (host.bad) use = PDB_SCHED_DATAFLOW;  // a row longer than kShortR
     }
 
@@ -1727,6 +1793,8 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     PDB_LAUNCHED();
     rc = read_ctrl(w.ctrl, &host, s);
     if (rc != PDB_OK) return rc;
+    // any level kernel whose wait gave up has left levels unfinished
+    if (host.err) return PDB_ERR_DEVICE;
     const int64_t L = host.max_level;
     if (L < 1 || L > n) return PDB_ERR_DEVICE;
     k_level_keys<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(lv->level, n, w.kB);
@@ -1746,4 +1814,45 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     lv->max_width_host = host.max_width;
     if (info) *info = pdb_schedule_info{use, rounds, L, (int64_t)host.max_width};
     return PDB_OK;
+}
+
+extern "C" int pdb_validate_schedule(const pdb_csr *csr, int64_t n, int64_t d,
+                                     const pdb_levels *lv, void *ws, size_t ws_bytes,
+                                     hipStream_t s) {
+    SchedWs w;
+    int rc = sched_common_checks(csr, n, d, ws, ws_bytes, &w);
+    if (rc != PDB_OK) return rc;
+    if (!lv || !lv->level_ptr || !lv->n_levels || (n > 0 && (!lv->level || !lv->perm)))
+        return PDB_ERR_INVALID_ARG;
+    int32_t L = 0;
+    PDB_HIP(hipMemcpyAsync(&L, lv->n_levels, sizeof(L), hipMemcpyDeviceToHost, s));
+    PDB_HIP(hipStreamSynchronize(s));
+    if (n == 0) {
+        int64_t first = -1;
+        PDB_HIP(hipMemcpyAsync(&first, lv->level_ptr, sizeof(first), hipMemcpyDeviceToHost, s));
+        PDB_HIP(hipStreamSynchronize(s));
+        return (L == 0 && first == 0) ? PDB_OK : PDB_ERR_DEVICE;
+    }
+    if (L < 1 || (int64_t)L > n) return PDB_ERR_DEVICE;
+    const int64_t nnz = csr->nnz;
+    Ctrl host{};
+    k_ctrl_init<<<1, 64, 0, s>>>(w.ctrl);
+    PDB_LAUNCHED();
+    // previous writers from the CSR itself (nothing of the schedule is used)
+    const uint32_t *sk, *sv;
+    rc = build_conflicts(csr, n, d, w, w.pn, w.col_ptr, nullptr, &sk, &sv, s);
+    if (rc != PDB_OK) return rc;
+    // the radix buffer pair that does not hold the sorted entries is free
+    uint32_t *seen = (sk == w.kA) ? w.kB : w.kA;
+    k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(reinterpret_cast<int32_t *>(seen), n,
+                                                             0);
+    k_val_levels<<<grid_for(n + 1, kBlock, 65536), kBlock, 0, s>>>(lv->level, lv->perm,
+                                                                    lv->level_ptr, n, L, seen,
+                                                                    w.ctrl);
+    k_val_order<<<grid_for(std::max(n, nnz), kBlock, 65536), kBlock, 0, s>>>(
+        lv->level, seen, n, w.pn, w.row_idx, lv->prev_nz, nnz, w.ctrl);
+    PDB_LAUNCHED();
+    rc = read_ctrl(w.ctrl, &host, s);
+    if (rc != PDB_OK) return rc;
+    return host.bad ? PDB_ERR_DEVICE : PDB_OK;
 }

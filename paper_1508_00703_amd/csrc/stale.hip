@@ -403,9 +403,9 @@ __global__ __launch_bounds__(kBlock) void k_stale_final(const int32_t *__restric
 
 template <int LOSS, bool VAL>
 int launch_stale(const pdb_csr *csr, const float *labels, int64_t n, float *w, float lr,
-                 int64_t delay, const int32_t *prev, StaleWs &ws, hipStream_t s) {
+                 int64_t delay, const int32_t *prev, StaleWs &ws, const Opts &opt, hipStream_t s) {
     const int64_t nnz = csr->nnz;
-    const int64_t timeout = spin_timeout_ticks();
+    const int64_t timeout = opt.timeout;
     k_stale_ctrl_zero<<<1, 64, 0, s>>>(ws.ctrl);
     PDB_LAUNCHED();
     if (nnz > 0) {
@@ -424,11 +424,10 @@ int launch_stale(const pdb_csr *csr, const float *labels, int64_t n, float *w, f
     // examples share a feature with the one before: one block then beats a
     // device-scope hop per example); elsewhere the sync-free one runs many
     // examples at once.  Read back: this call synchronises the stream.
-    const char *mode_env = getenv("PDB_STALE_MODE");
-    const int mode = mode_env ? atoi(mode_env) : 0;
+    const int mode = opt.stale_mode;
     const int64_t W = delay >= n ? std::max<int64_t>(n, 1) : delay + 1;  // no overflow at huge delays
     bool windowed = false;
-    if (mode != 1 && W <= kWinCap) {
+    if (mode != PDB_STALE_SYNCFREE && W <= kWinCap) {
         k_window_max<<<grid_for(cdiv(n, W), kBlock, 4096), kBlock, 0, s>>>(csr->row_ptr, n, W,
                                                                            ws.ctrl);
         PDB_LAUNCHED();
@@ -441,7 +440,7 @@ int launch_stale(const pdb_csr *csr, const float *labels, int64_t n, float *w, f
         PDB_HIP(hipMemcpyAsync(&host, ws.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, s));
         PDB_HIP(hipStreamSynchronize(s));
         const bool chain_like = 4 * (int64_t)host.chain_breaks <= n;
-        windowed = host.max_width <= kWinCap && (mode == 2 || chain_like);
+        windowed = host.max_width <= kWinCap && (mode == PDB_STALE_WINDOWED || chain_like);
     }
     if (windowed) {
         k_stale_window<LOSS, VAL><<<1, kWinThreads, 0, s>>>(csr->row_ptr, csr->col, csr->val,
@@ -494,8 +493,12 @@ extern "C" int pdb_stale_workspace_bytes(int64_t nnz, size_t *bytes) {
 
 extern "C" int pdb_stale_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
                                float *w, float lr, int loss, int64_t delay,
-                               const int32_t *prev_nz, void *ws, size_t ws_bytes, hipStream_t s) {
+                               const int32_t *prev_nz, void *ws, size_t ws_bytes,
+                               const pdb_options *opt, hipStream_t s) {
     if (!csr || !ws || n < 0 || d < 0 || delay < 0) return PDB_ERR_INVALID_ARG;
+    Opts o;
+    const int orc = resolve_opts(opt, &o);
+    if (orc != PDB_OK) return orc;
     if (n >= INT32_MAX || d >= INT32_MAX || csr->nnz >= INT32_MAX || csr->nnz < 0)
         return PDB_ERR_UNSUPPORTED;
     if (loss != PDB_LOGISTIC && loss != PDB_SQUARED) return PDB_ERR_INVALID_ARG;
@@ -506,8 +509,8 @@ extern "C" int pdb_stale_epoch(const pdb_csr *csr, const float *labels, int64_t 
     if (n == 0) return PDB_OK;
     const bool has_val = csr->val != nullptr;
     if (loss == PDB_LOGISTIC)
-        return has_val ? launch_stale<PDB_LOGISTIC, true>(csr, labels, n, w, lr, delay, prev_nz, lay, s)
-                       : launch_stale<PDB_LOGISTIC, false>(csr, labels, n, w, lr, delay, prev_nz, lay, s);
-    return has_val ? launch_stale<PDB_SQUARED, true>(csr, labels, n, w, lr, delay, prev_nz, lay, s)
-                   : launch_stale<PDB_SQUARED, false>(csr, labels, n, w, lr, delay, prev_nz, lay, s);
+        return has_val ? launch_stale<PDB_LOGISTIC, true>(csr, labels, n, w, lr, delay, prev_nz, lay, o, s)
+                       : launch_stale<PDB_LOGISTIC, false>(csr, labels, n, w, lr, delay, prev_nz, lay, o, s);
+    return has_val ? launch_stale<PDB_SQUARED, true>(csr, labels, n, w, lr, delay, prev_nz, lay, o, s)
+                   : launch_stale<PDB_SQUARED, false>(csr, labels, n, w, lr, delay, prev_nz, lay, o, s);
 }

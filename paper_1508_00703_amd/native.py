@@ -27,6 +27,8 @@ PDB_SCHED_AUTO, PDB_SCHED_CHAINSCAN, PDB_SCHED_DATAFLOW, PDB_SCHED_SPINE = 0, 1,
 PDB_SCHED_CHAIN = 4
 PDB_SCHED_WALK = 5
 PDB_SCHED_SHORT = 6
+PDB_EPOCH_AUTO, PDB_EPOCH_LEVELS, PDB_EPOCH_SYNCFREE = 0, 1, 2
+PDB_STALE_AUTO, PDB_STALE_SYNCFREE, PDB_STALE_WINDOWED = 0, 1, 2
 
 # every symbol declared in include/pdb.h
 EXPORTS = (
@@ -35,7 +37,9 @@ EXPORTS = (
     "pdb_validate_csr", "pdb_workspace_status", "pdb_transpose", "pdb_prev_writer",
     "pdb_check_reciprocal", "pdb_batch_schedule", "pdb_batch_epoch",
     "pdb_stale_workspace_bytes", "pdb_stale_epoch", "pdb_dense_plan",
-    "pdb_dense_workspace_bytes", "pdb_dense_gd",
+    "pdb_dense_workspace_bytes", "pdb_dense_gd", "pdb_options_init", "pdb_validate_schedule",
+    # include/pdb_mb.h
+    "pdb_mb_workspace_bytes", "pdb_mb_copy", "pdb_mb_hop", "pdb_mb_barrier",
 )
 
 
@@ -60,6 +64,14 @@ class PdbBatches(ctypes.Structure):
 class PdbScheduleInfo(ctypes.Structure):
     _fields_ = [("method_used", ctypes.c_int32), ("rounds", ctypes.c_int32),
                 ("n_levels", ctypes.c_int64), ("max_width", ctypes.c_int64)]
+
+
+class PdbOptions(ctypes.Structure):
+    _fields_ = [("epoch_mode", ctypes.c_int32), ("pipeline", ctypes.c_int32),
+                ("pipeline_width", ctypes.c_int32), ("thin_max", ctypes.c_int32),
+                ("hot_features", ctypes.c_int64), ("spin_timeout_us", ctypes.c_int64),
+                ("batch_thin_max", ctypes.c_int32), ("batch_syncfree_blocks", ctypes.c_int32),
+                ("stale_mode", ctypes.c_int32), ("dense_stream", ctypes.c_int32)]
 
 
 class PdbError(RuntimeError):
@@ -90,13 +102,17 @@ def load() -> ctypes.CDLL:
     lib.pdb_last_hip_error.argtypes = []
     lib.pdb_schedule_workspace_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(sz)]
     lib.pdb_epoch_workspace_bytes.argtypes = [i64, ctypes.POINTER(sz)]
+    O = ctypes.POINTER(PdbOptions)
+    lib.pdb_options_init.argtypes = [O]
     lib.pdb_schedule.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, ctypes.POINTER(PdbLevels),
-                                 ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, P]
+                                 ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, O, P]
     lib.pdb_sgd_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int,
-                                  ctypes.POINTER(PdbLevels), P, sz, P]
+                                  ctypes.POINTER(PdbLevels), P, sz, O, P]
     lib.pdb_mf_epoch.argtypes = [P, P, P, i64, P, i64, P, i64, i32, f32, f32,
-                                 ctypes.POINTER(PdbLevels), P, sz, P]
+                                 ctypes.POINTER(PdbLevels), P, sz, O, P]
     lib.pdb_validate_csr.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, sz, P]
+    lib.pdb_validate_schedule.argtypes = [ctypes.POINTER(PdbCsr), i64, i64,
+                                          ctypes.POINTER(PdbLevels), P, sz, P]
     lib.pdb_workspace_status.argtypes = [P, P]
     lib.pdb_transpose.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, P, P, sz, P]
     lib.pdb_prev_writer.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, P, P, sz, P]
@@ -105,15 +121,22 @@ def load() -> ctypes.CDLL:
                                          ctypes.POINTER(ctypes.c_uint32), P, sz, P]
     lib.pdb_batch_schedule.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, i64,
                                        ctypes.POINTER(PdbBatches), ctypes.POINTER(PdbLevels),
-                                       ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, P]
+                                       ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, O, P]
     lib.pdb_batch_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, i64, P, f32, ctypes.c_int,
-                                    ctypes.POINTER(PdbBatches), ctypes.POINTER(PdbLevels), P, sz, P]
+                                    ctypes.POINTER(PdbBatches), ctypes.POINTER(PdbLevels), P, sz,
+                                    O, P]
     lib.pdb_stale_workspace_bytes.argtypes = [i64, ctypes.POINTER(sz)]
     lib.pdb_stale_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int, i64,
-                                    P, P, sz, P]
+                                    P, P, sz, O, P]
     lib.pdb_dense_plan.argtypes = [i64, i64, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.pdb_dense_workspace_bytes.argtypes = [i64, i64, i64, i64, ctypes.POINTER(sz)]
-    lib.pdb_dense_gd.argtypes = [P, i64, P, i64, i64, P, f32, ctypes.c_int, i64, i64, i64, P, sz, P]
+    lib.pdb_dense_gd.argtypes = [P, i64, P, i64, i64, P, f32, ctypes.c_int, i64, i64, i64, P, sz,
+                                 O, P]
+    lib.pdb_mb_workspace_bytes.argtypes = [ctypes.POINTER(sz)]
+    lib.pdb_mb_copy.argtypes = [P, P, sz, P]
+    lib.pdb_mb_hop.argtypes = [i64, i32, P, sz, ctypes.POINTER(ctypes.c_double),
+                               ctypes.POINTER(i32), ctypes.POINTER(i32), O, P]
+    lib.pdb_mb_barrier.argtypes = [i64, i32, P, sz, ctypes.POINTER(ctypes.c_double), O, P]
     for name in EXPORTS:
         if name not in ("pdb_strerror",):
             getattr(lib, name).restype = ctypes.c_int
@@ -134,6 +157,27 @@ def _ptr(t):
     if not t.is_contiguous():
         raise ValueError("expected a contiguous tensor")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def options(**fields) -> PdbOptions:
+    """pdb_options with the library's defaults, then the given fields
+    (e.g. options(epoch_mode=PDB_EPOCH_LEVELS, hot_features=0))."""
+    o = PdbOptions()
+    _check(load().pdb_options_init(ctypes.byref(o)), "pdb_options_init")
+    for k, v in fields.items():
+        if k not in dict(PdbOptions._fields_):
+            raise TypeError("unknown option %r" % k)
+        setattr(o, k, int(v))
+    return o
+
+
+def _opt(opt):
+    """None (defaults), a PdbOptions, or a dict of fields."""
+    if opt is None:
+        return None
+    if isinstance(opt, dict):
+        opt = options(**opt)
+    return ctypes.byref(opt)
 
 
 def _stream(stream, device):
@@ -245,13 +289,13 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 
 
 def pdb_schedule(csr: Csr, labels, n: int, d: int, levels: Levels, method: int = PDB_SCHED_AUTO,
-                 ws: torch.Tensor | None = None, stream=None) -> dict:
+                 ws: torch.Tensor | None = None, stream=None, opt=None) -> dict:
     if ws is None:
         ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
     lv = levels.c()
     info = PdbScheduleInfo()
     _check(load().pdb_schedule(ctypes.byref(csr.c()), _ptr(labels), n, d, ctypes.byref(lv),
-                               method, ctypes.byref(info), _ptr(ws), ws.numel(),
+                               method, ctypes.byref(info), _ptr(ws), ws.numel(), _opt(opt),
                                _stream(stream, csr.device)), "pdb_schedule")
     levels.L_host, levels.max_width_host = lv.L_host, lv.max_width_host
     return dict(method_used=info.method_used, rounds=info.rounds, n_levels=info.n_levels,
@@ -259,7 +303,8 @@ def pdb_schedule(csr: Csr, labels, n: int, d: int, levels: Levels, method: int =
 
 
 def pdb_sgd_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor, lr: float,
-                  loss: int, levels: Levels, ws: torch.Tensor | None = None, stream=None):
+                  loss: int, levels: Levels, ws: torch.Tensor | None = None, stream=None,
+                  opt=None):
     if w.dtype != torch.float32 or labels.dtype != torch.float32:
         raise TypeError("w and labels must be float32")
     if w.numel() < d or labels.numel() < n:
@@ -268,12 +313,13 @@ def pdb_sgd_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tenso
         ws = workspace(pdb_epoch_workspace_bytes(d), csr.device)
     _check(load().pdb_sgd_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
                                 ctypes.c_float(lr), loss, ctypes.byref(levels.c()), _ptr(ws),
-                                ws.numel(), _stream(stream, csr.device)), "pdb_sgd_epoch")
+                                ws.numel(), _opt(opt), _stream(stream, csr.device)),
+           "pdb_sgd_epoch")
     return ws
 
 
 def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, rank: int,
-                 lr: float, reg: float, levels: Levels, ws=None, stream=None):
+                 lr: float, reg: float, levels: Levels, ws=None, stream=None, opt=None):
     for t, name in ((user, "user"), (item, "item")):
         if t.dtype != torch.int32 or t.numel() < n:
             raise TypeError("%s must be int32[n]" % name)
@@ -283,14 +329,14 @@ def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, r
         ws = workspace(pdb_epoch_workspace_bytes((n_users + n_items) * rank), U.device)
     _check(load().pdb_mf_epoch(_ptr(user), _ptr(item), _ptr(rating), n, _ptr(U), n_users,
                                _ptr(V), n_items, rank, ctypes.c_float(lr), ctypes.c_float(reg),
-                               ctypes.byref(levels.c()), _ptr(ws), ws.numel(),
+                               ctypes.byref(levels.c()), _ptr(ws), ws.numel(), _opt(opt),
                                _stream(stream, U.device)), "pdb_mf_epoch")
     return ws
 
 
 def pdb_batch_schedule(csr: Csr, n: int, d: int, batches: Batches, levels: Levels,
                        method: int = PDB_SCHED_AUTO, ws: torch.Tensor | None = None,
-                       stream=None) -> dict:
+                       stream=None, opt=None) -> dict:
     """levels: a Levels for nb = ceil(n / batch) rows and (for prev_nz) nnz entries."""
     if ws is None:
         ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
@@ -299,7 +345,7 @@ def pdb_batch_schedule(csr: Csr, n: int, d: int, batches: Batches, levels: Level
     info = PdbScheduleInfo()
     _check(load().pdb_batch_schedule(ctypes.byref(csr.c()), n, d, batches.batch, ctypes.byref(bt),
                                      ctypes.byref(lv), method, ctypes.byref(info), _ptr(ws),
-                                     ws.numel(), _stream(stream, csr.device)),
+                                     ws.numel(), _opt(opt), _stream(stream, csr.device)),
            "pdb_batch_schedule")
     batches.U_host = bt.U_host
     levels.L_host, levels.max_width_host = lv.L_host, lv.max_width_host
@@ -309,7 +355,7 @@ def pdb_batch_schedule(csr: Csr, n: int, d: int, batches: Batches, levels: Level
 
 def pdb_batch_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor, lr: float,
                     loss: int, batches: Batches, levels: Levels, ws: torch.Tensor | None = None,
-                    stream=None):
+                    stream=None, opt=None):
     if w.dtype != torch.float32 or labels.dtype != torch.float32:
         raise TypeError("w and labels must be float32")
     if w.numel() < d or labels.numel() < n:
@@ -318,7 +364,7 @@ def pdb_batch_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Ten
         ws = workspace(pdb_epoch_workspace_bytes(d), csr.device)
     _check(load().pdb_batch_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, batches.batch, _ptr(w),
                                   ctypes.c_float(lr), loss, ctypes.byref(batches.c()),
-                                  ctypes.byref(levels.c()), _ptr(ws), ws.numel(),
+                                  ctypes.byref(levels.c()), _ptr(ws), ws.numel(), _opt(opt),
                                   _stream(stream, csr.device)), "pdb_batch_epoch")
     return ws
 
@@ -331,7 +377,7 @@ def pdb_stale_workspace_bytes(nnz: int) -> int:
 
 def pdb_stale_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor, lr: float,
                     loss: int, delay: int, levels: Levels, ws: torch.Tensor | None = None,
-                    stream=None):
+                    stream=None, opt=None):
     """levels: from pdb_schedule on the same CSR (its prev_nz is used)."""
     if w.dtype != torch.float32 or labels.dtype != torch.float32:
         raise TypeError("w and labels must be float32")
@@ -343,7 +389,8 @@ def pdb_stale_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Ten
         ws = workspace(pdb_stale_workspace_bytes(csr.nnz), csr.device)
     _check(load().pdb_stale_epoch(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
                                   ctypes.c_float(lr), loss, delay, _ptr(levels.prev_nz), _ptr(ws),
-                                  ws.numel(), _stream(stream, csr.device)), "pdb_stale_epoch")
+                                  ws.numel(), _opt(opt), _stream(stream, csr.device)),
+           "pdb_stale_epoch")
     return ws
 
 
@@ -364,7 +411,7 @@ def pdb_dense_workspace_bytes(n: int, d: int, row_block: int, col_block: int) ->
 
 def pdb_dense_gd(X: torch.Tensor, labels: torch.Tensor, w: torch.Tensor, lr: float, loss: int,
                  iters: int, row_block: int = 0, col_block: int = 0,
-                 ws: torch.Tensor | None = None, stream=None):
+                 ws: torch.Tensor | None = None, stream=None, opt=None):
     """X: float32 device matrix n x d with unit column stride (any row stride
     >= d).  row_block = col_block = 0 takes pdb_dense_plan's blocking."""
     if X.dtype != torch.float32 or w.dtype != torch.float32 or labels.dtype != torch.float32:
@@ -382,7 +429,7 @@ def pdb_dense_gd(X: torch.Tensor, labels: torch.Tensor, w: torch.Tensor, lr: flo
     if not X.is_cuda:
         raise ValueError("expected a device tensor")
     _check(load().pdb_dense_gd(X.data_ptr() if X.numel() else None, ldx, _ptr(labels), n, d, _ptr(w), ctypes.c_float(lr), loss,
-                               iters, row_block, col_block, _ptr(ws), ws.numel(),
+                               iters, row_block, col_block, _ptr(ws), ws.numel(), _opt(opt),
                                _stream(stream, X.device)), "pdb_dense_gd")
     return ws
 
@@ -395,6 +442,18 @@ def pdb_validate_csr(csr: Csr, n: int, d: int, ws=None, stream=None) -> int:
                                  _stream(stream, csr.device))
     if rc not in (PDB_OK, PDB_ERR_BAD_CSR):
         raise PdbError(rc, "pdb_validate_csr")
+    return rc
+
+
+def pdb_validate_schedule(csr: Csr, n: int, d: int, levels: Levels, ws=None, stream=None) -> int:
+    """Returns PDB_OK or PDB_ERR_DEVICE (a schedule the epoch may not run);
+    raises on other errors."""
+    if ws is None:
+        ws = workspace(pdb_schedule_workspace_bytes(n, d, csr.nnz), csr.device)
+    rc = load().pdb_validate_schedule(ctypes.byref(csr.c()), n, d, ctypes.byref(levels.c()),
+                                      _ptr(ws), ws.numel(), _stream(stream, csr.device))
+    if rc not in (PDB_OK, PDB_ERR_DEVICE):
+        raise PdbError(rc, "pdb_validate_schedule")
     return rc
 
 
@@ -428,3 +487,44 @@ def pdb_check_reciprocal(lo_bits: int, hi_bits: int, device, ws=None, stream=Non
                                        _ptr(ws), ws.numel(), _stream(stream, device)),
            "pdb_check_reciprocal")
     return bad.value, first.value
+
+
+# ---------------------------------------------------------------------------
+# microbenchmarks (include/pdb_mb.h)
+
+def pdb_mb_workspace_bytes() -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().pdb_mb_workspace_bytes(ctypes.byref(out)), "pdb_mb_workspace_bytes")
+    return out.value
+
+
+def pdb_mb_copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
+    """Streams src into dst (same byte size, a multiple of 16) with the
+    library's copy kernel."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst must have the same size")
+    _check(load().pdb_mb_copy(_ptr(src), _ptr(dst), nbytes, _stream(stream, src.device)),
+           "pdb_mb_copy")
+
+
+def pdb_mb_hop(rounds: int, partner: int, device, ws=None, stream=None, opt=None):
+    """(ns per round trip, XCD of block 0, XCD of the partner block)."""
+    if ws is None:
+        ws = workspace(pdb_mb_workspace_bytes(), device)
+    ns = ctypes.c_double(0)
+    xa, xb = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(load().pdb_mb_hop(rounds, partner, _ptr(ws), ws.numel(), ctypes.byref(ns),
+                             ctypes.byref(xa), ctypes.byref(xb), _opt(opt),
+                             _stream(stream, device)), "pdb_mb_hop")
+    return ns.value, xa.value, xb.value
+
+
+def pdb_mb_barrier(rounds: int, blocks: int, device, ws=None, stream=None, opt=None) -> float:
+    """ns per grid-wide barrier over `blocks` resident blocks."""
+    if ws is None:
+        ws = workspace(pdb_mb_workspace_bytes(), device)
+    ns = ctypes.c_double(0)
+    _check(load().pdb_mb_barrier(rounds, blocks, _ptr(ws), ws.numel(), ctypes.byref(ns),
+                                 _opt(opt), _stream(stream, device)), "pdb_mb_barrier")
+    return ns.value

@@ -14,20 +14,20 @@ def csr_from_rows(rows):
     return row_ptr, col
 
 
-def gpu_schedule(native, dev, row_ptr, col, d, method, with_prev=True):
+def gpu_schedule(native, dev, row_ptr, col, d, method, with_prev=True, opt=None):
     import torch
 
     csr = native.Csr.from_numpy(row_ptr, col, None, dev)
     n = len(row_ptr) - 1
     lv = native.Levels(n, len(col), dev, with_prev_nz=with_prev)
-    info = native.pdb_schedule(csr, None, n, d, lv, method)
+    info = native.pdb_schedule(csr, None, n, d, lv, method, opt=opt)
     torch.cuda.synchronize()
     return lv, info
 
 
-def check_schedule(native, dev, row_ptr, col, d, method):
+def check_schedule(native, dev, row_ptr, col, d, method, opt=None):
     """GPU levels, perm, level_ptr, L equal the oracle's exactly."""
-    lv, info = gpu_schedule(native, dev, row_ptr, col, d, method)
+    lv, info = gpu_schedule(native, dev, row_ptr, col, d, method, opt=opt)
     level, perm, level_ptr, L = oracle.schedule(row_ptr, col, d)
     assert lv.L_host == L and int(lv.n_levels.item()) == L
     assert np.array_equal(lv.level.cpu().numpy(), level)
@@ -51,22 +51,22 @@ def check_prev_nz(row_ptr, col, d, pn):
     assert np.array_equal(rows, prev[has])
 
 
-def gpu_sgd(native, dev, g, lv, w0=None):
+def gpu_sgd(native, dev, g, lv, w0=None, opt=None):
     import torch
 
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], dev)
     y = torch.from_numpy(g["y"]).to(dev)
     w = torch.from_numpy(np.zeros(g["d"], np.float32) if w0 is None else w0.copy()).to(dev)
-    ws = native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv)
+    ws = native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv, opt=opt)
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     return w.cpu().numpy()
 
 
-def check_sgd(native, dev, g, lv, w0=None, tol=1e-5):
+def check_sgd(native, dev, g, lv, w0=None, tol=1e-5, opt=None):
     """Bitwise equal to the oracle in matched summation order; within tol of
     the natural-order oracle."""
-    got = gpu_sgd(native, dev, g, lv, w0)
+    got = gpu_sgd(native, dev, g, lv, w0, opt=opt)
     w_init = np.zeros(g["d"], np.float32) if w0 is None else w0
     ref_m = oracle.sgd_epoch(g["row_ptr"], g["col"], g["val"], g["y"], w_init, g["lr"], g["loss"],
                              oracle.MATCHED)
@@ -79,21 +79,22 @@ def check_sgd(native, dev, g, lv, w0=None, tol=1e-5):
     return got
 
 
-def gpu_mf(native, dev, g, lv):
+def gpu_mf(native, dev, g, lv, opt=None):
     import torch
 
     U = torch.from_numpy(g["U0"].copy()).to(dev)
     V = torch.from_numpy(g["V0"].copy()).to(dev)
     t = lambda a: torch.from_numpy(a).to(dev)
     ws = native.pdb_mf_epoch(t(g["user"]), t(g["item"]), t(g["rating"]), g["n"], U, g["n_users"],
-                             V, g["n_items"], g["rank"], float(g["lr"]), float(g["reg"]), lv)
+                             V, g["n_items"], g["rank"], float(g["lr"]), float(g["reg"]), lv,
+                             opt=opt)
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     return U.cpu().numpy(), V.cpu().numpy()
 
 
-def check_mf(native, dev, g, lv, tol=1e-5):
-    U, V = gpu_mf(native, dev, g, lv)
+def check_mf(native, dev, g, lv, tol=1e-5, opt=None):
+    U, V = gpu_mf(native, dev, g, lv, opt=opt)
     Um, Vm = oracle.mf_epoch(g["user"], g["item"], g["rating"], g["U0"], g["V0"], g["lr"], g["reg"],
                              oracle.MATCHED)
     assert np.array_equal(U.view(np.int32), Um.view(np.int32))

@@ -8,13 +8,18 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "pdb.h")
+INCLUDE = os.path.join(ROOT, "include")
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(pdb_[a-z_0-9]+)\s*\(", text)))
+    """Every pdb_* function declared in include/*.h."""
+    names = set()
+    for f in sorted(os.listdir(INCLUDE)):
+        if f.endswith(".h"):
+            text = open(os.path.join(INCLUDE, f)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(pdb_[a-z_0-9]+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -35,6 +40,59 @@ def test_header_declares_the_binding_exports():
 def test_library_exports_every_declared_symbol(lib):
     for name in declared_functions():
         assert hasattr(lib, name), name
+
+
+def test_options_defaults_and_layout(lib, tmp_path):
+    """pdb_options_init gives the documented defaults, and the binding's
+    struct has the header's size and field offsets (checked by a C program
+    compiled against include/pdb.h)."""
+    import subprocess
+
+    from paper_1508_00703_amd import native
+
+    o = native.options()
+    assert (o.epoch_mode, o.pipeline, o.pipeline_width, o.thin_max, o.hot_features,
+            o.spin_timeout_us, o.batch_thin_max, o.batch_syncfree_blocks, o.stale_mode,
+            o.dense_stream) == (0, 1, 4, 16, -1, 20000000, 2, 32, 0, 0)
+    fields = [f for f, _ in native.PdbOptions._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "pdb.h"\nint main(void) {\n'
+                   '  printf("%zu", sizeof(pdb_options));\n'
+                   + "".join('  printf(" %%zu", offsetof(pdb_options, %s));\n' % f for f in fields)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [ctypes.sizeof(native.PdbOptions)] + [getattr(native.PdbOptions, f).offset
+                                                 for f in fields]
+    assert got == want
+
+
+@pytest.mark.parametrize("field,value", [("epoch_mode", 3), ("epoch_mode", -1), ("pipeline", 2),
+                                         ("pipeline_width", 0), ("thin_max", 0),
+                                         ("hot_features", -2), ("spin_timeout_us", -1),
+                                         ("spin_timeout_us", 10 ** 12), ("batch_thin_max", 0),
+                                         ("batch_syncfree_blocks", 0), ("stale_mode", 3),
+                                         ("dense_stream", 2)])
+def test_options_out_of_range_are_rejected(lib, field, value):
+    """Checked on the host before any device work: with no examples a valid
+    option set returns PDB_OK without touching the device, an invalid one
+    PDB_ERR_INVALID_ARG."""
+    from paper_1508_00703_amd import native
+
+    csr = native.PdbCsr(None, None, None, 0)
+    lv = native.PdbLevels(None, None, None, None, None, 0, 0)
+    ws = ctypes.c_void_p(0x1000)  # never dereferenced: n = 0
+    good = native.options()
+    assert lib.pdb_sgd_epoch(ctypes.byref(csr), None, 0, 0, None, ctypes.c_float(0.1), 0,
+                             ctypes.byref(lv), ws, 4096, ctypes.byref(good), None) == native.PDB_OK
+    bad = native.options()
+    setattr(bad, field, value)
+    assert (lib.pdb_sgd_epoch(ctypes.byref(csr), None, 0, 0, None, ctypes.c_float(0.1), 0,
+                              ctypes.byref(lv), ws, 4096, ctypes.byref(bad), None)
+            == native.PDB_ERR_INVALID_ARG)
 
 
 def test_strerror_covers_every_status(lib):

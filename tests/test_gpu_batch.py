@@ -62,15 +62,16 @@ def check_batch_schedule(native, dev, row_ptr, col, d, B, method=0):
     return bt, lv
 
 
-def check_batch_epoch(native, dev, g, B, bt, lv, tol=1e-5):
+def check_batch_epoch(native, dev, g, B, bt, lv, tol=1e-5, opt=None):
     import torch
 
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], dev)
     y = torch.from_numpy(g["y"]).to(dev)
     w = torch.zeros(g["d"], dtype=torch.float32, device=dev)
-    ws = native.pdb_batch_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], bt, lv)
-    # (the default workspace holds a word per feature: sync-free unless
-    # PDB_EPOCH_MODE=1)
+    ws = native.pdb_batch_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], bt, lv,
+                                opt=opt)
+    # (the default workspace holds a word per feature: sync-free unless the
+    # options ask for batch levels)
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     got = w.cpu().numpy()
@@ -116,7 +117,7 @@ def structured_problem(rows, loss, with_val, seed, B=1):
     return dict(row_ptr=row_ptr, col=col, val=val, y=y, n=n, d=d, lr=lr, loss=loss)
 
 
-EPOCH_MODES = ["1", "2"]  # batch levels, sync-free
+EPOCH_MODES = [1, 2]  # batch levels, sync-free
 
 
 @pytest.mark.parametrize("name", sorted(structured_cases()))
@@ -124,12 +125,11 @@ EPOCH_MODES = ["1", "2"]  # batch levels, sync-free
 @pytest.mark.parametrize("with_val", [True, False])
 @pytest.mark.parametrize("B", [1, 3, 64])
 @pytest.mark.parametrize("mode", EPOCH_MODES)
-def test_structured_batch_epochs(gpu, name, loss, with_val, B, mode, monkeypatch):
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+def test_structured_batch_epochs(gpu, name, loss, with_val, B, mode):
     native = native_mod()
     g = structured_problem(structured_cases()[name], loss, with_val, B + loss, B)
     bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], B)
-    check_batch_epoch(native, gpu, g, B, bt, lv)
+    check_batch_epoch(native, gpu, g, B, bt, lv, opt=dict(epoch_mode=mode))
 
 
 def batch_workload(g, B):
@@ -143,21 +143,19 @@ def batch_workload(g, B):
 @pytest.mark.parametrize("cfg", [1, 2, 4])
 @pytest.mark.parametrize("B", [1, 5, 100, 1000, 4096])
 @pytest.mark.parametrize("mode", EPOCH_MODES)
-def test_random_batch_epochs(gpu, cfg, B, mode, monkeypatch):
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+def test_random_batch_epochs(gpu, cfg, B, mode):
     native = native_mod()
     g = batch_workload(datagen.generate(cfg, n=6000, d=3000 if cfg == 4 else 500, seed=31 + B), B)
     bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], B)
-    check_batch_epoch(native, gpu, g, B, bt, lv)
+    check_batch_epoch(native, gpu, g, B, bt, lv, opt=dict(epoch_mode=mode))
 
 
-@pytest.mark.parametrize("thin", ["1", "1000000"])
-def test_wide_and_narrow_batch_levels(gpu, thin, monkeypatch):
+@pytest.mark.parametrize("thin", [1, 1000000])
+def test_wide_and_narrow_batch_levels(gpu, thin):
     # disjoint pairs of rows then a shared feature: wide levels (the grid and
     # device barriers) and a chain of narrow ones (block 0), or everything in
     # one block
-    monkeypatch.setenv("PDB_BATCH_THIN_MAX", thin)
-    monkeypatch.setenv("PDB_EPOCH_MODE", "1")
+    opt = dict(batch_thin_max=thin, epoch_mode=1)
     native = native_mod()
     rows = [{2 * i, 2 * i + 1} for i in range(3000)] + [{0, 7 + i % 50} for i in range(500)]
     rows += [{10000 + i} for i in range(2000)]
@@ -165,7 +163,7 @@ def test_wide_and_narrow_batch_levels(gpu, thin, monkeypatch):
         g = structured_problem(rows, oracle.LOGISTIC, True, 5, B)
         bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], B)
         assert lv.max_width_host > 100
-        check_batch_epoch(native, gpu, g, B, bt, lv)
+        check_batch_epoch(native, gpu, g, B, bt, lv, opt=opt)
 
 
 def test_batch_of_one_equals_gpu_sgd(gpu):
@@ -208,10 +206,9 @@ def test_full_size_batch(gpu, cfg):
 
 
 @pytest.mark.parametrize("cfg", [2, 4])
-def test_full_size_batch_levels(gpu, cfg, monkeypatch):
+def test_full_size_batch_levels(gpu, cfg):
     # the batch-level execution at full size
-    monkeypatch.setenv("PDB_EPOCH_MODE", "1")
     native = native_mod()
     g = batch_workload(datagen.generate(cfg), 100)
     bt, lv = check_batch_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 100)
-    check_batch_epoch(native, gpu, g, 100, bt, lv)
+    check_batch_epoch(native, gpu, g, 100, bt, lv, opt=dict(epoch_mode=1))

@@ -1,0 +1,205 @@
+"""The schedule check (pdb_validate_schedule) and the device-error path.
+
+The check must accept every schedule pdb_schedule and the oracle produce,
+and flag schedules corrupted on the host (no epoch is run on them).  The
+error path is forced from the host: a zero watchdog makes the kernels' own
+bounded waits give up at once, every kernel exits normally, and the call or
+pdb_workspace_status reports PDB_ERR_DEVICE; the next call on the same
+workspace runs normally."""
+import numpy as np
+import pytest
+
+import datagen
+import oracle
+from pdbtest import check_schedule, check_sgd, csr_from_rows, gpu_schedule
+
+pytestmark = pytest.mark.gpu
+
+
+def native_mod():
+    from paper_1508_00703_amd import native
+    return native
+
+
+SCALED = {1: dict(), 2: dict(n=60_000, d=6_000), 3: dict(n=30_000, d=30_000),
+          4: dict(n=30_000, d=12_000)}
+
+
+@pytest.mark.parametrize("cfg", sorted(SCALED))
+def test_check_accepts_gpu_and_oracle_schedules(gpu, cfg):
+    native = native_mod()
+    g = datagen.generate(cfg, **SCALED[cfg])
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None, gpu)
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_OK
+    level, perm, level_ptr, L = oracle.schedule(g["row_ptr"], g["col"], g["d"])
+    olv = native.Levels.from_host(level, perm, level_ptr, gpu)
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], olv) == native.PDB_OK
+
+
+def test_check_accepts_a_permuted_level_order(gpu):
+    """Any order inside a level is a schedule (Theorem 2): reversing each
+    level's examples passes."""
+    native = native_mod()
+    g = datagen.generate(4, **SCALED[4])
+    level, perm, level_ptr, L = oracle.schedule(g["row_ptr"], g["col"], g["d"])
+    perm2 = perm.copy()
+    for l in range(L):
+        perm2[level_ptr[l]:level_ptr[l + 1]] = perm[level_ptr[l]:level_ptr[l + 1]][::-1]
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None, gpu)
+    lv = native.Levels.from_host(level, perm2, level_ptr, gpu)
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_OK
+
+
+def corrupted(level, perm, level_ptr, kind, row_ptr, col):
+    level, perm, level_ptr = level.copy(), perm.copy(), level_ptr.copy()
+    L = len(level_ptr) - 1
+    if kind == "conflict_in_one_level":
+        # an example moved into its previous writer's level
+        prev = oracle.prev_writer(row_ptr, col, int(col.max()) + 1)
+        p = int(np.nonzero(prev >= 0)[0][0])
+        i = int(np.searchsorted(row_ptr, p, side="right") - 1)
+        j = int(prev[p])
+        lo = level[j]
+        level[i] = lo
+        order = np.lexsort((np.arange(len(level)), level))
+        perm[:] = order
+        level_ptr[:] = np.searchsorted(level[order], np.arange(L + 1), side="right")
+        level_ptr[0] = 0
+    elif kind == "out_of_order":
+        # two conflicting examples in swapped levels
+        prev = oracle.prev_writer(row_ptr, col, int(col.max()) + 1)
+        p = int(np.nonzero(prev >= 0)[0][-1])
+        i = int(np.searchsorted(row_ptr, p, side="right") - 1)
+        j = int(prev[p])
+        level[i], level[j] = level[j], level[i]
+        order = np.lexsort((np.arange(len(level)), level))
+        perm[:] = order
+    elif kind == "duplicate_in_perm":
+        perm[1] = perm[0]
+    elif kind == "perm_out_of_range":
+        perm[len(perm) // 2] = len(perm) + 5
+    elif kind == "level_array_disagrees":
+        e = level_ptr[L - 1]
+        level[perm[e]] += 1
+    elif kind == "level_ptr_short":
+        level_ptr[L] -= 1
+    return level, perm, level_ptr
+
+
+KINDS = ["conflict_in_one_level", "out_of_order", "duplicate_in_perm", "perm_out_of_range",
+         "level_array_disagrees", "level_ptr_short"]
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("cfg", [1, 4])
+def test_check_flags_corrupted_schedules(gpu, cfg, kind):
+    native = native_mod()
+    g = datagen.generate(cfg, **SCALED[cfg])
+    level, perm, level_ptr, L = oracle.schedule(g["row_ptr"], g["col"], g["d"])
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None, gpu)
+    bad = native.Levels.from_host(*corrupted(level, perm, level_ptr, kind, g["row_ptr"], g["col"]),
+                                  gpu)
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], bad) == native.PDB_ERR_DEVICE
+
+
+def test_check_flags_wrong_previous_writers_and_level_count(gpu):
+    import torch
+
+    native = native_mod()
+    g = datagen.generate(1)
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], None, gpu)
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_OK
+    pn = lv.prev_nz.clone()
+    k = int(torch.nonzero(pn >= 0)[5])
+    lv.prev_nz[k] = -1                      # a previous writer dropped
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_ERR_DEVICE
+    lv.prev_nz.copy_(pn)
+    L = int(lv.n_levels.item())
+    lv.n_levels.fill_(L - 1)                # level count one short
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_ERR_DEVICE
+    lv.n_levels.fill_(g["n"] + 1)           # more levels than examples
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_ERR_DEVICE
+    lv.n_levels.fill_(L)
+    assert native.pdb_validate_schedule(csr, g["n"], g["d"], lv) == native.PDB_OK
+
+
+def test_check_edge_cases(gpu):
+    native = native_mod()
+    # no examples
+    csr = native.Csr.from_numpy(np.zeros(1, np.int64), np.zeros(0, np.int32), None, gpu)
+    lv, _ = gpu_schedule(native, gpu, np.zeros(1, np.int64), np.zeros(0, np.int32), 4, 0)
+    assert native.pdb_validate_schedule(csr, 0, 4, lv) == native.PDB_OK
+    # empty rows only, and one example
+    for rows in ([set()] * 9, [{3}]):
+        row_ptr, col = csr_from_rows(rows)
+        csr = native.Csr.from_numpy(row_ptr, col, None, gpu)
+        lv, _ = check_schedule(native, gpu, row_ptr, col, 5, 0)
+        assert native.pdb_validate_schedule(csr, len(rows), 5, lv) == native.PDB_OK
+
+
+def test_zero_watchdog_sync_free_epoch(gpu):
+    """Sync-free epoch on a chain-like input with a zero watchdog: the first
+    wait that is not met at once gives up, every kernel exits, the workspace
+    reports PDB_ERR_DEVICE once; the next epoch on it is the sequential one."""
+    import torch
+
+    native = native_mod()
+    g = datagen.generate(2, **SCALED[2])
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], gpu)
+    y = torch.from_numpy(g["y"]).to(gpu)
+    w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
+    ws = native.workspace(native.pdb_epoch_workspace_bytes(g["d"]), gpu)
+    native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv, ws=ws,
+                         opt=dict(epoch_mode=native.PDB_EPOCH_SYNCFREE, spin_timeout_us=0))
+    torch.cuda.synchronize()
+    assert native.pdb_workspace_status(ws) == native.PDB_ERR_DEVICE
+    assert native.pdb_workspace_status(ws) == native.PDB_OK      # cleared by the read
+    w.zero_()
+    native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv, ws=ws,
+                         opt=dict(epoch_mode=native.PDB_EPOCH_SYNCFREE))
+    torch.cuda.synchronize()
+    assert native.pdb_workspace_status(ws) == native.PDB_OK
+    ref = oracle.sgd_epoch(g["row_ptr"], g["col"], g["val"], g["y"], np.zeros(g["d"], np.float32),
+                           g["lr"], g["loss"], oracle.MATCHED)
+    assert np.array_equal(w.cpu().numpy().view(np.int32), ref.view(np.int32))
+
+
+def test_zero_watchdog_level_barriers(gpu):
+    """Level by level with wide levels (a grid barrier per level) and a zero
+    watchdog: the barrier waits give up, every block exits, PDB_ERR_DEVICE."""
+    import torch
+
+    native = native_mod()
+    g = datagen.generate(4, **SCALED[4])
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    assert lv.max_width_host > 16
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], gpu)
+    y = torch.from_numpy(g["y"]).to(gpu)
+    w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
+    ws = native.workspace(native.pdb_epoch_workspace_bytes(0), gpu)
+    native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv, ws=ws,
+                         opt=dict(epoch_mode=native.PDB_EPOCH_LEVELS, spin_timeout_us=0))
+    torch.cuda.synchronize()
+    assert native.pdb_workspace_status(ws) == native.PDB_ERR_DEVICE
+    w.zero_()
+    check_sgd(native, gpu, g, lv, opt=dict(epoch_mode=native.PDB_EPOCH_LEVELS))
+
+
+@pytest.mark.parametrize("method", [2, 6])  # dataflow, short-row walk
+def test_zero_watchdog_schedule(gpu, method):
+    """pdb_schedule whose level kernel waits on device: a zero watchdog makes
+    the call return PDB_ERR_DEVICE (no levels are bucketed); the next call
+    succeeds."""
+    native = native_mod()
+    if method == 6:
+        g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
+    else:
+        g = datagen.generate(4, **SCALED[4])
+    with pytest.raises(native.PdbError) as e:
+        gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], method,
+                     opt=dict(spin_timeout_us=0))
+    assert e.value.code == native.PDB_ERR_DEVICE
+    check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], method)

@@ -22,7 +22,7 @@ def native_mod():
     return native
 
 
-def run_gpu(native, dev, X, y, w0, lr, loss, iters, rb=0, cb=0, ws=None):
+def run_gpu(native, dev, X, y, w0, lr, loss, iters, rb=0, cb=0, ws=None, opt=None):
     import torch
 
     Xt = torch.from_numpy(np.ascontiguousarray(X)).to(dev) if X.flags.c_contiguous or X.size == 0 \
@@ -35,17 +35,17 @@ def run_gpu(native, dev, X, y, w0, lr, loss, iters, rb=0, cb=0, ws=None):
         Xt = bt.as_strided(X.shape, (X.strides[0] // 4, 1), off)
     yt = torch.from_numpy(np.ascontiguousarray(y, dtype=np.float32)).to(dev)
     wt = torch.from_numpy(np.array(w0, dtype=np.float32)).to(dev)
-    ws = native.pdb_dense_gd(Xt, yt, wt, float(lr), loss, iters, rb, cb, ws=ws)
+    ws = native.pdb_dense_gd(Xt, yt, wt, float(lr), loss, iters, rb, cb, ws=ws, opt=opt)
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     return wt.cpu().numpy(), ws
 
 
-def check_dense(native, dev, X, y, w0, lr, loss, iters, rb=0, cb=0, natural=True):
+def check_dense(native, dev, X, y, w0, lr, loss, iters, rb=0, cb=0, natural=True, opt=None):
     n, d = X.shape
     if rb == 0 and cb == 0:
         rb, cb = native.pdb_dense_plan(n, d)
-    got, _ = run_gpu(native, dev, X, y, w0, lr, loss, iters, rb, cb)
+    got, _ = run_gpu(native, dev, X, y, w0, lr, loss, iters, rb, cb, opt=opt)
     ref = oracle.dense_gd(X, y, w0, lr, loss, oracle.MATCHED, iters, rb, cb, ROW_CHUNK)
     bad = np.nonzero(got.view(np.int32) != ref.view(np.int32))[0]
     assert len(bad) == 0, "blocks %dx%d, first mismatches %s: gpu %s oracle %s" % (
@@ -82,30 +82,30 @@ def test_dense_blockings(gpu, n, d, rb, cb, loss, iters):
 
 
 @pytest.mark.parametrize("n,d,rb,cb", [(37, 301, 5, 16), (300, 1000, 0, 0), (200, 96, 10, 32)])
-def test_streaming_equals_resident(gpu, n, d, rb, cb, monkeypatch):
+def test_streaming_equals_resident(gpu, n, d, rb, cb):
     # the same blocking with the tile kept in LDS and streamed every iteration
     native = native_mod()
     X, y, w0, lr = problem(n, d, oracle.SQUARED, 3)
     a = check_dense(native, gpu, X, y, w0, lr, oracle.SQUARED, 5, rb, cb, natural=False)
-    monkeypatch.setenv("PDB_DENSE_STREAM", "1")
-    b = check_dense(native, gpu, X, y, w0, lr, oracle.SQUARED, 5, rb, cb, natural=False)
+    b = check_dense(native, gpu, X, y, w0, lr, oracle.SQUARED, 5, rb, cb, natural=False,
+                    opt=dict(dense_stream=1))
     assert np.array_equal(a.view(np.int32), b.view(np.int32))
 
 
-@pytest.mark.parametrize("stream", ["0", "1"])
-def test_strided_and_unaligned_rows(gpu, stream, monkeypatch):
+@pytest.mark.parametrize("stream", [0, 1])
+def test_strided_and_unaligned_rows(gpu, stream):
     # row stride not a multiple of 4, and a start one float past 16 bytes:
     # the scalar-load variants
-    monkeypatch.setenv("PDB_DENSE_STREAM", stream)
+    opt = dict(dense_stream=stream)
     native = native_mod()
     g = datagen.generate_dense(1, n=90, d=130, ldx=133, seed=7)
     X, y = g["X"], g["y"]
     lr = np.float32(0.002)
     w0 = np.zeros(130, np.float32)
-    check_dense(native, gpu, X, y, w0, lr, oracle.SQUARED, 3, 9, 32)
+    check_dense(native, gpu, X, y, w0, lr, oracle.SQUARED, 3, 9, 32, opt=opt)
     buf = np.zeros((90, 136), np.float32)
     buf[:, 1:131] = X
-    check_dense(native, gpu, buf[:, 1:131], y, w0, lr, oracle.SQUARED, 3, 9, 32)
+    check_dense(native, gpu, buf[:, 1:131], y, w0, lr, oracle.SQUARED, 3, 9, 32, opt=opt)
 
 
 def test_calls_compose(gpu):

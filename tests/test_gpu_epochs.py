@@ -36,11 +36,10 @@ def compare(got, g, B=0):
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
-@pytest.mark.parametrize("mode", ["1", "2"])
-def test_sgd_epochs_on_a_cached_schedule(gpu, cfg, mode, monkeypatch):
+@pytest.mark.parametrize("mode", [1, 2])
+def test_sgd_epochs_on_a_cached_schedule(gpu, cfg, mode):
     import torch
 
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     g = datagen.generate(cfg, n=20000, d=6000 if cfg == 4 else 1000, seed=9)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
@@ -49,18 +48,18 @@ def test_sgd_epochs_on_a_cached_schedule(gpu, cfg, mode, monkeypatch):
     w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
     ws = native.workspace(native.pdb_epoch_workspace_bytes(g["d"]), gpu)
     for _ in range(EPOCHS):
-        native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv, ws=ws)
+        native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv, ws=ws,
+                             opt=dict(epoch_mode=mode))
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     compare(w.cpu().numpy(), g)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
-@pytest.mark.parametrize("mode", ["1", "2"])
-def test_batch_epochs_on_a_cached_schedule(gpu, cfg, mode, monkeypatch):
+@pytest.mark.parametrize("mode", [1, 2])
+def test_batch_epochs_on_a_cached_schedule(gpu, cfg, mode):
     import torch
 
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
     native = native_mod()
     B = 100
     g = batch_workload(datagen.generate(cfg, n=20000, d=6000 if cfg == 4 else 1000, seed=10), B)
@@ -70,7 +69,8 @@ def test_batch_epochs_on_a_cached_schedule(gpu, cfg, mode, monkeypatch):
     w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
     ws = native.workspace(native.pdb_epoch_workspace_bytes(g["d"]), gpu)
     for _ in range(EPOCHS):
-        native.pdb_batch_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], bt, lv, ws=ws)
+        native.pdb_batch_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], bt, lv, ws=ws,
+                               opt=dict(epoch_mode=mode))
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     compare(w.cpu().numpy(), g, B)

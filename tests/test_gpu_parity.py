@@ -56,19 +56,14 @@ def test_no_examples(gpu):
     assert lv.L_host == 0 and int(lv.n_levels.item()) == 0
 
 
-EPOCH_MODES = ["1", "2"]  # level by level, sync-free
-
-
-def set_epoch_mode(monkeypatch, mode):
-    monkeypatch.setenv("PDB_EPOCH_MODE", mode)
+EPOCH_MODES = [1, 2]  # level by level, sync-free
 
 
 @pytest.mark.parametrize("name", sorted(structured_cases()))
 @pytest.mark.parametrize("loss", [0, 1])
 @pytest.mark.parametrize("with_val", [True, False])
 @pytest.mark.parametrize("mode", EPOCH_MODES)
-def test_structured_epochs(gpu, name, loss, with_val, mode, monkeypatch):
-    set_epoch_mode(monkeypatch, mode)
+def test_structured_epochs(gpu, name, loss, with_val, mode):
     native = native_mod()
     rows = structured_cases()[name]
     row_ptr, col = csr_from_rows(rows)
@@ -86,7 +81,7 @@ def test_structured_epochs(gpu, name, loss, with_val, mode, monkeypatch):
              y=(np.sign(rng.normal(size=n)) if loss == 0 else rng.normal(size=n)).astype(np.float32))
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     w0 = (0.1 * rng.normal(size=d)).astype(np.float32)
-    check_sgd(native, gpu, g, lv, w0=w0)
+    check_sgd(native, gpu, g, lv, w0=w0, opt=dict(epoch_mode=mode))
 
 
 SCALED = {
@@ -105,13 +100,12 @@ def test_config_schedules(gpu, cfg, method):
 
 
 @pytest.mark.parametrize("cfg", sorted(SCALED))
-@pytest.mark.parametrize("mode", ["0"] + EPOCH_MODES)
-def test_config_epochs(gpu, cfg, mode, monkeypatch):
-    set_epoch_mode(monkeypatch, mode)
+@pytest.mark.parametrize("mode", [0] + EPOCH_MODES)
+def test_config_epochs(gpu, cfg, mode):
     native = native_mod()
     g = datagen.generate(cfg, **SCALED[cfg])
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    check_sgd(native, gpu, g, lv)
+    check_sgd(native, gpu, g, lv, opt=dict(epoch_mode=mode))
 
 
 @pytest.mark.parametrize("cfg", [1, 4])
@@ -124,13 +118,12 @@ def test_epoch_with_oracle_schedule(gpu, cfg):
     check_sgd(native, gpu, g, lv)
 
 
-@pytest.mark.parametrize("mode", ["0"] + EPOCH_MODES)
-def test_mf_scaled(gpu, mode, monkeypatch):
-    set_epoch_mode(monkeypatch, mode)
+@pytest.mark.parametrize("mode", [0] + EPOCH_MODES)
+def test_mf_scaled(gpu, mode):
     native = native_mod()
     g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    check_mf(native, gpu, g, lv)
+    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode))
 
 
 def test_transpose_and_prev_writer(gpu):
@@ -212,32 +205,26 @@ def test_bad_csr_and_arguments(gpu):
     assert e.value.code == native.PDB_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("hot", ["0", "5", "64", None])
+@pytest.mark.parametrize("hot", [0, 5, 64, -1])
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-@pytest.mark.parametrize("width", ["1", "4", "16"])
-def test_width1_pipeline_hot_and_cold(gpu, cfg, hot, width, monkeypatch):
+@pytest.mark.parametrize("width", [1, 4, 16])
+def test_width1_pipeline_hot_and_cold(gpu, cfg, hot, width):
     """Runs of narrow levels (at most `width` examples each) through the
     staged pipeline, with the LDS weight cache shrunk so that cold features
     (ring, prefetch, forwarding) appear."""
-    if hot is not None:
-        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
-    monkeypatch.setenv("PDB_CHAIN_WIDTH", width)
     native = native_mod()
     g = datagen.generate(cfg, **SCALED[cfg])
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
     assert lv.prev_nz is not None
-    check_sgd(native, gpu, g, lv)
+    check_sgd(native, gpu, g, lv, opt=dict(hot_features=hot, pipeline_width=width))
 
 
-@pytest.mark.parametrize("width", ["2", "4", "8"])
-@pytest.mark.parametrize("hot", ["0", None])
-def test_pipeline_runs_of_narrow_levels(gpu, width, hot, monkeypatch):
+@pytest.mark.parametrize("width", [2, 4, 8])
+@pytest.mark.parametrize("hot", [0, -1])
+def test_pipeline_runs_of_narrow_levels(gpu, width, hot):
     """Levels of 1 to 5 examples (disjoint pairs and triples between shared
     features), with consecutive rows and without: the pipeline takes the
     examples of a run in level order, and the result is the sequential one."""
-    if hot is not None:
-        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
-    monkeypatch.setenv("PDB_CHAIN_WIDTH", width)
     native = native_mod()
     rng = np.random.default_rng(int(width))
     rows = []
@@ -257,27 +244,25 @@ def test_pipeline_runs_of_narrow_levels(gpu, width, hot, monkeypatch):
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     widths = set(np.diff(lv.level_ptr.cpu().numpy()[:lv.L_host + 1]).tolist())
     assert {1, 2, 3, 4, 5} <= widths
-    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
+    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32),
+              opt=dict(hot_features=hot, pipeline_width=width))
 
 
-def test_plain_path_matches_pipeline(gpu, monkeypatch):
+def test_plain_path_matches_pipeline(gpu):
     native = native_mod()
     g = datagen.generate(3, **SCALED[3])
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
     from pdbtest import gpu_sgd
     a = gpu_sgd(native, gpu, g, lv)
-    monkeypatch.setenv("PDB_CHAIN", "0")
-    b = gpu_sgd(native, gpu, g, lv)
+    b = gpu_sgd(native, gpu, g, lv, opt=dict(pipeline=0))
     assert np.array_equal(a.view(np.int32), b.view(np.int32))
 
 
-@pytest.mark.parametrize("hot", ["0", "40", None])
+@pytest.mark.parametrize("hot", [0, 40, -1])
 @pytest.mark.parametrize("with_val", [True, False])
-def test_width1_pipeline_long_rows(gpu, hot, with_val, monkeypatch):
+def test_width1_pipeline_long_rows(gpu, hot, with_val):
     """A chain (feature 0 everywhere) mixing 50- and 70-entry examples: the
     pipeline stops at each example over 64 entries and resumes after it."""
-    if hot is not None:
-        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
     native = native_mod()
     rows = [{0} | set(range(1 + i % 11, 1 + i % 11 + (69 if i % 5 == 3 else 49)))
             for i in range(400)]
@@ -289,7 +274,8 @@ def test_width1_pipeline_long_rows(gpu, hot, with_val, monkeypatch):
              y=np.sign(rng.normal(size=n)).astype(np.float32))
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     assert lv.L_host == n
-    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
+    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32),
+              opt=dict(hot_features=hot))
 
 
 @pytest.mark.parametrize("name", ["pairs_1_before_32", "pairs_16_before_32"])
@@ -319,13 +305,11 @@ def test_reciprocal_exhaustive(gpu):
         native.pdb_check_reciprocal(0x3F000000, 0x3F800000, gpu)   # below 1
 
 
-@pytest.mark.parametrize("hot", ["0", None])
-def test_extreme_logits(gpu, hot, monkeypatch):
+@pytest.mark.parametrize("hot", [0, -1])
+def test_extreme_logits(gpu, hot):
     """Logistic steps whose logits pass the exponent cap (z < -87), overflow
     exp (z > 88.7) or round the logistic value to 0 or 1, on both the plain
     path and the pipeline."""
-    if hot is not None:
-        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
     native = native_mod()
     zs = [-1e30, -200.0, -104.5, -88.0, -87.5, -87.0, -86.9, -30.0, -17.0, -1e-3, 0.0, 1e-3,
           17.0, 30.0, 88.8, 103.9, 104.5, 200.0, 1e30]
@@ -342,16 +326,14 @@ def test_extreme_logits(gpu, hot, monkeypatch):
     g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=0, lr=np.float32(0.5), val=val, y=y)
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     assert lv.L_host == n
-    check_sgd(native, gpu, g, lv, w0=w0)
+    check_sgd(native, gpu, g, lv, w0=w0, opt=dict(hot_features=hot))
 
 
-@pytest.mark.parametrize("hot", ["0", "3", None])
-def test_width1_pipeline_rows_with_gaps(gpu, hot, monkeypatch):
+@pytest.mark.parametrize("hot", [0, 3, -1])
+def test_width1_pipeline_rows_with_gaps(gpu, hot):
     """A run of width-1 levels whose examples are not consecutive rows (rows
     in between sit on level 1 with fresh features), so the pipeline matches
     each entry against the preceding examples' entry ranges."""
-    if hot is not None:
-        monkeypatch.setenv("PDB_HOT_FEATURES", hot)
     native = native_mod()
     rng = np.random.default_rng(21)
     rows = []
@@ -369,7 +351,8 @@ def test_width1_pipeline_rows_with_gaps(gpu, hot, monkeypatch):
     lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
     widths = np.diff(lv.level_ptr.cpu().numpy()[:lv.L_host + 1])
     assert widths[0] > 1 and np.all(widths[1:] == 1) and lv.L_host > 300
-    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32))
+    check_sgd(native, gpu, g, lv, w0=(0.1 * rng.normal(size=d)).astype(np.float32),
+              opt=dict(hot_features=hot))
 
 
 def test_spine_selection_and_fallback(gpu):
@@ -539,11 +522,10 @@ def test_spine_random_exceptions(gpu, seed):
 
 
 @pytest.mark.parametrize("mode", EPOCH_MODES)
-def test_mf_structured_pairs(gpu, mode, monkeypatch):
+def test_mf_structured_pairs(gpu, mode):
     """Ratings whose neighbours share a user or an item (a wave takes two
     ratings at once only when the second does not depend on the first),
     repeated users and items, and a hot item."""
-    set_epoch_mode(monkeypatch, mode)
     native = native_mod()
     rng = np.random.default_rng(77)
     n, nu, ni = 2000, 40, 25
@@ -561,4 +543,4 @@ def test_mf_structured_pairs(gpu, mode, monkeypatch):
              V0=(0.2 * rng.normal(size=(ni, 32))).astype(np.float32),
              n=n, n_users=nu, n_items=ni, rank=32, lr=np.float32(0.01), reg=np.float32(0.05))
     lv, _ = check_schedule(native, gpu, row_ptr, col, nu + ni, 0)
-    check_mf(native, gpu, g, lv)
+    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode))

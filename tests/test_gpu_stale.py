@@ -18,20 +18,21 @@ def native_mod():
     return native
 
 
-def gpu_stale(native, dev, g, lv, delay, w0=None):
+def gpu_stale(native, dev, g, lv, delay, w0=None, opt=None):
     import torch
 
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], dev)
     y = torch.from_numpy(g["y"]).to(dev)
     w = torch.from_numpy(np.zeros(g["d"], np.float32) if w0 is None else w0.copy()).to(dev)
-    ws = native.pdb_stale_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], delay, lv)
+    ws = native.pdb_stale_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], delay, lv,
+                                opt=opt)
     torch.cuda.synchronize()
     assert native.pdb_workspace_status(ws) == native.PDB_OK
     return w.cpu().numpy()
 
 
-def check_stale(native, dev, g, lv, delay, w0=None, tol=1e-5):
-    got = gpu_stale(native, dev, g, lv, delay, w0)
+def check_stale(native, dev, g, lv, delay, w0=None, tol=1e-5, opt=None):
+    got = gpu_stale(native, dev, g, lv, delay, w0, opt=opt)
     w_init = np.zeros(g["d"], np.float32) if w0 is None else w0
     args = (g["row_ptr"], g["col"], g["val"], g["y"], w_init, g["lr"], g["loss"])
     ref_m = oracle.stale_epoch(*args, oracle.MATCHED, delay)
@@ -59,7 +60,7 @@ def structured_problem(rows, loss, with_val, seed):
     return dict(row_ptr=row_ptr, col=col, val=val, y=y, n=n, d=d, lr=lr, loss=loss)
 
 
-STALE_MODES = ["2", "1"]  # windowed where the windows fit, sync-free
+STALE_MODES = [2, 1]  # windowed where the windows fit, sync-free
 
 
 @pytest.mark.parametrize("name", sorted(structured_cases()))
@@ -67,25 +68,23 @@ STALE_MODES = ["2", "1"]  # windowed where the windows fit, sync-free
 @pytest.mark.parametrize("with_val", [True, False])
 @pytest.mark.parametrize("delay", [0, 1, 3, 17, 1000])
 @pytest.mark.parametrize("mode", STALE_MODES)
-def test_structured_stale_epochs(gpu, name, loss, with_val, delay, mode, monkeypatch):
-    monkeypatch.setenv("PDB_STALE_MODE", mode)
+def test_structured_stale_epochs(gpu, name, loss, with_val, delay, mode):
     native = native_mod()
     g = structured_problem(structured_cases()[name], loss, with_val, delay + 7 * loss)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    check_stale(native, gpu, g, lv, delay)
+    check_stale(native, gpu, g, lv, delay, opt=dict(stale_mode=mode))
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4])
 @pytest.mark.parametrize("delay", [0, 2, 8, 64])
 @pytest.mark.parametrize("mode", STALE_MODES)
-def test_random_stale_epochs(gpu, cfg, delay, mode, monkeypatch):
-    monkeypatch.setenv("PDB_STALE_MODE", mode)
+def test_random_stale_epochs(gpu, cfg, delay, mode):
     native = native_mod()
     g = datagen.generate(cfg, n=8000, d=4000 if cfg == 4 else 500, seed=40 + delay)
     g["lr"] = np.float32(g["lr"] / 4)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
     w0 = (0.05 * np.random.default_rng(delay).normal(size=g["d"])).astype(np.float32)
-    check_stale(native, gpu, g, lv, delay, w0)
+    check_stale(native, gpu, g, lv, delay, w0, opt=dict(stale_mode=mode))
 
 
 def test_delay_zero_equals_gpu_sgd(gpu):
@@ -118,8 +117,7 @@ def test_stale_errors(gpu):
     check_stale(native, gpu, g, lv, 1)
 
 
-def test_windows_too_large_fall_back(gpu, monkeypatch):
-    monkeypatch.setenv("PDB_STALE_MODE", "2")
+def test_windows_too_large_fall_back(gpu):
     # 60 entries per example: windows of 40 examples hold 2400 entries, over
     # the block's 2048, so the sync-free execution runs; 30 fit
     native = native_mod()
@@ -127,26 +125,26 @@ def test_windows_too_large_fall_back(gpu, monkeypatch):
     g = structured_problem(rows, 1, True, 3)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
     for delay in (29, 39):
-        check_stale(native, gpu, g, lv, delay)
+        check_stale(native, gpu, g, lv, delay, opt=dict(stale_mode=2))
 
 
-@pytest.mark.parametrize("mode", ["0", "2"])
-def test_empty_rows_and_window_edges(gpu, mode, monkeypatch):
-    monkeypatch.setenv("PDB_STALE_MODE", mode)
+@pytest.mark.parametrize("mode", [0, 2])
+def test_empty_rows_and_window_edges(gpu, mode):
+    opt = dict(stale_mode=mode)
     # empty examples, a last window shorter than delay + 1, one example
     native = native_mod()
     rows = [set(), {0, 1}, set(), {1, 2}, {2}, set(), {0, 2, 3}, {3}, set(), {1}, {0}]
     for delay in (0, 1, 2, 3, 4, 10, 11, 50):
         g = structured_problem(rows, 0, True, delay)
         lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-        check_stale(native, gpu, g, lv, delay)
+        check_stale(native, gpu, g, lv, delay, opt=opt)
     g = structured_problem([{5}], 1, False, 2)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    check_stale(native, gpu, g, lv, 3)
+    check_stale(native, gpu, g, lv, 3, opt=opt)
     # the largest delay: every read at the initial weights
     g = structured_problem(rows, 0, True, 9)
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    check_stale(native, gpu, g, lv, 2 ** 63 - 1)
+    check_stale(native, gpu, g, lv, 2 ** 63 - 1, opt=opt)
 
 
 @pytest.mark.parametrize("cfg,delay", [(2, 8), (4, 8)])
