@@ -432,6 +432,17 @@ __device__ __forceinline__ bool bw_wait_slots(unsigned long long *base, const in
     }
 }
 
+// A value every thread of the block reads from the same LDS word after a
+// barrier, made wave-uniform for the compiler: the ticket loop's exits and
+// the block barriers inside it then compile to scalar branches, so every
+// wave runs the same sequence of barriers by construction.
+__device__ __forceinline__ int block_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t block_uniform64(int64_t v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // LDS of a sync-free batch block: steps; for staged batches the weights of
 // the union features, each entry's union feature, and per occurrence its
 // example and value
@@ -480,7 +491,7 @@ __device__ bool general_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev
     }
     if (!ok && lane == 0) Sh.ok = 0;
     __syncthreads();
-    if (!Sh.ok) return false;
+    if (block_uniform(Sh.ok) == 0) return false;
     // phase 1: every example against the weights the batch read
     for (int64_t i = i0 + wave; i < i1; i += kBWaves) {
         const int64_t p0 = op.row_ptr[i], m = op.row_ptr[i + 1] - p0;
@@ -585,7 +596,7 @@ __device__ bool fast_batch(const BatchOp<LOSS, VAL> &op, const int32_t *uprev,
         if (ub + threadIdx.x + (int64_t)kBB * h < ue) Sh.uw[threadIdx.x + kBB * h] = word_value(v[h]);
     if (!ok && lane == 0) Sh.ok = 0;
     __syncthreads();
-    if (!Sh.ok) return false;
+    if (block_uniform(Sh.ok) == 0) return false;
     // phase 1 from LDS
 #pragma unroll
     for (int j = 0; j < kG; ++j) {
@@ -639,7 +650,7 @@ __global__ __launch_bounds__(kBB) void k_batch_syncfree(BatchOp<LOSS, VAL> op,
             Sh.ok = 1;
         }
         __syncthreads();
-        const int64_t b = Sh.ticket;
+        const int64_t b = block_uniform64(Sh.ticket);
         if (b >= nb) return;
         const int64_t i0 = b * op.B, i1 = min(i0 + op.B, op.n);
         const int64_t pb = op.row_ptr[i0], pe = op.row_ptr[i1];

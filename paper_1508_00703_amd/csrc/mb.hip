@@ -9,11 +9,23 @@ namespace {
 
 constexpr size_t kMbWs = 1024;  // control block + one 256-byte line for the hop word
 
-__global__ __launch_bounds__(kBlock) void k_mb_copy(const uint4 *__restrict__ src,
-                                                    uint4 *__restrict__ dst, int64_t count) {
+// Four 16-byte chunks per thread per step, all loads issued before the
+// stores; consecutive lanes take consecutive chunks (each wave moves 1 KiB
+// per load instruction).
+constexpr int kCopyUnroll = 4;
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(kBlock) void k_mb_copy(const u32x4 *__restrict__ src,
+                                                    u32x4 *__restrict__ dst, int64_t count) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += stride)
-        dst[i] = src[i];
+    int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    for (; i + (kCopyUnroll - 1) * stride < count; i += kCopyUnroll * stride) {
+        u32x4 v[kCopyUnroll];
+#pragma unroll
+        for (int k = 0; k < kCopyUnroll; ++k) v[k] = __builtin_nontemporal_load(&src[i + k * stride]);
+#pragma unroll
+        for (int k = 0; k < kCopyUnroll; ++k) __builtin_nontemporal_store(v[k], &dst[i + k * stride]);
+    }
+    for (; i < count; i += stride) dst[i] = src[i];
 }
 
 __device__ __forceinline__ int xcd_id() {
@@ -107,10 +119,10 @@ extern "C" int pdb_mb_copy(const void *src, void *dst, size_t bytes, hipStream_t
     int dev = 0, cus = 0;
     PDB_HIP(hipGetDevice(&dev));
     PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    // eight blocks per compute unit keep enough loads in flight to cover
-    // HBM latency; each thread then takes every stride-th 16-byte chunk
-    const int grid = grid_for(count, kBlock, (int64_t)std::max(cus, 1) * 8);
-    k_mb_copy<<<grid, kBlock, 0, s>>>(static_cast<const uint4 *>(src), static_cast<uint4 *>(dst),
+    // eight blocks per compute unit, four chunks per thread in flight: enough
+    // outstanding loads to cover HBM latency
+    const int grid = grid_for(count, (int64_t)kBlock * kCopyUnroll, (int64_t)std::max(cus, 1) * 8);
+    k_mb_copy<<<grid, kBlock, 0, s>>>(static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst),
                                       count);
     PDB_LAUNCHED();
     return PDB_OK;

@@ -173,9 +173,15 @@ def test_zero_watchdog_level_barriers(gpu):
     import torch
 
     native = native_mod()
-    g = datagen.generate(4, **SCALED[4])
+    # eight levels of 1000 examples each: example i touches feature i mod 1000
+    rows = [{i % 1000, 1000 + i} for i in range(8000)]
+    row_ptr, col = csr_from_rows(rows)
+    rng = np.random.default_rng(3)
+    g = dict(row_ptr=row_ptr, col=col, n=len(rows), d=int(col.max()) + 1, loss=1,
+             lr=np.float32(0.05), val=rng.normal(size=len(col)).astype(np.float32),
+             y=rng.normal(size=len(rows)).astype(np.float32))
     lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    assert lv.max_width_host > 16
+    assert lv.L_host == 8 and lv.max_width_host == 1000
     csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], gpu)
     y = torch.from_numpy(g["y"]).to(gpu)
     w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
