@@ -229,6 +229,22 @@ int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
                   float lr, int loss, const pdb_levels *levels, void *ws, size_t ws_bytes,
                   const pdb_options *opt, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, hosts that forbid allocation): pdb_sgd_epoch with the
+ * workspace replaced by a scratch array the library holds in device memory
+ * of each GPU it runs on (the control block and one 8-byte word per feature,
+ * 16 MiB + 512 bytes, kept until the process ends).  Same arguments, result
+ * and executions as pdb_sgd_epoch; d at most 2^21 (2,097,152), else
+ * PDB_ERR_UNSUPPORTED.  It calls no allocating routine.  status: device,
+ * [1], or NULL: after the epoch a kernel on the stream writes 0 there, or a
+ * nonzero device error code (watchdog) -- the report pdb_workspace_status
+ * gives for pdb_sgd_epoch.  Every call on one GPU uses that GPU's scratch:
+ * calls that overlap on one GPU (other streams, other threads) race and must
+ * be ordered by the caller.  Asynchronous. */
+int pdb_sgd_epoch_noalloc(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
+                          float *w, float lr, int loss, const pdb_levels *levels, int32_t *status,
+                          const pdb_options *opt, hipStream_t stream);
+
 /* One matrix-completion SGD epoch (rank 32).  Rating t's loss is Eq. 2's
  * squared error with its L2 regulariser on the two factor rows it touches,
  * (r_t - <U_u, V_i>)^2 / 2 + reg (|U_u|^2 + |V_i|^2) / 2, and its update is

@@ -33,6 +33,7 @@
 // between two steps is arithmetic.  Features written a few examples back come
 // from a small LDS ring; all other cold features are prefetched from global
 // memory kD examples ahead (their last writer finished before the prefetch).
+#include <atomic>
 #include <climits>
 
 #include "pdb_math.h"
@@ -1154,12 +1155,61 @@ int sgd_epoch_impl(const pdb_csr *csr, const float *labels, int64_t n, int64_t d
     return PDB_ERR_INVALID_ARG;
 }
 
+// Scratch of pdb_sgd_epoch_noalloc: the control block, then one packed word
+// per feature for the sync-free execution.  Each GPU holds its own copy from
+// module load to process end; host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device.
+constexpr int64_t kScratchMaxD = int64_t(1) << 21;
+constexpr size_t kScratchBytes = sizeof(Ctrl) + 8 * (size_t)kScratchMaxD;
+static_assert(sizeof(Ctrl) % 256 == 0, "the packed words start 256-byte aligned");
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::atomic<void *> g_scratch[kMaxScratchDevices];
+
+// The device address of `scratch` on the current device, looked up once per
+// device (concurrent first calls look up the same address).
+int scratch_address(void **out) {
+    int dev = 0;
+    PDB_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxScratchDevices) return PDB_ERR_UNSUPPORTED;
+    void *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (!p) {
+        PDB_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return PDB_ERR_HIP;
+        g_scratch[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return PDB_OK;
+}
+
+__global__ void k_status_out(const Ctrl *ctrl, int32_t *status) { *status = ctrl->err; }
 }  // namespace
 
 extern "C" int pdb_sgd_epoch(const pdb_csr *csr, const float *labels, int64_t n, int64_t d,
                              float *w, float lr, int loss, const pdb_levels *lv, void *ws,
                              size_t ws_bytes, const pdb_options *opt, hipStream_t s) {
     return sgd_epoch_impl(csr, labels, n, d, w, lr, loss, lv, ws, ws_bytes, opt, s);
+}
+
+extern "C" int pdb_sgd_epoch_noalloc(const pdb_csr *csr, const float *labels, int64_t n,
+                                     int64_t d, float *w, float lr, int loss,
+                                     const pdb_levels *lv, int32_t *status,
+                                     const pdb_options *opt, hipStream_t s) {
+    if (d < 0 || n < 0) return PDB_ERR_INVALID_ARG;
+    if (d > kScratchMaxD) return PDB_ERR_UNSUPPORTED;
+    void *ws = nullptr;
+    int rc = scratch_address(&ws);
+    if (rc != PDB_OK) return rc;
+    // the previous call's control block is still there: start from zero
+    // (also when there is nothing to run and the status is read at once)
+    k_ctrl_zero<<<1, 64, 0, s>>>(static_cast<Ctrl *>(ws));
+    PDB_LAUNCHED();
+    rc = sgd_epoch_impl(csr, labels, n, d, w, lr, loss, lv, ws, kScratchBytes, opt, s);
+    if (rc != PDB_OK || !status) return rc;
+    k_status_out<<<1, 1, 0, s>>>(static_cast<const Ctrl *>(ws), status);
+    PDB_LAUNCHED();
+    return PDB_OK;
 }
 
 extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const float *rating,

@@ -38,6 +38,7 @@ EXPORTS = (
     "pdb_check_reciprocal", "pdb_batch_schedule", "pdb_batch_epoch",
     "pdb_stale_workspace_bytes", "pdb_stale_epoch", "pdb_dense_plan",
     "pdb_dense_workspace_bytes", "pdb_dense_gd", "pdb_options_init", "pdb_validate_schedule",
+    "pdb_sgd_epoch_noalloc",
     # include/pdb_mb.h
     "pdb_mb_workspace_bytes", "pdb_mb_copy", "pdb_mb_hop", "pdb_mb_barrier",
 )
@@ -108,6 +109,8 @@ def load() -> ctypes.CDLL:
                                  ctypes.c_int, ctypes.POINTER(PdbScheduleInfo), P, sz, O, P]
     lib.pdb_sgd_epoch.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32, ctypes.c_int,
                                   ctypes.POINTER(PdbLevels), P, sz, O, P]
+    lib.pdb_sgd_epoch_noalloc.argtypes = [ctypes.POINTER(PdbCsr), P, i64, i64, P, f32,
+                                          ctypes.c_int, ctypes.POINTER(PdbLevels), P, O, P]
     lib.pdb_mf_epoch.argtypes = [P, P, P, i64, P, i64, P, i64, i32, f32, f32,
                                  ctypes.POINTER(PdbLevels), P, sz, O, P]
     lib.pdb_validate_csr.argtypes = [ctypes.POINTER(PdbCsr), i64, i64, P, sz, P]
@@ -316,6 +319,23 @@ def pdb_sgd_epoch(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tenso
                                 ws.numel(), _opt(opt), _stream(stream, csr.device)),
            "pdb_sgd_epoch")
     return ws
+
+
+def pdb_sgd_epoch_noalloc(csr: Csr, labels: torch.Tensor, n: int, d: int, w: torch.Tensor,
+                          lr: float, loss: int, levels: Levels, status: torch.Tensor | None = None,
+                          stream=None, opt=None):
+    """pdb_sgd_epoch on the library's own scratch (no workspace); status: an
+    int32 device tensor of one element that receives the device error code."""
+    if w.dtype != torch.float32 or labels.dtype != torch.float32:
+        raise TypeError("w and labels must be float32")
+    if w.numel() < d or labels.numel() < n:
+        raise ValueError("w must hold d entries and labels n entries")
+    if status is not None and (status.dtype != torch.int32 or status.numel() < 1):
+        raise TypeError("status must be an int32 device tensor")
+    _check(load().pdb_sgd_epoch_noalloc(ctypes.byref(csr.c()), _ptr(labels), n, d, _ptr(w),
+                                        ctypes.c_float(lr), loss, ctypes.byref(levels.c()),
+                                        _ptr(status), _opt(opt), _stream(stream, csr.device)),
+           "pdb_sgd_epoch_noalloc")
 
 
 def pdb_mf_epoch(user, item, rating, n: int, U, n_users: int, V, n_items: int, rank: int,
