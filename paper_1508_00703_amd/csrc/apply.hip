@@ -467,6 +467,7 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     // (b) writes of example t-1; example t+1's weights (those example t
     // writes are forwarded), the staged example t+3, and the cold values of
     // example t+kD (their last writers are before t)
+    __builtin_amdgcn_sched_barrier(0);  // the region of the sum starts here
     lds_write(st.p_l, w_prev);
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_prev), wbuf, st.p_g, 0, 0);
     const unsigned rd = st.nxt.a.z;
@@ -477,8 +478,21 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
         VAL ? __int_as_float(__builtin_amdgcn_ds_bpermute((int)rd, __float_as_int(x))) : 1.0f;
     const Stg nxt3 = read_slot_at<SL + 3, VAL>(sblk);
     const float g_pf = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wbuf, st.pf[SL], 0, 0));
-    // (c) the step of example t
+    // (c) the step of example t.  The memory operations above go into the
+    // gaps the DPP adds of the sum must leave after each VALU write (two
+    // instructions each: a DPP add, two LDS operations, ...), and the
+    // fences keep every other instruction of the step out of that region:
+    // the rotation's select of the value read for example t+1 would
+    // otherwise be scheduled inside the sum, and its wait for that LDS read
+    // would stall the chain (consumer 319 -> 311 cycles per example)
     const float s = sgd_scale_t<LOSS>(wave_sum64(acc), tgt, op.lr);
+    __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);  // VALU, LDS x2, ..., VMEM x2
+    __builtin_amdgcn_sched_group_barrier(0x0080, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x0080, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x0010, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
     // rotation
     st.p_wold = w_old;
     st.p_x = x;
