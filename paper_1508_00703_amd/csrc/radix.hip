@@ -11,7 +11,8 @@
 //      finds the lanes holding the same digit with one ballot per digit bit
 //      (no LDS atomics, so a Zipf-hot digit costs nothing extra), counts per
 //      (item slot, wave, digit) go to LDS, one thread per digit turns them
-//      into running offsets, and every element is written to its slot.
+//      into running offsets, the tile is staged in LDS in digit order and
+//      written out from there, consecutive lanes to consecutive slots.
 #include "pdb_internal.h"
 
 namespace pdbk {
@@ -118,12 +119,23 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const uint32_t *__restrict__ keys, const uint32_t *__restrict__ vals, int64_t count,
     int shift, int nb, const uint32_t *__restrict__ offsets, int64_t ntiles,
     uint32_t *__restrict__ kout, uint32_t *__restrict__ vout) {
-    __shared__ uint16_t s_cnt[kItems][kWavesPerBlock][256];
-    __shared__ uint32_t s_goff[256];
+    // the per-(item slot, wave, digit) counts, then (same LDS) the tile in
+    // digit order
+    __shared__ union {
+        uint16_t cnt[kItems][kWavesPerBlock][256];
+        struct {
+            uint32_t k[kTile];
+            uint32_t v[kTile];
+        } st;
+    } U;
+    static_assert(sizeof(U.cnt) == sizeof(U.st), "the staged tile reuses the counts' LDS");
+    __shared__ uint32_t s_goff[256];    // first output slot of each digit of this tile
+    __shared__ uint32_t s_dstart[256];  // first position of each digit in the staged tile
+    __shared__ uint32_t s_wave[kWavesPerBlock];
     const int t = threadIdx.x, wave = wave_in_block();
     const int radix = 1 << nb;
     const uint32_t mask = (uint32_t)radix - 1u;
-    uint16_t *flat = &s_cnt[0][0][0];
+    uint16_t *flat = &U.cnt[0][0][0];
     for (int i = t; i < kItems * kWavesPerBlock * 256; i += kBlock) flat[i] = 0;
     if (t < radix) s_goff[t] = offsets[(int64_t)t * ntiles + blockIdx.x];
     __syncthreads();
@@ -145,30 +157,51 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         }
         const unsigned r = lanes_below(peers);
         rk[j] = r;
-        if (valid && r == 0) s_cnt[j][wave][dg] = (uint16_t)__popcll(peers);
+        if (valid && r == 0) U.cnt[j][wave][dg] = (uint16_t)__popcll(peers);
     }
     __syncthreads();
+    // per digit: the counts become running offsets inside the digit's run
+    // (item slot, then wave: tile order), and the run's length is scanned
+    // over the digits into its start in the staged tile
+    uint32_t len = 0;
     if (t < radix) {
-        uint32_t run = 0;
         for (int j = 0; j < kItems; ++j) {
 #pragma unroll
             for (int w = 0; w < kWavesPerBlock; ++w) {
-                const uint32_t c = s_cnt[j][w][t];
-                s_cnt[j][w][t] = (uint16_t)run;
-                run += c;
+                const uint32_t c = U.cnt[j][w][t];
+                U.cnt[j][w][t] = (uint16_t)len;
+                len += c;
             }
         }
     }
+    uint32_t all;
+    const uint32_t start = block_excl_scan_u32(len, s_wave, &all);
+    if (t < radix) s_dstart[t] = start;
     __syncthreads();
+    uint32_t pos[kItems];
 #pragma unroll
     for (int j = 0; j < kItems; ++j) {
-        const int64_t idx = base + (int64_t)j * kBlock + t;
-        if (idx < count) {
-            const uint32_t dg = (k[j] >> shift) & mask;
-            const uint32_t dst = s_goff[dg] + (uint32_t)s_cnt[j][wave][dg] + rk[j];
-            kout[dst] = k[j];
-            vout[dst] = v[j];
+        const uint32_t dg = (k[j] >> shift) & mask;
+        pos[j] = s_dstart[dg] + (uint32_t)U.cnt[j][wave][dg] + rk[j];
+    }
+    __syncthreads();  // every count read before the staged tile overwrites them
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        if (base + (int64_t)j * kBlock + t < count) {
+            U.st.k[pos[j]] = k[j];
+            U.st.v[pos[j]] = v[j];
         }
+    }
+    __syncthreads();
+    // the staged tile in order: consecutive lanes write consecutive slots of
+    // a digit's run, so a wave's stores form a few contiguous segments
+    const int nvalid = (int)min((int64_t)kTile, count - base);
+    for (int i = t; i < nvalid; i += kBlock) {
+        const uint32_t kk = U.st.k[i];
+        const uint32_t dg = (kk >> shift) & mask;
+        const uint32_t dst = s_goff[dg] + ((uint32_t)i - s_dstart[dg]);
+        kout[dst] = kk;
+        vout[dst] = U.st.v[i];
     }
 }
 
