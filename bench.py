@@ -598,7 +598,8 @@ def main():
         ("-d%d" % delay if delay >= 0 else "")
     # the epoch kernel the library runs (the rule of pdb_sgd_epoch / pdb_mf_epoch)
     mode = args.epoch_mode
-    syncfree = mode == 2 or (mode == 0 and L > 0 and n >= 8 * L)
+    one_cu = mf and L > 0 and n < 16 * L and (g["n_users"] + g["n_items"]) * 32 < 2 ** 31 - 65
+    syncfree = mode == 2 or (mode == 0 and L > 0 and (n >= 8 * L or one_cu))
     if batch:
         kernel = "k_batch_syncfree (mini-batch epoch)" if mode != 1 else \
             "k_batch_levels (mini-batch epoch)"
@@ -606,7 +607,8 @@ def main():
         kernel = ("k_stale_window or k_stale_epoch (bounded-delay epoch; the library picks "
                   "per call, windowed on chain-like inputs)")
     elif syncfree:
-        kernel = "k_mf_syncfree (epoch)" if mf else "k_sgd_syncfree (epoch)"
+        kernel = ("k_mf_onecu (epoch)" if one_cu else "k_mf_syncfree (epoch)") if mf \
+            else "k_sgd_syncfree (epoch)"
     else:
         kernel = "k_levels_apply (epoch)"
     digest = source_digest(bool(batch), delay >= 0)

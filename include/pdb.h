@@ -142,6 +142,12 @@ typedef struct pdb_options {
     int32_t stale_mode;            /* pdb_stale_mode (default PDB_STALE_AUTO) */
     int32_t dense_stream;          /* pdb_dense_gd: 1 streams the tiles from memory even when they
                                       fit in LDS, 0 (default) keeps them resident when they fit */
+    int32_t mf_one_cu;             /* sync-free pdb_mf_epoch: 1 runs every rating on one compute
+                                      unit (hand-overs through its LDS and L1 cache), 0 spreads the
+                                      ratings over the device (device-scope hand-overs), -1
+                                      (default) one compute unit when levels are narrow (n < 16 L)
+                                      and (n_users + n_items) * 32 < 2^31; 1 falls back to the
+                                      device-wide execution when the words do not fit that bound */
 } pdb_options;
 
 /* Fills *opt with the defaults above.  Host only. */
@@ -252,9 +258,12 @@ int pdb_sgd_epoch_noalloc(const pdb_csr *csr, const float *labels, int64_t n, in
  * top of this header; both rows from their values before the step).  Rating
  * t touches user row U[user[t]] (device [n_users*32]) and item row
  * V[item[t]] (device [n_items*32]); levels from pdb_schedule on the CSR whose
- * row t is {user[t], n_users + item[t]}.  Runs level by level or sync-free under the
- * rule of pdb_sgd_epoch (the sync-free run needs levels->prev_nz and
- * pdb_epoch_workspace_bytes((n_users + n_items) * 32)).  Asynchronous. */
+ * row t is {user[t], n_users + item[t]}.  Runs level by level or sync-free
+ * (the sync-free run needs levels->prev_nz and
+ * pdb_epoch_workspace_bytes((n_users + n_items) * 32)); under
+ * PDB_EPOCH_AUTO sync-free when levels are wide (n >= 8 L) or when the
+ * one-compute-unit execution applies (pdb_options.mf_one_cu), else level by
+ * level.  Every execution gives bitwise the same U and V.  Asynchronous. */
 int pdb_mf_epoch(const int32_t *user, const int32_t *item, const float *rating, int64_t n,
                  float *U, int64_t n_users, float *V, int64_t n_items, int32_t rank, float lr,
                  float reg, const pdb_levels *levels, void *ws, size_t ws_bytes,

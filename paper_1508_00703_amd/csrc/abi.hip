@@ -73,6 +73,7 @@ int resolve_opts(const pdb_options *o, Opts *out) {
         return PDB_ERR_INVALID_ARG;
     if ((o->pipeline != 0 && o->pipeline != 1) || (o->dense_stream != 0 && o->dense_stream != 1))
         return PDB_ERR_INVALID_ARG;
+    if (o->mf_one_cu < -1 || o->mf_one_cu > 1) return PDB_ERR_INVALID_ARG;
     if (o->pipeline_width < 1 || o->thin_max < 1 || o->batch_thin_max < 1 ||
         o->batch_syncfree_blocks < 1 || o->hot_features < -1 || o->spin_timeout_us < 0)
         return PDB_ERR_INVALID_ARG;
@@ -88,6 +89,7 @@ int resolve_opts(const pdb_options *o, Opts *out) {
     out->batch_sf_blocks = o->batch_syncfree_blocks;
     out->stale_mode = o->stale_mode;
     out->dense_stream = o->dense_stream != 0;
+    out->mf_one_cu = o->mf_one_cu;
     return PDB_OK;
 }
 
@@ -122,6 +124,7 @@ extern "C" int pdb_options_init(pdb_options *o) {
     o->batch_syncfree_blocks = 32;
     o->stale_mode = PDB_STALE_AUTO;
     o->dense_stream = 0;
+    o->mf_one_cu = -1;
     return PDB_OK;
 }
 

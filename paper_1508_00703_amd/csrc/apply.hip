@@ -190,17 +190,6 @@ __device__ __forceinline__ float target_of(float y) {
     return LOSS == PDB_LOGISTIC ? (y > 0.0f ? 1.0f : 0.0f) : y;
 }
 
-template <int LOSS>
-__device__ __forceinline__ float sgd_scale_t(float z, float tgt, float lr) {
-    float g;
-    if (LOSS == PDB_LOGISTIC) {
-        g = logistic_grad(z, tgt);
-    } else {
-        g = z - tgt;
-    }
-    return lr * g;
-}
-
 // Producer wave pid (0..2): stages examples t of the run (batches of kPB, in
 // turn), never more than kRB ahead of the consumer.  For every entry it finds
 // whether the previous writer is among the kD examples before it and picks
@@ -458,7 +447,6 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     const float tgt = VAL ? st.cur.t : __uint_as_float(st.cur.a.x);
     // (a) example t-1's step lands: its new weights, and this example's
     // weights (forwarded lanes apply that step to the pair they took)
-    const float w_prev = __builtin_fmaf(-st.s_prev, st.p_x, st.p_wold);
     const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
     // binary logistic: the product w * 1 + 0 differs from w only for w = -0,
     // which changes z at most in the sign of a zero sum, and the logistic
@@ -468,6 +456,7 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     // writes are forwarded), the staged example t+3, and the cold values of
     // example t+kD (their last writers are before t)
     __builtin_amdgcn_sched_barrier(0);  // the region of the sum starts here
+    const float w_prev = __builtin_fmaf(-st.s_prev, st.p_x, st.p_wold);
     lds_write(st.p_l, w_prev);
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(w_prev), wbuf, st.p_g, 0, 0);
     const unsigned rd = st.nxt.a.z;
@@ -485,13 +474,36 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     // the rotation's select of the value read for example t+1 would
     // otherwise be scheduled inside the sum, and its wait for that LDS read
     // would stall the chain (consumer 319 -> 311 cycles per example)
-    const float s = sgd_scale_t<LOSS>(wave_sum64(acc), tgt, op.lr);
-    __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);  // VALU, LDS x2, ..., VMEM x2
+    const float z = wave_sum64_lane63(acc);  // the sum is in lane 63
+    __builtin_amdgcn_sched_group_barrier(0x0002, 2, 0);  // VALU x2, LDS x2, ..., VMEM x2
     __builtin_amdgcn_sched_group_barrier(0x0080, 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x0080, 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x0010, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // (d) the step runs on every lane and is read out of lane 63.  The
+    // rotation's selects sit between the exponential and the reciprocal,
+    // long after the LDS read they wait for, where they fill gaps of the
+    // chain instead of delaying the next example's forwarded values
+    // (consumer 311 -> 301 cycles per example with the step's first write
+    // moved into the sum and the read-out after the step)
+    float s, cur_v;
+    bool cur_fwd;
+    if (LOSS == PDB_LOGISTIC) {
+        const float sub = logistic_sub(z, tgt);
+        const float e = dev_exp87(-z);
+        __builtin_amdgcn_sched_barrier(0);
+        cur_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
+        cur_fwd = rd < 256u;
+        s = op.lr * logistic_from_exp(e, sub);
+    } else {
+        s = op.lr * (z - tgt);
+        __builtin_amdgcn_sched_barrier(0);
+        cur_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
+        cur_fwd = rd < 256u;
+    }
+    s = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 63));
     __builtin_amdgcn_sched_barrier(0);
     // rotation
     st.p_wold = w_old;
@@ -499,12 +511,12 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     st.p_l = st.cur.a.y;
     st.p_g = st.cur.a.w;
     st.s_prev = s;
-    st.cur_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
+    st.cur_v = cur_v;
     st.gv[SL] = g_pf;
     st.cur = st.nxt;
     st.cur_fw = fw1;
     st.cur_fx = fx1;
-    st.cur_fwd = rd < 256u;
+    st.cur_fwd = cur_fwd;
     st.nxt = st.nxt2;
     st.nxt2 = nxt3;
 }
@@ -1035,6 +1047,288 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
 // writer's wave from running) and about 8 levels' worth of examples in
 // flight, at least a block per four CUs (more only adds waiting waves and
 // polling traffic).
+// Matrix completion on one compute unit (k_mf_onecu): the Read Protocol of
+// Sec. 5 at row grain, as in k_mf_syncfree, but one block runs every rating,
+// so a hand-over between two ratings is met inside the compute unit -- the
+// LDS for the hottest rows, the unit's L1 cache (workgroup scope) for the
+// others -- instead of at the device-wide coherence point.  Measured
+// hand-overs between two waves of one block: 205 ns through global memory at
+// workgroup scope, 100 ns through LDS, against 420-680 ns at device scope.
+// That wins on inputs whose levels are narrow (the chain of hand-overs is
+// long) while one compute unit's throughput, about 35 ns per rating, keeps
+// up.
+//  * The producer wave streams each rating's user, item, value and previous
+//    ratings into an LDS ring in rating order, and touches its cold rows'
+//    words so they are in the L2 cache when a worker gets there.
+//  * Fifteen workers take tickets of two consecutive ratings in turn, one
+//    rating per 32-lane half (lane j: component j), both halves at once
+//    unless the second depends on the first.  A worker waits until its two
+//    rows' words carry the expected previous ratings, computes the step
+//    (the same arithmetic as MfOp) and publishes both rows tagged with its
+//    rating.
+//  * Rows with the smallest ids (the Zipf-hot ones of the generator) live in
+//    LDS as (value, rating) words for the whole epoch and are written back at
+//    the end.
+//  * Progress: tickets go to the workers in index order and every ticket
+//    waits only on earlier ratings, so the earliest unfinished ticket is
+//    never blocked; the producer waits only for ring slots the slowest
+//    worker has released.
+constexpr int kMfThreads = 1024;  // one block of 16 waves: 15 workers and the producer
+constexpr int kMfWorkers = kMfThreads / kWave - 1;
+constexpr int kMfRing = 1024;     // ratings staged ahead (power of two)
+constexpr int kMfPB = 256;        // ratings per producer batch (4 per lane)
+constexpr int kMfLds = 160 * 1024;  // LDS of one compute unit (gfx950): ring + hot rows
+
+struct MfShared {
+    int4 rec[kMfRing];     // user, item, previous rating on the user, on the item (-1 none)
+    float r[kMfRing];
+    int ready;             // ratings staged: 0 .. ready-1
+    int prog[kMfWorkers];  // first rating each worker may still read (INT_MAX when done)
+    int stop;              // a wave gave up: every loop ends, nothing is written back
+    unsigned long long sink[64];  // LDS words of lanes whose row is not in LDS
+};
+// the hot rows' words follow MfShared in dynamic LDS, 256-byte aligned
+constexpr int kMfHotOff = (int)((sizeof(MfShared) + 255) / 256 * 256);
+constexpr int kMfHotRows = (kMfLds - kMfHotOff) / 256;
+
+typedef __attribute__((address_space(3))) unsigned long long lds_u64;
+__device__ __forceinline__ unsigned long long lword_get(unsigned a) {
+    return __hip_atomic_load((lds_u64 *)(uintptr_t)a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lword_put(unsigned a, unsigned long long w) {
+    __hip_atomic_store((lds_u64 *)(uintptr_t)a, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+struct MfBatch {
+    int u[4], it[4];
+    float r[4];
+    int2 p[4];
+};
+
+__device__ __forceinline__ MfBatch mf_batch_load(const int32_t *__restrict__ user,
+                                                 const int32_t *__restrict__ item,
+                                                 const float *__restrict__ rating,
+                                                 const int32_t *__restrict__ prev_nz, int64_t q0,
+                                                 int64_t n) {
+    MfBatch m;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        const int64_t q = q0 + lane_id() + 64 * x;
+        const int64_t qc = q < n ? q : n - 1;  // past the end: rating n - 1, not staged
+        m.u[x] = user[qc];
+        m.it[x] = item[qc];
+        m.r[x] = rating[qc];
+        m.p[x] = *reinterpret_cast<const int2 *>(prev_nz + 2 * qc);
+    }
+    return m;
+}
+
+__device__ bool mf_give_up(MfShared &S, Ctrl *ctrl, int64_t t0, int64_t timeout) {
+    if (lds_load(&S.stop) || aborted(ctrl)) {
+        lds_store(&S.stop, 1);
+        return true;
+    }
+    if (now_ticks() - t0 > timeout) {
+        record_error(ctrl, DERR_WAIT_TIMEOUT);
+        lds_store(&S.stop, 1);
+        return true;
+    }
+    return false;
+}
+
+__device__ void mf_producer(const int32_t *__restrict__ user, const int32_t *__restrict__ item,
+                            const float *__restrict__ rating, const int32_t *__restrict__ prev_nz,
+                            const unsigned long long *uvw, int64_t n_users, int64_t n, int hot_u,
+                            int hot_i, MfShared &S, Ctrl *ctrl, int64_t timeout) {
+    const int lane = lane_id();
+    // batch b's entries are loaded during batch b - 1, and its cold words
+    // touched during batch b; the touched values are consumed one batch
+    // later, so no wait of the loop is for a load issued in the same batch
+    MfBatch cur = mf_batch_load(user, item, rating, prev_nz, 0, n);
+    unsigned long long touch[16], sink = 0;
+#pragma unroll
+    for (int x = 0; x < 16; ++x) touch[x] = 0;
+    for (int64_t q0 = 0; q0 < n; q0 += kMfPB) {
+        // ring space: every worker is past rating q0 + kMfPB - kMfRing
+        int64_t t0 = 0;
+        bool quit = false;
+        for (int round = 0;; ++round) {
+            const int pv = lane < kMfWorkers ? lds_load(&S.prog[lane]) : INT_MAX;
+            int mn = pv;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) mn = min(mn, __shfl_xor(mn, o));
+            if ((int64_t)mn + kMfRing >= q0 + kMfPB) break;
+            if (round == 0) t0 = now_ticks();
+            if ((round & 31) == 31 && mf_give_up(S, ctrl, t0, timeout)) {
+                quit = true;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+        }
+        if (quit) break;
+        const MfBatch nxt = mf_batch_load(user, item, rating, prev_nz, q0 + kMfPB, n);
+#pragma unroll
+        for (int x = 0; x < 16; ++x) sink ^= touch[x];
+        // touch both 128-byte lines of each cold row's words (32 words of 8
+        // bytes), so the rows are in the L2 cache when the workers read them;
+        // a hot row's lanes touch the first row instead
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            const unsigned long long *ru = uvw + (cur.u[x] < hot_u ? 0 : (int64_t)cur.u[x] * 32);
+            const unsigned long long *ri =
+                uvw + (cur.it[x] < hot_i ? 0 : (n_users + cur.it[x]) * 32);
+            touch[4 * x] = __hip_atomic_load(ru, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            touch[4 * x + 1] =
+                __hip_atomic_load(ru + 16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            touch[4 * x + 2] = __hip_atomic_load(ri, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            touch[4 * x + 3] =
+                __hip_atomic_load(ri + 16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            const int slot = (int)((q0 + lane + 64 * x) & (kMfRing - 1));
+            S.rec[slot] = make_int4(cur.u[x], cur.it[x], cur.p[x].x < 0 ? -1 : (cur.p[x].x >> 1),
+                                    cur.p[x].y < 0 ? -1 : (cur.p[x].y >> 1));
+            S.r[slot] = cur.r[x];
+        }
+        compiler_fence();  // LDS executes one wave's operations in order
+        if (lane == 0) lds_store(&S.ready, (int)min(q0 + kMfPB, n));
+        compiler_fence();
+        cur = nxt;
+    }
+#pragma unroll
+    for (int x = 0; x < 16; ++x) sink ^= touch[x];
+    __asm__ volatile("" ::"v"(sink));
+}
+
+__global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
+    const int32_t *__restrict__ user, const int32_t *__restrict__ item,
+    const float *__restrict__ rating, const int32_t *__restrict__ prev_nz,
+    unsigned long long *uvw, int64_t n_users, int64_t n, int hot_u, int hot_i, float lr,
+    float reg, Ctrl *ctrl, int64_t timeout) {
+    extern __shared__ __align__(256) unsigned char mf_lds[];
+    MfShared &S = *reinterpret_cast<MfShared *>(mf_lds);
+    unsigned long long *hotw = reinterpret_cast<unsigned long long *>(mf_lds + kMfHotOff);
+    const int wave = threadIdx.x / kWave;
+    if (threadIdx.x < kMfWorkers) S.prog[threadIdx.x] = 0;
+    if (threadIdx.x == 0) {
+        S.ready = 0;
+        S.stop = 0;
+    }
+    // hot rows: users 0 .. hot_u - 1, then items 0 .. hot_i - 1
+    for (int x = threadIdx.x; x < hot_u * 32; x += kMfThreads) hotw[x] = uvw[x];
+    for (int x = threadIdx.x; x < hot_i * 32; x += kMfThreads)
+        hotw[hot_u * 32 + x] = uvw[n_users * 32 + x];
+    __syncthreads();
+    if (wave == kMfWorkers) {
+        mf_producer(user, item, rating, prev_nz, uvw, n_users, n, hot_u, hot_i, S, ctrl, timeout);
+    } else {
+        const int lane = lane_id();
+        const int h = lane >> 5, j = lane & 31;
+        const int n_tk = (int)((n + 1) / 2);
+        const unsigned hot_base = (unsigned)(uintptr_t)(lds_u64 *)hotw + (unsigned)j * 8u;
+        // lanes whose row is not in LDS read and write these LDS words, lanes
+        // whose row is read an unused global word and write a sink word
+        const unsigned lsink = (unsigned)(uintptr_t)(lds_u64 *)&S.sink[lane];
+        unsigned long long *gsink = reinterpret_cast<unsigned long long *>(ctrl->sink) + j;
+        const int iu_base = (int)n_users * 32 + j;
+        int ready = 0;  // last value read of S.ready
+        bool quit = false;
+        for (int k = wave; k < n_tk && !quit; k += kMfWorkers) {
+            const int q0 = 2 * k;
+            const bool has1 = q0 + 1 < n;
+            const int need = q0 + (has1 ? 2 : 1);
+            if (ready < need) {
+                int64_t t0 = 0;
+                for (int round = 0; (ready = lds_load(&S.ready)) < need; ++round) {
+                    if (round == 0) t0 = now_ticks();
+                    if ((round & 31) == 31 && mf_give_up(S, ctrl, t0, timeout)) {
+                        quit = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                if (quit) break;
+                compiler_fence();
+            }
+            const int q = has1 ? q0 + h : q0;  // an idle second half mirrors the first
+            const int slot = q & (kMfRing - 1);
+            const int4 rc = S.rec[slot];
+            const float r = S.r[slot];
+            // rc.x user, rc.y item, rc.z / rc.w their previous ratings
+            const bool uh = rc.x < hot_u, ih = rc.y < hot_i;
+            const unsigned ula = uh ? hot_base + (unsigned)rc.x * 256u : lsink;
+            const unsigned ila = ih ? hot_base + (unsigned)(hot_u + rc.y) * 256u : lsink;
+            unsigned long long *ug = uh ? gsink : uvw + (rc.x * 32 + j);
+            unsigned long long *ig = ih ? gsink : uvw + (iu_base + rc.y * 32);
+            unsigned long long wu, wi;
+            {
+                const unsigned long long lu = lword_get(ula), li = lword_get(ila);
+                const unsigned long long gu = word_get_wg(ug, 0), gi = word_get_wg(ig, 0);
+                wu = uh ? lu : gu;
+                wi = ih ? li : gi;
+            }
+            // the second rating depends on the first: one after the other
+            const bool dep = has1 && (__builtin_amdgcn_readlane(rc.z, 32) == q0 ||
+                                      __builtin_amdgcn_readlane(rc.w, 32) == q0);
+            for (int p = 0; p < (dep ? 2 : 1); ++p) {
+                const bool act = dep ? h == p : (h == 0 || has1);
+                bool need_u = act && word_tag(wu) != rc.z;
+                bool need_i = act && word_tag(wi) != rc.w;
+                if (__ballot(need_u || need_i)) {
+                    int64_t t0 = now_ticks();
+                    for (int round = 0;; ++round) {
+                        if (round > 0 && __ballot((need_u && !uh) || (need_i && !ih)))
+                            __builtin_amdgcn_s_sleep(1);
+                        const unsigned long long lu = lword_get(ula), li = lword_get(ila);
+                        const unsigned long long gu = word_get_wg(ug, 0), gi = word_get_wg(ig, 0);
+                        if (need_u) wu = uh ? lu : gu;
+                        if (need_i) wi = ih ? li : gi;
+                        need_u = need_u && word_tag(wu) != rc.z;
+                        need_i = need_i && word_tag(wi) != rc.w;
+                        if (__ballot(need_u || need_i) == 0ull) break;
+                        // the watchdog and the abort flag (a device-scope load)
+                        // every 32 rounds, not on the path of every poll
+                        if ((round & 31) == 31 && mf_give_up(S, ctrl, t0, timeout)) {
+                            quit = true;
+                            break;
+                        }
+                    }
+                    if (quit) break;
+                }
+                const float uj = act ? word_value(wu) : 0.0f, vj = act ? word_value(wi) : 0.0f;
+                const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
+                const float ea = err * vj, eb = reg * uj;
+                const float a2 = err * uj, b2 = reg * vj;
+                const unsigned long long nu = word_pack(__builtin_fmaf(lr, ea - eb, uj), q);
+                const unsigned long long ni = word_pack(__builtin_fmaf(lr, a2 - b2, vj), q);
+                // inactive lanes write the sinks
+                lword_put(act ? ula : lsink, nu);
+                lword_put(act ? ila : lsink, ni);
+                word_put_wg(act ? ug : gsink, 0, nu);
+                word_put_wg(act ? ig : gsink, 0, ni);
+                if (dep && p == 0) {
+                    // the second rating reads what the first just wrote
+                    const unsigned long long lu = lword_get(ula), li = lword_get(ila);
+                    const unsigned long long gu = word_get_wg(ug, 0), gi = word_get_wg(ig, 0);
+                    wu = uh ? lu : gu;
+                    wi = ih ? li : gi;
+                }
+            }
+            // done with the ring slots of this ticket (every lane stores the same value)
+            lds_store(&S.prog[wave], q0 + 2 * kMfWorkers);
+        }
+        lds_store(&S.prog[wave], INT_MAX);
+    }
+    __syncthreads();
+    // the hot rows go back to their words (unless a wave gave up)
+    if (!S.stop) {
+        for (int x = threadIdx.x; x < hot_u * 32; x += kMfThreads) uvw[x] = hotw[x];
+        for (int x = threadIdx.x; x < hot_i * 32; x += kMfThreads)
+            uvw[n_users * 32 + x] = hotw[hot_u * 32 + x];
+    }
+}
+
 int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *grid) {
     int dev = 0, cus = 0, per_cu = 0;
     PDB_HIP(hipGetDevice(&dev));
@@ -1048,7 +1342,8 @@ int syncfree_grid(const void *fn, int64_t n, int64_t L, int per_block, int64_t *
 }
 
 int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_t n_users,
-                       int64_t n_items, int64_t L, void *ws, int64_t timeout, hipStream_t s) {
+                       int64_t n_items, int64_t L, void *ws, int64_t timeout, bool one_cu,
+                       hipStream_t s) {
     Ctrl *ctrl = static_cast<Ctrl *>(ws);
     unsigned long long *uvw =
         reinterpret_cast<unsigned long long *>(static_cast<char *>(ws) + sizeof(Ctrl));
@@ -1060,17 +1355,30 @@ int launch_mf_syncfree(const MfOp &op, const int32_t *prev_nz, int64_t n, int64_
         k_wv_in<<<grid_for(n_items * 32, kBlock, 8192), kBlock, 0, s>>>(op.V, uvw + n_users * 32,
                                                                        n_items * 32);
     PDB_LAUNCHED();
-    const void *fn = reinterpret_cast<const void *>(&k_mf_syncfree);
-    int64_t grid = 1;
-    int rc = syncfree_grid(fn, n, L, 2 * kWavesPerBlock, &grid);
-    if (rc != PDB_OK) return rc;
-    // cooperative: the whole grid resident (the waves wait on each other)
-    const int32_t *a_user = op.user, *a_item = op.item;
-    const float *a_rating = op.rating;
-    float a_lr = op.lr, a_reg = op.reg;
-    void *args[] = {&a_user, &a_item, &a_rating, &prev_nz, &uvw, &n_users, &n_items, &n,
-                    &a_lr, &a_reg, &ctrl, const_cast<int64_t *>(&timeout)};
-    PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, s));
+    if (one_cu) {
+        // the hottest rows in LDS: as many items as users, each side capped
+        // by its count
+        const int hot_i = (int)std::min<int64_t>(n_items, kMfHotRows / 2);
+        const int hot_u = (int)std::min<int64_t>(n_users, kMfHotRows - hot_i);
+        PDB_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(&k_mf_onecu),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, kMfLds));
+        k_mf_onecu<<<1, kMfThreads, kMfLds, s>>>(op.user, op.item, op.rating, prev_nz, uvw,
+                                                n_users, n, hot_u, hot_i, op.lr, op.reg, ctrl,
+                                                timeout);
+        PDB_LAUNCHED();
+    } else {
+        const void *fn = reinterpret_cast<const void *>(&k_mf_syncfree);
+        int64_t grid = 1;
+        int rc = syncfree_grid(fn, n, L, 2 * kWavesPerBlock, &grid);
+        if (rc != PDB_OK) return rc;
+        // cooperative: the whole grid resident (the waves wait on each other)
+        const int32_t *a_user = op.user, *a_item = op.item;
+        const float *a_rating = op.rating;
+        float a_lr = op.lr, a_reg = op.reg;
+        void *args[] = {&a_user, &a_item, &a_rating, &prev_nz, &uvw, &n_users, &n_items, &n,
+                        &a_lr, &a_reg, &ctrl, const_cast<int64_t *>(&timeout)};
+        PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kBlock), args, 0, s));
+    }
     if (n_users > 0)
         k_wv_out<<<grid_for(n_users * 32, kBlock, 8192), kBlock, 0, s>>>(uvw, op.U, n_users * 32);
     if (n_items > 0)
@@ -1246,10 +1554,16 @@ extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const floa
                        (int64_t)ws_bytes >= syncfree_ws_bytes((n_users + n_items) * 32) &&
                        n < INT32_MAX / 2;
     const bool wide = lv->L_host > 0 && n >= 8 * lv->L_host;
-    if (sf_ok &&
-        (o.epoch_mode == PDB_EPOCH_SYNCFREE || (o.epoch_mode == PDB_EPOCH_AUTO && wide)))
+    // one compute unit: its words are indexed with 32-bit integers, and it
+    // wins while levels are narrow (about 35 ns per rating on one unit
+    // against a device-scope hand-over of about 0.8 us per level)
+    const bool one_cu_fits = (n_users + n_items) * 32 < (int64_t)INT32_MAX - 64;
+    const bool narrow = lv->L_host > 0 && n < 16 * lv->L_host;
+    const bool one_cu = one_cu_fits && (o.mf_one_cu == 1 || (o.mf_one_cu == -1 && narrow));
+    if (sf_ok && (o.epoch_mode == PDB_EPOCH_SYNCFREE ||
+                  (o.epoch_mode == PDB_EPOCH_AUTO && (wide || one_cu))))
         return launch_mf_syncfree(op, lv->prev_nz, n, n_users, n_items, lv->L_host, ws, o.timeout,
-                                  s);
+                                  one_cu, s);
     return launch_levels(op, lv, n_users + n_items, false, static_cast<Ctrl *>(ws), o, s);
 }
 

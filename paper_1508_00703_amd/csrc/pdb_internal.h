@@ -89,6 +89,7 @@ struct Opts {
     int64_t batch_sf_blocks;
     int stale_mode;          // pdb_stale_mode
     bool dense_stream;
+    int mf_one_cu;           // -1 auto, 0 device-wide, 1 one compute unit
 };
 // PDB_ERR_INVALID_ARG for out-of-range fields; NULL gives the defaults.
 int resolve_opts(const pdb_options *o, Opts *out);

@@ -50,9 +50,12 @@ __device__ __forceinline__ float recip_normal(float b) {
 // exact.  A NaN z gives a NaN g (the logistic function of NaN is NaN); the
 // NaN enters through the subtrahend, chosen while the exponential is still
 // being evaluated.
+__device__ __forceinline__ float logistic_sub(float z, float tgt) { return (z == z) ? tgt : -z; }
+__device__ __forceinline__ float logistic_from_exp(float e, float sub) {
+    return recip_normal(1.0f + e) - sub;
+}
 __device__ __forceinline__ float logistic_grad(float z, float tgt) {
-    const float sub = (z == z) ? tgt : -z;
-    return recip_normal(1.0f + dev_exp87(-z)) - sub;
+    return logistic_from_exp(dev_exp87(-z), logistic_sub(z, tgt));
 }
 
 // v + v[partner] with the partner chosen by a DPP lane pattern
@@ -81,12 +84,15 @@ __device__ __forceinline__ float butterfly16(float v) {
 // swapped, which IEEE addition does not notice.  Rows without a source lane
 // add their own value; they are not read.  The result is read out of lane 63
 // as a wave-uniform value: two DPP adds and a readlane instead of two
-// cross-row swaps.
-__device__ __forceinline__ float wave_sum64(float v) {
+// cross-row swaps.  wave_sum64_lane63 leaves the sum in lane 63 (a caller
+// that computes on from there reads its result out of lane 63 later).
+__device__ __forceinline__ float wave_sum64_lane63(float v) {
     v = butterfly16(v);
     v = dpp_add<0x142>(v);  // row_bcast:15
-    v = dpp_add<0x143>(v);  // row_bcast:31
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+    return dpp_add<0x143>(v);  // row_bcast:31
+}
+__device__ __forceinline__ float wave_sum64(float v) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wave_sum64_lane63(v)), 63));
 }
 
 // The butterfly over each 32-lane half (o = 1..16); lanes of half h get half

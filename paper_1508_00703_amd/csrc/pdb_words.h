@@ -26,6 +26,17 @@ __device__ __forceinline__ void word_put(unsigned long long *base, int64_t i,
     __hip_atomic_store(&base[i], w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// workgroup-scope 64-bit accesses: the waves of one block share the compute
+// unit's vector L1 cache, which serves these without a trip to the L2
+__device__ __forceinline__ unsigned long long word_get_wg(const unsigned long long *base,
+                                                          int64_t i) {
+    return __hip_atomic_load(&base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void word_put_wg(unsigned long long *base, int64_t i,
+                                            unsigned long long w) {
+    __hip_atomic_store(&base[i], w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 // Sleeps about 2^min(round, 3) x 64 cycles (s_sleep takes a constant).
 __device__ __forceinline__ void word_backoff(int round) {
     switch (round < 3 ? round : 3) {

@@ -72,7 +72,8 @@ class PdbOptions(ctypes.Structure):
                 ("pipeline_width", ctypes.c_int32), ("thin_max", ctypes.c_int32),
                 ("hot_features", ctypes.c_int64), ("spin_timeout_us", ctypes.c_int64),
                 ("batch_thin_max", ctypes.c_int32), ("batch_syncfree_blocks", ctypes.c_int32),
-                ("stale_mode", ctypes.c_int32), ("dense_stream", ctypes.c_int32)]
+                ("stale_mode", ctypes.c_int32), ("dense_stream", ctypes.c_int32),
+                ("mf_one_cu", ctypes.c_int32)]
 
 
 class PdbError(RuntimeError):

@@ -53,7 +53,7 @@ def test_options_defaults_and_layout(lib, tmp_path):
     o = native.options()
     assert (o.epoch_mode, o.pipeline, o.pipeline_width, o.thin_max, o.hot_features,
             o.spin_timeout_us, o.batch_thin_max, o.batch_syncfree_blocks, o.stale_mode,
-            o.dense_stream) == (0, 1, 4, 16, -1, 20000000, 2, 32, 0, 0)
+            o.dense_stream, o.mf_one_cu) == (0, 1, 4, 16, -1, 20000000, 2, 32, 0, 0, -1)
     fields = [f for f, _ in native.PdbOptions._fields_]
     src = tmp_path / "layout.c"
     src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "pdb.h"\nint main(void) {\n'
@@ -75,7 +75,8 @@ def test_options_defaults_and_layout(lib, tmp_path):
                                          ("hot_features", -2), ("spin_timeout_us", -1),
                                          ("spin_timeout_us", 10 ** 12), ("batch_thin_max", 0),
                                          ("batch_syncfree_blocks", 0), ("stale_mode", 3),
-                                         ("dense_stream", 2)])
+                                         ("dense_stream", 2), ("mf_one_cu", 2),
+                                         ("mf_one_cu", -2)])
 def test_options_out_of_range_are_rejected(lib, field, value):
     """Checked on the host before any device work: with no examples a valid
     option set returns PDB_OK without touching the device, an invalid one

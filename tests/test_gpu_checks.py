@@ -167,6 +167,40 @@ def test_zero_watchdog_sync_free_epoch(gpu):
     assert np.array_equal(w.cpu().numpy().view(np.int32), ref.view(np.int32))
 
 
+@pytest.mark.parametrize("one_cu", [0, 1])
+def test_zero_watchdog_sync_free_mf(gpu, one_cu):
+    """Sync-free matrix completion with a zero watchdog (both placements):
+    a wait that is not met soon gives up, every wave of the epoch exits, the
+    workspace reports PDB_ERR_DEVICE; the next epoch on it is the sequential
+    one."""
+    import torch
+
+    native = native_mod()
+    g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
+    lv, _ = gpu_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    t = lambda a: torch.from_numpy(a).to(gpu)
+    user, item, rating = t(g["user"]), t(g["item"]), t(g["rating"])
+    ws = native.workspace(native.pdb_epoch_workspace_bytes((g["n_users"] + g["n_items"]) * 32),
+                          gpu)
+
+    def run(opt):
+        U, V = t(g["U0"].copy()), t(g["V0"].copy())
+        native.pdb_mf_epoch(user, item, rating, g["n"], U, g["n_users"], V, g["n_items"], 32,
+                            float(g["lr"]), float(g["reg"]), lv, ws=ws, opt=opt)
+        torch.cuda.synchronize()
+        return U.cpu().numpy(), V.cpu().numpy()
+
+    run(dict(epoch_mode=native.PDB_EPOCH_SYNCFREE, mf_one_cu=one_cu, spin_timeout_us=0))
+    assert native.pdb_workspace_status(ws) == native.PDB_ERR_DEVICE
+    assert native.pdb_workspace_status(ws) == native.PDB_OK      # cleared by the read
+    U, V = run(dict(epoch_mode=native.PDB_EPOCH_SYNCFREE, mf_one_cu=one_cu))
+    assert native.pdb_workspace_status(ws) == native.PDB_OK
+    Um, Vm = oracle.mf_epoch(g["user"], g["item"], g["rating"], g["U0"], g["V0"], g["lr"],
+                             g["reg"], oracle.MATCHED)
+    assert np.array_equal(U.view(np.int32), Um.view(np.int32))
+    assert np.array_equal(V.view(np.int32), Vm.view(np.int32))
+
+
 def test_zero_watchdog_level_barriers(gpu):
     """Level by level with wide levels (a grid barrier per level) and a zero
     watchdog: the barrier waits give up, every block exits, PDB_ERR_DEVICE."""

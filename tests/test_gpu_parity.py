@@ -118,12 +118,29 @@ def test_epoch_with_oracle_schedule(gpu, cfg):
     check_sgd(native, gpu, g, lv)
 
 
-@pytest.mark.parametrize("mode", [0] + EPOCH_MODES)
-def test_mf_scaled(gpu, mode):
+# (epoch_mode, mf_one_cu): auto, level by level, sync-free over the device
+# and sync-free on one compute unit
+MF_RUNS = [(0, -1), (1, -1), (2, 0), (2, 1)]
+
+
+@pytest.mark.parametrize("mode,one_cu", MF_RUNS)
+def test_mf_scaled(gpu, mode, one_cu):
     native = native_mod()
     g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
     lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
-    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode))
+    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode, mf_one_cu=one_cu))
+
+
+@pytest.mark.parametrize("n,nu,ni", [(1, 1, 1), (2, 1, 1), (7, 3, 2), (4097, 5, 3000),
+                                     (30_001, 2_000, 700)])
+def test_mf_one_cu_shapes(gpu, n, nu, ni):
+    """The one-compute-unit execution on odd counts, fewer rows than the LDS
+    holds (every row hot), more items than it holds (hot and cold rows in one
+    rating), and a ring that wraps many times."""
+    native = native_mod()
+    g = datagen.generate_mf(5, n=n, n_users=nu, n_items=ni)
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=2, mf_one_cu=1))
 
 
 def test_transpose_and_prev_writer(gpu):
@@ -521,8 +538,8 @@ def test_spine_random_exceptions(gpu, seed):
     assert lv.L_host > np.bincount(col).max()
 
 
-@pytest.mark.parametrize("mode", EPOCH_MODES)
-def test_mf_structured_pairs(gpu, mode):
+@pytest.mark.parametrize("mode,one_cu", MF_RUNS[1:])
+def test_mf_structured_pairs(gpu, mode, one_cu):
     """Ratings whose neighbours share a user or an item (a wave takes two
     ratings at once only when the second does not depend on the first),
     repeated users and items, and a hot item."""
@@ -543,4 +560,4 @@ def test_mf_structured_pairs(gpu, mode):
              V0=(0.2 * rng.normal(size=(ni, 32))).astype(np.float32),
              n=n, n_users=nu, n_items=ni, rank=32, lr=np.float32(0.01), reg=np.float32(0.05))
     lv, _ = check_schedule(native, gpu, row_ptr, col, nu + ni, 0)
-    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode))
+    check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode, mf_one_cu=one_cu))
