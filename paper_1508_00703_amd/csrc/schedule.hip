@@ -601,13 +601,16 @@ __global__ __launch_bounds__(kBlock) void k_levels_rowwave(const int64_t *__rest
                 r1 |= v1 != 0;
                 if (__ballot(!(r0 && r1)) == 0ull) break;
                 if (round == 0) t0 = now_ticks();
-                if (aborted(ctrl)) return;
-                if (now_ticks() - t0 > timeout) {
-                    record_error(ctrl, DERR_WAIT_TIMEOUT);
-                    return;
+                // the abort flag (a device-scope load) and the watchdog
+                // every 8 rounds, a short back-off every round
+                if ((round & 7) == 7) {
+                    if (aborted(ctrl)) return;
+                    if (now_ticks() - t0 > timeout) {
+                        record_error(ctrl, DERR_WAIT_TIMEOUT);
+                        return;
+                    }
                 }
-                if (round < 3) __builtin_amdgcn_s_sleep(1);
-                else __builtin_amdgcn_s_sleep(4);
+                __builtin_amdgcn_s_sleep(1);
             }
             mx = max(mx, max(v0, v1));
         }
