@@ -117,13 +117,14 @@ SchedWs sched_ws_layout(void *base, int64_t n, int64_t d, int64_t nnz);
 size_t scan_tmp_elems(int64_t count);
 hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t count, uint32_t *tmp,
                               hipStream_t s);
-// Stable LSD sort of (key, value) pairs on the low `bits` bits of the key.
+// Stable LSD sort of (key, value) pairs on bits [lo_bit, bits) of the key.
 // vals_in == NULL means value = position.  Result in (*keys_out, *vals_out),
-// which is one of the two buffer pairs.
+// which is one of the two buffer pairs (the inputs themselves when
+// lo_bit >= bits; vals_in must then not be NULL).
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, int64_t count,
                             int bits, uint32_t *kA, uint32_t *vA, uint32_t *kB, uint32_t *vB,
                             uint32_t *hist, uint32_t *scan_tmp, uint32_t **keys_out,
-                            uint32_t **vals_out, hipStream_t s);
+                            uint32_t **vals_out, hipStream_t s, int lo_bit = 0);
 
 // ----------------------------------------------------------------------------
 // device helpers

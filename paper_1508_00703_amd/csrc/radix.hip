@@ -222,15 +222,20 @@ hipError_t exclusive_scan_u32(const uint32_t *in, uint32_t *out, int64_t count, 
 hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, int64_t count,
                             int bits, uint32_t *kA, uint32_t *vA, uint32_t *kB, uint32_t *vB,
                             uint32_t *hist, uint32_t *scan_tmp, uint32_t **keys_out,
-                            uint32_t **vals_out, hipStream_t s) {
+                            uint32_t **vals_out, hipStream_t s, int lo_bit) {
     if (bits < 1) bits = 1;
     *keys_out = kA;
     *vals_out = vA;
     if (count <= 0) return hipSuccess;
+    if (lo_bit >= bits) {  // nothing to sort: the input is the result
+        *keys_out = const_cast<uint32_t *>(keys_in);
+        *vals_out = const_cast<uint32_t *>(vals_in);
+        return hipSuccess;
+    }
     const int64_t ntiles = cdiv(count, kTile);
     const uint32_t *ck = keys_in, *cv = vals_in;
     uint32_t *dk = kA, *dv = vA;
-    for (int shift = 0; shift < bits; shift += 8) {
+    for (int shift = lo_bit; shift < bits; shift += 8) {
         const int nb = bits - shift < 8 ? bits - shift : 8;
         k_radix_hist<<<(unsigned)ntiles, kBlock, 0, s>>>(ck, count, shift, nb, hist, ntiles);
         hipError_t e = exclusive_scan_u32(hist, hist, (int64_t)(1 << nb) * ntiles, scan_tmp, s);

@@ -113,16 +113,32 @@ __global__ __launch_bounds__(kBlock) void k_row_index(const int64_t *__restrict_
 
 // K2: previous writer of every entry from the feature-sorted order: pn[p] =
 // the entry just before p in p's feature list (its CSR index), -1 at a head.
-__global__ __launch_bounds__(kBlock) void k_prev_writer(
+// K2 in two streaming passes instead of a scatter.  Scattered 4-byte stores
+// of prev_nz in entry order land one per 32-byte sector and wrote 8x the
+// array (config 3: 16 GB for 2 GB, 21 ms).  Here:
+//   1. k_prev_pairs: in feature order, each entry's previous entry on its
+//      feature (the entry before it in the sorted order, when it has the same
+//      feature) as an (entry, previous) pair, written in order; col_ptr and
+//      csc_row as before;
+//   2. the pairs sorted by entry index above its low kPlaceBits bits (the
+//      stable radix sort's passes on the high digits only);
+//   3. k_prev_place: entry indices are a permutation of 0 .. nnz-1, so block
+//      b finds exactly the entries [b 2^kPlaceBits, (b+1) 2^kPlaceBits) at
+//      those positions of the sorted pairs; it places their previous entries
+//      in LDS and writes the range out in order.
+constexpr int kPlaceBits = 13;  // 8192 entries, 32 KB of LDS per block
+
+__global__ __launch_bounds__(kBlock) void k_prev_pairs(
     const uint32_t *__restrict__ skeys, const uint32_t *__restrict__ svals, int64_t nnz,
-    int64_t d, const int32_t *__restrict__ row_idx, int32_t *__restrict__ pn,
-    int64_t *__restrict__ col_ptr, int32_t *__restrict__ csc_row) {
+    int64_t d, const int32_t *__restrict__ row_idx, uint32_t *__restrict__ pk,
+    uint32_t *__restrict__ pv, int64_t *__restrict__ col_ptr, int32_t *__restrict__ csc_row) {
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nnz;
          q += (int64_t)gridDim.x * blockDim.x) {
         const uint32_t f = skeys[q];
         const uint32_t p = svals[q];
         const bool head = (q == 0) || skeys[q - 1] != f;
-        pn[p] = head ? -1 : (int32_t)svals[q - 1];
+        pk[q] = p;
+        pv[q] = head ? 0xFFFFFFFFu : svals[q - 1];
         if (head) {
             const int64_t lo = (q == 0) ? 0 : (int64_t)skeys[q - 1] + 1;
             const int64_t hi = min((int64_t)f, d - 1);  // columns >= d: malformed input
@@ -132,6 +148,21 @@ __global__ __launch_bounds__(kBlock) void k_prev_writer(
             for (int64_t g = (int64_t)f + 1; g <= d; ++g) col_ptr[g] = nnz;
         if (csc_row) csc_row[q] = row_idx[p];
     }
+}
+
+// pv may be pn itself: a block reads all of its range before writing it.
+__global__ __launch_bounds__(kBlock) void k_prev_place(const uint32_t *__restrict__ pk,
+                                                       const uint32_t *pv, int64_t nnz,
+                                                       int32_t *pn) {
+    __shared__ int32_t s_prev[1 << kPlaceBits];
+    const int64_t base = (int64_t)blockIdx.x << kPlaceBits;
+    const int cnt = (int)min((int64_t)1 << kPlaceBits, nnz - base);
+    for (int i = threadIdx.x; i < cnt; i += kBlock) {
+        const uint32_t off = pk[base + i] - (uint32_t)base;
+        if (off < (uint32_t)cnt) s_prev[off] = (int32_t)pv[base + i];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < cnt; i += kBlock) pn[base + i] = s_prev[i];
 }
 
 // Previous-writer row of every entry: prev_row[p] = row of pn[p], -1 if none.
@@ -1459,8 +1490,20 @@ int build_conflicts(const pdb_csr *csr, int64_t n, int64_t d, SchedWs &w, int32_
     PDB_HIP(radix_sort_pairs(reinterpret_cast<const uint32_t *>(csr->col), nullptr, nnz, bits,
                              w.kA, w.vA, w.kB, w.vB, w.hist, w.scan_tmp, &sk, &sv, s));
     if (nnz > 0) {
-        k_prev_writer<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(
-            sk, sv, nnz, d, w.row_idx, pn, col_ptr, csc_row);
+        // the radix pair not holding the sorted entries takes the pairs; the
+        // sort's other buffers are the candidates array and pn itself
+        uint32_t *fk = (sk == w.kA) ? w.kB : w.kA;
+        uint32_t *fv = (sv == w.vA) ? w.vB : w.vA;
+        k_prev_pairs<<<grid_for(nnz, kBlock, 1 << 16), kBlock, 0, s>>>(
+            sk, sv, nnz, d, w.row_idx, fk, fv, col_ptr, csc_row);
+        PDB_LAUNCHED();
+        uint32_t *ok = nullptr, *ov = nullptr;
+        PDB_HIP(radix_sort_pairs(fk, fv, nnz, bit_length((uint64_t)(nnz > 1 ? nnz - 1 : 1)),
+                                 reinterpret_cast<uint32_t *>(w.cand),
+                                 reinterpret_cast<uint32_t *>(pn), fk, fv, w.hist, w.scan_tmp,
+                                 &ok, &ov, s, kPlaceBits));
+        k_prev_place<<<(unsigned)cdiv(nnz, (int64_t)1 << kPlaceBits), kBlock, 0, s>>>(ok, ov, nnz,
+                                                                                      pn);
         PDB_LAUNCHED();
     } else {
         k_fill_i64<<<grid_for(d + 1, kBlock, 4096), kBlock, 0, s>>>(col_ptr, d + 1, 0);
