@@ -40,8 +40,9 @@
  *   correctly rounded division (the cap keeps 1 + exp below 2^126; it only
  *   changes results for z < -87, where the logistic value is below 1.7e-38),
  *   exp by Cody-Waite reduction (k = rint(x log2 e), ln 2 split into two
- *   floats) and the degree-7 Taylor polynomial of e^r evaluated by Estrin's
- *   scheme, scaled by 2^k;   least squares: g = z - y;
+ *   floats) and the degree-7 Taylor polynomial of e^r, pairs c_j + c_{j+1} r
+ *   combined by Horner's rule in r^2 (p01 + r^2 (p23 + r^2 (p45 + r^2 p67))),
+ *   scaled by 2^k;   least squares: g = z - y;
  *   s = lr * g;  w[c_k] = fma(-s, x_k, w[c_k]) (values read before any write).
  * Matrix completion (rank 32): q_j = fma(U_u[j], V_i[j], 0), butterfly over
  *   o = 1..16, e = r - q_0;  U_u[j] = fma(lr, e*V_i[j] - reg*U_u[j], U_u[j]),

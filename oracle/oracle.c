@@ -27,7 +27,8 @@
  *            p[l] + p[l xor off]; z is the common final value.
  * The logistic function is 1/(1 + expf(-z)) in natural mode and, in matched
  * mode, orc_sigmoid below: the same with orc_exp (Cody-Waite range reduction
- * and the degree-7 Taylor polynomial of e^r evaluated by Estrin's scheme)
+ * and the degree-7 Taylor polynomial of e^r, its coefficient pairs combined
+ * by Horner's rule in r^2)
  * and the exponent argument capped at 87.
  */
 #include <math.h>
@@ -40,9 +41,9 @@ enum { ORC_LOGISTIC = 0, ORC_SQUARED = 1 };
 
 /* ------------------------------------------------------------------------ */
 /* exp(x) = 2^k * e^r with k = rint(x log2 e), r = x - k ln 2 (ln 2 split in
- * two floats so r carries the low bits), e^r by its Taylor series to r^7,
- * evaluated by Estrin's scheme: pairs c_j + c_{j+1} r, combined with r^2,
- * then r^4. */
+ * two floats so r carries the low bits), e^r by its Taylor series to r^7:
+ * pairs c_j + c_{j+1} r, combined by Horner's rule in r^2
+ * (p01 + r^2 (p23 + r^2 (p45 + r^2 p67))). */
 float orc_exp(float x) {
     if (x != x) return x;
     if (x > 89.0f) return INFINITY;
@@ -58,11 +59,9 @@ float orc_exp(float x) {
     const float c4 = 0x1.555556p-5f, c5 = 0x1.111112p-7f, c6 = 0x1.6c16c2p-10f,
                 c7 = 0x1.a01a02p-13f;
     float r2 = r * r;
-    float r4 = r2 * r2;
     float p01 = fmaf(c1, r, c0), p23 = fmaf(c3, r, c2);
     float p45 = fmaf(c5, r, c4), p67 = fmaf(c7, r, c6);
-    float p03 = fmaf(p23, r2, p01), p47 = fmaf(p67, r2, p45);
-    float q = fmaf(p47, r4, p03);
+    float q = fmaf(fmaf(fmaf(p67, r2, p45), r2, p23), r2, p01);
     int ki = (int)k;
     float two_k;
     if (ki > 127) {

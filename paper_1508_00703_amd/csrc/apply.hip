@@ -491,9 +491,9 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     float s, cur_v;
     bool cur_fwd;
     if (LOSS == PDB_LOGISTIC) {
-        const float sub = logistic_sub(z, tgt);
         const float e = dev_exp87(-z);
         __builtin_amdgcn_sched_barrier(0);
+        const float sub = logistic_sub(z, tgt);  // NaN select off the head of the chain
         cur_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
         cur_fwd = rd < 256u;
         s = op.lr * logistic_from_exp(e, sub);
