@@ -1350,17 +1350,32 @@ __global__ void k_level_ptr(const uint32_t *__restrict__ skeys, const uint32_t *
 // its previous writer.  An entry's previous writer lies in an earlier row, so
 // it is row i-1 exactly when the previous entry's index is at least
 // row_ptr[i-1].  One wave per row.
+// The caller only needs to know whether there are no breaks, or at most n/4:
+// every 64 rows a wave adds its count to the total and stops once the total
+// is past n/4 (an input like config 4, where almost every example breaks,
+// then reads a quarter of the previous writers instead of all of them).
 __global__ __launch_bounds__(kBlock) void k_chain_check(const int64_t *__restrict__ row_ptr,
                                                         int64_t n, const int32_t *__restrict__ pn,
                                                         Ctrl *ctrl) {
     const int lane = lane_id();
     const int64_t nw = (int64_t)gridDim.x * (kBlock / kWave);
-    int breaks = 0;
+    const int64_t enough = n / 4 + 1;
+    int breaks = 0, rows = 0;
     for (int64_t i = 1 + blockIdx.x * (int64_t)(kBlock / kWave) + wave_in_block(); i < n; i += nw) {
         const int64_t lo = row_ptr[i - 1], b = row_ptr[i], e = row_ptr[i + 1];
         bool found = false;
         for (int64_t p = b + lane; p < e && !found; p += kWave) found = pn[p] >= lo;
         if (__ballot(found) == 0ull) ++breaks;
+        if (++rows == 64) {
+            int total = 0;
+            if (lane == 0) total = breaks ? atomicAdd(&ctrl->chain_breaks, breaks) + breaks
+                                          : __hip_atomic_load(&ctrl->chain_breaks, __ATOMIC_RELAXED,
+                                                              __HIP_MEMORY_SCOPE_AGENT);
+            total = __builtin_amdgcn_readfirstlane(total);
+            breaks = 0;
+            rows = 0;
+            if (total >= enough) return;
+        }
     }
     if (lane == 0 && breaks) atomicAdd(&ctrl->chain_breaks, breaks);
 }
