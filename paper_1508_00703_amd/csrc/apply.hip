@@ -57,6 +57,8 @@ struct SgdOp {
     float lr;
     static constexpr int kUnits = 1;  // examples per wave per step
     static constexpr bool kChain = true;
+    // the pipeline's select-free step is checked for logistic loss only
+    static constexpr bool kFastCheck = LOSS == PDB_LOGISTIC;
 
     __device__ __forceinline__ void operator()(int64_t e, int64_t end) const {
         (void)end;
@@ -103,6 +105,7 @@ struct MfOp {
     float lr, reg;
     static constexpr int kUnits = 2;  // two ratings per wave, one per 32-lane half
     static constexpr bool kChain = false;
+    static constexpr bool kFastCheck = false;
 
     __device__ __forceinline__ void operator()(int64_t e, int64_t end) const {
         const int lane = lane_id();
@@ -438,7 +441,7 @@ struct ChainState {
 // early in the step) are free to fill its stalls.  Order that matters: the
 // writes of t-1 precede the reads for t+1 (a value t-1 writes may be one
 // t+1 reads) and the prefetch (a cold value t-1 writes may be prefetched).
-template <int SL, int LOSS, bool VAL>
+template <int SL, int LOSS, bool VAL, bool FAST>
 __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL> &op,
                                            SlotBlock sblk, __amdgpu_buffer_rsrc_t wbuf,
                                            unsigned gsrc_a) {
@@ -447,7 +450,12 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     const float tgt = VAL ? st.cur.t : __uint_as_float(st.cur.a.x);
     // (a) example t-1's step lands: its new weights, and this example's
     // weights (forwarded lanes apply that step to the pair they took)
-    const float w_old = st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw) : st.cur_v;
+    // FAST: every lane takes the fma, lanes whose weight came from memory with
+    // x = 0 (the rotation put the memory value in cur_fw), which k_pipe_decide
+    // has shown to give the same bits for this epoch
+    const float w_old = FAST ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw)
+                             : (st.cur_fwd ? __builtin_fmaf(-st.s_prev, st.cur_fx, st.cur_fw)
+                                           : st.cur_v);
     // binary logistic: the product w * 1 + 0 differs from w only for w = -0,
     // which changes z at most in the sign of a zero sum, and the logistic
     // function is the same at +0 and -0; lanes without an entry hold 0
@@ -493,7 +501,8 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     if (LOSS == PDB_LOGISTIC) {
         const float e = dev_exp87(-z);
         __builtin_amdgcn_sched_barrier(0);
-        const float sub = logistic_sub(z, tgt);  // NaN select off the head of the chain
+        // NaN select off the head of the chain; FAST: z is never NaN
+        const float sub = FAST ? tgt : logistic_sub(z, tgt);
         cur_v = (rd == gsrc_a) ? st.gv[(SL + 1) % kD] : v1;
         cur_fwd = rd < 256u;
         s = op.lr * logistic_from_exp(e, sub);
@@ -514,8 +523,8 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     st.cur_v = cur_v;
     st.gv[SL] = g_pf;
     st.cur = st.nxt;
-    st.cur_fw = fw1;
-    st.cur_fx = fx1;
+    st.cur_fw = FAST ? (cur_fwd ? fw1 : cur_v) : fw1;
+    st.cur_fx = FAST ? (cur_fwd ? fx1 : 0.0f) : fx1;
     st.cur_fwd = cur_fwd;
     st.nxt = st.nxt2;
     st.nxt2 = nxt3;
@@ -547,7 +556,7 @@ static_assert(kD == 16, "PDB_CHAIN_STEPS lists kD steps");
 // Consumer: runs examples t = 0.. of the run in order.  Returns the number
 // processed: len, or the position of the first example with more than 64
 // entries (the caller runs that one on the plain path).
-template <int LOSS, bool VAL>
+template <int LOSS, bool VAL, bool FAST>
 __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64_t d,
                                   ChainShared &S, Ctrl *ctrl) {
     const int lane = lane_id();
@@ -567,7 +576,9 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
     st.nxt = read_slot(S, 1);
     st.nxt2 = read_slot(S, 2);
     st.cur_v = (st.cur.a.z == gsrc_a) ? st.gv[0] : lds_read(st.cur.a.z);
-    st.cur_fw = st.cur_fx = 0.0f;
+    // the run's first example forwards nothing (FAST: fma(-0, 0, w) = w)
+    st.cur_fw = FAST ? st.cur_v : 0.0f;
+    st.cur_fx = 0.0f;
     st.cur_fwd = false;
     st.s_prev = 0.0f;
     // no example before the first: its "writes" go to the sinks
@@ -583,7 +594,7 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
         chain_prefetch_offsets(st, S, t0 + kD);
         lds_store(&S.ctl[0], (int)(t0 + 2));
         const SlotBlock sblk = slot_block(S, (int)(t0 & (kRB - 1)));
-#define PDB_STEP(SL) chain_step<SL>(st, op, sblk, wbuf, gsrc_a);
+#define PDB_STEP(SL) chain_step<SL, LOSS, VAL, FAST>(st, op, sblk, wbuf, gsrc_a);
         PDB_CHAIN_STEPS(PDB_STEP)
 #undef PDB_STEP
     }
@@ -591,7 +602,7 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
         chain_prefetch_offsets(st, S, t0 + kD);
         const SlotBlock sblk = slot_block(S, (int)(t0 & (kRB - 1)));
 #define PDB_STEP(SL) \
-    if (SL < kD - 1 && t0 + SL < stop) chain_step<SL>(st, op, sblk, wbuf, gsrc_a);
+    if (SL < kD - 1 && t0 + SL < stop) chain_step<SL, LOSS, VAL, FAST>(st, op, sblk, wbuf, gsrc_a);
         PDB_CHAIN_STEPS(PDB_STEP)
 #undef PDB_STEP
     }
@@ -612,7 +623,7 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
 // level of the run has one example, so the examples have increasing indices.
 template <int LOSS, bool VAL>
 __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_end, int hot,
-                          int64_t d, Ctrl *ctrl, bool width1) {
+                          int64_t d, Ctrl *ctrl, bool width1, bool fast) {
     __shared__ ChainShared S;
     __shared__ int64_t s_done;
     const int wave = wave_in_block();
@@ -630,7 +641,14 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
         }
         __syncthreads();
         if (wave == 0) {
-            const int64_t done = chain_consumer(op, e_end - pos, d, S, ctrl);
+            int64_t done;
+            if constexpr (LOSS == PDB_LOGISTIC) {
+                done = fast ? chain_consumer<LOSS, VAL, true>(op, e_end - pos, d, S, ctrl)
+                            : chain_consumer<LOSS, VAL, false>(op, e_end - pos, d, S, ctrl);
+            } else {
+                (void)fast;
+                done = chain_consumer<LOSS, VAL, false>(op, e_end - pos, d, S, ctrl);
+            }
             if (lane_id() == 0) s_done = done;
         } else if (dense_r0 >= 0) {
             chain_producer<LOSS, VAL, true>(op, wave - 1, pos, e_end - pos, dense_r0, hot, S);
@@ -712,6 +730,8 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
                                                          int64_t chain_width) {
     constexpr int U = Op::kUnits;
     const int64_t L = *n_levels;
+    // the pipeline's select-free step, when k_pipe_decide found it exact
+    const bool fast = __builtin_amdgcn_readfirstlane(ctrl->pipe_fast) != 0;
     const int wave = wave_in_block();
     const bool single = gridDim.x == 1;
     const int64_t gw = (int64_t)blockIdx.x * kWavesPerBlock + wave;
@@ -737,7 +757,7 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
                             // to the next such run or wider level
                             const int64_t l3 = find_run_end(l2, L, level_ptr, 1);
                             if (l3 - l2 >= kChainMin) {
-                                chain_run(op, beg, level_ptr[l3], hot, d, ctrl, true);
+                                chain_run(op, beg, level_ptr[l3], hot, d, ctrl, true, fast);
                                 l2 = l3;
                                 continue;
                             }
@@ -745,7 +765,7 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
                             if (chain_width > 1) {
                                 l4 = narrow_run_end(l2, L, level_ptr, chain_width);
                                 if (level_ptr[l4] - beg >= kChainMin) {
-                                    chain_run(op, beg, level_ptr[l4], hot, d, ctrl, false);
+                                    chain_run(op, beg, level_ptr[l4], hot, d, ctrl, false, fast);
                                     l2 = l4;
                                     continue;
                                 }
@@ -798,6 +818,59 @@ __global__ __launch_bounds__(kBlock) void k_check_recip(uint32_t lo, uint32_t hi
     }
 }
 
+// The width-1 pipeline's select-free step (FAST) computes every lane's weight
+// as fma(-s, x', w') -- for a lane whose weight came from memory x' = 0 and
+// w' is that weight -- instead of selecting between the forwarded value and
+// the memory value, and drops the logistic step's NaN select.  Both give
+// bitwise the same result when
+//   (a) no weight the epoch reads is -0 (w + (-s * 0) is +0 for w = -0 and
+//       s < 0): w0 holds no -0, and the epoch never writes one, since
+//       fma(a, b, c) is -0 only when c is;
+//   (b) no step s is infinite or NaN (-s * 0 would be NaN) and no z is NaN:
+//       with finite inputs and the logistic loss, |g| <= 1 and |s| <= |lr|, so
+//       every weight stays within W = max|w0| + n |lr| max|x| and every dot
+//       product within nnz W max|x|; k_pipe_decide asks that to be below
+//       2^100.
+// k_pipe_check reduces max|w0|, max|x| and the flags into the control block.
+__global__ __launch_bounds__(kBlock) void k_pipe_check(const float *__restrict__ w, int64_t d,
+                                                       const float *__restrict__ val, int64_t nnz,
+                                                       Ctrl *ctrl) {
+    unsigned wm = 0, xm = 0;
+    bool bad = false;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < d; i += stride) {
+        const unsigned b = __float_as_uint(w[i]);
+        bad |= (b & 0x7F800000u) == 0x7F800000u || b == 0x80000000u;  // inf, NaN, -0
+        wm = max(wm, b & 0x7FFFFFFFu);
+    }
+    if (val)
+        for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nnz; i += stride) {
+            const unsigned b = __float_as_uint(val[i]);
+            bad |= (b & 0x7F800000u) == 0x7F800000u;
+            xm = max(xm, b & 0x7FFFFFFFu);
+        }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        wm = max(wm, (unsigned)__shfl_xor((int)wm, o));
+        xm = max(xm, (unsigned)__shfl_xor((int)xm, o));
+    }
+    const bool any_bad = __ballot(bad) != 0ull;
+    if (lane_id() == 0) {
+        atomicMax(&ctrl->pipe_wmax, wm);
+        atomicMax(&ctrl->pipe_xmax, xm);
+        if (any_bad) atomicOr(&ctrl->pipe_bad, 1);
+    }
+}
+
+__global__ void k_pipe_decide(Ctrl *ctrl, float lr, int64_t n, int64_t nnz, int has_val) {
+    const double wmax = (double)__uint_as_float(ctrl->pipe_wmax);
+    const double xmax = has_val ? (double)__uint_as_float(ctrl->pipe_xmax) : 1.0;
+    const double alr = fabs((double)lr);
+    const double W = wmax + (double)n * alr * xmax;
+    const bool ok = !ctrl->pipe_bad && isfinite(lr) && (double)nnz * W * xmax < 0x1p100;
+    ctrl->pipe_fast = ok ? 1 : 0;
+}
+
 __global__ void k_ctrl_zero(Ctrl *c) {
     int *w = reinterpret_cast<int *>(c);
     for (int i = threadIdx.x; i < (int)(sizeof(Ctrl) / sizeof(int)); i += blockDim.x) w[i] = 0;
@@ -805,7 +878,7 @@ __global__ void k_ctrl_zero(Ctrl *c) {
 
 template <class Op>
 int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, Ctrl *ctrl,
-                  const Opts &opt, hipStream_t s) {
+                  const Opts &opt, hipStream_t s, int64_t n = 0, int64_t nnz = 0) {
     // the caller's options: widest level run by block 0 alone, a cap on the
     // number of weights cached in LDS by the width-1 pipeline, and the
     // widest level a pipeline run may include (a level of w examples costs
@@ -833,6 +906,12 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
         hot = (int)h;
         lds = (size_t)std::max<int64_t>(h, 1) * 4;
         PDB_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        if constexpr (Op::kFastCheck) {
+            k_pipe_check<<<grid_for(std::max(d, nnz), kBlock, 1024), kBlock, 0, s>>>(op.w, d, op.val,
+                                                                                  nnz, ctrl);
+            k_pipe_decide<<<1, 1, 0, s>>>(ctrl, op.lr, n, nnz, op.val != nullptr);
+            PDB_LAUNCHED();
+        }
     }
     int grid = 1;
     const int64_t widest = lv->max_width_host;
@@ -1467,7 +1546,7 @@ int sgd_epoch_impl(const pdb_csr *csr, const float *labels, int64_t n, int64_t d
     if (loss == LS && has_val == HV) {                                                       \
         SgdOp<LS, HV> op{csr->row_ptr, csr->col, csr->val, labels, w, lv->perm, lv->prev_nz, lr}; \
         if (syncfree) return launch_syncfree(op, n, d, lv->L_host, ws, o.timeout, s);         \
-        return launch_levels(op, lv, d, chain_ok, ctrl, o, s);                               \
+        return launch_levels(op, lv, d, chain_ok, ctrl, o, s, n, csr->nnz);                  \
     }
     PDB_SGD_CASE(PDB_LOGISTIC, true)
     PDB_SGD_CASE(PDB_LOGISTIC, false)

@@ -69,7 +69,12 @@ struct Ctrl {
     int spine_status;  // 0 solved, 1 too many exceptional rows or entries
     int spine_rounds;
     int chain_breaks;  // rows that do not conflict with the row before them
-    int pad[38];
+    // width-1 pipeline: the exactness check of its select-free step
+    unsigned pipe_wmax;  // bits of max |w0|
+    unsigned pipe_xmax;  // bits of max |x|
+    int pipe_bad;        // some w0 is not finite or is -0, or some x is not finite
+    int pipe_fast;       // the select-free step is exact for this epoch
+    int pad[34];
     float sink[64];  // target of stores from lanes with nothing to store
 };
 static_assert(sizeof(Ctrl) == 512, "Ctrl is two 256-byte lines");

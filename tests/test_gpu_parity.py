@@ -561,3 +561,50 @@ def test_mf_structured_pairs(gpu, mode, one_cu):
              n=n, n_users=nu, n_items=ni, rank=32, lr=np.float32(0.01), reg=np.float32(0.05))
     lv, _ = check_schedule(native, gpu, row_ptr, col, nu + ni, 0)
     check_mf(native, gpu, g, lv, opt=dict(epoch_mode=mode, mf_one_cu=one_cu))
+
+
+@pytest.mark.parametrize("case,fast", [("plain", 1), ("valued", 1), ("negzero", 0),
+                                       ("nan_w0", 0), ("inf_x", 0), ("huge_lr", 0),
+                                       ("squares", 0)])
+def test_pipeline_select_free_guard(gpu, case, fast):
+    """The width-1 pipeline's select-free step runs only when the epoch's
+    check shows it exact (logistic loss; w0 finite with no -0; x finite;
+    n |lr| max|x| bounded): the control block records the decision, and
+    where the run is finite the weights are bitwise the matched oracle's.
+    A -0 in w0 on a feature read from memory would turn into +0 on the
+    select-free step, so that case must take the selecting step."""
+    import torch
+
+    native = native_mod()
+    rng = np.random.default_rng(31)
+    n, d = 3000, 400
+    # a chain through feature 0, plus three features per row from the rest
+    rows = [{0} | set((1 + rng.choice(d - 1, 3, replace=False)).tolist()) for _ in range(n)]
+    row_ptr, col = csr_from_rows(rows)
+    val = None
+    if case in ("valued", "inf_x"):
+        val = (0.5 * rng.normal(size=len(col))).astype(np.float32)
+        if case == "inf_x":
+            val[len(col) // 2] = np.inf
+    w0 = (0.1 * rng.normal(size=d)).astype(np.float32)
+    if case == "negzero":
+        w0[1::7] = -0.0
+    if case == "nan_w0":
+        w0[5] = np.nan
+    lr = np.float32(1e30 if case == "huge_lr" else 0.05)
+    loss = 1 if case == "squares" else 0
+    y = np.sign(rng.normal(size=n)).astype(np.float32)
+    g = dict(row_ptr=row_ptr, col=col, n=n, d=d, loss=loss, lr=lr, val=val, y=y)
+    lv, _ = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert lv.L_host == n
+    csr = native.Csr.from_numpy(row_ptr, col, val, gpu)
+    w = torch.from_numpy(w0.copy()).to(gpu)
+    ws = native.pdb_sgd_epoch(csr, torch.from_numpy(y).to(gpu), n, d, w, float(lr), loss, lv,
+                              opt=dict(epoch_mode=native.PDB_EPOCH_LEVELS))
+    torch.cuda.synchronize()
+    # control block: pipe_bad at byte 112, pipe_fast at byte 116
+    ctrl = ws[:512].cpu().numpy().view(np.int32)
+    assert ctrl[29] == fast, (case, ctrl[26:30])
+    if case in ("plain", "valued", "negzero", "squares"):
+        ref = oracle.sgd_epoch(row_ptr, col, val, y, w0, lr, loss, oracle.MATCHED)
+        assert np.array_equal(w.cpu().numpy().view(np.int32), ref.view(np.int32))
