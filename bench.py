@@ -598,7 +598,7 @@ def main():
         ("-d%d" % delay if delay >= 0 else "")
     # the epoch kernel the library runs (the rule of pdb_sgd_epoch / pdb_mf_epoch)
     mode = args.epoch_mode
-    one_cu = mf and L > 0 and n < 16 * L and (g["n_users"] + g["n_items"]) * 32 < 2 ** 31 - 65
+    one_cu = mf and L > 0 and n < 16 * L and (g["n_users"] + g["n_items"]) * 256 <= 2 ** 32
     syncfree = mode == 2 or (mode == 0 and L > 0 and (n >= 8 * L or one_cu))
     if batch:
         kernel = "k_batch_syncfree (mini-batch epoch)" if mode != 1 else \

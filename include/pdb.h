@@ -147,8 +147,9 @@ typedef struct pdb_options {
                                       unit (hand-overs through its LDS and L1 cache), 0 spreads the
                                       ratings over the device (device-scope hand-overs), -1
                                       (default) one compute unit when levels are narrow (n < 16 L)
-                                      and (n_users + n_items) * 32 < 2^31; 1 falls back to the
-                                      device-wide execution when the words do not fit that bound */
+                                      and (n_users + n_items) * 256 <= 2^32 (the words are
+                                      addressed with 32-bit byte offsets); 1 falls back to the
+                                      device-wide execution when they do not fit that bound */
 } pdb_options;
 
 /* Fills *opt with the defaults above.  Host only. */

@@ -1134,37 +1134,81 @@ __global__ __launch_bounds__(kBlock) void k_mf_syncfree(
 // hand-overs between two waves of one block: 205 ns through global memory at
 // workgroup scope, 100 ns through LDS, against 420-680 ns at device scope.
 // That wins on inputs whose levels are narrow (the chain of hand-overs is
-// long) while one compute unit's throughput, about 35 ns per rating, keeps
-// up.
+// long) while one compute unit's throughput keeps up.
 //  * The producer wave streams each rating's user, item, value and previous
 //    ratings into an LDS ring in rating order, and touches its cold rows'
 //    words so they are in the L2 cache when a worker gets there.
-//  * Fifteen workers take tickets of two consecutive ratings in turn, one
-//    rating per 32-lane half (lane j: component j), both halves at once
-//    unless the second depends on the first.  A worker waits until its two
-//    rows' words carry the expected previous ratings, computes the step
-//    (the same arithmetic as MfOp) and publishes both rows tagged with its
-//    rating.
+//  * Fifteen workers take tickets of two consecutive ratings from an LDS
+//    counter as they become free, one rating per 32-lane half (lane j:
+//    component j).  Each half computes the step (the same arithmetic as
+//    MfOp) and publishes its rows tagged with its rating as soon as both
+//    rows' words carry the expected previous ratings, so a second rating
+//    that depends on the first simply sees the first's tag.  A worker held
+//    by a wait holds only its own ticket: the next ratings go to whichever
+//    worker is free (dealing tickets in turn tied every hot row's chain of
+//    ratings to the slowest of the workers it passed through).
 //  * Rows with the smallest ids (the Zipf-hot ones of the generator) live in
 //    LDS as (value, rating) words for the whole epoch and are written back at
-//    the end.
-//  * Progress: tickets go to the workers in index order and every ticket
-//    waits only on earlier ratings, so the earliest unfinished ticket is
-//    never blocked; the producer waits only for ring slots the slowest
-//    worker has released.
+//    the end.  Almost every wait is for one of them, so a poll rereads only
+//    the words still awaited, and LDS ones only unless a lane awaits a word
+//    in global memory.
+//  * Issue priority: the compute unit's vector issue is its busiest
+//    resource (mostly busy on a Zipf input), so a wave polling for a word
+//    runs above the ticket work and the step that follows a wait above both
+//    -- they are the chain of hand-overs that bounds the epoch.
+//  * Progress: tickets are handed out in index order and every ticket waits
+//    only on earlier ratings, so the earliest unfinished ticket is held by a
+//    worker and never blocked; the producer reuses a ring entry only when no
+//    worker may still read it.
 constexpr int kMfThreads = 1024;  // one block of 16 waves: 15 workers and the producer
 constexpr int kMfWorkers = kMfThreads / kWave - 1;
 constexpr int kMfRing = 1024;     // ratings staged ahead (power of two)
 constexpr int kMfPB = 256;        // ratings per producer batch (4 per lane)
 constexpr int kMfLds = 160 * 1024;  // LDS of one compute unit (gfx950): ring + hot rows
+// a factor row's 32 components over kMfGroup lanes, kMfComp consecutive
+// components per lane; a worker's ticket is kMfTicket consecutive ratings.
+// One component per lane: two or four (tickets of four or eight ratings)
+// issue fewer instructions per rating where nothing waits, but hold more
+// ratings behind each wait, and on Zipf-hot rows that costs more
+constexpr int kMfComp = 1;
+constexpr int kMfGroup = 32 / kMfComp;
+constexpr int kMfTicket = kWave / kMfGroup;
+constexpr unsigned long long kMfGroupMask = (1ull << kMfGroup) - 1ull;
+static_assert(kMfComp == 1 || kMfComp == 2 || kMfComp == 4, "1, 2 or 4 components per lane");
+
+// <U_u, V_i> over one group, bitwise the butterfly over the 32 products
+// (p_l <- p_l + p_{l xor o}, o = 1, 2, ..., 16): the offsets below kMfComp
+// pair components held by one lane, the others pair lanes of the group --
+// offset o * kMfComp is lane offset o, whose partner the DPP patterns of
+// butterfly16 reach within each 16-lane row (o = 1, 2 quad permutations,
+// o = 4, 8 mirrors once the partners hold equal values).
+__device__ __forceinline__ float mf_group_sum(const float (&p)[kMfComp]) {
+    float v;
+    if constexpr (kMfComp == 1) {
+        v = p[0];
+    } else if constexpr (kMfComp == 2) {
+        v = p[0] + p[1];
+    } else {
+        v = (p[0] + p[1]) + (p[2] + p[3]);
+    }
+    if constexpr (kMfGroup == 32) {
+        return butterfly32(v);
+    } else if constexpr (kMfGroup == 16) {
+        return butterfly16(v);
+    } else {
+        v = dpp_add<0xB1>(v);      // quad_perm [1,0,3,2]
+        v = dpp_add<0x4E>(v);      // quad_perm [2,3,0,1]
+        return dpp_add<0x141>(v);  // row_half_mirror
+    }
+}
 
 struct MfShared {
     int4 rec[kMfRing];     // user, item, previous rating on the user, on the item (-1 none)
     float r[kMfRing];
     int ready;             // ratings staged: 0 .. ready-1
-    int prog[kMfWorkers];  // first rating each worker may still read (INT_MAX when done)
+    int next_tk;           // next ticket to hand out
+    int prog[kMfWorkers];  // lowest rating whose ring entry each worker may still read
     int stop;              // a wave gave up: every loop ends, nothing is written back
-    unsigned long long sink[64];  // LDS words of lanes whose row is not in LDS
 };
 // the hot rows' words follow MfShared in dynamic LDS, 256-byte aligned
 constexpr int kMfHotOff = (int)((sizeof(MfShared) + 255) / 256 * 256);
@@ -1232,8 +1276,13 @@ __device__ void mf_producer(const int32_t *__restrict__ user, const int32_t *__r
         int64_t t0 = 0;
         bool quit = false;
         for (int round = 0;; ++round) {
+            // the ticket counter first, then the workers' entries: a worker
+            // publishes its entry before it takes a ticket, so a ticket
+            // taken after the counter was read is at or above it
+            const int nt = lds_load(&S.next_tk);
+            compiler_fence();
             const int pv = lane < kMfWorkers ? lds_load(&S.prog[lane]) : INT_MAX;
-            int mn = pv;
+            int mn = min(pv, (int)min((int64_t)nt * kMfTicket, (int64_t)INT_MAX));
 #pragma unroll
             for (int o = 1; o < 64; o <<= 1) mn = min(mn, __shfl_xor(mn, o));
             if ((int64_t)mn + kMfRing >= q0 + kMfPB) break;
@@ -1280,6 +1329,37 @@ __device__ void mf_producer(const int32_t *__restrict__ user, const int32_t *__r
     __asm__ volatile("" ::"v"(sink));
 }
 
+// A lane's kMfComp words of a row: from LDS at address la when the row is
+// hot, else from uvw at byte offset ga (workgroup scope: every reader and
+// writer of the words is in this block).  Both loads are issued, into
+// separate registers, so that neither waits for the other: a cold row's la
+// is the first hot row, and a hot row's global words are not used until the
+// end of the epoch.
+__device__ __forceinline__ void mf_words_get(bool hot, unsigned la, unsigned ga, const char *uvb,
+                                             unsigned long long (&w)[kMfComp]) {
+#pragma unroll
+    for (int c = 0; c < kMfComp; ++c) {
+        const unsigned long long lw = lword_get(la + 8u * c);
+        const unsigned long long gw = __hip_atomic_load(
+            reinterpret_cast<const unsigned long long *>(uvb + (size_t)(ga + 8u * c)),
+            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        w[c] = hot ? lw : gw;
+    }
+}
+__device__ __forceinline__ void mf_words_put(bool hot, unsigned a, unsigned long long *uvw,
+                                             const unsigned long long (&w)[kMfComp]) {
+    if (hot) {
+#pragma unroll
+        for (int c = 0; c < kMfComp; ++c) lword_put(a + 8u * c, w[c]);
+    } else {
+        char *uvb = reinterpret_cast<char *>(uvw);
+#pragma unroll
+        for (int c = 0; c < kMfComp; ++c)
+            __hip_atomic_store(reinterpret_cast<unsigned long long *>(uvb + (size_t)(a + 8u * c)),
+                               w[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+}
+
 __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
     const int32_t *__restrict__ user, const int32_t *__restrict__ item,
     const float *__restrict__ rating, const int32_t *__restrict__ prev_nz,
@@ -1289,9 +1369,10 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
     MfShared &S = *reinterpret_cast<MfShared *>(mf_lds);
     unsigned long long *hotw = reinterpret_cast<unsigned long long *>(mf_lds + kMfHotOff);
     const int wave = threadIdx.x / kWave;
-    if (threadIdx.x < kMfWorkers) S.prog[threadIdx.x] = 0;
+    if (threadIdx.x < kMfWorkers) S.prog[threadIdx.x] = INT_MAX;
     if (threadIdx.x == 0) {
         S.ready = 0;
+        S.next_tk = 0;
         S.stop = 0;
     }
     // hot rows: users 0 .. hot_u - 1, then items 0 .. hot_i - 1
@@ -1303,20 +1384,35 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
         mf_producer(user, item, rating, prev_nz, uvw, n_users, n, hot_u, hot_i, S, ctrl, timeout);
     } else {
         const int lane = lane_id();
-        const int h = lane >> 5, j = lane & 31;
-        const int n_tk = (int)((n + 1) / 2);
-        const unsigned hot_base = (unsigned)(uintptr_t)(lds_u64 *)hotw + (unsigned)j * 8u;
-        // lanes whose row is not in LDS read and write these LDS words, lanes
-        // whose row is read an unused global word and write a sink word
-        const unsigned lsink = (unsigned)(uintptr_t)(lds_u64 *)&S.sink[lane];
-        unsigned long long *gsink = reinterpret_cast<unsigned long long *>(ctrl->sink) + j;
-        const int iu_base = (int)n_users * 32 + j;
+        const int g = lane / kMfGroup, jj = lane % kMfGroup;  // rating of the ticket, lane in it
+        const int n_tk = (int)((n + kMfTicket - 1) / kMfTicket);
+        // where this lane's first word of a row is: an LDS address for a hot
+        // row, a byte offset into uvw (below 2^32) for the others
+        const unsigned hot_base =
+            (unsigned)(uintptr_t)(lds_u64 *)hotw + (unsigned)(jj * kMfComp) * 8u;
+        const unsigned ucol = (unsigned)(jj * kMfComp) * 8u;
+        const unsigned icol = (unsigned)n_users * 256u + ucol;
+        const char *const uvb = reinterpret_cast<const char *>(uvw);
+        const unsigned long long gmask = kMfGroupMask << (g * kMfGroup);  // this lane's group
         int ready = 0;  // last value read of S.ready
         bool quit = false;
-        for (int k = wave; k < n_tk && !quit; k += kMfWorkers) {
-            const int q0 = 2 * k;
-            const bool has1 = q0 + 1 < n;
-            const int need = q0 + (has1 ? 2 : 1);
+        while (!quit) {
+            // take the next ticket: first publish a bound below it (the
+            // counter as it reads now), then the ticket itself, so the
+            // producer never reuses an entry this worker has yet to read
+            lds_store(&S.prog[wave],
+                      (int)min((int64_t)kMfTicket * lds_load(&S.next_tk), (int64_t)INT_MAX));
+            int k = 0;
+            if (lane == 0) k = atomicAdd(&S.next_tk, 1);
+            k = __builtin_amdgcn_readfirstlane(k);
+            if (k >= n_tk) break;
+            const int q0 = kMfTicket * k;
+            lds_store(&S.prog[wave], q0);
+            // normal issue priority for the ticket's own work; the wait and
+            // the step after it go higher (they are on the chain of hand-overs)
+            __builtin_amdgcn_s_setprio(1);
+            const int cnt = min(kMfTicket, (int)n - q0);
+            const int need = q0 + cnt;
             if (ready < need) {
                 int64_t t0 = 0;
                 for (int round = 0; (ready = lds_load(&S.ready)) < need; ++round) {
@@ -1330,72 +1426,88 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
                 if (quit) break;
                 compiler_fence();
             }
-            const int q = has1 ? q0 + h : q0;  // an idle second half mirrors the first
+            const bool valid = g < cnt;
+            const int q = valid ? q0 + g : q0;  // an idle group mirrors the first
             const int slot = q & (kMfRing - 1);
             const int4 rc = S.rec[slot];
             const float r = S.r[slot];
+            // the ring entries are read (one wave's LDS operations run in order)
+            lds_store(&S.prog[wave], INT_MAX);
             // rc.x user, rc.y item, rc.z / rc.w their previous ratings
             const bool uh = rc.x < hot_u, ih = rc.y < hot_i;
-            const unsigned ula = uh ? hot_base + (unsigned)rc.x * 256u : lsink;
-            const unsigned ila = ih ? hot_base + (unsigned)(hot_u + rc.y) * 256u : lsink;
-            unsigned long long *ug = uh ? gsink : uvw + (rc.x * 32 + j);
-            unsigned long long *ig = ih ? gsink : uvw + (iu_base + rc.y * 32);
-            unsigned long long wu, wi;
-            {
-                const unsigned long long lu = lword_get(ula), li = lword_get(ila);
-                const unsigned long long gu = word_get_wg(ug, 0), gi = word_get_wg(ig, 0);
-                wu = uh ? lu : gu;
-                wi = ih ? li : gi;
-            }
-            // the second rating depends on the first: one after the other
-            const bool dep = has1 && (__builtin_amdgcn_readlane(rc.z, 32) == q0 ||
-                                      __builtin_amdgcn_readlane(rc.w, 32) == q0);
-            for (int p = 0; p < (dep ? 2 : 1); ++p) {
-                const bool act = dep ? h == p : (h == 0 || has1);
-                bool need_u = act && word_tag(wu) != rc.z;
-                bool need_i = act && word_tag(wi) != rc.w;
-                if (__ballot(need_u || need_i)) {
-                    int64_t t0 = now_ticks();
-                    for (int round = 0;; ++round) {
-                        if (round > 0 && __ballot((need_u && !uh) || (need_i && !ih)))
-                            __builtin_amdgcn_s_sleep(1);
-                        const unsigned long long lu = lword_get(ula), li = lword_get(ila);
-                        const unsigned long long gu = word_get_wg(ug, 0), gi = word_get_wg(ig, 0);
-                        if (need_u) wu = uh ? lu : gu;
-                        if (need_i) wi = ih ? li : gi;
-                        need_u = need_u && word_tag(wu) != rc.z;
-                        need_i = need_i && word_tag(wi) != rc.w;
-                        if (__ballot(need_u || need_i) == 0ull) break;
-                        // the watchdog and the abort flag (a device-scope load)
-                        // every 32 rounds, not on the path of every poll
-                        if ((round & 31) == 31 && mf_give_up(S, ctrl, t0, timeout)) {
-                            quit = true;
-                            break;
-                        }
+            const unsigned ul = uh ? hot_base + (unsigned)rc.x * 256u : hot_base;
+            const unsigned il = ih ? hot_base + (unsigned)(hot_u + rc.y) * 256u : hot_base;
+            const unsigned ug = ucol + (unsigned)rc.x * 256u, ig = icol + (unsigned)rc.y * 256u;
+            unsigned long long wu[kMfComp], wi[kMfComp];
+            mf_words_get(uh, ul, ug, uvb, wu);
+            mf_words_get(ih, il, ig, uvb, wi);
+            // each rating goes as soon as all its words carry the expected
+            // previous ratings -- a rating that depends on an earlier one of
+            // the same ticket sees its tag once that one has published -- so
+            // a wait on one hot row holds up only its own rating
+            bool pend = valid;
+            int64_t t0 = 0;
+            for (int round = 0;; ++round) {
+                bool bad_u = false, bad_i = false;
+#pragma unroll
+                for (int c = 0; c < kMfComp; ++c) {
+                    bad_u = bad_u || word_tag(wu[c]) != rc.z;
+                    bad_i = bad_i || word_tag(wi[c]) != rc.w;
+                }
+                const unsigned long long nr = __ballot(pend && (bad_u || bad_i));
+                const bool go = pend && (nr & gmask) == 0ull;
+                if (__ballot(go)) {
+                    if (round > 0) __builtin_amdgcn_s_setprio(3);
+                    float uv[kMfComp], vv[kMfComp], pr[kMfComp];
+#pragma unroll
+                    for (int c = 0; c < kMfComp; ++c) {
+                        uv[c] = word_value(wu[c]);
+                        vv[c] = word_value(wi[c]);
+                        pr[c] = __builtin_fmaf(uv[c], vv[c], 0.0f);
                     }
-                    if (quit) break;
+                    const float err = r - mf_group_sum(pr);
+                    unsigned long long nu[kMfComp], ni[kMfComp];
+#pragma unroll
+                    for (int c = 0; c < kMfComp; ++c) {
+                        const float ea = err * vv[c], eb = reg * uv[c];
+                        const float a2 = err * uv[c], b2 = reg * vv[c];
+                        nu[c] = word_pack(__builtin_fmaf(lr, ea - eb, uv[c]), q);
+                        ni[c] = word_pack(__builtin_fmaf(lr, a2 - b2, vv[c]), q);
+                    }
+                    if (go) {
+                        mf_words_put(uh, uh ? ul : ug, uvw, nu);
+                        mf_words_put(ih, ih ? il : ig, uvw, ni);
+                    }
+                    pend = pend && !go;
+                    if (__ballot(pend) == 0ull) break;
                 }
-                const float uj = act ? word_value(wu) : 0.0f, vj = act ? word_value(wi) : 0.0f;
-                const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
-                const float ea = err * vj, eb = reg * uj;
-                const float a2 = err * uj, b2 = reg * vj;
-                const unsigned long long nu = word_pack(__builtin_fmaf(lr, ea - eb, uj), q);
-                const unsigned long long ni = word_pack(__builtin_fmaf(lr, a2 - b2, vj), q);
-                // inactive lanes write the sinks
-                lword_put(act ? ula : lsink, nu);
-                lword_put(act ? ila : lsink, ni);
-                word_put_wg(act ? ug : gsink, 0, nu);
-                word_put_wg(act ? ig : gsink, 0, ni);
-                if (dep && p == 0) {
-                    // the second rating reads what the first just wrote
-                    const unsigned long long lu = lword_get(ula), li = lword_get(ila);
-                    const unsigned long long gu = word_get_wg(ug, 0), gi = word_get_wg(ig, 0);
-                    wu = uh ? lu : gu;
-                    wi = ih ? li : gi;
+                if (round == 0) {
+                    t0 = now_ticks();
+                } else {
+                    // the watchdog and the abort flag (a device-scope load)
+                    // every 32 rounds, not on the path of every poll
+                    if ((round & 31) == 0 && mf_give_up(S, ctrl, t0, timeout)) {
+                        quit = true;
+                        break;
+                    }
+                }
+                // almost every wait is for a Zipf-hot row in LDS: unless a
+                // lane awaits a word in global memory, the round rereads LDS
+                // only (a cache round trip would cost several LDS ones)
+                if (__ballot(pend && ((bad_u && !uh) || (bad_i && !ih)))) {
+                    if (round > 0) __builtin_amdgcn_s_sleep(1);
+                    if (pend && bad_u) mf_words_get(uh, ul, ug, uvb, wu);
+                    if (pend && bad_i) mf_words_get(ih, il, ig, uvb, wi);
+                } else {
+                    __builtin_amdgcn_s_setprio(2);
+#pragma unroll
+                    for (int c = 0; c < kMfComp; ++c) {
+                        if (pend && bad_u) wu[c] = lword_get(ul + 8u * c);
+                        if (pend && bad_i) wi[c] = lword_get(il + 8u * c);
+                    }
                 }
             }
-            // done with the ring slots of this ticket (every lane stores the same value)
-            lds_store(&S.prog[wave], q0 + 2 * kMfWorkers);
+            if (quit) break;
         }
         lds_store(&S.prog[wave], INT_MAX);
     }
@@ -1636,7 +1748,8 @@ extern "C" int pdb_mf_epoch(const int32_t *user, const int32_t *item, const floa
     // one compute unit: its words are indexed with 32-bit integers, and it
     // wins while levels are narrow (about 35 ns per rating on one unit
     // against a device-scope hand-over of about 0.8 us per level)
-    const bool one_cu_fits = (n_users + n_items) * 32 < (int64_t)INT32_MAX - 64;
+    // the one-unit kernel addresses the words with 32-bit byte offsets
+    const bool one_cu_fits = (n_users + n_items) * 256 <= ((int64_t)1 << 32);
     const bool narrow = lv->L_host > 0 && n < 16 * lv->L_host;
     const bool one_cu = one_cu_fits && (o.mf_one_cu == 1 || (o.mf_one_cu == -1 && narrow));
     if (sf_ok && (o.epoch_mode == PDB_EPOCH_SYNCFREE ||
