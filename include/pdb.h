@@ -89,10 +89,11 @@ typedef enum pdb_sched_method {
                                 LDS; dataflow runs instead when a row holds more than 16384
                                 entries */
     PDB_SCHED_SHORT = 6      /* short rows (matrix completion): one block settles sub-chunks of
-                                64 consecutive rows strictly in order, one wave per sub-chunk in
-                                turn, each by rounds of lane shuffles, with the levels of the
-                                last 64 sub-chunks kept in an LDS ring; dataflow runs instead
-                                when a row holds more than 4 entries */
+                                64 consecutive rows strictly in order, the waves taking turns of
+                                several consecutive sub-chunks, each sub-chunk by as many rounds
+                                of lane shuffles as its longest chain of in-sub-chunk writers,
+                                with the levels of the last 256 sub-chunks kept in an LDS ring;
+                                dataflow runs instead when a row holds more than 4 entries */
 } pdb_sched_method;
 /* Two dataflow forms.  The wave-per-example form runs when the chain check
  * ran (PDB_SCHED_AUTO or PDB_SCHED_CHAIN), found the input not chain-like

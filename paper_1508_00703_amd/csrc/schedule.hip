@@ -653,27 +653,43 @@ __global__ __launch_bounds__(kBlock) void k_levels_rowwave(const int64_t *__rest
 // ---- K3r short-row walk --------------------------------------------------
 // One block walks the examples in sub-chunks of 64 consecutive rows, one row
 // per lane, for inputs whose rows hold at most kShortR entries (matrix
-// completion: a user and an item).  Sub-chunk q belongs to wave q mod
-// kShortWaves; the sub-chunks are settled strictly in order, handed on by an
-// LDS counter (s_done = number of settled sub-chunks).  Settling q:
+// completion: a user and an item).  The sub-chunks are settled strictly in
+// order, kShortPer consecutive ones per turn of a wave: turn t (sub-chunks
+// kShortPer t ...) belongs to wave t mod kShortWaves, and the turns are
+// handed on by an LDS counter (s_done = number of settled sub-chunks).
+// Settling sub-chunk q (kShortPer = short_per<R>()):
 //   known(i) = max level of i's writers before q (the last kShortRing
 //              sub-chunks from an LDS ring, older ones loaded from global
-//              memory sixteen sub-chunks ahead);
+//              memory a turn of every wave ahead);
 //   level(i) = 1 + max(known(i), level(in-q writers)), the fixed point of
-//              Jacobi rounds across the wave's lanes (one round per link of
-//              the longest chain inside q, plus one).
+//              Jacobi rounds across the wave's lanes, one round per link of
+//              the longest chain inside q (counted from the structure while
+//              the wave waits for its turn).
 // A round is a lane shuffle, where waiting on another workgroup's published
-// level costs a device-scope round trip.  Visibility of the global levels:
-// a wave waits for its own earlier stores (a workgroup-scope release) before
-// it settles a sub-chunk, so when a wave observes s_done past q + 16 the
-// stores of every sub-chunk up to q are complete; it loads only writers
-// kShortRing sub-chunks back, long past that.  A row with more than kShortR
+// level costs a device-scope round trip; a hand-over from wave to wave costs
+// about a third of a sub-chunk's settling, hence several sub-chunks a turn.
+// Visibility of the global levels: a wave waits for its own earlier stores
+// (a workgroup-scope release) before it settles a turn, so once s_done has
+// passed the first sub-chunk of turn u + kShortWaves the stores of turn u
+// are complete.  A wave loads the global levels of turn t + kShortWaves
+// right after settling turn t, and only of writers kShortRing sub-chunks or
+// more before them: kShortRing >= 2 kShortWaves kShortPer puts those writers
+// kShortWaves turns or more behind turn t.  A row with more than kShortR
 // entries sets ctrl->bad and stops the block (the host then runs dataflow);
 // every wait is bounded by the spin budget.
 constexpr int kShortWaves = 16;
 constexpr int kShortThreads = kShortWaves * 64;
 constexpr int kShortR = 4;
-constexpr int kShortRing = 64;  // sub-chunks whose levels stay in LDS
+constexpr int kShortRing = 256;  // sub-chunks whose levels stay in LDS
+// sub-chunks a wave settles per turn (fewer for rows of up to kShortR
+// entries, whose per-row state would otherwise spill registers)
+template <int R>
+constexpr int short_per() {
+    return R <= 2 ? 8 : 4;
+}
+static_assert(kShortRing >= 2 * kShortWaves * short_per<2>() &&
+                  kShortRing >= 2 * kShortWaves * short_per<kShortR>(),
+              "loads of levels too recent");
 
 template <int R>
 struct ShortRow {
@@ -708,6 +724,7 @@ __global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *_
                                                                 const int32_t *__restrict__ prev_row,
                                                                 int64_t n, int32_t *level,
                                                                 Ctrl *ctrl, int64_t timeout) {
+    constexpr int kShortPer = short_per<R>();
     __shared__ int s_ring[kShortRing][64];
     __shared__ int s_done, s_stop;
     const int lane = lane_id(), wave = wave_in_block();
@@ -717,27 +734,67 @@ __global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *_
     }
     __syncthreads();
     const int64_t nsub = (n + 63) / 64;
-    int64_t q = wave;
-    if (q >= nsub) return;
-    ShortRow<R> cur = short_fetch<R>(row_ptr, prev_row, level, n, 64 * q, 64 * (q - kShortRing));
-    for (; q < nsub; q += kShortWaves) {
-        // this wave's earlier stores complete before it settles q (see above)
+    int64_t t = wave;  // this wave's turn
+    if (kShortPer * t >= nsub) return;
+    ShortRow<R> cur[kShortPer];
+    auto fetch_turn = [&](int64_t u) {
+#pragma unroll
+        for (int j = 0; j < kShortPer; ++j) {
+            const int64_t q = kShortPer * u + j;  // past the end: rows >= n, nothing loaded
+            cur[j] = short_fetch<R>(row_ptr, prev_row, level, n, 64 * q, 64 * (q - kShortRing));
+        }
+    };
+    fetch_turn(t);
+    for (; kShortPer * t < nsub; t += kShortWaves) {
+        const int64_t q0 = kShortPer * t;
+        const int nq = (int)min((int64_t)kShortPer, nsub - q0);
+        // this wave's earlier stores complete before it settles the turn (see above)
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        if (__ballot(cur.m > R) != 0ull) {
+        bool long_row = false;
+#pragma unroll
+        for (int j = 0; j < kShortPer; ++j) long_row = long_row || cur[j].m > R;
+        if (__ballot(long_row) != 0ull) {
             if (lane == 0) {
                 ctrl->bad = 1;
                 __hip_atomic_store(&s_stop, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
             return;
         }
-        // wait for the sub-chunks before q: far from its turn a wave sleeps
-        // between polls; the next in line polls s_done alone, and looks at
-        // the stop flag and the clock every 32nd poll
+        // before the wait, from the structure alone: each row's writers
+        // inside its sub-chunk (lane, -1 none) and the sub-chunk's depth,
+        // the most links on a chain of such writers -- the settling then
+        // runs exactly that many Jacobi rounds
+        int pin[kShortPer][R], depth[kShortPer];
+#pragma unroll
+        for (int j = 0; j < kShortPer; ++j) {
+            const int64_t r0 = 64 * (q0 + j);
+#pragma unroll
+            for (int k = 0; k < R; ++k) {
+                const int p = cur[j].pr[k];
+                pin[j][k] = p >= r0 ? (int)(p - r0) : -1;
+            }
+            int d = 0;
+            for (;;) {
+                int nd = 0;
+#pragma unroll
+                for (int k = 0; k < R; ++k) {
+                    const int o = __shfl(d, pin[j][k] < 0 ? lane : pin[j][k]);
+                    if (pin[j][k] >= 0) nd = max(nd, o + 1);
+                }
+                const bool ch = nd != d;
+                d = nd;
+                if (__ballot(ch) == 0ull) break;
+            }
+            depth[j] = __builtin_amdgcn_readfirstlane(wave_max_dpp(d));
+        }
+        // wait for the sub-chunks before the turn: far from its turn a wave
+        // sleeps between polls; the next in line polls s_done alone, and
+        // looks at the stop flag and the clock every 32nd poll
         const int64_t t0 = now_ticks();
         for (int it = 1;; ++it) {
             const int dn = __hip_atomic_load(&s_done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            if (dn == (int)q) break;
-            if ((int)q - dn > 1) {
+            if (dn == (int)q0) break;
+            if ((int)q0 - dn > kShortPer) {
                 __builtin_amdgcn_s_sleep(8);
                 it = 0;
             }
@@ -754,46 +811,58 @@ __global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *_
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
         __builtin_amdgcn_s_setprio(3);  // the block waits on this wave: issue it first
-        const int64_t r0 = 64 * q, ring0 = r0 - 64 * kShortRing;
-        // every ring read issued at once (lanes without one read slot 0 and
-        // ignore it), then the bounds folded in
-        int known = 0, rv[R], pin[R];
-        bool in_ring[R];
+        int lvs[kShortPer];
 #pragma unroll
-        for (int k = 0; k < R; ++k) {
-            const int p = cur.pr[k];  // -1: no writer, or past the row's end
-            in_ring[k] = p >= 0 && p >= ring0 && p < r0;
-            rv[k] = s_ring[in_ring[k] ? (p >> 6) & (kShortRing - 1) : 0][in_ring[k] ? p & 63 : 0];
-            pin[k] = p >= r0 ? (int)(p - r0) : -1;
-        }
-#pragma unroll
-        for (int k = 0; k < R; ++k) {
-            const int p = cur.pr[k];
-            if (p >= 0 && p < ring0) known = max(known, cur.v[k]);
-            if (in_ring[k]) known = max(known, rv[k]);
-        }
-        const bool live = r0 + lane < n;
-        int lv = known + 1;
-        for (;;) {
-            int nl = known + 1;
+        for (int j = 0; j < kShortPer; ++j) {
+            lvs[j] = 0;
+            if (j >= nq) continue;
+            const ShortRow<R> &c = cur[j];
+            const int64_t r0 = 64 * (q0 + j), ring0 = r0 - 64 * kShortRing;
+            // every ring read issued at once (lanes without one read slot 0
+            // and ignore it), then the bounds folded in; sub-chunks settled
+            // earlier in this turn are in the ring already (one wave's LDS
+            // operations run in order)
+            int known = 0, rv[R];
+            bool in_ring[R];
 #pragma unroll
             for (int k = 0; k < R; ++k) {
-                const int o = __shfl(lv, pin[k] < 0 ? lane : pin[k]);
-                if (pin[k] >= 0) nl = max(nl, o + 1);
+                const int p = c.pr[k];  // -1: no writer, or past the row's end
+                in_ring[k] = p >= 0 && p >= ring0 && p < r0;
+                rv[k] = s_ring[in_ring[k] ? (p >> 6) & (kShortRing - 1) : 0][in_ring[k] ? p & 63 : 0];
             }
-            const bool ch = live && nl != lv;
-            lv = nl;
-            if (__ballot(ch) == 0ull) break;
+#pragma unroll
+            for (int k = 0; k < R; ++k) {
+                const int p = c.pr[k];
+                if (p >= 0 && p < ring0) known = max(known, c.v[k]);
+                if (in_ring[k]) known = max(known, rv[k]);
+            }
+            // after r rounds every chain of at most r links inside the
+            // sub-chunk has been followed: depth[j] rounds reach the fixed point
+            int lv = known + 1;
+            for (int round = 0; round < depth[j]; ++round) {
+                int nl = known + 1;
+#pragma unroll
+                for (int k = 0; k < R; ++k) {
+                    const int o = __shfl(lv, pin[j][k] < 0 ? lane : pin[j][k]);
+                    if (pin[j][k] >= 0) nl = max(nl, o + 1);
+                }
+                lv = nl;
+            }
+            s_ring[(q0 + j) & (kShortRing - 1)][lane] = lv;
+            lvs[j] = lv;
         }
-        s_ring[q & (kShortRing - 1)][lane] = lv;
         __asm__ __volatile__("" ::: "memory");  // one wave's LDS operations run in order
-        if (lane == 0) __hip_atomic_store(&s_done, (int)q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (lane == 0)
+            __hip_atomic_store(&s_done, (int)(q0 + nq), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         __builtin_amdgcn_s_setprio(0);
-        if (live) level[r0 + lane] = lv;
-        // the wave's next sub-chunk: writers before its ring window were
-        // settled at least kShortRing - kShortWaves sub-chunks before q
-        const int64_t qn = q + kShortWaves;
-        if (qn < nsub) cur = short_fetch<R>(row_ptr, prev_row, level, n, 64 * qn, 64 * (qn - kShortRing));
+#pragma unroll
+        for (int j = 0; j < kShortPer; ++j) {
+            const int64_t r = 64 * (q0 + j) + lane;
+            if (j < nq && r < n) level[r] = lvs[j];
+        }
+        // the wave's next turn: writers before its ring window were settled
+        // at least kShortWaves turns before this one
+        if (kShortPer * (t + kShortWaves) < nsub) fetch_turn(t + kShortWaves);
     }
 }
 
