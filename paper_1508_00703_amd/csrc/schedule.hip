@@ -1423,14 +1423,17 @@ __global__ void k_level_ptr(const uint32_t *__restrict__ skeys, const uint32_t *
 // every 64 rows a wave adds its count to the total and stops once the total
 // is past n/4 (an input like config 4, where almost every example breaks,
 // then reads a quarter of the previous writers instead of all of them).
+constexpr int64_t kChainPrefix = 65536;  // rows the chain check reads first
+// Rows 1 .. lim - 1 are checked (lim <= n): a prefix first, so that an input
+// whose prefix already breaks often is not read further.
 __global__ __launch_bounds__(kBlock) void k_chain_check(const int64_t *__restrict__ row_ptr,
-                                                        int64_t n, const int32_t *__restrict__ pn,
+                                                        int64_t lim, const int32_t *__restrict__ pn,
                                                         Ctrl *ctrl) {
     const int lane = lane_id();
     const int64_t nw = (int64_t)gridDim.x * (kBlock / kWave);
-    const int64_t enough = n / 4 + 1;
+    const int64_t enough = lim / 4 + 1;
     int breaks = 0, rows = 0;
-    for (int64_t i = 1 + blockIdx.x * (int64_t)(kBlock / kWave) + wave_in_block(); i < n; i += nw) {
+    for (int64_t i = 1 + blockIdx.x * (int64_t)(kBlock / kWave) + wave_in_block(); i < lim; i += nw) {
         const int64_t lo = row_ptr[i - 1], b = row_ptr[i], e = row_ptr[i + 1];
         bool found = false;
         for (int64_t p = b + lane; p < e && !found; p += kWave) found = pn[p] >= lo;
@@ -1729,11 +1732,24 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
     bool chain_like = false, chain_checked = false;
     if (method == PDB_SCHED_AUTO || method == PDB_SCHED_CHAIN) {
         chain_checked = true;
-        k_chain_check<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n, pn,
-                                                                            w.ctrl);
+        // a prefix of the rows first: when more than a quarter of it breaks,
+        // the input is no chain and is taken as not chain-like without
+        // reading the rest (every method is exact; this only picks one)
+        const int64_t lim0 = std::min<int64_t>(n, kChainPrefix);
+        k_chain_check<<<grid_for(lim0, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, lim0,
+                                                                               pn, w.ctrl);
         PDB_LAUNCHED();
         rc = read_ctrl(w.ctrl, &host, s);
         if (rc != PDB_OK) return rc;
+        const bool prefix_breaks = lim0 < n && 4 * (int64_t)host.chain_breaks > lim0;
+        if (lim0 < n && !prefix_breaks) {
+            k_fill_i32<<<1, 64, 0, s>>>(&w.ctrl->chain_breaks, 1, 0);
+            k_chain_check<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n,
+                                                                                pn, w.ctrl);
+            PDB_LAUNCHED();
+            rc = read_ctrl(w.ctrl, &host, s);
+            if (rc != PDB_OK) return rc;
+        }
         if (host.chain_breaks == 0) {
             k_chain_levels<<<grid_for(n + 1, kBlock, 65536), kBlock, 0, s>>>(
                 n, lv->level, lv->perm, lv->level_ptr, lv->n_levels);
@@ -1746,7 +1762,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         }
         if (method == PDB_SCHED_CHAIN) method = PDB_SCHED_DATAFLOW;
         // most examples conflict with their predecessor: the walk pays
-        chain_like = 4 * (int64_t)host.chain_breaks <= n;
+        chain_like = !prefix_breaks && 4 * (int64_t)host.chain_breaks <= n;
     }
 
     // which method: the spine when the most frequent feature misses at most
