@@ -421,6 +421,56 @@ def run_dense(args):
     print(json.dumps(out))
 
 
+def widest_level(native, g, lv, lp, L, mf, dev, stream, run_one, reps=20):
+    """The epoch kernel on the widest level alone: a one-level schedule over
+    that level's examples, run level by level (they share no feature), timed
+    with events on the library's stream.  The whole epoch is bounded by its
+    chain of levels; this is the bandwidth the apply reaches where a level is
+    wide.  Bytes as algorithmic_bytes, for the level's examples only."""
+    import numpy as np
+    import torch
+
+    widths = np.diff(lp[:L + 1])
+    lvl = int(np.argmax(widths))
+    width = int(widths[lvl])
+    rec = {"level": lvl + 1, "width": width}
+    if width < 64:
+        rec["skipped"] = "narrow (fewer than 64 examples)"
+        return rec
+    b0, b1 = int(lp[lvl]), int(lp[lvl + 1])
+    sub = native.Levels(0, 0, dev, with_prev_nz=False)
+    sub.perm = lv.perm[b0:b1]
+    sub.level = lv.level
+    sub.level_ptr = torch.tensor([0, width], dtype=torch.int64, device=dev)
+    sub.n_levels.fill_(1)
+    sub.prev_nz = lv.prev_nz
+    sub.L_host = 1
+    sub.max_width_host = width
+    if mf:
+        nbytes = width * (16 + 512) + 8
+    else:
+        rows = lv.perm[b0:b1].cpu().numpy().astype(np.int64)
+        m = g["row_ptr"][rows + 1] - g["row_ptr"][rows]
+        per_nz = 4 + 8 + (4 if g["val"] is not None else 0)
+        nbytes = int(m.sum()) * per_nz + width * (8 + 4 + 4) + 8
+        rec["entries"] = int(m.sum())
+    opt1 = native.options(epoch_mode=1)
+    run_one(sub, opt1)  # warm-up
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        run_one(sub, opt1)
+        b.record(stream)
+        times.append((a, b))
+    torch.cuda.synchronize()
+    us = trimmed_mean([a.elapsed_time(b) for a, b in times]) * 1e3
+    gbs = nbytes / (us * 1e-6) / 1e9
+    rec.update({"algorithmic_bytes": nbytes, "us_per_call": us, "achieved_gbs": gbs,
+                "frac": gbs / HBM_PEAK_GBS, "kernel": "k_levels_apply (one level)"})
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -619,6 +669,27 @@ def main():
     if delay < 0:
         gpu_levels = (lv.level.cpu().numpy(), lv.perm.cpu().numpy(), lv.level_ptr.cpu().numpy(),
                       L)
+    # the apply on the widest level alone (outside the timed steps and after
+    # the result was copied out; it changes the weights, which are not used
+    # again)
+    widest = None
+    width_stats = {}
+    if delay < 0 and not batch and L > 0:
+        widths = np.diff(gpu_levels[2][:L + 1])
+        width_stats = {"mean_level_width": float(widths.mean()),
+                       "median_level_width": float(np.median(widths))}
+        if mf:
+            def run_one(sub, o):
+                native.pdb_mf_epoch(user, item, rating, n, U, g["n_users"], V, g["n_items"],
+                                    g["rank"], float(g["lr"]), float(g["reg"]), sub, ws=ws_e,
+                                    opt=o)
+        else:
+            def run_one(sub, o):
+                native.pdb_sgd_epoch(csr, y, n, d, w, float(g["lr"]), g["loss"], sub, ws=ws_e,
+                                     opt=o)
+        widest = widest_level(native, g, lv, gpu_levels[2], L, mf, dev, stream, run_one)
+        if native.pdb_workspace_status(ws_e) != native.PDB_OK:
+            raise SystemExit("device-side failure on the widest level")
     peak = copy_peak(dev)
     out = {
         "metric": METRIC,
@@ -640,6 +711,7 @@ def main():
                    "n": n, "d": d, "nnz": nnz,
                    "seed": g["seed"], "levels": None if delay >= 0 else L,
                    "max_level_width": None if delay >= 0 else lv.max_width_host,
+                   **width_stats,
                    "schedule_method": info.get("method_used"),
                    "schedule_rounds": info.get("rounds"), "epoch_mode": args.epoch_mode},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -656,6 +728,9 @@ def main():
         "schedule_ms": trimmed_mean([a.elapsed_time(b) for a, b in sched_ms]),
         "epoch_ms": ep,
     }
+    if widest is not None:
+        out["roofline"]["widest_level"] = widest
+
     sched = natural = None
     if not args.no_cpu_baseline:
         out["cpu_baseline"], sched, natural = cpu_baseline(g, cfg_id, args.cpu_budget, batch,
@@ -672,6 +747,9 @@ def main():
         if not out["parity"]["ok"]:
             out["invalid"] = "parity with the oracle failed: the value is not counted"
             out["value"] = 0.0
+    if mf:
+        # each rating updates a 32-component user row and item row
+        out["param_updates_per_s"] = out["value"] * 2 * g["rank"]
     print(json.dumps(out))
 
 
