@@ -1165,42 +1165,13 @@ constexpr int kMfWorkers = kMfThreads / kWave - 1;
 constexpr int kMfRing = 1024;     // ratings staged ahead (power of two)
 constexpr int kMfPB = 256;        // ratings per producer batch (4 per lane)
 constexpr int kMfLds = 160 * 1024;  // LDS of one compute unit (gfx950): ring + hot rows
-// a factor row's 32 components over kMfGroup lanes, kMfComp consecutive
-// components per lane; a worker's ticket is kMfTicket consecutive ratings.
-// One component per lane: two or four (tickets of four or eight ratings)
-// issue fewer instructions per rating where nothing waits, but hold more
-// ratings behind each wait, and on Zipf-hot rows that costs more
-constexpr int kMfComp = 1;
-constexpr int kMfGroup = 32 / kMfComp;
-constexpr int kMfTicket = kWave / kMfGroup;
-constexpr unsigned long long kMfGroupMask = (1ull << kMfGroup) - 1ull;
-static_assert(kMfComp == 1 || kMfComp == 2 || kMfComp == 4, "1, 2 or 4 components per lane");
-
-// <U_u, V_i> over one group, bitwise the butterfly over the 32 products
-// (p_l <- p_l + p_{l xor o}, o = 1, 2, ..., 16): the offsets below kMfComp
-// pair components held by one lane, the others pair lanes of the group --
-// offset o * kMfComp is lane offset o, whose partner the DPP patterns of
-// butterfly16 reach within each 16-lane row (o = 1, 2 quad permutations,
-// o = 4, 8 mirrors once the partners hold equal values).
-__device__ __forceinline__ float mf_group_sum(const float (&p)[kMfComp]) {
-    float v;
-    if constexpr (kMfComp == 1) {
-        v = p[0];
-    } else if constexpr (kMfComp == 2) {
-        v = p[0] + p[1];
-    } else {
-        v = (p[0] + p[1]) + (p[2] + p[3]);
-    }
-    if constexpr (kMfGroup == 32) {
-        return butterfly32(v);
-    } else if constexpr (kMfGroup == 16) {
-        return butterfly16(v);
-    } else {
-        v = dpp_add<0xB1>(v);      // quad_perm [1,0,3,2]
-        v = dpp_add<0x4E>(v);      // quad_perm [2,3,0,1]
-        return dpp_add<0x141>(v);  // row_half_mirror
-    }
-}
+// a worker's ticket: two consecutive ratings, one per 32-lane half (lane j
+// of a half holds component j of the rating's rows).  Spreading a rating
+// over 16 or 8 lanes (tickets of four or eight ratings) issues fewer
+// instructions per rating where nothing waits, but holds more ratings
+// behind each wait, and on Zipf-hot rows that costs more
+constexpr int kMfTicket = 2;
+constexpr unsigned long long kMfHalfMask = 0xFFFFFFFFull;
 
 struct MfShared {
     int4 rec[kMfRing];     // user, item, previous rating on the user, on the item (-1 none)
@@ -1329,34 +1300,29 @@ __device__ void mf_producer(const int32_t *__restrict__ user, const int32_t *__r
     __asm__ volatile("" ::"v"(sink));
 }
 
-// A lane's kMfComp words of a row: from LDS at address la when the row is
-// hot, else from uvw at byte offset ga (workgroup scope: every reader and
-// writer of the words is in this block).  Both loads are issued, into
-// separate registers, so that neither waits for the other: a cold row's la
-// is the first hot row, and a hot row's global words are not used until the
-// end of the epoch.
-__device__ __forceinline__ void mf_words_get(bool hot, unsigned la, unsigned ga, const char *uvb,
-                                             unsigned long long (&w)[kMfComp]) {
-#pragma unroll
-    for (int c = 0; c < kMfComp; ++c) {
-        const unsigned long long lw = lword_get(la + 8u * c);
-        const unsigned long long gw = __hip_atomic_load(
-            reinterpret_cast<const unsigned long long *>(uvb + (size_t)(ga + 8u * c)),
-            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        w[c] = hot ? lw : gw;
-    }
+// A lane's word of a row: from LDS at address la when the row is hot, else
+// from uvw at byte offset ga (workgroup scope: every reader and writer of the
+// words is in this block).  Both loads are issued, into separate registers,
+// so that neither waits for the other: a cold row's la is the first hot row,
+// and a hot row's global words are not used until the end of the epoch.
+__device__ __forceinline__ unsigned long long mf_word_get(bool hot, unsigned la, unsigned ga,
+                                                          const char *uvb) {
+    const unsigned long long lw = lword_get(la);
+    const unsigned long long gw = __hip_atomic_load(
+        reinterpret_cast<const unsigned long long *>(uvb + (size_t)ga), __ATOMIC_RELAXED,
+        __HIP_MEMORY_SCOPE_WORKGROUP);
+    return hot ? lw : gw;
 }
-__device__ __forceinline__ void mf_words_put(bool hot, unsigned a, unsigned long long *uvw,
-                                             const unsigned long long (&w)[kMfComp]) {
+// Stores a lane's word of a row: to LDS at address a when the row is hot,
+// else to uvw at byte offset a.  Only the lanes that call take part.
+__device__ __forceinline__ void mf_word_put(bool hot, unsigned a, unsigned long long *uvw,
+                                            unsigned long long w) {
     if (hot) {
-#pragma unroll
-        for (int c = 0; c < kMfComp; ++c) lword_put(a + 8u * c, w[c]);
+        lword_put(a, w);
     } else {
-        char *uvb = reinterpret_cast<char *>(uvw);
-#pragma unroll
-        for (int c = 0; c < kMfComp; ++c)
-            __hip_atomic_store(reinterpret_cast<unsigned long long *>(uvb + (size_t)(a + 8u * c)),
-                               w[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __hip_atomic_store(
+            reinterpret_cast<unsigned long long *>(reinterpret_cast<char *>(uvw) + (size_t)a), w,
+            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
 }
 
@@ -1384,16 +1350,15 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
         mf_producer(user, item, rating, prev_nz, uvw, n_users, n, hot_u, hot_i, S, ctrl, timeout);
     } else {
         const int lane = lane_id();
-        const int g = lane / kMfGroup, jj = lane % kMfGroup;  // rating of the ticket, lane in it
+        const int g = lane >> 5, j = lane & 31;  // rating of the ticket, component
         const int n_tk = (int)((n + kMfTicket - 1) / kMfTicket);
-        // where this lane's first word of a row is: an LDS address for a hot
+        // where this lane's word of a row is: an LDS address for a hot
         // row, a byte offset into uvw (below 2^32) for the others
-        const unsigned hot_base =
-            (unsigned)(uintptr_t)(lds_u64 *)hotw + (unsigned)(jj * kMfComp) * 8u;
-        const unsigned ucol = (unsigned)(jj * kMfComp) * 8u;
+        const unsigned hot_base = (unsigned)(uintptr_t)(lds_u64 *)hotw + (unsigned)j * 8u;
+        const unsigned ucol = (unsigned)j * 8u;
         const unsigned icol = (unsigned)n_users * 256u + ucol;
         const char *const uvb = reinterpret_cast<const char *>(uvw);
-        const unsigned long long gmask = kMfGroupMask << (g * kMfGroup);  // this lane's group
+        const unsigned long long gmask = kMfHalfMask << (32 * g);  // this lane's half
         int ready = 0;  // last value read of S.ready
         bool quit = false;
         while (!quit) {
@@ -1438,9 +1403,8 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
             const unsigned ul = uh ? hot_base + (unsigned)rc.x * 256u : hot_base;
             const unsigned il = ih ? hot_base + (unsigned)(hot_u + rc.y) * 256u : hot_base;
             const unsigned ug = ucol + (unsigned)rc.x * 256u, ig = icol + (unsigned)rc.y * 256u;
-            unsigned long long wu[kMfComp], wi[kMfComp];
-            mf_words_get(uh, ul, ug, uvb, wu);
-            mf_words_get(ih, il, ig, uvb, wi);
+            unsigned long long wu = mf_word_get(uh, ul, ug, uvb);
+            unsigned long long wi = mf_word_get(ih, il, ig, uvb);
             // each rating goes as soon as all its words carry the expected
             // previous ratings -- a rating that depends on an earlier one of
             // the same ticket sees its tag once that one has published -- so
@@ -1448,35 +1412,20 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
             bool pend = valid;
             int64_t t0 = 0;
             for (int round = 0;; ++round) {
-                bool bad_u = false, bad_i = false;
-#pragma unroll
-                for (int c = 0; c < kMfComp; ++c) {
-                    bad_u = bad_u || word_tag(wu[c]) != rc.z;
-                    bad_i = bad_i || word_tag(wi[c]) != rc.w;
-                }
+                const bool bad_u = word_tag(wu) != rc.z, bad_i = word_tag(wi) != rc.w;
                 const unsigned long long nr = __ballot(pend && (bad_u || bad_i));
                 const bool go = pend && (nr & gmask) == 0ull;
                 if (__ballot(go)) {
                     if (round > 0) __builtin_amdgcn_s_setprio(3);
-                    float uv[kMfComp], vv[kMfComp], pr[kMfComp];
-#pragma unroll
-                    for (int c = 0; c < kMfComp; ++c) {
-                        uv[c] = word_value(wu[c]);
-                        vv[c] = word_value(wi[c]);
-                        pr[c] = __builtin_fmaf(uv[c], vv[c], 0.0f);
-                    }
-                    const float err = r - mf_group_sum(pr);
-                    unsigned long long nu[kMfComp], ni[kMfComp];
-#pragma unroll
-                    for (int c = 0; c < kMfComp; ++c) {
-                        const float ea = err * vv[c], eb = reg * uv[c];
-                        const float a2 = err * uv[c], b2 = reg * vv[c];
-                        nu[c] = word_pack(__builtin_fmaf(lr, ea - eb, uv[c]), q);
-                        ni[c] = word_pack(__builtin_fmaf(lr, a2 - b2, vv[c]), q);
-                    }
+                    const float uj = word_value(wu), vj = word_value(wi);
+                    const float err = r - butterfly32(__builtin_fmaf(uj, vj, 0.0f));
+                    const float ea = err * vj, eb = reg * uj;
+                    const float a2 = err * uj, b2 = reg * vj;
+                    const unsigned long long nu = word_pack(__builtin_fmaf(lr, ea - eb, uj), q);
+                    const unsigned long long ni = word_pack(__builtin_fmaf(lr, a2 - b2, vj), q);
                     if (go) {
-                        mf_words_put(uh, uh ? ul : ug, uvw, nu);
-                        mf_words_put(ih, ih ? il : ig, uvw, ni);
+                        mf_word_put(uh, uh ? ul : ug, uvw, nu);
+                        mf_word_put(ih, ih ? il : ig, uvw, ni);
                     }
                     pend = pend && !go;
                     if (__ballot(pend) == 0ull) break;
@@ -1496,15 +1445,12 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_onecu(
                 // only (a cache round trip would cost several LDS ones)
                 if (__ballot(pend && ((bad_u && !uh) || (bad_i && !ih)))) {
                     if (round > 0) __builtin_amdgcn_s_sleep(1);
-                    if (pend && bad_u) mf_words_get(uh, ul, ug, uvb, wu);
-                    if (pend && bad_i) mf_words_get(ih, il, ig, uvb, wi);
+                    if (pend && bad_u) wu = mf_word_get(uh, ul, ug, uvb);
+                    if (pend && bad_i) wi = mf_word_get(ih, il, ig, uvb);
                 } else {
                     __builtin_amdgcn_s_setprio(2);
-#pragma unroll
-                    for (int c = 0; c < kMfComp; ++c) {
-                        if (pend && bad_u) wu[c] = lword_get(ul + 8u * c);
-                        if (pend && bad_i) wi[c] = lword_get(il + 8u * c);
-                    }
+                    if (pend && bad_u) wu = lword_get(ul);
+                    if (pend && bad_i) wi = lword_get(il);
                 }
             }
             if (quit) break;
