@@ -441,10 +441,12 @@ def test_walk_selection_windows_and_fallback(gpu):
 @pytest.mark.parametrize("n", [1, 1023, 1024, 1025, 5000, 12295])
 def test_short_selection_chunks_and_fallback(gpu, n):
     """Rows of at most 4 entries take the short-row walk under auto: one block
-    settles chunks of 1024 rows by rounds in LDS, with writers in the same
-    chunk, the previous one (LDS) and older ones (loaded a chunk ahead).  Hot
-    features make long chains inside a chunk; empty rows and ragged chunk
-    ends are included.  A row of 5 entries falls back to dataflow."""
+    settles 64-row sub-chunks in order, a wave taking several consecutive ones
+    per turn, by rounds of lane shuffles, with writers in the same sub-chunk,
+    the last 256 sub-chunks (an LDS ring) and older ones (loaded a turn of
+    every wave ahead).  Hot features make long chains inside a sub-chunk;
+    empty rows, ragged sub-chunks and ragged turns are included.  A row of 5
+    entries falls back to dataflow."""
     native = native_mod()
     rng = np.random.default_rng(n)
     rows = []
@@ -466,6 +468,34 @@ def test_short_selection_chunks_and_fallback(gpu, n):
     row_ptr, col = csr_from_rows(rows)
     _, info = check_schedule(native, gpu, row_ptr, col, max(d, 5), 6)
     assert info["method_used"] == 2
+
+
+@pytest.mark.parametrize("prefix_breaks", [True, False])
+def test_chain_check_prefix(gpu, prefix_breaks):
+    """The chain check reads a 65536-row prefix first.  Rows chain through
+    features c_i (row i holds c_i and c_i+1 and four rarely shared ones); a
+    break row drops c_i.  Breaks in every other row of the prefix only: the
+    prefix decides 'not chain-like' without reading the rest, so dataflow
+    runs although the whole input breaks in fewer than a quarter of its rows
+    (the walk's rule); breaks in every eighth row after the prefix only: the
+    full count decides, and the walk runs.  Every method is exact: levels equal the oracle's."""
+    native = native_mod()
+    rng = np.random.default_rng(17)
+    n, prefix = 200_000, 65_536
+    rows = []
+    extra = rng.integers(0, 1 << 22, size=(n, 4)) + (n + 2)
+    for i in range(n):
+        # every other row of the prefix, or every eighth row after it
+        brk = i > 0 and ((i < prefix and prefix_breaks and i % 2 == 1) or
+                         (i >= prefix and not prefix_breaks and i % 8 == 1))
+        r = {i + 1} | set(int(x) for x in extra[i])
+        if not brk:
+            r.add(i)
+        rows.append(r)
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1
+    _, info = check_schedule(native, gpu, row_ptr, col, d, 0)
+    assert info["method_used"] == (2 if prefix_breaks else 5)
 
 
 @pytest.mark.parametrize("seed", range(3))
