@@ -376,23 +376,28 @@ def run_dense(args):
     workload = "dense%d" % args.dense
     digest = source_digest(dense=True)
     got = w.cpu().numpy()
-    import oracle
+    if args.no_parity:
+        parity = None
+    else:
+        import oracle
 
-    t0 = time.perf_counter()
-    w0 = np.zeros(d, np.float32)
-    nat = oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.NATURAL, iters)
-    mat = oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.MATCHED, iters, rb, cb, 32)
-    tol = 1e-4 * float(np.abs(nat).max(initial=0.0)) + 1e-6
-    parity = {"scope": "whole workload", "levels_equal": None,
-              "max_abs_dw_natural": float(np.max(np.abs(got - nat), initial=0.0)),
-              "tol_natural": tol,
-              "bitwise_matched": bool(np.array_equal(got.view(np.int32), mat.view(np.int32))),
-              "oracle_s": time.perf_counter() - t0}
-    parity["ok"] = parity["bitwise_matched"] and parity["max_abs_dw_natural"] <= tol
+        t0 = time.perf_counter()
+        w0 = np.zeros(d, np.float32)
+        nat = oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.NATURAL, iters)
+        mat = oracle.dense_gd(g["X"], g["y"], w0, g["lr"], g["loss"], oracle.MATCHED, iters, rb,
+                              cb, 32)
+        tol = 1e-4 * float(np.abs(nat).max(initial=0.0)) + 1e-6
+        parity = {"scope": "whole workload", "levels_equal": None,
+                  "max_abs_dw_natural": float(np.max(np.abs(got - nat), initial=0.0)),
+                  "tol_natural": tol,
+                  "bitwise_matched": bool(np.array_equal(got.view(np.int32), mat.view(np.int32))),
+                  "oracle_s": time.perf_counter() - t0}
+        parity["ok"] = parity["bitwise_matched"] and parity["max_abs_dw_natural"] <= tol
+    ok = parity is not None and parity["ok"]
     peak = copy_peak(dev)
     out = {
         "metric": METRIC,
-        "value": n * d * iters * args.steps / elapsed if parity["ok"] else 0.0,
+        "value": n * d * iters * args.steps / elapsed if ok else 0.0,
         "unit": "nnz-updates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": elapsed * 1e3 / args.steps,
@@ -414,7 +419,9 @@ def run_dense(args):
                      "us_per_iteration": ms * 1e3 / max(iters, 1)},
         "epoch_ms": ms,
     }
-    if not parity["ok"]:
+    if parity is None:
+        out["invalid"] = "parity not checked (--no-parity): the value is not counted"
+    elif not parity["ok"]:
         out["invalid"] = "parity with the oracle failed: the value is not counted"
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = dense_cpu_baseline(g, args.cpu_budget)
