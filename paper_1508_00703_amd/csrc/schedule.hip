@@ -691,6 +691,16 @@ static_assert(kShortRing >= 2 * kShortWaves * short_per<2>() &&
                   kShortRing >= 2 * kShortWaves * short_per<kShortR>(),
               "loads of levels too recent");
 
+// an LDS word by its byte address, so that which word a lane reads can be
+// settled before the read, as plain data in a register
+typedef __attribute__((address_space(3))) int lds_i32;
+__device__ __forceinline__ int lds_addr(const int *p) {
+    return (int)(uintptr_t)(const lds_i32 *)p;
+}
+__device__ __forceinline__ int lds_read_i32(int a) {
+    return *(const lds_i32 *)(uintptr_t)(unsigned)a;
+}
+
 template <int R>
 struct ShortRow {
     int m;        // entries (R + 1 stands for more)
@@ -726,11 +736,12 @@ __global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *_
                                                                 Ctrl *ctrl, int64_t timeout) {
     constexpr int kShortPer = short_per<R>();
     __shared__ int s_ring[kShortRing][64];
-    __shared__ int s_done, s_stop;
+    __shared__ int s_done, s_stop, s_zero;
     const int lane = lane_id(), wave = wave_in_block();
     if (threadIdx.x == 0) {
         s_done = 0;
         s_stop = 0;
+        s_zero = 0;
     }
     __syncthreads();
     const int64_t nsub = (n + 63) / 64;
@@ -761,26 +772,42 @@ __global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *_
             return;
         }
         // before the wait, from the structure alone: each row's writers
-        // inside its sub-chunk (lane, -1 none) and the sub-chunk's depth,
-        // the most links on a chain of such writers -- the settling then
-        // runs exactly that many Jacobi rounds
-        int pin[kShortPer][R], depth[kShortPer];
+        // inside its sub-chunk (as a lane-shuffle address, and an increment
+        // that is 1 for a writer and far below any level for none) and the
+        // sub-chunk's depth, the most links on a chain of such writers -- the
+        // settling then runs exactly that many Jacobi rounds; also the LDS
+        // address of each writer's ring slot (a zero word when the writer is
+        // not in the ring window) and the largest level of older writers
+        int sha[kShortPer][R], inc[kShortPer][R], rad[kShortPer][R], old[kShortPer],
+            depth[kShortPer];
 #pragma unroll
         for (int j = 0; j < kShortPer; ++j) {
-            const int64_t r0 = 64 * (q0 + j);
+            const int64_t r0 = 64 * (q0 + j), ring0 = r0 - 64 * kShortRing;
+            int bk = 0;
 #pragma unroll
             for (int k = 0; k < R; ++k) {
-                const int p = cur[j].pr[k];
-                pin[j][k] = p >= r0 ? (int)(p - r0) : -1;
+                const int p = cur[j].pr[k];  // -1: no writer, or past the row's end
+                const bool in = p >= r0;
+                sha[j][k] = (in ? (int)(p - r0) : lane) * 4;
+                inc[j][k] = in ? 1 : -(1 << 30);
+                const bool ring = p >= 0 && p >= ring0 && p < r0;
+                rad[j][k] = ring ? lds_addr(&s_ring[(p >> 6) & (kShortRing - 1)][p & 63])
+                                 : lds_addr(&s_zero);
+                if (p >= 0 && p < ring0) bk = max(bk, cur[j].v[k]);
             }
+            old[j] = bk;
+            // computed now, while the wave waits, and kept: the compiler
+            // would otherwise redo the tests on the serial path after the wait
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+                __asm__ volatile("" : "+v"(rad[j][k]), "+v"(sha[j][k]), "+v"(inc[j][k]));
+            __asm__ volatile("" : "+v"(old[j]));
             int d = 0;
             for (;;) {
                 int nd = 0;
 #pragma unroll
-                for (int k = 0; k < R; ++k) {
-                    const int o = __shfl(d, pin[j][k] < 0 ? lane : pin[j][k]);
-                    if (pin[j][k] >= 0) nd = max(nd, o + 1);
-                }
+                for (int k = 0; k < R; ++k)
+                    nd = max(nd, __builtin_amdgcn_ds_bpermute(sha[j][k], d) + inc[j][k]);
                 const bool ch = nd != d;
                 d = nd;
                 if (__ballot(ch) == 0ull) break;
@@ -816,36 +843,20 @@ __global__ __launch_bounds__(kShortThreads) void k_levels_short(const int64_t *_
         for (int j = 0; j < kShortPer; ++j) {
             lvs[j] = 0;
             if (j >= nq) continue;
-            const ShortRow<R> &c = cur[j];
-            const int64_t r0 = 64 * (q0 + j), ring0 = r0 - 64 * kShortRing;
-            // every ring read issued at once (lanes without one read slot 0
-            // and ignore it), then the bounds folded in; sub-chunks settled
-            // earlier in this turn are in the ring already (one wave's LDS
-            // operations run in order)
-            int known = 0, rv[R];
-            bool in_ring[R];
+            // the ring reads (sub-chunks settled earlier in this turn are in
+            // the ring already: one wave's LDS operations run in order)
+            int known = old[j];
 #pragma unroll
-            for (int k = 0; k < R; ++k) {
-                const int p = c.pr[k];  // -1: no writer, or past the row's end
-                in_ring[k] = p >= 0 && p >= ring0 && p < r0;
-                rv[k] = s_ring[in_ring[k] ? (p >> 6) & (kShortRing - 1) : 0][in_ring[k] ? p & 63 : 0];
-            }
-#pragma unroll
-            for (int k = 0; k < R; ++k) {
-                const int p = c.pr[k];
-                if (p >= 0 && p < ring0) known = max(known, c.v[k]);
-                if (in_ring[k]) known = max(known, rv[k]);
-            }
+            for (int k = 0; k < R; ++k) known = max(known, lds_read_i32(rad[j][k]));
             // after r rounds every chain of at most r links inside the
             // sub-chunk has been followed: depth[j] rounds reach the fixed point
-            int lv = known + 1;
+            const int base = known + 1;
+            int lv = base;
             for (int round = 0; round < depth[j]; ++round) {
-                int nl = known + 1;
+                int nl = base;
 #pragma unroll
-                for (int k = 0; k < R; ++k) {
-                    const int o = __shfl(lv, pin[j][k] < 0 ? lane : pin[j][k]);
-                    if (pin[j][k] >= 0) nl = max(nl, o + 1);
-                }
+                for (int k = 0; k < R; ++k)
+                    nl = max(nl, __builtin_amdgcn_ds_bpermute(sha[j][k], lv) + inc[j][k]);
                 lv = nl;
             }
             s_ring[(q0 + j) & (kShortRing - 1)][lane] = lv;
