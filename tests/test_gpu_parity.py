@@ -438,20 +438,23 @@ def test_walk_selection_windows_and_fallback(gpu):
     assert info["method_used"] == 2
 
 
-@pytest.mark.parametrize("n", [1, 1023, 1024, 1025, 5000, 12295])
-def test_short_selection_chunks_and_fallback(gpu, n):
+@pytest.mark.parametrize("n,width", [(1, 4), (1023, 4), (1024, 4), (1025, 4), (5000, 4), (12295, 4),
+                                     (40000, 4), (40000, 2), (5000, 2)])
+def test_short_selection_chunks_and_fallback(gpu, n, width):
     """Rows of at most 4 entries take the short-row walk under auto: one block
     settles 64-row sub-chunks in order, a wave taking several consecutive ones
     per turn, by rounds of lane shuffles, with writers in the same sub-chunk,
     the last 256 sub-chunks (an LDS ring) and older ones (loaded a turn of
-    every wave ahead).  Hot features make long chains inside a sub-chunk;
+    every wave ahead; 40000 rows are 625 sub-chunks, and cold features recur
+    about 16000 rows apart).  Rows of at most 2 entries take the kernel's
+    two-writer form.  Hot features make long chains inside a sub-chunk;
     empty rows, ragged sub-chunks and ragged turns are included.  A row of 5
     entries falls back to dataflow."""
     native = native_mod()
-    rng = np.random.default_rng(n)
+    rng = np.random.default_rng(n + width)
     rows = []
     for i in range(n):
-        k = int(rng.integers(0, 5))                   # 0..4 entries
+        k = int(rng.integers(0, width + 1))           # 0..width entries
         r = set()
         for _ in range(k):
             u = rng.random()
