@@ -22,8 +22,10 @@
 // Runs of width-1 levels are a dependent chain: example t+1 reads what
 // example t wrote.  Runs of levels at most `chain_width` wide (default 4) go
 // the same way, their examples one after another in level order, which is a
-// sequential order of them (Theorem 2).  There one wave runs the chain and
-// the three other waves
+// sequential order of them (Theorem 2).  When every level is that narrow,
+// the whole epoch is one such run over the rows in plain index order, the
+// sequential order itself.  There one wave runs the chain and the three
+// other waves
 // of the block stage upcoming examples (columns, values, and the CSR index
 // of each entry's previous writer) into LDS.  Weights of features below
 // `hot` live in LDS for the whole run; a feature that example t just wrote is
@@ -62,8 +64,11 @@ struct SgdOp {
 
     __device__ __forceinline__ void operator()(int64_t e, int64_t end) const {
         (void)end;
+        row(perm[e]);
+    }
+    // example i (a row index), by one wave
+    __device__ __forceinline__ void row(int64_t i) const {
         const int lane = lane_id();
-        const int64_t i = perm[e];
         const int64_t b = row_ptr[i];
         const int m = (int)(row_ptr[i + 1] - b);
         const float yi = y[i];
@@ -621,9 +626,11 @@ __device__ int64_t chain_consumer(const SgdOp<LOSS, VAL> &op, int64_t len, int64
 // Runs perm[e_beg .. e_end) (consecutive narrow levels, in level order: a
 // sequential order of their examples) with the whole block.  width1: every
 // level of the run has one example, so the examples have increasing indices.
+// idx_r0 >= 0: the run is rows idx_r0, idx_r0 + 1, ... in index order
+// instead (perm is not read).
 template <int LOSS, bool VAL>
 __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_end, int hot,
-                          int64_t d, Ctrl *ctrl, bool width1, bool fast) {
+                          int64_t d, Ctrl *ctrl, bool width1, bool fast, int64_t idx_r0 = -1) {
     __shared__ ChainShared S;
     __shared__ int64_t s_done;
     const int wave = wave_in_block();
@@ -631,8 +638,11 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
     while (pos < e_end) {
         // examples of a width-1 run have increasing indices: the run is a range
         // of consecutive examples exactly when its ends differ by its length - 1
-        const int64_t r_first = op.perm[pos], r_last = op.perm[e_end - 1];
-        const int64_t dense_r0 = (width1 && r_last - r_first == e_end - 1 - pos) ? r_first : -1;
+        int64_t dense_r0 = idx_r0 + (pos - e_beg);
+        if (idx_r0 < 0) {
+            const int64_t r_first = op.perm[pos], r_last = op.perm[e_end - 1];
+            dense_r0 = (width1 && r_last - r_first == e_end - 1 - pos) ? r_first : -1;
+        }
         for (int i = threadIdx.x; i < hot; i += kBlock) g_wcache[i] = op.w[i];
         for (int i = threadIdx.x; i < kRB; i += kBlock) S.seq[i] = INT_MIN;
         if (threadIdx.x < 4) {
@@ -661,7 +671,12 @@ __device__ void chain_run(const SgdOp<LOSS, VAL> &op, int64_t e_beg, int64_t e_e
         pos += s_done;
         if (pos < e_end) {
             // an example with more than 64 entries: plain path, then resume
-            if (wave == 0) op(pos, pos + 1);
+            if (wave == 0) {
+                if (idx_r0 >= 0)
+                    op.row(idx_r0 + (pos - e_beg));
+                else
+                    op(pos, pos + 1);
+            }
             __syncthreads();
             ++pos;
         }
@@ -727,11 +742,24 @@ __global__ __launch_bounds__(kBlock) void k_levels_apply(Op op, const int64_t *l
                                                          const int32_t *n_levels,
                                                          int64_t thin_max, int hot, int64_t d,
                                                          Ctrl *ctrl, int64_t timeout,
-                                                         int64_t chain_width) {
+                                                         int64_t chain_width, int index_order) {
     constexpr int U = Op::kUnits;
     const int64_t L = *n_levels;
     // the pipeline's select-free step, when k_pipe_decide found it exact
     const bool fast = __builtin_amdgcn_readfirstlane(ctrl->pipe_fast) != 0;
+    if constexpr (Op::kChain) {
+        // every level is narrow (one block): the epoch is one pipeline run
+        // over the rows in index order -- itself a sequential order of the
+        // levels (Theorem 2), so every weight sees the same updates in the
+        // same order -- with no entry matched against a window and no
+        // boundary between runs
+        if (index_order) {
+            chain_run(op, 0, level_ptr[L], hot, d, ctrl, true, fast, 0);
+            return;
+        }
+    } else {
+        (void)index_order;
+    }
     const int wave = wave_in_block();
     const bool single = gridDim.x == 1;
     const int64_t gw = (int64_t)blockIdx.x * kWavesPerBlock + wave;
@@ -923,18 +951,25 @@ int launch_levels(const Op &op, const pdb_levels *lv, int64_t d, bool chain_ok, 
         if (widest > 0) g = std::min<int64_t>(g, cdiv(widest, (int64_t)kWavesPerBlock * Op::kUnits));
         grid = (int)std::max<int64_t>(g, 1);
     }
+    // every level at most chain_width wide, and enough examples for the
+    // pipeline: one run over the rows in index order, on one block
+    const int index_order =
+        (Op::kChain && hot >= 0 && widest >= 1 && widest <= chain_width &&
+         n >= kChainMin) ? 1 : 0;
+    if (index_order) grid = 1;
     Op o = op;
     const int64_t *level_ptr = lv->level_ptr;
     const int32_t *n_levels = lv->n_levels;
     if (grid == 1) {
         k_levels_apply<Op><<<1, kBlock, lds, s>>>(o, level_ptr, n_levels, thin, hot, d, ctrl,
-                                                  timeout, chain_width);
+                                                  timeout, chain_width, index_order);
         PDB_LAUNCHED();
     } else {
         int64_t thin_arg = thin, to = timeout, cw = chain_width;
         int hot_arg = hot;
         int64_t d_arg = d;
-        void *args[] = {&o, &level_ptr, &n_levels, &thin_arg, &hot_arg, &d_arg, &ctrl, &to, &cw};
+        int io = index_order;
+        void *args[] = {&o, &level_ptr, &n_levels, &thin_arg, &hot_arg, &d_arg, &ctrl, &to, &cw, &io};
         PDB_HIP(hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBlock), args, lds, s));
     }
     return PDB_OK;

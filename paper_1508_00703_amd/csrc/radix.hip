@@ -2,7 +2,8 @@
 // hand-written for gfx950 (wave64).  Used to build per-feature occurrence
 // lists (sort stored entries by feature) and to group examples by level.
 //
-// One pass over d-bit digits (d <= 8):
+// The key bits go in as few passes as 8-bit digits need, spread evenly over
+// them (21 bits: three 7-bit digits).  One pass over d-bit digits (d <= 8):
 //   1. histogram: each 4096-element tile counts its digits in LDS
 //      (per-wave private counters), writes counts digit-major;
 //   2. exclusive prefix sum over the digit-major table gives, for every
@@ -235,8 +236,13 @@ hipError_t radix_sort_pairs(const uint32_t *keys_in, const uint32_t *vals_in, in
     const int64_t ntiles = cdiv(count, kTile);
     const uint32_t *ck = keys_in, *cv = vals_in;
     uint32_t *dk = kA, *dv = vA;
-    for (int shift = lo_bit; shift < bits; shift += 8) {
-        const int nb = bits - shift < 8 ? bits - shift : 8;
+    // as few passes as 8-bit digits need, with the bits spread evenly over
+    // them: fewer digits per pass make each tile's runs of one digit longer,
+    // so its writes cover whole cache lines more often
+    const int passes = (bits - lo_bit + 7) / 8;
+    const int step = (bits - lo_bit + passes - 1) / passes;
+    for (int shift = lo_bit; shift < bits; shift += step) {
+        const int nb = bits - shift < step ? bits - shift : step;
         k_radix_hist<<<(unsigned)ntiles, kBlock, 0, s>>>(ck, count, shift, nb, hist, ntiles);
         hipError_t e = exclusive_scan_u32(hist, hist, (int64_t)(1 << nb) * ntiles, scan_tmp, s);
         if (e != hipSuccess) return e;
