@@ -275,6 +275,40 @@ def test_plain_path_matches_pipeline(gpu):
     assert np.array_equal(a.view(np.int32), b.view(np.int32))
 
 
+def test_pipeline_index_order_when_every_level_is_narrow(gpu):
+    """Config 1 (levels 1-3 wide, level order not index order): with every
+    level at most pipeline_width wide the epoch is one pipeline run over the
+    rows in index order (the control block counts one run of n rows), and the
+    weights are bitwise the matched oracle's; with pipeline_width 1 the same
+    levels run as width-1 and narrow runs in level order, to the same bits
+    (Theorem 2: both orders give every weight the same updates in the same
+    order)."""
+    import torch
+
+    native = native_mod()
+    g = datagen.generate(1)
+    lv, _ = check_schedule(native, gpu, g["row_ptr"], g["col"], g["d"], 0)
+    perm = lv.perm.cpu().numpy()
+    assert not np.array_equal(perm, np.arange(g["n"]))      # level order is not index order
+    assert 2 <= lv.max_width_host <= 4
+    ref = oracle.sgd_epoch(g["row_ptr"], g["col"], g["val"], g["y"], np.zeros(g["d"], np.float32),
+                           g["lr"], g["loss"], oracle.MATCHED)
+    csr = native.Csr.from_numpy(g["row_ptr"], g["col"], g["val"], gpu)
+    y = torch.from_numpy(g["y"]).to(gpu)
+    runs = {}
+    for width in (4, 1):
+        w = torch.zeros(g["d"], dtype=torch.float32, device=gpu)
+        ws = native.pdb_sgd_epoch(csr, y, g["n"], g["d"], w, float(g["lr"]), g["loss"], lv,
+                                  opt=dict(epoch_mode=native.PDB_EPOCH_LEVELS, pipeline_width=width))
+        torch.cuda.synchronize()
+        assert np.array_equal(w.cpu().numpy().view(np.int32), ref.view(np.int32)), width
+        # control block: examples run and runs started by the pipeline (int64 8 and 9)
+        st = ws[:512].cpu().numpy().view(np.int64)
+        runs[width] = (int(st[8]), int(st[9]))
+    assert runs[4] == (g["n"], 1)
+    assert runs[1][1] > 1
+
+
 @pytest.mark.parametrize("hot", [0, 40, -1])
 @pytest.mark.parametrize("with_val", [True, False])
 def test_width1_pipeline_long_rows(gpu, hot, with_val):
