@@ -87,7 +87,10 @@ typedef enum pdb_sched_method {
                                 dataflow runs.  Auto tries this first. */
     PDB_SCHED_WALK = 5,      /* one block walks the rows in order, windows of rows staged in
                                 LDS; dataflow runs instead when a row holds more than 16384
-                                entries */
+                                entries.  Under auto, when the rows form at most one run per
+                                512 rows (a run: rows that each share a feature with the row
+                                before) and n >= 65536, a grid settles the runs one after
+                                another instead, each by a prefix maximum over its rows */
     PDB_SCHED_SHORT = 6      /* short rows (matrix completion): one block settles sub-chunks of
                                 64 consecutive rows strictly in order, the waves taking turns of
                                 several consecutive sub-chunks, each sub-chunk by as many rounds

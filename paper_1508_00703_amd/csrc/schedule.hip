@@ -1089,6 +1089,163 @@ __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__r
     }
 }
 
+// ---- K3 walk over few runs ---------------------------------------------------
+// When a chain-like input has few runs (a run: rows each of which has the row
+// before it as a previous writer), a grid settles the runs one after another
+// instead of one block walking every window.  With M_t the largest level
+// among row t's writers before the run's first row a (0 if none), the walk's
+// prefix maximum gives level(j) = j + 1 + max over a <= t <= j of (M_t - t):
+// writers inside the run never decide a level, since levels rise by one at
+// least along it.  Each block owns a stretch of every run's rows.  A run
+// takes two steps, each ended by a device barrier:
+//   (1) every entry of the run whose writer lies before the run raises M of
+//       its row (atomic maximum).  A writer in the run just settled has no
+//       final level yet (its block writes it in this same step): its level
+//       is formed from that run's staged prefix maxima and stretch maxima;
+//   (2) each block scans its stretch: prefix maxima of M_t - t, staged, and
+//       the stretch's maximum published.
+// After (2) every block forms the maxima of the stretches before each
+// stretch; its levels are written in the next run's step (1).
+constexpr int kRunThreads = 1024;
+constexpr int kRunBlocks = 16;
+constexpr int64_t kRunRowsPer = 512;  // at most one run per this many rows
+constexpr int64_t kRunMinN = 65536;
+
+// flag[i] = 1 when row i starts a run (no entry's previous writer in row i - 1)
+__global__ __launch_bounds__(kBlock) void k_run_flags(const int64_t *__restrict__ row_ptr, int64_t n,
+                                                      const int32_t *__restrict__ pn,
+                                                      uint32_t *__restrict__ flag) {
+    const int lane = lane_id();
+    const int64_t nw = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t i = blockIdx.x * (int64_t)(kBlock / kWave) + wave_in_block(); i < n; i += nw) {
+        bool found = false;
+        if (i > 0) {
+            const int64_t lo = row_ptr[i - 1], b = row_ptr[i], e = row_ptr[i + 1];
+            for (int64_t p = b + lane; p < e && !found; p += kWave) found = pn[p] >= lo;
+        }
+        const bool cont = __ballot(found) != 0ull;
+        if (lane == 0) flag[i] = cont ? 0u : 1u;
+    }
+}
+
+// starts[r] = first row of run r (pos: the exclusive scan of the flags, R runs),
+// starts[R] = n
+__global__ __launch_bounds__(kBlock) void k_run_starts(const uint32_t *__restrict__ pos, int64_t n,
+                                                       int64_t R, int32_t *__restrict__ starts) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t next = i + 1 < n ? (int64_t)pos[i + 1] : R;
+        if (next > (int64_t)pos[i]) starts[pos[i]] = (int32_t)i;
+        if (i == n - 1) starts[R] = (int32_t)n;
+    }
+}
+
+// Device barrier on an arrival counter that only grows (target: blocks times
+// barriers so far); the host clears it afterwards.  The abort flag and the
+// watchdog are read every 16th poll.
+__device__ __forceinline__ bool runs_barrier(Ctrl *c, unsigned target, int64_t timeout) {
+    __shared__ int ok_s;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int ok = 1;
+        __hip_atomic_fetch_add(&c->bar_count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        const int64_t t0 = now_ticks();
+        for (int it = 1;
+             __hip_atomic_load(&c->bar_count, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target;
+             ++it) {
+            if ((it & 15) == 0) {
+                if (aborted(c)) {
+                    ok = 0;
+                    break;
+                }
+                if (now_ticks() - t0 > timeout) {
+                    record_error(c, DERR_BARRIER_TIMEOUT);
+                    ok = 0;
+                    break;
+                }
+            }
+        }
+        ok_s = ok;
+    }
+    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return ok_s != 0;
+}
+
+__global__ __launch_bounds__(kRunThreads) void k_levels_runs(
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ prow,
+    const int32_t *__restrict__ row_idx, int64_t R, const int32_t *__restrict__ starts,
+    int32_t *M, int32_t *stg, int32_t *level, int32_t *bmax, Ctrl *ctrl, int64_t timeout) {
+    constexpr int kNone = INT_MIN / 2;
+    __shared__ int s_w[kRunThreads / kWave];
+    __shared__ int s_pre[kWave];  // the run just settled: max of the stretch maxima before each
+    const int tid = threadIdx.x, lane = lane_id(), wave = wave_in_block();
+    const int G = (int)gridDim.x, j = (int)blockIdx.x;
+    const int64_t gt = (int64_t)j * kRunThreads + tid, gn = (int64_t)G * kRunThreads;
+    unsigned target = 0;
+    int64_t pa = 0, ps = 1, plo = 0, phi = 0;  // the run just settled, its span, this block's stretch
+    for (int64_t k = 0; k <= R; ++k) {
+        // (1) levels of this block's stretch of the run just settled, and M
+        // of the next run's rows
+        if (k > 0) {
+            const int before = s_pre[j];
+            for (int64_t t = plo + tid; t < phi; t += kRunThreads)
+                level[t] = (int)t + 1 + max(before, stg[t]);
+        }
+        if (k == R) break;
+        const int64_t a = starts[k], b = starts[k + 1];
+        const int64_t e1 = row_ptr[b];
+        for (int64_t p = row_ptr[a] + gt; p < e1; p += gn) {
+            const int32_t w = prow[p];
+            if (w >= 0 && w < a) {
+                int lw;
+                if (k > 0 && w >= pa)
+                    lw = w + 1 + max(s_pre[(int)((w - pa) / ps)], stg[w]);
+                else
+                    lw = level[w];
+                atomicMax(&M[row_idx[p]], lw);
+            }
+        }
+        target += (unsigned)G;
+        if (!runs_barrier(ctrl, target, timeout)) return;
+        // (2) this block's stretch: prefix maxima of M_t - t
+        const int64_t span = (b - a + G - 1) / G;
+        const int64_t lo = min(b, a + (int64_t)j * span), hi = min(b, lo + span);
+        int carry = kNone;
+        for (int64_t c0 = lo; c0 < hi; c0 += kRunThreads) {
+            const int64_t t = c0 + tid;
+            int pm = wave_prefix_max(t < hi ? M[t] - (int)t : kNone);
+            if (lane == kWave - 1) s_w[wave] = pm;
+            __syncthreads();
+            int before = carry, all = carry;
+#pragma unroll
+            for (int w2 = 0; w2 < kRunThreads / kWave; ++w2) {
+                if (w2 < wave) before = max(before, s_w[w2]);
+                all = max(all, s_w[w2]);
+            }
+            if (t < hi) stg[t] = max(pm, before);
+            __syncthreads();
+            carry = all;
+        }
+        if (tid == 0) bmax[(k & 1) * kWave + j] = carry;
+        target += (unsigned)G;
+        if (!runs_barrier(ctrl, target, timeout)) return;
+        // the maxima of the stretches before each stretch of this run
+        if (wave == 0) {
+            const int v = lane < G ? bmax[(k & 1) * kWave + lane] : kNone;
+            const int incl = wave_prefix_max(v);
+            const int excl = __shfl_up(incl, 1);
+            s_pre[lane] = lane == 0 ? kNone : excl;
+        }
+        __syncthreads();
+        pa = a;
+        ps = span;
+        plo = lo;
+        phi = hi;
+    }
+}
+
 // ---- K3 spine --------------------------------------------------------------
 // When one feature f* is held by all rows but a few (the exceptional rows E),
 // the rows holding it form a spine c_0 < c_1 < ... < c_{K-1}.  Consecutive
@@ -1838,12 +1995,51 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
                                                                         w.cand);
             PDB_LAUNCHED();
         }
-        k_levels_walk<<<1, kWalkThreads, 0, s>>>(csr->row_ptr, n, w.cand, w.row_idx, lv->level,
-                                                 w.ctrl);
-        PDB_LAUNCHED();
-        rc = read_ctrl(w.ctrl, &host, s);
-        if (rc != PDB_OK) return rc;
-        if (host.bad) use = PDB_SCHED_DATAFLOW;  // a row longer than a window
+        // the number of runs is known exactly when the chain check counted
+        // every break; few runs: the grid settles them one after another
+        const int64_t R = (int64_t)host.chain_breaks + 1;
+        if (chain_checked && n >= kRunMinN && R * kRunRowsPer <= n && n <= INT_MAX) {
+            uint32_t *pos = reinterpret_cast<uint32_t *>(free_k);
+            int32_t *M = reinterpret_cast<int32_t *>((sv == w.vA) ? w.vB : w.vA);
+            int32_t *stg = reinterpret_cast<int32_t *>(pos);  // the scan is spent by then
+            int32_t *starts = lv->perm;  // R + 1 run starts, then 2 x 64 stretch maxima
+            int32_t *bmax = lv->perm + R + 1;
+            k_run_flags<<<grid_for(n, kBlock / kWave, 65536), kBlock, 0, s>>>(csr->row_ptr, n, pn,
+                                                                              pos);
+            PDB_HIP(exclusive_scan_u32(pos, pos, n, w.scan_tmp, s));
+            k_run_starts<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(pos, n, R, starts);
+            k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(M, n, 0);
+            PDB_LAUNCHED();
+            int dev = 0, cus = 0;
+            PDB_HIP(hipGetDevice(&dev));
+            PDB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+            const void *fn = reinterpret_cast<const void *>(&k_levels_runs);
+            int per_cu = 0;
+            PDB_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kRunThreads, 0));
+            const int grid = std::max(1, std::min(kRunBlocks, cus * std::max(per_cu, 1)));
+            const int64_t *rp = csr->row_ptr;
+            const int32_t *prow = w.cand, *ridx = w.row_idx;
+            const int32_t *st = starts;
+            int32_t *lvl = lv->level;
+            Ctrl *ctrl = w.ctrl;
+            int64_t Rv = R, to = timeout;
+            void *args[] = {&rp, &prow, &ridx, &Rv, &st, &M, &stg, &lvl, &bmax, &ctrl, &to};
+            PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kRunThreads), args, 0,
+                                               s));
+            // the barrier's arrival counter back to zero for later grid barriers
+            k_fill_i32<<<1, 64, 0, s>>>(reinterpret_cast<int32_t *>(&w.ctrl->bar_count), 1, 0);
+            PDB_LAUNCHED();
+            rc = read_ctrl(w.ctrl, &host, s);
+            if (rc != PDB_OK) return rc;
+            if (host.err) return PDB_ERR_DEVICE;  // a barrier's wait gave up
+        } else {
+            k_levels_walk<<<1, kWalkThreads, 0, s>>>(csr->row_ptr, n, w.cand, w.row_idx,
+                                                     lv->level, w.ctrl);
+            PDB_LAUNCHED();
+            rc = read_ctrl(w.ctrl, &host, s);
+            if (rc != PDB_OK) return rc;
+            if (host.bad) use = PDB_SCHED_DATAFLOW;  // a row longer than a window
+        }
     }
 
     if (use == PDB_SCHED_SHORT) {

@@ -472,6 +472,29 @@ def test_walk_selection_windows_and_fallback(gpu):
     assert info["method_used"] == 2
 
 
+@pytest.mark.parametrize("run_len", [700, 300])
+def test_walk_few_runs(gpu, run_len):
+    """Chain-like rows in runs (features 0 and 1 take turns every run_len
+    rows, so no feature covers nearly all rows and the spine does not apply)
+    with cold features whose previous writers lie many runs back.  With at
+    most one run per 512 rows (run_len 700) auto settles the runs one after
+    another over a grid; with more (run_len 300) it walks windows of rows.
+    Levels equal the oracle's either way."""
+    native = native_mod()
+    rng = np.random.default_rng(run_len)
+    n = 100_000
+    rows = []
+    for i in range(n):
+        r = {(i // run_len) % 2}
+        r |= {10 + int(x) for x in rng.integers(0, 20000, size=rng.integers(0, 6))}
+        rows.append(r)
+    row_ptr, col = csr_from_rows(rows)
+    d = int(col.max()) + 1
+    for method in (0, 5):
+        _, info = check_schedule(native, gpu, row_ptr, col, d, method)
+        assert info["method_used"] == 5
+
+
 @pytest.mark.parametrize("n,width", [(1, 4), (1023, 4), (1024, 4), (1025, 4), (5000, 4), (12295, 4),
                                      (40000, 4), (40000, 2), (5000, 2)])
 def test_short_selection_chunks_and_fallback(gpu, n, width):
