@@ -633,8 +633,10 @@ __global__ __launch_bounds__(kBlock) void k_levels_rowwave(const int64_t *__rest
                 if (__ballot(!(r0 && r1)) == 0ull) break;
                 if (round == 0) t0 = now_ticks();
                 // the abort flag (a device-scope load) and the watchdog
-                // every 8 rounds, a short back-off every round
-                if ((round & 7) == 7) {
+                // every 64 rounds (a waiter reading the flag when its
+                // writer's level lands sees it a load later; every 8 rounds
+                // cost config 4 0.5 ms), a short back-off every round
+                if ((round & 63) == 63) {
                     if (aborted(ctrl)) return;
                     if (now_ticks() - t0 > timeout) {
                         record_error(ctrl, DERR_WAIT_TIMEOUT);
