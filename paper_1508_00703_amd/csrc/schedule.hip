@@ -1143,8 +1143,8 @@ __global__ __launch_bounds__(kBlock) void k_run_starts(const uint32_t *__restric
 }
 
 // Device barrier on an arrival counter that only grows (target: blocks times
-// barriers so far); the host clears it afterwards.  The abort flag and the
-// watchdog are read every 16th poll.
+// barriers so far); the host clears it afterwards.  The watchdog is read
+// after the first poll and every 16th after it, the abort flag every 16th.
 __device__ __forceinline__ bool runs_barrier(Ctrl *c, unsigned target, int64_t timeout) {
     __shared__ int ok_s;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -1156,16 +1156,14 @@ __device__ __forceinline__ bool runs_barrier(Ctrl *c, unsigned target, int64_t t
         for (int it = 1;
              __hip_atomic_load(&c->bar_count, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target;
              ++it) {
-            if ((it & 15) == 0) {
-                if (aborted(c)) {
-                    ok = 0;
-                    break;
-                }
-                if (now_ticks() - t0 > timeout) {
-                    record_error(c, DERR_BARRIER_TIMEOUT);
-                    ok = 0;
-                    break;
-                }
+            if ((it & 15) == 1 && now_ticks() - t0 > timeout) {
+                record_error(c, DERR_BARRIER_TIMEOUT);
+                ok = 0;
+                break;
+            }
+            if ((it & 15) == 0 && aborted(c)) {
+                ok = 0;
+                break;
             }
         }
         ok_s = ok;

@@ -228,14 +228,29 @@ def test_zero_watchdog_level_barriers(gpu):
     check_sgd(native, gpu, g, lv, opt=dict(epoch_mode=native.PDB_EPOCH_LEVELS))
 
 
-@pytest.mark.parametrize("method", [2, 6])  # dataflow, short-row walk
+def few_runs_input(n=100_000, run_len=700, seed=700):
+    """Chain-like rows in runs of run_len (features 0 and 1 take turns) with
+    cold features: auto settles it as few runs over a grid."""
+    rng = np.random.default_rng(seed)
+    rows = [{(i // run_len) % 2} | {10 + int(x) for x in rng.integers(0, 20000, size=rng.integers(0, 6))}
+            for i in range(n)]
+    row_ptr = np.zeros(n + 1, np.int64)
+    row_ptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.array([c for r in rows for c in sorted(r)], np.int32)
+    return dict(row_ptr=row_ptr, col=col, d=int(col.max()) + 1)
+
+
+@pytest.mark.parametrize("method", [2, 6, 0])  # dataflow, short-row walk, auto on few runs
 def test_zero_watchdog_schedule(gpu, method):
-    """pdb_schedule whose level kernel waits on device: a zero watchdog makes
+    """pdb_schedule whose level kernel waits on device (dataflow, the
+    short-row walk, the grid's barriers between runs): a zero watchdog makes
     the call return PDB_ERR_DEVICE (no levels are bucketed); the next call
     succeeds."""
     native = native_mod()
     if method == 6:
         g = datagen.generate_mf(5, n=300_000, n_users=15_000, n_items=3_000)
+    elif method == 0:
+        g = few_runs_input()
     else:
         g = datagen.generate(4, **SCALED[4])
     with pytest.raises(native.PdbError) as e:
