@@ -131,7 +131,9 @@ typedef struct pdb_options {
     int32_t epoch_mode;            /* pdb_epoch_mode (default PDB_EPOCH_AUTO) */
     int32_t pipeline;              /* level-by-level epoch: 1 runs of narrow levels go through the
                                       one-block pipeline (default), 0 every level on the plain path */
-    int32_t pipeline_width;        /* widest level a pipeline run may include (>= 1, default 4) */
+    int32_t pipeline_width;        /* widest level a pipeline run may include (>= 1, default 4);
+                                      when no level is wider, the whole epoch is one pipeline run
+                                      over the examples in index order (the same result) */
     int32_t thin_max;              /* widest level run by one block alone (>= 1, default 16) */
     int64_t hot_features;          /* cap on the weights the pipeline caches in LDS; -1 (default)
                                       all that fit */
