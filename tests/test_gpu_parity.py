@@ -479,7 +479,8 @@ def test_walk_few_runs(gpu, run_len):
     with cold features whose previous writers lie many runs back.  With at
     most one run per 512 rows (run_len 700) auto settles the runs one after
     another over a grid; with more (run_len 300) it walks windows of rows.
-    Levels equal the oracle's either way."""
+    Empty rows make runs of a single row.  Levels equal the oracle's either
+    way."""
     native = native_mod()
     rng = np.random.default_rng(run_len)
     n = 100_000
@@ -488,6 +489,10 @@ def test_walk_few_runs(gpu, run_len):
         r = {(i // run_len) % 2}
         r |= {10 + int(x) for x in rng.integers(0, 20000, size=rng.integers(0, 6))}
         rows.append(r)
+    # 20 empty rows: runs of one row each (shorter than the grid's blocks),
+    # and the rows after them start runs too
+    for i in range(1234, n, 4999):
+        rows[i] = set()
     row_ptr, col = csr_from_rows(rows)
     d = int(col.max()) + 1
     for method in (0, 5):
