@@ -494,6 +494,12 @@ __device__ __forceinline__ void chain_step(ChainState &st, const SgdOp<LOSS, VAL
     __builtin_amdgcn_sched_group_barrier(0x0080, 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x0010, 2, 0);
+    if constexpr (VAL) {
+        // stored values: the slot's two reads fill the wait before the first
+        // cross-row add instead of delaying the last row add
+        __builtin_amdgcn_sched_group_barrier(0x0002, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0080, 2, 0);
+    }
     __builtin_amdgcn_sched_barrier(0);
     // (d) the step runs on every lane and is read out of lane 63.  The
     // rotation's selects sit between the exponential and the reciprocal,
