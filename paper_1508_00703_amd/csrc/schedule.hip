@@ -1098,20 +1098,20 @@ __global__ __launch_bounds__(kWalkThreads) void k_levels_walk(const int64_t *__r
 // among row t's writers before the run's first row a (0 if none), the walk's
 // prefix maximum gives level(j) = j + 1 + max over a <= t <= j of (M_t - t):
 // writers inside the run never decide a level, since levels rise by one at
-// least along it.  Each block owns a stretch of every run's rows.  A run
-// takes two steps, each ended by a device barrier:
-//   (1) every entry of the run whose writer lies before the run raises M of
-//       its row (atomic maximum).  A writer in the run just settled has no
-//       final level yet (its block writes it in this same step): its level
-//       is formed from that run's staged prefix maxima and stretch maxima;
-//   (2) each block scans its stretch: prefix maxima of M_t - t, staged, and
-//       the stretch's maximum published.
-// After (2) every block forms the maxima of the stretches before each
-// stretch; its levels are written in the next run's step (1).
+// least along it.  Each block owns a stretch of every run's rows, and a run
+// takes one device barrier: each block raises M of its stretch's rows from
+// their entries whose writer lies before the run (atomic maxima in LDS,
+// 8192 rows at a time), scans the stretch -- prefix maxima of M_t - t,
+// staged -- and publishes the stretch's maximum.  After the barrier every
+// block forms the maxima of the stretches before each stretch; its levels
+// are written at the start of the next run, whose gathers therefore form
+// the level of a writer in the run just settled from that run's staged
+// prefix maxima and stretch maxima.
 constexpr int kRunThreads = 1024;
 constexpr int kRunBlocks = 16;
 constexpr int64_t kRunRowsPer = 512;  // at most one run per this many rows
 constexpr int64_t kRunMinN = 65536;
+constexpr int kRunChunk = 8192;  // rows whose M one block gathers in LDS at a time
 
 // flag[i] = 1 when row i starts a run (no entry's previous writer in row i - 1)
 __global__ __launch_bounds__(kBlock) void k_run_flags(const int64_t *__restrict__ row_ptr, int64_t n,
@@ -1176,18 +1176,17 @@ __device__ __forceinline__ bool runs_barrier(Ctrl *c, unsigned target, int64_t t
 __global__ __launch_bounds__(kRunThreads) void k_levels_runs(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ prow,
     const int32_t *__restrict__ row_idx, int64_t R, const int32_t *__restrict__ starts,
-    int32_t *M, int32_t *stg, int32_t *level, int32_t *bmax, Ctrl *ctrl, int64_t timeout) {
+    int32_t *stg, int32_t *level, int32_t *bmax, Ctrl *ctrl, int64_t timeout) {
     constexpr int kNone = INT_MIN / 2;
+    __shared__ int s_m[kRunChunk];  // M_t of a chunk of this block's stretch
     __shared__ int s_w[kRunThreads / kWave];
     __shared__ int s_pre[kWave];  // the run just settled: max of the stretch maxima before each
     const int tid = threadIdx.x, lane = lane_id(), wave = wave_in_block();
     const int G = (int)gridDim.x, j = (int)blockIdx.x;
-    const int64_t gt = (int64_t)j * kRunThreads + tid, gn = (int64_t)G * kRunThreads;
     unsigned target = 0;
     int64_t pa = 0, ps = 1, plo = 0, phi = 0;  // the run just settled, its span, this block's stretch
     for (int64_t k = 0; k <= R; ++k) {
-        // (1) levels of this block's stretch of the run just settled, and M
-        // of the next run's rows
+        // levels of this block's stretch of the run just settled
         if (k > 0) {
             const int before = s_pre[j];
             for (int64_t t = plo + tid; t < phi; t += kRunThreads)
@@ -1195,38 +1194,44 @@ __global__ __launch_bounds__(kRunThreads) void k_levels_runs(
         }
         if (k == R) break;
         const int64_t a = starts[k], b = starts[k + 1];
-        const int64_t e1 = row_ptr[b];
-        for (int64_t p = row_ptr[a] + gt; p < e1; p += gn) {
-            const int32_t w = prow[p];
-            if (w >= 0 && w < a) {
-                int lw;
-                if (k > 0 && w >= pa)
-                    lw = w + 1 + max(s_pre[(int)((w - pa) / ps)], stg[w]);
-                else
-                    lw = level[w];
-                atomicMax(&M[row_idx[p]], lw);
-            }
-        }
-        target += (unsigned)G;
-        if (!runs_barrier(ctrl, target, timeout)) return;
-        // (2) this block's stretch: prefix maxima of M_t - t
         const int64_t span = (b - a + G - 1) / G;
         const int64_t lo = min(b, a + (int64_t)j * span), hi = min(b, lo + span);
+        // this block's stretch, in chunks of rows: M_t from the writers before
+        // the run (their levels are final, or formed from the run just
+        // settled), then prefix maxima of M_t - t, staged
         int carry = kNone;
-        for (int64_t c0 = lo; c0 < hi; c0 += kRunThreads) {
-            const int64_t t = c0 + tid;
-            int pm = wave_prefix_max(t < hi ? M[t] - (int)t : kNone);
-            if (lane == kWave - 1) s_w[wave] = pm;
+        for (int64_t c0 = lo; c0 < hi; c0 += kRunChunk) {
+            const int64_t c1 = min(hi, c0 + (int64_t)kRunChunk);
+            for (int i = tid; i < (int)(c1 - c0); i += kRunThreads) s_m[i] = 0;
             __syncthreads();
-            int before = carry, all = carry;
-#pragma unroll
-            for (int w2 = 0; w2 < kRunThreads / kWave; ++w2) {
-                if (w2 < wave) before = max(before, s_w[w2]);
-                all = max(all, s_w[w2]);
+            const int64_t e1 = row_ptr[c1];
+            for (int64_t p = row_ptr[c0] + tid; p < e1; p += kRunThreads) {
+                const int32_t w = prow[p];
+                if (w >= 0 && w < a) {
+                    int lw;
+                    if (k > 0 && w >= pa)
+                        lw = w + 1 + max(s_pre[(int)((w - pa) / ps)], stg[w]);
+                    else
+                        lw = level[w];
+                    atomicMax(&s_m[row_idx[p] - (int)c0], lw);
+                }
             }
-            if (t < hi) stg[t] = max(pm, before);
             __syncthreads();
-            carry = all;
+            for (int64_t s0 = c0; s0 < c1; s0 += kRunThreads) {
+                const int64_t t = s0 + tid;
+                int pm = wave_prefix_max(t < c1 ? s_m[t - c0] - (int)t : kNone);
+                if (lane == kWave - 1) s_w[wave] = pm;
+                __syncthreads();
+                int before = carry, all = carry;
+#pragma unroll
+                for (int w2 = 0; w2 < kRunThreads / kWave; ++w2) {
+                    if (w2 < wave) before = max(before, s_w[w2]);
+                    all = max(all, s_w[w2]);
+                }
+                if (t < c1) stg[t] = max(pm, before);
+                __syncthreads();
+                carry = all;
+            }
         }
         if (tid == 0) bmax[(k & 1) * kWave + j] = carry;
         target += (unsigned)G;
@@ -2000,7 +2005,6 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
         const int64_t R = (int64_t)host.chain_breaks + 1;
         if (chain_checked && n >= kRunMinN && R * kRunRowsPer <= n && n <= INT_MAX) {
             uint32_t *pos = reinterpret_cast<uint32_t *>(free_k);
-            int32_t *M = reinterpret_cast<int32_t *>((sv == w.vA) ? w.vB : w.vA);
             int32_t *stg = reinterpret_cast<int32_t *>(pos);  // the scan is spent by then
             int32_t *starts = lv->perm;  // R + 1 run starts, then 2 x 64 stretch maxima
             int32_t *bmax = lv->perm + R + 1;
@@ -2008,7 +2012,6 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
                                                                               pos);
             PDB_HIP(exclusive_scan_u32(pos, pos, n, w.scan_tmp, s));
             k_run_starts<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(pos, n, R, starts);
-            k_fill_i32<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(M, n, 0);
             PDB_LAUNCHED();
             int dev = 0, cus = 0;
             PDB_HIP(hipGetDevice(&dev));
@@ -2023,7 +2026,7 @@ extern "C" int pdb_schedule(const pdb_csr *csr, const float *labels, int64_t n, 
             int32_t *lvl = lv->level;
             Ctrl *ctrl = w.ctrl;
             int64_t Rv = R, to = timeout;
-            void *args[] = {&rp, &prow, &ridx, &Rv, &st, &M, &stg, &lvl, &bmax, &ctrl, &to};
+            void *args[] = {&rp, &prow, &ridx, &Rv, &st, &stg, &lvl, &bmax, &ctrl, &to};
             PDB_HIP(hipLaunchCooperativeKernel(fn, dim3((unsigned)grid), dim3(kRunThreads), args, 0,
                                                s));
             // the barrier's arrival counter back to zero for later grid barriers
