@@ -1112,6 +1112,7 @@ constexpr int kRunBlocks = 16;
 constexpr int64_t kRunRowsPer = 512;  // at most one run per this many rows
 constexpr int64_t kRunMinN = 65536;
 constexpr int kRunChunk = 8192;  // rows whose M one block gathers in LDS at a time
+constexpr int kRunPer = 8;       // entries a thread gathers at a time
 
 // flag[i] = 1 when row i starts a run (no entry's previous writer in row i - 1)
 __global__ __launch_bounds__(kBlock) void k_run_flags(const int64_t *__restrict__ row_ptr, int64_t n,
@@ -1204,16 +1205,35 @@ __global__ __launch_bounds__(kRunThreads) void k_levels_runs(
             const int64_t c1 = min(hi, c0 + (int64_t)kRunChunk);
             for (int i = tid; i < (int)(c1 - c0); i += kRunThreads) s_m[i] = 0;
             __syncthreads();
+            // kRunPer entries a thread at a time, every load issued before
+            // the first is used (the writers' level and staged value both
+            // loaded, from row 0 when there is no writer before the run)
             const int64_t e1 = row_ptr[c1];
-            for (int64_t p = row_ptr[c0] + tid; p < e1; p += kRunThreads) {
-                const int32_t w = prow[p];
-                if (w >= 0 && w < a) {
-                    int lw;
-                    if (k > 0 && w >= pa)
-                        lw = w + 1 + max(s_pre[(int)((w - pa) / ps)], stg[w]);
-                    else
-                        lw = level[w];
-                    atomicMax(&s_m[row_idx[p] - (int)c0], lw);
+            for (int64_t p0 = row_ptr[c0] + tid; p0 < e1; p0 += kRunPer * kRunThreads) {
+                int32_t w[kRunPer], r[kRunPer];
+#pragma unroll
+                for (int u = 0; u < kRunPer; ++u) {
+                    const int64_t p = p0 + (int64_t)u * kRunThreads;
+                    const bool in = p < e1;
+                    w[u] = in ? prow[min(p, e1 - 1)] : -1;
+                    r[u] = row_idx[min(p, e1 - 1)];
+                }
+                int lv[kRunPer], sv[kRunPer];
+#pragma unroll
+                for (int u = 0; u < kRunPer; ++u) {
+                    const bool before = w[u] >= 0 && w[u] < a;
+                    const int32_t q = before ? w[u] : 0;
+                    lv[u] = level[q];
+                    sv[u] = stg[q];
+                }
+#pragma unroll
+                for (int u = 0; u < kRunPer; ++u) {
+                    if (w[u] >= 0 && w[u] < a) {
+                        const int lw = (k > 0 && w[u] >= pa)
+                                           ? w[u] + 1 + max(s_pre[(int)((w[u] - pa) / ps)], sv[u])
+                                           : lv[u];
+                        atomicMax(&s_m[r[u] - (int)c0], lw);
+                    }
                 }
             }
             __syncthreads();
