@@ -510,8 +510,8 @@ def main():
                          "(a plain copy of known size, for scaling HBM traffic counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: the path does not shard across GPUs "
-              "(see DESIGN.md, 'More than one GPU'); use --gpus 1", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the path does not shard across GPUs; "
+              "use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
